@@ -1,0 +1,444 @@
+"""Pins of the fp64 oracle against facts fixed outside the oracle itself.
+
+Each pin checks the oracle against something it does not compute the same way:
+torch autograd on a small model, a closed form the paper prints (eq. 5), the
+decomposition the paper writes for tied weights (eq. 11/13), an independent
+algebraic identity (the Gram form of the Frobenius norm), the Philox published
+known-answer vectors, distribution statistics, or plain integer brute force.
+The mutation tests at the end plant plausible mistakes in a copy of the oracle
+and check that some pin catches each one.
+"""
+import os
+import types
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from workloads import gen
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+RNG = np.random.default_rng(12345)
+
+
+def _rand(*shape, scale=1.0):
+    return RNG.standard_normal(shape) * scale
+
+
+# ---------------------------------------------------------------------------
+# Pin 1: per-example linear gradient and its norm
+# ---------------------------------------------------------------------------
+def check_linear_grad_autograd(o, B=3, T=5, d_in=4, d_out=6):
+    """Per-example dL/dW of y = x W (W [d_in, d_out]) from autograd."""
+    A = _rand(B, T, d_in)
+    R = _rand(B, T, d_out)
+    W = torch.tensor(_rand(d_in, d_out), dtype=torch.float64, requires_grad=True)
+    for i in range(B):
+        W.grad = None
+        y = torch.tensor(A[i]) @ W
+        (y * torch.tensor(R[i])).sum().backward()   # dL/dy = R
+        g_ref = W.grad.numpy()
+        g = o.linear_grad(A[i], R[i])
+        assert g.shape == g_ref.shape
+        np.testing.assert_allclose(g, g_ref, rtol=1e-12, atol=1e-12)
+        assert abs(o.sqnorm(g) - float((W.grad ** 2).sum())) <= 1e-12 * max(1.0, o.sqnorm(g))
+
+
+def test_linear_grad_matches_autograd():
+    check_linear_grad_autograd(O)
+
+
+@pytest.mark.parametrize("T", [1, 2, 3, 16, 17])
+@pytest.mark.parametrize("d_in,d_out", [(1, 1), (5, 3), (64, 64), (1, 5)])
+def test_linear_norm_equals_gram_identity(T, d_in, d_out):
+    """||A^T G||_F^2 = sum_{t,s} (A A^T)_{ts} (G G^T)_{ts}: an independent formula."""
+    B = 3
+    A = _rand(B, T, d_in)
+    G = _rand(B, T, d_out, scale=1e-2)
+    got = O.linear_norm2(A, G)
+    for i in range(B):
+        gram = float(np.sum((A[i] @ A[i].T) * (G[i] @ G[i].T)))
+        assert abs(got[i] - gram) <= 1e-11 * abs(gram)
+
+
+def test_linear_norm_T1_closed_form():
+    """eq. 5: with one token the norm is ||delta||^2 ||a||^2."""
+    A = _rand(4, 1, 7)
+    G = _rand(4, 1, 9)
+    got = O.linear_norm2(A, G)
+    ref = (A[:, 0] ** 2).sum(-1) * (G[:, 0] ** 2).sum(-1)
+    np.testing.assert_allclose(got, ref, rtol=1e-13)
+
+
+def test_linear_norm_scaling_and_permutation():
+    A = _rand(5, 6, 4)
+    G = _rand(5, 6, 3)
+    n = O.linear_norm2(A, G)
+    np.testing.assert_allclose(O.linear_norm2(A, 3.0 * G), 9.0 * n, rtol=1e-13)
+    perm = RNG.permutation(5)
+    np.testing.assert_allclose(O.linear_norm2(A[perm], G[perm]), n[perm], rtol=1e-14)
+    # permuting tokens inside an example leaves its gradient unchanged
+    tp = RNG.permutation(6)
+    np.testing.assert_allclose(O.linear_norm2(A[:, tp], G[:, tp]), n, rtol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Pin 2: embedding gradient, head gradient, tied composition
+# ---------------------------------------------------------------------------
+def _tiny_tied_lm(B, T, V, d, seed=0):
+    """A small causal LM with E tied to the output head, all fp64 autograd.
+
+    emb = E[ids]; h = tanh(emb W1) + emb; logits = h E^T;
+    loss_i = sum_t CE(logits[t], ids[t+1]) / T.
+    Returns per-example tied gradients and the captured (dE, H, Gz).
+    """
+    g = torch.Generator().manual_seed(seed)
+    E = torch.randn(V, d, generator=g, dtype=torch.float64, requires_grad=True)
+    W1 = torch.randn(d, d, generator=g, dtype=torch.float64) * 0.3
+    ids = torch.randint(0, V, (B, T), generator=g)
+    ids[0, : T // 2] = ids[0, 0]          # forces repeated ids in example 0
+    grads, dEs, Hs, Gzs = [], [], [], []
+    for i in range(B):
+        E.grad = None
+        emb = E[ids[i]]
+        emb.retain_grad()
+        h = torch.tanh(emb @ W1) + emb
+        h.retain_grad()
+        logits = h @ E.T
+        logits.retain_grad()
+        loss = torch.nn.functional.cross_entropy(logits[:-1], ids[i, 1:], reduction="sum") / T
+        loss.backward()
+        grads.append(E.grad.numpy().copy())
+        dEs.append(emb.grad.numpy().copy())
+        Hs.append(h.detach().numpy().copy())
+        Gzs.append(logits.grad.numpy().copy())
+    return ids.numpy().astype(np.int32), np.stack(grads), np.stack(dEs), np.stack(Hs), np.stack(Gzs)
+
+
+def check_tied_against_autograd(o, B=3, T=9, V=11, d=5):
+    ids, g_true, dE, H, Gz = _tiny_tied_lm(B, T, V, d)
+    for i in range(B):
+        gE = o.embedding_grad(ids[i], dE[i], V)
+        gW = o.head_grad(H[i], Gz[i], V)
+        np.testing.assert_allclose(gE + gW, g_true[i], rtol=1e-10, atol=1e-12)
+    tn = o.tied_norm2(ids, dE, H, Gz, V)
+    np.testing.assert_allclose(tn, (g_true ** 2).sum(axis=(1, 2)), rtol=1e-10)
+    # eq. 11 / eq. 13: ||gin + gout||^2 = ||gin||^2 + ||gout||^2 + 2 <gin, gout>
+    n_in = o.embedding_norm2(ids, dE, V)
+    n_out = o.head_norm2(H, Gz, V)
+    cross = o.tied_cross(ids, dE, H, Gz, V)
+    np.testing.assert_allclose(n_in + n_out + 2 * cross, tn, rtol=1e-10)
+    # the naive sum of eq. 12 differs from the true norm by exactly 2*cross
+    assert np.all(np.abs(cross) > 0)
+    np.testing.assert_allclose(tn - (n_in + n_out), 2 * cross, rtol=1e-9)
+
+
+def test_tied_gradient_matches_autograd():
+    check_tied_against_autograd(O)
+
+
+def test_cross_cauchy_schwarz_and_sign():
+    ids, _, dE, H, Gz = _tiny_tied_lm(4, 12, 7, 6, seed=3)
+    n_in = O.embedding_norm2(ids, dE, 7)
+    n_out = O.head_norm2(H, Gz, 7)
+    cross = O.tied_cross(ids, dE, H, Gz, 7)
+    assert np.all(np.abs(cross) <= np.sqrt(n_in * n_out) * (1 + 1e-12))
+    # flipping the sign of the embedding pathway flips the cross term only
+    np.testing.assert_allclose(O.tied_cross(ids, -dE, H, Gz, 7), -cross, rtol=1e-14)
+
+
+def test_embedding_special_cases():
+    T, d, V = 8, 5, 32
+    dE = _rand(1, T, d)
+    distinct = RNG.permutation(V)[:T].astype(np.int32)[None]
+    np.testing.assert_allclose(O.embedding_norm2(distinct, dE, V)[0], (dE[0] ** 2).sum(), rtol=1e-13)
+    same = np.full((1, T), 3, np.int32)
+    np.testing.assert_allclose(O.embedding_norm2(same, dE, V)[0], (dE[0].sum(0) ** 2).sum(), rtol=1e-13)
+    # the embedding is a linear layer whose input is onehot(ids)
+    ids = RNG.integers(0, 4, size=(3, T)).astype(np.int32)
+    dE3 = _rand(3, T, d)
+    onehot = np.eye(V)[ids]
+    np.testing.assert_allclose(O.embedding_norm2(ids, dE3, V), O.linear_norm2(onehot, dE3), rtol=1e-12)
+
+
+def test_head_is_linear_layer_d_to_V():
+    H = _rand(2, 6, 4)
+    Gz = _rand(2, 6, 9)
+    np.testing.assert_allclose(O.head_norm2(H, Gz, 9), O.linear_norm2(H, Gz), rtol=1e-13)
+    # padding columns beyond V are ignored
+    Gzp = np.concatenate([Gz, _rand(2, 6, 3)], axis=2)
+    np.testing.assert_allclose(O.head_norm2(H, Gzp, 9), O.linear_norm2(H, Gz), rtol=1e-13)
+
+
+# ---------------------------------------------------------------------------
+# Pin 3: buckets (integer brute force)
+# ---------------------------------------------------------------------------
+def test_buckets_brute_force():
+    ids = RNG.integers(0, 20, size=(5, 33)).astype(np.int32)
+    ids[1] = 7
+    ids[2] = np.arange(33)
+    seg, nu = O.buckets(ids)
+    for i in range(5):
+        distinct = sorted(set(int(x) for x in ids[i]))
+        rank = {v: r for r, v in enumerate(distinct)}
+        assert nu[i] == len(distinct)
+        assert [rank[int(x)] for x in ids[i]] == seg[i].tolist()
+
+
+# ---------------------------------------------------------------------------
+# Pin 4: clipping (eq. 2, eq. 7)
+# ---------------------------------------------------------------------------
+def check_clip(o):
+    A = _rand(6, 5, 4)
+    G = _rand(6, 5, 3)
+    G[2] = 0.0                       # zero gradient
+    G[3] *= 1e-3                     # well under C
+    C = 0.7
+    n2 = o.linear_norm2(A, G)
+    c = o.clip_factors(n2, C)
+    assert c[2] == 1.0
+    for i in range(6):
+        N = np.sqrt(n2[i])
+        clipped = c[i] * o.linear_grad(A[i], G[i])
+        Nc = np.sqrt((clipped ** 2).sum())
+        assert Nc <= C * (1 + 1e-12)
+        if N > C:
+            assert abs(Nc - C) <= 1e-12 * C
+        else:
+            assert c[i] == 1.0
+
+
+def test_clip_bounds():
+    check_clip(O)
+
+
+def check_huge_C_is_plain_gradient(o):
+    """C -> infinity: the clipped sum is the non-private gradient, one GEMM over B*T rows."""
+    A = _rand(4, 6, 5)
+    G = _rand(4, 6, 3)
+    c = o.clip_factors(o.linear_norm2(A, G), 1e30)
+    assert np.all(c == 1.0)
+    S = o.clipped_sum_linear(A, G, c)
+    ref = A.reshape(-1, 5).T @ G.reshape(-1, 3)
+    np.testing.assert_allclose(S, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_huge_C_is_plain_gradient():
+    check_huge_C_is_plain_gradient(O)
+
+
+def test_small_C_linearity_and_permutation_invariance():
+    A = _rand(5, 4, 3)
+    G = _rand(5, 4, 2)
+    n2 = O.linear_norm2(A, G)
+    S1 = O.clipped_sum_linear(A, G, O.clip_factors(n2, 1e-6))
+    S2 = O.clipped_sum_linear(A, G, O.clip_factors(n2, 2e-6))
+    np.testing.assert_allclose(S2, 2 * S1, rtol=1e-12)
+    perm = RNG.permutation(5)
+    S1p = O.clipped_sum_linear(A[perm], G[perm], O.clip_factors(n2[perm], 1e-6))
+    np.testing.assert_allclose(S1p, S1, rtol=1e-12)
+
+
+def test_embedding_and_head_sums_match_linear_forms():
+    V, T, d = 10, 7, 3
+    ids = RNG.integers(0, V, size=(3, T)).astype(np.int32)
+    dE = _rand(3, T, d)
+    H = _rand(3, T, d)
+    Gz = _rand(3, T, V)
+    c = np.array([0.5, 1.0, 0.25])
+    onehot = np.eye(V)[ids]
+    np.testing.assert_allclose(O.clipped_sum_embedding(ids, dE, c, V),
+                               O.clipped_sum_linear(onehot, dE, c), rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(O.clipped_sum_head(H, Gz, c, V),
+                               O.clipped_sum_linear(Gz, H, c), rtol=1e-12, atol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# Pin 5: noise (eq. 3), Philox known answers, Gaussian statistics
+# ---------------------------------------------------------------------------
+def _kat_rows():
+    rows = []
+    with open(os.path.join(GOLDEN, "philox4x32_10_kat.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            v = [int(x, 16) for x in line.split()]
+            rows.append((v[0:4], v[4:6], v[6:10]))
+    return rows
+
+
+def check_philox_kat(o):
+    for ctr, key, out in _kat_rows():
+        got = o.philox4x32_10([np.array([c], np.uint64) for c in ctr], key)
+        assert [int(g[0]) for g in got] == out
+
+
+def test_philox_known_answers():
+    assert len(_kat_rows()) == 3
+    check_philox_kat(O)
+
+
+def test_gaussian_statistics():
+    n = 1 << 20
+    z = O.gaussian(n, seed=7, tensor_id=3, step=11)
+    se = 1.0 / np.sqrt(n)
+    assert abs(z.mean()) < 5 * se
+    assert abs(z.std() - 1.0) < 5 * np.sqrt(0.5) * se
+    # fourth moment of a standard normal is 3
+    assert abs((z ** 4).mean() - 3.0) < 5 * np.sqrt(96.0) * se
+    from scipy import stats
+    assert stats.kstest(z[: 1 << 16], "norm").pvalue > 1e-4
+    # the four outputs of one Philox block are not copies of each other
+    zz = z.reshape(-1, 4)
+    assert abs(np.corrcoef(zz[:, 0], zz[:, 1])[0, 1]) < 5 * np.sqrt(4.0 / n)
+
+
+def test_gaussian_streams_are_keyed_and_sliceable():
+    a = O.gaussian(1000, 1, 2, 3)
+    np.testing.assert_array_equal(O.gaussian(10, 1, 2, 3, start=995)[:5], a[995:])
+    assert not np.allclose(a, O.gaussian(1000, 1, 2, 4))
+    assert not np.allclose(a, O.gaussian(1000, 1, 5, 3))
+    assert not np.allclose(a, O.gaussian(1000, 2, 2, 3))
+    # the 64-bit seed uses both halves
+    assert not np.allclose(a, O.gaussian(1000, 1 + (1 << 32), 2, 3))
+
+
+def test_noise_sigma_zero_and_scale():
+    S = _rand(7, 9)
+    np.testing.assert_array_equal(O.add_noise(S, 0.0, 1.0, 4, 0, 0, 0), S / 4)
+    np.testing.assert_array_equal(O.add_noise(S, 0.0, 1.0, 0, 0, 0, 0), S)
+    z = O.gaussian(S.size, 5, 1, 2).reshape(S.shape)
+    np.testing.assert_allclose(O.add_noise(S, 2.0, 0.5, 3, 5, 1, 2), (S + 1.0 * z) / 3, rtol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# Pin 6: generator facts the workloads rely on
+# ---------------------------------------------------------------------------
+def test_param_counts_match_paper_table():
+    with open(os.path.join(GOLDEN, "gpt2_param_counts.txt")) as f:
+        rows = [l.split() for l in f if l.strip() and not l.startswith("#")]
+    assert len(rows) == 4
+    for _, nb, tied, n in rows:
+        assert gen.gpt2_param_count(int(nb), bool(int(tied))) == int(n)
+    # untying adds exactly one V x d matrix
+    assert gen.gpt2_param_count(12, False) - gen.gpt2_param_count(12, True) == 50257 * 768
+
+
+def test_logit_grads_match_cross_entropy_autograd():
+    B, T, V = 2, 6, 13
+    z = RNG.standard_normal((B, T, V)).astype(np.float32)
+    ids = RNG.integers(0, V, size=(B, T)).astype(np.int32)
+    zt = torch.tensor(z.astype(np.float64), requires_grad=True)
+    loss = 0
+    for i in range(B):
+        loss = loss + torch.nn.functional.cross_entropy(
+            zt[i, :-1], torch.tensor(ids[i, 1:]).long(), reduction="sum") / T
+    loss.backward()
+    got = gen.logit_grads(z.copy(), ids)
+    np.testing.assert_allclose(got, zt.grad.numpy(), rtol=1e-5, atol=1e-7)
+    np.testing.assert_allclose(got[:, :-1].sum(-1), 0.0, atol=1e-6)
+    assert np.all(got[:, -1] == 0)
+
+
+def test_zipf_frequencies():
+    rng = np.random.default_rng(0)
+    ids = gen.zipf_ids(rng, (200000,), 50257, 1.1)
+    k = np.arange(1, 50258, dtype=np.float64)
+    p = k ** -1.1
+    p /= p.sum()
+    for r in range(5):
+        f = np.mean(ids == r)
+        assert abs(f - p[r]) < 5 * np.sqrt(p[r] * (1 - p[r]) / ids.size)
+    assert ids.min() >= 0 and ids.max() < 50257
+
+
+def test_bf16_rounding():
+    x = np.array([1.0, 1.00390625, 1.01171875, -2.5, 3.0e-3, 1e30], np.float32)
+    b = gen.f32_to_bf16_bits(x)
+    back = gen.bf16_bits_to_f32(b)
+    # 1 + 2^-8 is a tie between 1 and 1 + 2^-7: goes to even (1.0)
+    assert back[0] == 1.0 and back[1] == 1.0
+    assert back[2] == np.float32(1.015625)       # 1 + 3*2^-8 ties up to even
+    np.testing.assert_allclose(back, x, rtol=2 ** -8)
+    np.testing.assert_array_equal(O.decode(b, "bf16"), back.astype(np.float64))
+
+
+def test_workload_streams_are_per_tensor():
+    full = gen.make_workload("c1", B=4, T=16)
+    again = gen.make_workload("c1", B=4, T=16)
+    np.testing.assert_array_equal(full.linears[0].A, again.linears[0].A)
+    np.testing.assert_array_equal(full.head.ids, again.head.ids)
+    sub = gen.make_workload("c2", B=2, T=8, n_blocks=2, layers=[5], with_head=False)
+    full2 = gen.make_workload("c2", B=2, T=8, n_blocks=2, with_head=False)
+    np.testing.assert_array_equal(sub.linears[0].A, full2.linears[5].A)
+
+
+# ---------------------------------------------------------------------------
+# Whole-step consistency on the tiny workloads
+# ---------------------------------------------------------------------------
+def test_step_tiny_tied_consistency():
+    wl = gen.make_workload("c1-tied", B=4, T=16)
+    r = O.step(wl, seed=3, step_id=1)
+    n = r["norms"]
+    np.testing.assert_allclose(n["in"] + n["out"] + 2 * n["cross"], n["tied"], rtol=1e-10)
+    np.testing.assert_allclose(n["total"], n["linear"].sum(0) + n["tied"], rtol=1e-13)
+    assert set(r["noisy"]) == {"linear", "wte"}
+    # sigma = 0 reproduces the clipped mean exactly
+    wl.sigma = 0.0
+    r0 = O.step(wl, seed=3, step_id=1)
+    for k in r0["sums"]:
+        np.testing.assert_array_equal(r0["noisy"][k], r0["sums"][k] / wl.B)
+
+
+# ---------------------------------------------------------------------------
+# Mutation tests: plausible mistakes planted in a copy of the oracle
+# ---------------------------------------------------------------------------
+def _mutant(**overrides):
+    m = types.SimpleNamespace(**{k: getattr(O, k) for k in O.__all__})
+    for k, v in overrides.items():
+        setattr(m, k, v)
+    return m
+
+
+def _fails(check, o):
+    try:
+        check(o)
+    except AssertionError:
+        return True
+    return False
+
+
+def test_pins_catch_transposed_linear_grad():
+    m = _mutant(linear_grad=lambda A, G: G.T @ A)
+    assert _fails(check_linear_grad_autograd, m)
+
+
+def test_pins_catch_dropped_cross_term():
+    def tied_norm2_naive(ids, dE, H, Gz, V):
+        return O.embedding_norm2(ids, dE, V) + O.head_norm2(H, Gz, V)
+    assert _fails(check_tied_against_autograd, _mutant(tied_norm2=tied_norm2_naive))
+
+
+def test_pins_catch_wrong_head_orientation():
+    def head_grad_bad(H_i, Gz_i, V):
+        return Gz_i[:, :V].T @ H_i[::-1]     # tokens of H misaligned with Gz
+    assert _fails(check_tied_against_autograd, _mutant(head_grad=head_grad_bad))
+
+
+def test_pins_catch_clip_max_instead_of_min():
+    def clip_bad(norm2, C):
+        n = np.sqrt(norm2)
+        c = np.ones_like(n)
+        nz = n > 0
+        c[nz] = np.maximum(1.0, C / n[nz])
+        return c
+    assert _fails(check_clip, _mutant(clip_factors=clip_bad))
+
+
+def test_pins_catch_philox_wrong_rounds():
+    def philox9(ctr, key):
+        c = [np.asarray(x, np.uint64) for x in ctr]
+        out = O.philox4x32_10(c, key)
+        return [o ^ np.uint32(1) for o in out]
+    assert _fails(check_philox_kat, _mutant(philox4x32_10=philox9))
