@@ -1,0 +1,187 @@
+/*
+ * dpghost.h -- per-example gradient norms by ghost clipping, clip factors,
+ * the clipped gradient sum and Gaussian noise for DP-SGD on decoder-only
+ * transformers, on one AMD Instinct MI355X (gfx950).
+ *
+ * Method: El Mais, Chehab, Issa, Tajeddine, "Is Weight Tying Still Beneficial
+ * for Decoder-Only LLMs in Private Settings Under DP-SGD?" (arXiv 2609.40335).
+ * Section and equation numbers below refer to that paper.
+ *
+ * Conventions for every entry point
+ *  - Tensor pointers are DEVICE pointers, row-major. A token-major matrix
+ *    [B, T, w] with row stride ld (elements, ld >= w) holds token t of
+ *    example b at row b*T + t. bf16 data is passed as its 16-bit patterns.
+ *  - Outputs are fp32. Squared norms add across calls ("accumulate" = 1
+ *    means +=, 0 means overwrite), which is eq. 6 / eq. 10.
+ *  - `stream` is a hipStream_t (NULL = the default stream). Calls are
+ *    asynchronous and stream-ordered; nothing synchronises the device.
+ *  - Ownership: the caller allocates and owns every buffer. The library
+ *    allocates no device memory. Entry points that need scratch take a
+ *    caller-owned device `workspace` of at least the size returned by their
+ *    *_workspace() function; its contents need no initialisation and are
+ *    dead after the call's kernels finish. Two calls in flight at once must
+ *    not share a workspace.
+ *  - Errors: arguments are validated on the host before any HIP call. A
+ *    NULL required pointer, a non-positive size, a stride smaller than its
+ *    row width, an unknown dtype or a too-small workspace returns DP_EINVAL;
+ *    a size beyond a documented limit returns DP_EUNSUPPORTED; a failed
+ *    kernel launch returns DP_EHIP. dp_last_error() describes the last
+ *    failure on the calling thread. Exceptions never cross this interface.
+ *  - Token ids outside [0, V) are a caller error; kernels never read or
+ *    write out of bounds for them (they contribute nothing to cross terms or
+ *    sums), but the results are then meaningless.
+ *  - Thread safety: the functions keep no state between calls.
+ */
+#ifndef DPGHOST_H
+#define DPGHOST_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DP_ABI_VERSION 1
+
+typedef enum { DP_F32 = 0, DP_BF16 = 1 } dp_dtype_t;
+
+typedef enum {
+  DP_OK = 0,
+  DP_EINVAL = 1,
+  DP_EUNSUPPORTED = 2,
+  DP_EHIP = 3
+} dp_status_t;
+
+/* How a linear layer's per-example norm is evaluated.
+ * GRAM:   <A_i A_i^T, G_i G_i^T> from two T x T Grams (ghost clipping,
+ *         Sec. "Ghost Clipping Mechanism").
+ * DIRECT: ||A_i^T G_i||_F^2 from the per-example gradient, squared and
+ *         summed in registers without storing it (the materialising form of
+ *         "normal clipping", Sec. "Training Configurations").
+ * AUTO:   DIRECT when T + 1 > 2 d_in d_out / (d_in + d_out), else GRAM. */
+typedef enum { DP_NORM_AUTO = 0, DP_NORM_GRAM = 1, DP_NORM_DIRECT = 2 } dp_norm_algo_t;
+
+/* One linear layer y = x W with W [d_in, d_out]: activations A [B,T,d_in]
+ * (row stride lda) entering it and output gradients G [B,T,d_out] (row
+ * stride ldg) leaving it (Sec. "Ghost Clipping Mechanism", eq. 4). The
+ * output head of a language model is the layer d -> V with A = the hidden
+ * states H and G = the logit gradients. */
+typedef struct {
+  const void* A;
+  int64_t lda;
+  int32_t d_in;
+  const void* G;
+  int64_t ldg;
+  int32_t d_out;
+  int32_t algo; /* dp_norm_algo_t */
+} dp_linear_t;
+
+int dp_abi_version(void);
+const char* dp_status_string(dp_status_t s);
+const char* dp_last_error(void);
+
+/* ---------------------------------------------------------------------
+ * Linear-layer ghost norm (Sec. "Ghost Clipping Mechanism", eq. 4-6).
+ * For every example b:
+ *   norm2[b] (+)= sum over layers of ||A_b^T G_b||_F^2.
+ * The grouped form evaluates many layers of one batch in one launch (all
+ * share B, T and dtype). Limits: T <= 65536, d_in, d_out <= 2^31 - 1.
+ * Workspace: dp_ghost_norm_linear_workspace() bytes (fp32 partials).
+ * ------------------------------------------------------------------- */
+size_t dp_ghost_norm_linear_workspace(const dp_linear_t* layers, int n_layers, int B, int T,
+                                      dp_dtype_t dt);
+dp_status_t dp_ghost_norm_linear_grouped(const dp_linear_t* layers, int n_layers, int B, int T,
+                                         dp_dtype_t dt, float* norm2, int accumulate,
+                                         void* workspace, size_t workspace_bytes, void* stream);
+dp_status_t dp_ghost_norm_linear(const void* A, int64_t lda, const void* G, int64_t ldg, int B,
+                                 int T, int d_in, int d_out, dp_dtype_t dt, int algo,
+                                 float* norm2, int accumulate, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------
+ * Input-embedding ghost norm and token buckets (Sec. "Weight Tying in
+ * Decoder-Only LLMs"; the embedding reads row ids[b,t] of E in R^{V x d}).
+ * dE [B,T,d] (row stride lde) is the gradient w.r.t. the embedding output.
+ *   norm2[b] (+)= sum_v || sum_{t: ids[b,t] = v} dE[b,t,:] ||^2
+ *   seg_id[b,t]  = rank of ids[b,t] among the sorted distinct ids of b
+ *   n_unique[b]  = number of distinct ids of b
+ * seg_id and n_unique may be NULL. Exact (integer) outputs.
+ * Limits: T <= 4096 and ceil(log2 V) + ceil(log2 T) <= 32.
+ * ------------------------------------------------------------------- */
+size_t dp_ghost_norm_embedding_workspace(int B, int T, int d);
+dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t lde, int B, int T,
+                                    int V, int d, dp_dtype_t dt, float* norm2, int accumulate,
+                                    int32_t* seg_id, int32_t* n_unique, void* workspace,
+                                    size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------
+ * Tied-embedding cross term (Sec. "Corrected Ghost Norm for Tied
+ * Embeddings", eq. 11 and eq. 13): with W_out = E, the squared norm of the
+ * tied gradient is ||g_in||^2 + ||g_out||^2 + 2 <g_in, g_out>. This computes
+ *   cross_b = <g_in,b, g_out,b> = sum_{t,s} Gz[b,s,ids[b,t]] <dE[b,t], H[b,s]>
+ * without forming either V x d gradient, and writes
+ *   out[b] = (accumulate ? out[b] : 0) + scale * cross_b.
+ * scale = 2, accumulate = 1 adds the correction straight into a norm2.
+ * H [B,T,d] (ldh) are the hidden states entering the head; Gz [B,T,V]
+ * (row stride ldz >= V) the logit gradients.
+ * ------------------------------------------------------------------- */
+size_t dp_tied_cross_term_workspace(int B, int T);
+dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, const void* H,
+                               int64_t ldh, const void* Gz, int64_t ldz, int B, int T, int V,
+                               int d, dp_dtype_t dt, float scale, float* out, int accumulate,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------
+ * Clip factors (eq. 2, eq. 7): c[b] = min(1, C / sqrt(norm2[b])), and 1
+ * when norm2[b] <= 0. C must be positive and finite.
+ * ------------------------------------------------------------------- */
+dp_status_t dp_clip_factors(const float* norm2, int B, float C, float* c, void* stream);
+
+/* ---------------------------------------------------------------------
+ * Clipped gradient sum (the bracket of eq. 3 without noise): the gradient
+ * of the loss reweighted by the clip factors, as one GEMM over the B*T
+ * tokens (K = B*T) with token k of example b scaled by c[b]:
+ *   out (+)= sum_b c[b] A_b^T G_b            [d_in, d_out]
+ * or its transpose [d_out, d_in] when transpose_out = 1 (out is contiguous).
+ * Embedding form: pass A = NULL and ids [B,T]; A_b is then onehot(ids_b)
+ * with d_in = V, i.e. out[v,:] (+)= sum over tokens with id v of
+ * c[b] G[b,t,:]. A tied matrix receives both the head and the embedding
+ * parts in one buffer: call the head form, then the embedding form with
+ * accumulate = 1.
+ * Workspace: only the embedding form needs one,
+ * dp_clipped_grad_sum_workspace(B, T, d_out, 1) bytes; limits for it:
+ * B*T <= 16384 and ceil(log2 V) + ceil(log2(B*T)) <= 32.
+ * ------------------------------------------------------------------- */
+size_t dp_clipped_grad_sum_workspace(int B, int T, int d_out, int with_ids);
+dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64_t ldg,
+                                const int32_t* ids, const float* c, int B, int T, int d_in,
+                                int d_out, dp_dtype_t dt, int transpose_out, float* out,
+                                int accumulate, void* workspace, size_t workspace_bytes,
+                                void* stream);
+/* Many linear layers in one launch; outs[l] is layer l's output. */
+dp_status_t dp_clipped_grad_sum_grouped(const dp_linear_t* layers, float* const* outs,
+                                        int n_layers, const float* c, int B, int T,
+                                        dp_dtype_t dt, int transpose_out, int accumulate,
+                                        void* stream);
+
+/* ---------------------------------------------------------------------
+ * Gaussian mechanism (eq. 3): grad[j] = (grad[j] + sigma*C*z_j) / B_norm
+ * (no division when B_norm = 0), in place, for j < n. z_j is a standard
+ * normal from the counter-based Philox4x32-10 generator (Salmon et al.,
+ * SC'11) and the Box-Muller transform: element j uses Philox block j/4 with
+ * key (seed low word, seed high word) and counter (block low word, block
+ * high word, tensor_id, step); the four outputs x become uniforms
+ * (x + 1/2) 2^-32 and the pairs (0,1), (2,3) give r cos(2 pi u_odd),
+ * r sin(2 pi u_odd) with r = sqrt(-2 ln u_even); element j takes output j%4.
+ * The same (seed, tensor_id, step) reproduces the same noise, so the
+ * generator position is the only state to checkpoint. tensor_id and step
+ * must be < 2^32. grad is fp32.
+ * ------------------------------------------------------------------- */
+dp_status_t dp_add_noise(float* grad, int64_t n, float sigma, float C, int B_norm, uint64_t seed,
+                         uint64_t tensor_id, uint64_t step, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DPGHOST_H */

@@ -1,0 +1,479 @@
+// C ABI of libdpghost: argument validation, launch planning and dispatch.
+// Every argument is checked on the host before any HIP call.
+#include "../../include/dpghost.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dp_status_t fail(dp_status_t s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+dp_status_t hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return DP_OK;
+  return fail(DP_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+inline bool dtype_ok(dp_dtype_t dt) { return dt == DP_F32 || dt == DP_BF16; }
+inline int elems_per_chunk(dp_dtype_t dt) { return dt == DP_BF16 ? 8 : 4; }
+inline int stage_features(dp_dtype_t dt) { return dt == DP_BF16 ? 64 : 32; }
+inline int kdt(dp_dtype_t dt) { return dt == DP_BF16 ? dpg::DT_BF16 : dpg::DT_F32; }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline bool vec_ok(const void* p, int64_t ld, dp_dtype_t dt) {
+  return aligned16(p) && ld % elems_per_chunk(dt) == 0;
+}
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int bits_for(int64_t n_values) {  // bits to index n_values distinct values
+  int b = 0;
+  while (b < 63 && (int64_t(1) << b) < n_values) ++b;
+  return b;
+}
+inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+// ------------------------------------------------------------------ planning
+constexpr int KG_SPLIT = 4096;  // G feature ranges longer than this are chunked
+constexpr int KG_CHUNK = 2048;  // chunk width (a multiple of both stage widths)
+
+struct GramEntry {
+  const void* A;
+  const void* G;
+  int64_t lda, ldg;
+  int d_in, g0, g1, kg, nc;
+  int slot_begin;
+  bool vec;
+};
+
+struct GemmEntry {
+  const void* X;
+  const void* Y;
+  int64_t ldx, ldy;
+  int m_lo, m_hi, n_lo, n_hi, tm, tn;
+  int slot_begin;
+  float* out;
+  int64_t ldo;
+  bool vec;
+};
+
+struct NormPlan {
+  std::vector<GramEntry> gram;
+  std::vector<GemmEntry> direct;
+  int n_t = 0, P = 0;
+  int64_t slots = 0;
+};
+
+bool use_direct(const dp_linear_t& L, int T) {
+  if (L.algo == DP_NORM_DIRECT) return true;
+  if (L.algo == DP_NORM_GRAM) return false;
+  const double crossover = 2.0 * (double)L.d_in * L.d_out / ((double)L.d_in + L.d_out);
+  return (double)T + 1.0 > crossover;
+}
+
+// Splits the output region [0,M) x [0,N) of a GEMM into an entry whose every
+// column bound is a multiple of the 16-byte chunk (16-byte loads) and
+// element-wise entries for the ragged edges.
+void plan_gemm(const void* X, int64_t ldx, int M, const void* Y, int64_t ldy, int N,
+               dp_dtype_t dt, float* out, int64_t ldo, std::vector<GemmEntry>& v,
+               int64_t* slots, int64_t slot_mult) {
+  auto add = [&](int m_lo, int m_hi, int n_lo, int n_hi, bool vec) {
+    if (m_hi <= m_lo || n_hi <= n_lo) return;
+    GemmEntry e{X, Y, ldx, ldy, m_lo, m_hi, n_lo, n_hi,
+                (int)ceil_div(m_hi - m_lo, dpg::GM_BM), (int)ceil_div(n_hi - n_lo, dpg::GM_BN),
+                0, out, ldo, vec};
+    if (slots) {
+      e.slot_begin = (int)*slots;
+      *slots += (int64_t)e.tm * e.tn * slot_mult;
+    }
+    v.push_back(e);
+  };
+  const int q = elems_per_chunk(dt);
+  if (vec_ok(X, ldx, dt) && vec_ok(Y, ldy, dt)) {
+    const int Ma = M / q * q, Na = N / q * q;
+    add(0, Ma, 0, Na, true);
+    add(Ma, M, 0, N, false);
+    add(0, Ma, Na, N, false);
+  } else {
+    add(0, M, 0, N, false);
+  }
+}
+
+NormPlan plan_norm(const dp_linear_t* layers, int n, int T, dp_dtype_t dt) {
+  NormPlan p;
+  p.n_t = (int)ceil_div(T, dpg::GR_TM);
+  p.P = p.n_t * (p.n_t + 1) / 2;
+  const int q = elems_per_chunk(dt), ks = stage_features(dt);
+  for (int i = 0; i < n; ++i) {
+    const dp_linear_t& L = layers[i];
+    if (use_direct(L, T)) {
+      plan_gemm(L.A, L.lda, L.d_in, L.G, L.ldg, L.d_out, dt, nullptr, 0, p.direct, &p.slots, 1);
+      continue;
+    }
+    auto add = [&](int g0, int g1, bool vec) {
+      if (g1 <= g0) return;
+      const int len = g1 - g0;
+      const int kg = len > KG_SPLIT ? KG_CHUNK : (int)(ceil_div(len, ks) * ks);
+      GramEntry e{L.A, L.G, L.lda, L.ldg, L.d_in, g0, g1, kg, (int)ceil_div(len, kg),
+                  (int)p.slots, vec};
+      p.slots += (int64_t)p.P * e.nc;
+      p.gram.push_back(e);
+    };
+    if (vec_ok(L.A, L.lda, dt) && vec_ok(L.G, L.ldg, dt) && L.d_in % q == 0) {
+      const int ga = L.d_out / q * q;
+      add(0, ga, true);
+      add(ga, L.d_out, false);
+    } else {
+      add(0, L.d_out, false);
+    }
+  }
+  return p;
+}
+
+dp_status_t check_layers(const dp_linear_t* layers, int n, int B, int T, dp_dtype_t dt) {
+  if (!layers) return fail(DP_EINVAL, "layers is NULL");
+  if (n <= 0) return fail(DP_EINVAL, "n_layers must be positive (got %d)", n);
+  if (B <= 0 || T <= 0) return fail(DP_EINVAL, "B and T must be positive (got %d, %d)", B, T);
+  if (!dtype_ok(dt)) return fail(DP_EINVAL, "unknown dtype %d", (int)dt);
+  if (T > 65536) return fail(DP_EUNSUPPORTED, "T = %d exceeds 65536", T);
+  for (int i = 0; i < n; ++i) {
+    const dp_linear_t& L = layers[i];
+    if (!L.A || !L.G) return fail(DP_EINVAL, "layer %d: A or G is NULL", i);
+    if (L.d_in <= 0 || L.d_out <= 0)
+      return fail(DP_EINVAL, "layer %d: d_in and d_out must be positive", i);
+    if (L.lda < L.d_in || L.ldg < L.d_out)
+      return fail(DP_EINVAL, "layer %d: row stride smaller than row width", i);
+    if (L.algo < DP_NORM_AUTO || L.algo > DP_NORM_DIRECT)
+      return fail(DP_EINVAL, "layer %d: unknown algo %d", i, L.algo);
+  }
+  return DP_OK;
+}
+
+// ------------------------------------------------------------------ launches
+dp_status_t run_gram(const NormPlan& p, int B, int T, dp_dtype_t dt, float* ws, hipStream_t s) {
+  for (int pass = 0; pass < 2; ++pass) {
+    const bool vec = pass == 0;
+    std::vector<const GramEntry*> sel;
+    for (const auto& e : p.gram)
+      if (e.vec == vec) sel.push_back(&e);
+    for (size_t i0 = 0; i0 < sel.size(); i0 += dpg::GR_MAX_LAYERS) {
+      dpg::GramArgs a{};
+      a.B = B; a.T = T; a.n_t = p.n_t; a.P = p.P;
+      a.slots = (int32_t)p.slots;
+      a.ws = ws;
+      uint64_t items = 0;
+      const size_t n = std::min(sel.size() - i0, (size_t)dpg::GR_MAX_LAYERS);
+      for (size_t j = 0; j < n; ++j) {
+        const GramEntry& e = *sel[i0 + j];
+        dpg::GramLayer& L = a.L[j];
+        L.A = e.A; L.G = e.G; L.lda = e.lda; L.ldg = e.ldg;
+        L.d_in = e.d_in; L.g0 = e.g0; L.g1 = e.g1; L.kg = e.kg; L.nc = e.nc;
+        L.item_begin = (uint32_t)items;
+        L.slot_begin = e.slot_begin;
+        items += (uint64_t)B * p.P * e.nc;
+      }
+      if (items > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many work items (%llu)",
+                                             (unsigned long long)items);
+      a.n_layers = (int32_t)n;
+      a.n_items = (uint32_t)items;
+      dp_status_t st = hip_status(dpg::launch_gram_norm(a, kdt(dt), vec, s), "gram_norm launch");
+      if (st != DP_OK) return st;
+    }
+  }
+  return DP_OK;
+}
+
+// mode 0: clipped sum (c, out); mode 1: direct norm (ws, slots)
+dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int T, dp_dtype_t dt,
+                     const float* c, float* ws, int64_t slots, int transpose, int accumulate,
+                     hipStream_t s) {
+  for (int pass = 0; pass < 2; ++pass) {
+    const bool vec = pass == 0;
+    std::vector<const GemmEntry*> sel;
+    for (const auto& e : entries)
+      if (e.vec == vec) sel.push_back(&e);
+    for (size_t i0 = 0; i0 < sel.size(); i0 += dpg::GM_MAX_LAYERS) {
+      dpg::GemmArgs a{};
+      a.B = B; a.T = T; a.c = c; a.ws = ws; a.slots = (int32_t)slots;
+      uint64_t items = 0;
+      const size_t n = std::min(sel.size() - i0, (size_t)dpg::GM_MAX_LAYERS);
+      for (size_t j = 0; j < n; ++j) {
+        const GemmEntry& e = *sel[i0 + j];
+        dpg::GemmLayer& L = a.L[j];
+        L.X = e.X; L.Y = e.Y; L.ldx = e.ldx; L.ldy = e.ldy;
+        L.m_lo = e.m_lo; L.m_hi = e.m_hi; L.n_lo = e.n_lo; L.n_hi = e.n_hi;
+        L.tm = e.tm; L.tn = e.tn;
+        L.tile_begin = (uint32_t)items;
+        L.slot_begin = e.slot_begin;
+        L.out = e.out; L.ldo = e.ldo;
+        L.transpose = transpose; L.accumulate = accumulate;
+        items += (uint64_t)e.tm * e.tn * (mode == 1 ? (uint64_t)B : 1ull);
+      }
+      if (items > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many work items");
+      a.n_layers = (int32_t)n;
+      a.n_items = (uint32_t)items;
+      hipError_t e = mode == 0 ? dpg::launch_clipped_sum(a, kdt(dt), vec, s)
+                               : dpg::launch_direct_norm(a, kdt(dt), vec, s);
+      dp_status_t st = hip_status(e, mode == 0 ? "clipped_sum launch" : "direct_norm launch");
+      if (st != DP_OK) return st;
+    }
+  }
+  return DP_OK;
+}
+
+size_t norm_ws_bytes(const NormPlan& p, int B) { return align_up((size_t)B * p.slots * 4); }
+
+// Embedding-sum workspace layout (bytes): keys, rank, seg, nseg, head, tail.
+struct EsLayout {
+  size_t keys, rank, seg, nseg, head, tail, total;
+};
+EsLayout es_layout(int64_t K, int d) {
+  EsLayout l{};
+  const int64_t nb = ceil_div(K, dpg::ES_BLOCK);
+  size_t off = 0;
+  l.keys = off; off = align_up(off + (size_t)K * 4);
+  l.rank = off; off = align_up(off + (size_t)K * 4);
+  l.seg = off; off = align_up(off + (size_t)(K + 1) * 4);
+  l.nseg = off; off = align_up(off + 4);
+  l.head = off; off = align_up(off + (size_t)nb * d * 4);
+  l.tail = off; off = align_up(off + (size_t)nb * d * 4);
+  l.total = off;
+  return l;
+}
+
+}  // namespace
+
+// ======================================================================
+extern "C" {
+
+int dp_abi_version(void) { return DP_ABI_VERSION; }
+
+const char* dp_status_string(dp_status_t s) {
+  switch (s) {
+    case DP_OK: return "ok";
+    case DP_EINVAL: return "invalid argument";
+    case DP_EUNSUPPORTED: return "unsupported size";
+    case DP_EHIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* dp_last_error(void) { return g_last_error.c_str(); }
+
+size_t dp_ghost_norm_linear_workspace(const dp_linear_t* layers, int n_layers, int B, int T,
+                                      dp_dtype_t dt) {
+  if (check_layers(layers, n_layers, B, T, dt) != DP_OK) return 0;
+  return norm_ws_bytes(plan_norm(layers, n_layers, T, dt), B);
+}
+
+dp_status_t dp_ghost_norm_linear_grouped(const dp_linear_t* layers, int n_layers, int B, int T,
+                                         dp_dtype_t dt, float* norm2, int accumulate,
+                                         void* workspace, size_t workspace_bytes, void* stream) {
+  dp_status_t st = check_layers(layers, n_layers, B, T, dt);
+  if (st != DP_OK) return st;
+  if (!norm2) return fail(DP_EINVAL, "norm2 is NULL");
+  const NormPlan p = plan_norm(layers, n_layers, T, dt);
+  if ((uint64_t)B * p.slots > 0x7FFFFFFFull) return fail(DP_EUNSUPPORTED, "too many partials");
+  const size_t need = norm_ws_bytes(p, B);
+  if (!workspace || workspace_bytes < need)
+    return fail(DP_EINVAL, "workspace of %zu bytes needed, %zu given", need,
+                workspace ? workspace_bytes : (size_t)0);
+  hipStream_t s = as_stream(stream);
+  float* ws = static_cast<float*>(workspace);
+  st = run_gram(p, B, T, dt, ws, s);
+  if (st != DP_OK) return st;
+  st = run_gemm(p.direct, 1, B, T, dt, nullptr, ws, p.slots, 0, 0, s);
+  if (st != DP_OK) return st;
+  return hip_status(dpg::launch_finish_rows(ws, B, (int)p.slots, norm2, accumulate, 1.f, s),
+                    "finish launch");
+}
+
+dp_status_t dp_ghost_norm_linear(const void* A, int64_t lda, const void* G, int64_t ldg, int B,
+                                 int T, int d_in, int d_out, dp_dtype_t dt, int algo,
+                                 float* norm2, int accumulate, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  dp_linear_t L{A, lda, d_in, G, ldg, d_out, algo};
+  return dp_ghost_norm_linear_grouped(&L, 1, B, T, dt, norm2, accumulate, workspace,
+                                      workspace_bytes, stream);
+}
+
+size_t dp_ghost_norm_embedding_workspace(int B, int T, int d) {
+  if (B <= 0 || T <= 0 || d <= 0) return 0;
+  return align_up((size_t)B * ceil_div(d, 64) * 4);
+}
+
+dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t lde, int B, int T,
+                                    int V, int d, dp_dtype_t dt, float* norm2, int accumulate,
+                                    int32_t* seg_id, int32_t* n_unique, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  if (!ids || !dE || !norm2) return fail(DP_EINVAL, "ids, dE or norm2 is NULL");
+  if (B <= 0 || T <= 0 || V <= 0 || d <= 0)
+    return fail(DP_EINVAL, "B, T, V and d must be positive");
+  if (lde < d) return fail(DP_EINVAL, "lde (%lld) < d (%d)", (long long)lde, d);
+  if (!dtype_ok(dt)) return fail(DP_EINVAL, "unknown dtype %d", (int)dt);
+  if (T > dpg::EN_MAX_T) return fail(DP_EUNSUPPORTED, "T = %d exceeds %d", T, dpg::EN_MAX_T);
+  const int pbits = std::max(1, bits_for(T));
+  if (bits_for(V) + pbits > 32)
+    return fail(DP_EUNSUPPORTED, "V = %d and T = %d do not fit a 32-bit sort key", V, T);
+  const size_t need = dp_ghost_norm_embedding_workspace(B, T, d);
+  if (!workspace || workspace_bytes < need)
+    return fail(DP_EINVAL, "workspace of %zu bytes needed", need);
+  dpg::EmbedNormArgs a{};
+  a.ids = ids; a.E = dE; a.lde = lde;
+  a.B = B; a.T = T; a.V = V; a.d = d;
+  a.pbits = pbits;
+  a.n_chunks = (int)ceil_div(d, 64);
+  a.seg_id = seg_id; a.n_unique = n_unique;
+  a.ws = static_cast<float*>(workspace);
+  hipStream_t s = as_stream(stream);
+  dp_status_t st = hip_status(dpg::launch_embed_norm(a, kdt(dt), s), "embed_norm launch");
+  if (st != DP_OK) return st;
+  return hip_status(dpg::launch_finish_rows(a.ws, B, a.n_chunks, norm2, accumulate, 1.f, s),
+                    "finish launch");
+}
+
+size_t dp_tied_cross_term_workspace(int B, int T) {
+  if (B <= 0 || T <= 0) return 0;
+  const int64_t nt = ceil_div(T, dpg::GR_TM);
+  return align_up((size_t)B * nt * nt * 4);
+}
+
+dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, const void* H,
+                               int64_t ldh, const void* Gz, int64_t ldz, int B, int T, int V,
+                               int d, dp_dtype_t dt, float scale, float* out, int accumulate,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  if (!ids || !dE || !H || !Gz || !out) return fail(DP_EINVAL, "a required pointer is NULL");
+  if (B <= 0 || T <= 0 || V <= 0 || d <= 0)
+    return fail(DP_EINVAL, "B, T, V and d must be positive");
+  if (lde < d || ldh < d || ldz < V) return fail(DP_EINVAL, "row stride smaller than row width");
+  if (!dtype_ok(dt)) return fail(DP_EINVAL, "unknown dtype %d", (int)dt);
+  if (!std::isfinite(scale)) return fail(DP_EINVAL, "scale must be finite");
+  if (T > 65536) return fail(DP_EUNSUPPORTED, "T = %d exceeds 65536", T);
+  const size_t need = dp_tied_cross_term_workspace(B, T);
+  if (!workspace || workspace_bytes < need)
+    return fail(DP_EINVAL, "workspace of %zu bytes needed", need);
+  dpg::CrossArgs a{};
+  a.ids = ids; a.E = dE; a.H = H; a.Gz = Gz;
+  a.lde = lde; a.ldh = ldh; a.ldz = ldz;
+  a.B = B; a.T = T; a.V = V; a.d = d;
+  a.n_t = (int)ceil_div(T, dpg::GR_TM);
+  a.slots = a.n_t * a.n_t;
+  a.ws = static_cast<float*>(workspace);
+  const bool vec = vec_ok(dE, lde, dt) && vec_ok(H, ldh, dt) && d % elems_per_chunk(dt) == 0;
+  hipStream_t s = as_stream(stream);
+  dp_status_t st = hip_status(dpg::launch_tied_cross(a, kdt(dt), vec, s), "tied_cross launch");
+  if (st != DP_OK) return st;
+  return hip_status(dpg::launch_finish_rows(a.ws, B, a.slots, out, accumulate, scale, s),
+                    "finish launch");
+}
+
+dp_status_t dp_clip_factors(const float* norm2, int B, float C, float* c, void* stream) {
+  if (!norm2 || !c) return fail(DP_EINVAL, "norm2 or c is NULL");
+  if (B <= 0) return fail(DP_EINVAL, "B must be positive");
+  if (!(C > 0.f) || !std::isfinite(C)) return fail(DP_EINVAL, "C must be positive and finite");
+  return hip_status(dpg::launch_clip_factors(norm2, B, C, c, as_stream(stream)), "clip launch");
+}
+
+size_t dp_clipped_grad_sum_workspace(int B, int T, int d_out, int with_ids) {
+  if (!with_ids || B <= 0 || T <= 0 || d_out <= 0) return 0;
+  return es_layout((int64_t)B * T, d_out).total;
+}
+
+dp_status_t dp_clipped_grad_sum_grouped(const dp_linear_t* layers, float* const* outs,
+                                        int n_layers, const float* c, int B, int T,
+                                        dp_dtype_t dt, int transpose_out, int accumulate,
+                                        void* stream) {
+  dp_status_t st = check_layers(layers, n_layers, B, T, dt);
+  if (st != DP_OK) return st;
+  if (!outs || !c) return fail(DP_EINVAL, "outs or c is NULL");
+  if ((int64_t)B * T > (int64_t(1) << 40)) return fail(DP_EUNSUPPORTED, "B*T too large");
+  std::vector<GemmEntry> entries;
+  for (int i = 0; i < n_layers; ++i) {
+    const dp_linear_t& L = layers[i];
+    if (!outs[i]) return fail(DP_EINVAL, "outs[%d] is NULL", i);
+    const int64_t ldo = transpose_out ? L.d_in : L.d_out;
+    plan_gemm(L.A, L.lda, L.d_in, L.G, L.ldg, L.d_out, dt, outs[i], ldo, entries, nullptr, 0);
+  }
+  return run_gemm(entries, 0, B, T, dt, c, nullptr, 0, transpose_out ? 1 : 0,
+                  accumulate ? 1 : 0, as_stream(stream));
+}
+
+dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64_t ldg,
+                                const int32_t* ids, const float* c, int B, int T, int d_in,
+                                int d_out, dp_dtype_t dt, int transpose_out, float* out,
+                                int accumulate, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  if (!ids) {
+    dp_linear_t L{A, lda, d_in, G, ldg, d_out, DP_NORM_AUTO};
+    return dp_clipped_grad_sum_grouped(&L, &out, 1, c, B, T, dt, transpose_out, accumulate,
+                                       stream);
+  }
+  // Embedding form: A = onehot(ids), d_in = V.
+  if (A) return fail(DP_EINVAL, "pass either A or ids, not both");
+  if (!G || !c || !out) return fail(DP_EINVAL, "G, c or out is NULL");
+  if (B <= 0 || T <= 0 || d_in <= 0 || d_out <= 0)
+    return fail(DP_EINVAL, "B, T, d_in (= V) and d_out must be positive");
+  if (ldg < d_out) return fail(DP_EINVAL, "ldg < d_out");
+  if (!dtype_ok(dt)) return fail(DP_EINVAL, "unknown dtype %d", (int)dt);
+  const int64_t K = (int64_t)B * T;
+  if (K > dpg::ES_MAX_K)
+    return fail(DP_EUNSUPPORTED, "B*T = %lld exceeds %d", (long long)K, dpg::ES_MAX_K);
+  const int pbits = std::max(1, bits_for(K));
+  if (bits_for(d_in) + pbits > 32)
+    return fail(DP_EUNSUPPORTED, "V and B*T do not fit a 32-bit sort key");
+  const EsLayout l = es_layout(K, d_out);
+  if (!workspace || workspace_bytes < l.total)
+    return fail(DP_EINVAL, "workspace of %zu bytes needed", l.total);
+  hipStream_t s = as_stream(stream);
+  if (!accumulate) {
+    dp_status_t st = hip_status(dpg::launch_fill_zero(out, (int64_t)d_in * d_out, s), "fill");
+    if (st != DP_OK) return st;
+  }
+  char* w = static_cast<char*>(workspace);
+  dpg::EmbedSumArgs a{};
+  a.ids = ids; a.E = G; a.lde = ldg; a.c = c;
+  a.B = B; a.K = (int32_t)K; a.T = T; a.V = d_in; a.d = d_out;
+  a.pbits = pbits;
+  a.keys = reinterpret_cast<uint32_t*>(w + l.keys);
+  a.rank = reinterpret_cast<int32_t*>(w + l.rank);
+  a.seg = reinterpret_cast<int32_t*>(w + l.seg);
+  a.nseg = reinterpret_cast<int32_t*>(w + l.nseg);
+  a.head = reinterpret_cast<float*>(w + l.head);
+  a.tail = reinterpret_cast<float*>(w + l.tail);
+  a.out = out;
+  a.ldo = transpose_out ? d_in : d_out;
+  a.transpose = transpose_out ? 1 : 0;
+  return hip_status(dpg::launch_embed_sum(a, kdt(dt), s), "embed_sum launch");
+}
+
+dp_status_t dp_add_noise(float* grad, int64_t n, float sigma, float C, int B_norm, uint64_t seed,
+                         uint64_t tensor_id, uint64_t step, void* stream) {
+  if (n < 0) return fail(DP_EINVAL, "n must be >= 0");
+  if (n > 0 && !grad) return fail(DP_EINVAL, "grad is NULL");
+  if (!(sigma >= 0.f) || !std::isfinite(sigma)) return fail(DP_EINVAL, "sigma must be >= 0");
+  if (!(C > 0.f) || !std::isfinite(C)) return fail(DP_EINVAL, "C must be positive and finite");
+  if (B_norm < 0) return fail(DP_EINVAL, "B_norm must be >= 0");
+  if (tensor_id >> 32 || step >> 32) return fail(DP_EINVAL, "tensor_id and step must be < 2^32");
+  const float sigma_c = (float)((double)sigma * (double)C);
+  return hip_status(dpg::launch_add_noise(grad, n, sigma_c, B_norm > 0 ? 1 : 0, (float)B_norm,
+                                          seed, (uint32_t)tensor_id, (uint32_t)step,
+                                          as_stream(stream)),
+                    "noise launch");
+}
+
+}  // extern "C"

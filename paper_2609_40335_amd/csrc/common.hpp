@@ -1,0 +1,100 @@
+// Shared device helpers for the gfx950 (CDNA4) kernels of libdpghost.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernels.hpp"
+
+namespace dpg {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int WAVE = 64;
+constexpr int N_XCD = 8;
+
+// The hardware dispatcher hands consecutive workgroup ids to the 8 XCDs in
+// turn. Remap so that each XCD walks one contiguous range of logical work
+// items: neighbouring items (which share rows of the same example) then run
+// on the same XCD and share its L2.
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t bid, uint32_t nwg) {
+  const uint32_t xcd = bid % N_XCD, local = bid / N_XCD;
+  const uint32_t q = nwg / N_XCD, r = nwg % N_XCD;
+  return xcd * q + (xcd < r ? xcd : r) + local;
+}
+
+// 16-byte chunk c (0..7) of a 128-byte LDS row r lives at physical chunk
+// swz(r, c): conflict-free for row-contiguous writes, for column-strided
+// writes of 8-row groups, and for 32-row MFMA operand reads.
+__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r ^ (r >> 3)) & 7); }
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float(((uint32_t)h) << 16);
+}
+
+// fp32 -> bf16, round to nearest even (inputs here are finite).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, WAVE);
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, WAVE);
+  return v;
+}
+
+// 32x32 output block MFMA step; K per call is 16 (bf16) or 2 (fp32).
+__device__ __forceinline__ f32x16 mfma32_bf16(const u32x4& a, const u32x4& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mfma32_f32(float a, float b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+// Chunk loaders: 16 bytes = 8 bf16 or 4 fp32 starting at element `col` of a
+// row. Elements at or past `ncol` read as zero.
+template <int DT>
+__device__ __forceinline__ u32x4 load_chunk_elems(const void* row, int64_t col, int64_t ncol) {
+  u32x4 r = {0u, 0u, 0u, 0u};
+  if constexpr (DT == DT_BF16) {
+    const uint16_t* p = (const uint16_t*)row;
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (col + e < ncol) w[e >> 1] |= ((uint32_t)p[col + e]) << ((e & 1) * 16);
+    }
+    r[0] = w[0]; r[1] = w[1]; r[2] = w[2]; r[3] = w[3];
+  } else {
+    const uint32_t* p = (const uint32_t*)row;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (col + e < ncol) r[e] = p[col + e];
+    }
+  }
+  return r;
+}
+
+__device__ __forceinline__ u32x4 load_chunk16(const void* row, int64_t col, int es) {
+  return *(const u32x4*)((const char*)row + col * es);
+}
+
+// How a thread's chunk [col, col + EPC) of a row relates to the valid columns.
+enum ChunkKind { CHUNK_FULL = 0, CHUNK_PART = 1, CHUNK_NONE = 2 };
+template <int DT>
+__device__ __forceinline__ int chunk_kind(int64_t col, int64_t ncol) {
+  constexpr int EPC = (DT == DT_BF16) ? 8 : 4;
+  return col + EPC <= ncol ? CHUNK_FULL : (col < ncol ? CHUNK_PART : CHUNK_NONE);
+}
+
+}  // namespace dpg

@@ -1,0 +1,286 @@
+// Token-id keyed kernels: bucketing, the input-embedding ghost norm and the
+// input-embedding part of the clipped sum.
+//
+// The input embedding looks up row x_t of E for every token (Sec. "Weight
+// Tying in Decoder-Only LLMs"), so its per-example gradient has one nonzero
+// row per distinct id v: the sum of the output-gradients dE_t of the tokens
+// with x_t = v. Its squared norm is sum_v ||sum_{t: x_t = v} dE_t||^2.
+//
+// Bucketing sorts the packed keys (id << pbits | position) of one example in
+// LDS (bitonic), marks the first token of each run of equal ids, and turns the
+// marks into dense ranks with a wavefront-shuffle prefix scan. The norm then
+// sums each bucket's rows (lanes = 64 features, coalesced row reads) and
+// squares. The clipped sum sorts all B*T tokens of the batch the same way and
+// reduces runs of equal ids in fixed 32-token blocks; a run that crosses a
+// block boundary is closed by a fix-up pass that adds the block partials in
+// order. Every output row is written by exactly one wave: no atomics, and
+// results are bitwise reproducible.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace dpg {
+
+constexpr int EN_THREADS = 256;
+constexpr int ES_THREADS = 1024;
+constexpr int ES_WAVES = 4;  // waves per workgroup of the block and fix-up passes
+
+// Ascending bitonic sort of n (a power of two) keys in LDS.
+__device__ void bitonic_sort(uint32_t* keys, int n, int tid, int nthreads) {
+  for (int k = 2; k <= n; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < n; i += nthreads) {
+        const int p = i ^ j;
+        if (p > i) {
+          const uint32_t x = keys[i], y = keys[p];
+          const bool up = (i & k) == 0;
+          if ((x > y) == up) { keys[i] = y; keys[p] = x; }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// Inclusive prefix sum of one value per thread across the workgroup:
+// shuffles within each wavefront, then the wave totals through LDS.
+__device__ int block_inclusive_scan(int v, int* wave_tot, int tid, int nthreads, int* total) {
+  const int lane = tid & 63, w = tid >> 6, nw = nthreads >> 6;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int u = __shfl_up(v, off, 64);
+    if (lane >= off) v += u;
+  }
+  if (lane == 63) wave_tot[w] = v;
+  __syncthreads();
+  int base = 0, tot = 0;
+  for (int i = 0; i < nw; ++i) {
+    if (i < w) base += wave_tot[i];
+    tot += wave_tot[i];
+  }
+  __syncthreads();
+  *total = tot;
+  return v + base;
+}
+
+// For n sorted keys: dense rank of every sorted position (rank[p]) and the
+// first sorted position of every bucket (seg[r], with seg[n_buckets] = n).
+// Returns the number of buckets. Each thread handles a contiguous run.
+__device__ int rank_sorted(const uint32_t* keys, int n, int pbits, int32_t* rank, int32_t* seg,
+                           int* wave_tot, int tid, int nthreads) {
+  const int per = (n + nthreads - 1) / nthreads;
+  const int p0 = min(tid * per, n), p1 = min(p0 + per, n);
+  int cnt = 0;
+  for (int p = p0; p < p1; ++p)
+    cnt += (p == 0 || (keys[p] >> pbits) != (keys[p - 1] >> pbits)) ? 1 : 0;
+  int total;
+  const int incl = block_inclusive_scan(cnt, wave_tot, tid, nthreads, &total);
+  int r = incl - cnt;
+  for (int p = p0; p < p1; ++p) {
+    if (p == 0 || (keys[p] >> pbits) != (keys[p - 1] >> pbits)) seg[r++] = p;
+    rank[p] = r - 1;
+  }
+  if (tid == 0) seg[total] = n;
+  __syncthreads();
+  return total;
+}
+
+template <int DT>
+__device__ __forceinline__ float load_elem(const void* base, int64_t idx) {
+  if constexpr (DT == DT_BF16)
+    return bf16_to_f32(((const uint16_t*)base)[idx]);
+  else
+    return ((const float*)base)[idx];
+}
+
+// ---------------------------------------------------------------------------
+// Per-example bucketing and input-embedding norm. Grid (B, ceil(d/64)).
+// ---------------------------------------------------------------------------
+template <int DT>
+__global__ __launch_bounds__(EN_THREADS) void embed_norm_kernel(EmbedNormArgs a) {
+  __shared__ uint32_t keys[EN_MAX_T];
+  __shared__ int32_t rank[EN_MAX_T];
+  __shared__ int32_t seg[EN_MAX_T + 1];
+  __shared__ int wave_tot[EN_THREADS / WAVE];
+  __shared__ float red[EN_THREADS / WAVE];
+  const int b = blockIdx.x, chunk = blockIdx.y, tid = threadIdx.x;
+  const int T = a.T;
+  int n2 = 1;
+  while (n2 < T) n2 <<= 1;
+  const uint32_t pmask = (1u << a.pbits) - 1u;
+  const int32_t* ids = a.ids + (int64_t)b * T;
+  for (int p = tid; p < n2; p += EN_THREADS)
+    keys[p] = p < T ? ((((uint32_t)ids[p]) << a.pbits) | (uint32_t)p) : 0xFFFFFFFFu;
+  __syncthreads();
+  bitonic_sort(keys, n2, tid, EN_THREADS);
+  const int nseg = rank_sorted(keys, T, a.pbits, rank, seg, wave_tot, tid, EN_THREADS);
+  if (chunk == 0) {
+    if (a.seg_id)
+      for (int p = tid; p < T; p += EN_THREADS)
+        a.seg_id[(int64_t)b * T + (keys[p] & pmask)] = rank[p];
+    if (a.n_unique && tid == 0) a.n_unique[b] = nseg;
+  }
+  const int lane = tid & 63, w = tid >> 6;
+  const int f = chunk * WAVE + lane;
+  const int nw = EN_THREADS / WAVE;
+  float sq = 0.f;
+  if (f < a.d) {
+    const int64_t row0 = (int64_t)b * T;
+    for (int r = w; r < nseg; r += nw) {
+      float acc = 0.f;
+      const int e = seg[r + 1];
+#pragma unroll 4
+      for (int p = seg[r]; p < e; ++p)
+        acc += load_elem<DT>(a.E, (row0 + (keys[p] & pmask)) * a.lde + f);
+      sq += acc * acc;
+    }
+  }
+  sq = wave_sum(sq);
+  if (lane == 0) red[w] = sq;
+  __syncthreads();
+  if (tid == 0) a.ws[(int64_t)b * a.n_chunks + chunk] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// ---------------------------------------------------------------------------
+// Batch-wide clipped sum of the input embedding:
+// out[v, f] (+)= sum over tokens k with ids[k] = v of c[k / T] * E[k, f].
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(ES_THREADS) void embed_sort_kernel(EmbedSumArgs a) {
+  __shared__ uint32_t keys[ES_MAX_K];
+  __shared__ int wave_tot[ES_THREADS / WAVE];
+  const int tid = threadIdx.x, K = a.K;
+  int n2 = 1;
+  while (n2 < K) n2 <<= 1;
+  for (int p = tid; p < n2; p += ES_THREADS)
+    keys[p] = p < K ? ((((uint32_t)a.ids[p]) << a.pbits) | (uint32_t)p) : 0xFFFFFFFFu;
+  __syncthreads();
+  bitonic_sort(keys, n2, tid, ES_THREADS);
+  for (int p = tid; p < K; p += ES_THREADS) a.keys[p] = keys[p];
+  const int nseg = rank_sorted(keys, K, a.pbits, a.rank, a.seg, wave_tot, tid, ES_THREADS);
+  if (tid == 0) *a.nseg = nseg;
+}
+
+__device__ __forceinline__ float example_scale(const float* c, int64_t k, double invT, int B) {
+  int64_t e = (int64_t)(((double)k + 0.5) * invT);
+  if (e >= B) e = B - 1;
+  return c[e];
+}
+
+__device__ __forceinline__ void out_add(const EmbedSumArgs& a, uint32_t v, int f, float val) {
+  if (v >= (uint32_t)a.V) return;  // invalid id: contributes nothing
+  float* o = a.transpose ? a.out + (int64_t)f * a.ldo + v : a.out + (int64_t)v * a.ldo + f;
+  *o += val;
+}
+
+// One wave per (block of ES_BLOCK sorted tokens, 64-feature chunk).
+template <int DT>
+__global__ __launch_bounds__(ES_WAVES * WAVE) void embed_block_kernel(EmbedSumArgs a) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n_fc = (a.d + WAVE - 1) / WAVE;
+  const int n_blocks = (a.K + ES_BLOCK - 1) / ES_BLOCK;
+  const int unit = blockIdx.x * ES_WAVES + w;
+  if (unit >= n_blocks * n_fc) return;
+  const int q = unit / n_fc, fc = unit - q * n_fc;
+  const int f = fc * WAVE + lane;
+  const bool fok = f < a.d;
+  const int K = a.K, pb = a.pbits;
+  const uint32_t pmask = (1u << pb) - 1u;
+  const int p0 = q * ES_BLOCK, p1 = min(p0 + ES_BLOCK, K);
+  const double invT = 1.0 / (double)a.T;
+  const bool starts_before = p0 > 0 && (a.keys[p0 - 1] >> pb) == (a.keys[p0] >> pb);
+  const bool ends_after = p1 < K && (a.keys[p1] >> pb) == (a.keys[p1 - 1] >> pb);
+  float acc = 0.f;
+  int run_start = p0;
+  uint32_t key = a.keys[p0];
+  for (int p = p0; p < p1; ++p) {
+    const uint32_t next = (p + 1 < K) ? a.keys[p + 1] : 0xFFFFFFFFu;
+    const int64_t k = key & pmask;
+    if (fok) acc += example_scale(a.c, k, invT, a.B) * load_elem<DT>(a.E, k * a.lde + f);
+    const bool last = (p + 1 == p1) || ((next >> pb) != (key >> pb));
+    if (last) {
+      const bool open_head = (run_start == p0) && starts_before;
+      const bool open_tail = (p + 1 == p1) && ends_after;
+      if (fok) {
+        if (open_head)
+          a.head[(int64_t)q * a.d + f] = acc;
+        else if (open_tail)
+          a.tail[(int64_t)q * a.d + f] = acc;
+        else
+          out_add(a, key >> pb, f, acc);
+      }
+      acc = 0.f;
+      run_start = p + 1;
+    }
+    key = next;
+  }
+}
+
+// One wave per (block, feature chunk): closes the run that starts in block q
+// and continues past it, adding the partials of the blocks it spans in order.
+__global__ __launch_bounds__(ES_WAVES * WAVE) void embed_fixup_kernel(EmbedSumArgs a) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n_fc = (a.d + WAVE - 1) / WAVE;
+  const int n_blocks = (a.K + ES_BLOCK - 1) / ES_BLOCK;
+  const int unit = blockIdx.x * ES_WAVES + w;
+  if (unit >= n_blocks * n_fc) return;
+  const int q = unit / n_fc, fc = unit - q * n_fc;
+  const int f = fc * WAVE + lane;
+  const int K = a.K, pb = a.pbits;
+  const int p0 = q * ES_BLOCK, p1 = min(p0 + ES_BLOCK, K);
+  if (p1 >= K) return;
+  const uint32_t id = a.keys[p1 - 1] >> pb;
+  if ((a.keys[p1] >> pb) != id) return;             // last run ends in this block
+  if (a.seg[a.rank[p1 - 1]] < p0) return;           // it started in an earlier block
+  if (f >= a.d) return;
+  float acc = a.tail[(int64_t)q * a.d + f];
+  for (int qq = q + 1; qq < n_blocks; ++qq) {
+    acc += a.head[(int64_t)qq * a.d + f];
+    const int e = min(qq * ES_BLOCK + ES_BLOCK, K);
+    if (e >= K || (a.keys[e] >> pb) != id) break;   // the run ends in block qq
+  }
+  out_add(a, id, f, acc);
+}
+
+__global__ void fill_zero_kernel(float* p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0.f;
+}
+
+hipError_t launch_embed_norm(const EmbedNormArgs& a, int dt, hipStream_t s) {
+  if (a.B == 0) return hipSuccess;
+  const dim3 g(a.B, a.n_chunks), blk(EN_THREADS);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(embed_norm_kernel<DT_BF16>, g, blk, 0, s, a);
+  else
+    hipLaunchKernelGGL(embed_norm_kernel<DT_F32>, g, blk, 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_sum(const EmbedSumArgs& a, int dt, hipStream_t s) {
+  if (a.K == 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_sort_kernel, dim3(1), dim3(ES_THREADS), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int n_fc = (a.d + WAVE - 1) / WAVE;
+  const int n_blocks = (a.K + ES_BLOCK - 1) / ES_BLOCK;
+  const int units = n_blocks * n_fc;
+  const dim3 g((units + ES_WAVES - 1) / ES_WAVES), blk(ES_WAVES * WAVE);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(embed_block_kernel<DT_BF16>, g, blk, 0, s, a);
+  else
+    hipLaunchKernelGGL(embed_block_kernel<DT_F32>, g, blk, 0, s, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(embed_fixup_kernel, g, blk, 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  int64_t nb = (n + 255) / 256;
+  if (nb > 65536) nb = 65536;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)nb), dim3(256), 0, s, p, n);
+  return hipGetLastError();
+}
+
+}  // namespace dpg

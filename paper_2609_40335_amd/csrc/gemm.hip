@@ -1,0 +1,271 @@
+// GEMMs whose two operands are both stored token-major: X [K, M] and Y [K, N]
+// with the contraction index k (a token of an example) on the rows.
+//
+// Clipped sum (eq. 3 without the noise; the reweighted second backward of
+// Sec. "Ghost Clipping Mechanism"): S = sum_i c_i A_i^T G_i. Stacking the B
+// examples' tokens gives one GEMM with K = B*T in which row k of X is scaled
+// by c[k / T]. The backward pass is linear in the upstream gradient, so this
+// equals the gradient of the loss reweighted by the clip factors.
+//
+// Direct norm (the materialising alternative, "normal clipping" of Sec.
+// "Training Configurations"): ||A_i^T G_i||_F^2 for one example, from the same
+// GEMM restricted to the example's T rows; each 256x256 output tile is
+// squared and summed in registers and never stored. It beats the Gram form
+// when T exceeds about 2 d_in d_out / (d_in + d_out).
+//
+// MFMA wants 8 consecutive k per lane, but both operands are contiguous along
+// M/N. Each thread loads an 8(k) x 8(m) block with 16-byte loads, scales it
+// (bf16: exact widening, fp32 multiply, v_cvt_pk_bf16_f32 rounding), and
+// transposes it in registers into 8 k-contiguous chunks written to LDS.
+// Tile 256x256x64 (bf16) or 256x256x32 (fp32); 4 waves, each a 128x128
+// quadrant of 4x4 32x32 blocks.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace dpg {
+
+constexpr int GM_THREADS = 256;
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+enum { MODE_SUM = 0, MODE_NORM = 1 };
+
+// Two bf16 held in one dword, each multiplied by s in fp32 and rounded back
+// to bf16 (round to nearest even).
+__device__ __forceinline__ uint32_t scale_bf16x2(uint32_t w, float s) {
+  f32x2 v = {__uint_as_float(w << 16) * s, __uint_as_float(w & 0xFFFF0000u) * s};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+template <int DT>
+struct KT {
+  static constexpr int RPT = (DT == DT_BF16) ? 8 : 4;  // k rows per thread per stage
+  static constexpr int KS = 8 * RPT;                   // k rows per stage
+  static constexpr int ES = (DT == DT_BF16) ? 2 : 4;
+  static constexpr int EPC = 16 / ES;                  // elements per 16-byte chunk
+};
+
+// Loads this thread's block of one operand for the stage starting at row k0:
+// rows k0 + kg*RPT + j, columns col .. col+7. raw[j*CPR + h] is 16 bytes.
+template <int DT, bool VEC>
+__device__ __forceinline__ void load_block(const char* base, int64_t ld, int64_t k0, int64_t k_end,
+                                           int64_t col, int64_t ncol, u32x4 (&raw)[8]) {
+  using P = KT<DT>;
+  constexpr int CPR = 8 / P::RPT;  // 16-byte chunks per 8-column segment: 1 (bf16) or 2 (fp32)
+#pragma unroll
+  for (int j = 0; j < P::RPT; ++j) {
+    const int64_t k = k0 + j;
+#pragma unroll
+    for (int h = 0; h < CPR; ++h) {
+      const int64_t cc = col + h * P::EPC;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (k < k_end && cc < ncol) {
+        const char* row = base + k * ld;
+        v = VEC ? load_chunk16(row, cc, P::ES) : load_chunk_elems<DT>(row, cc, ncol);
+      }
+      raw[j * CPR + h] = v;
+    }
+  }
+}
+
+// Scales row j of the block by s[j], transposes to 8 column chunks of RPT
+// consecutive k, and writes them to LDS rows m_row0 .. m_row0+7, chunk kg.
+template <int DT, bool SCALE>
+__device__ __forceinline__ void store_block_t(u32x4* lds, u32x4 (&raw)[8], const float (&s)[8],
+                                              int m_row0, int kg) {
+  if constexpr (DT == DT_BF16) {
+    if (SCALE) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int p = 0; p < 4; ++p) raw[j][p] = scale_bf16x2(raw[j][p], s[j]);
+    }
+#pragma unroll
+    for (int mm = 0; mm < 8; ++mm) {
+      const int p = mm >> 1;
+      const uint32_t sel = (mm & 1) ? 0x07060302u : 0x05040100u;
+      u32x4 o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        o[q] = __builtin_amdgcn_perm(raw[2 * q + 1][p], raw[2 * q][p], sel);
+      const int r = m_row0 + mm;
+      lds[r * 8 + swz(r, kg)] = o;
+    }
+  } else {
+#pragma unroll
+    for (int mm = 0; mm < 8; ++mm) {
+      const int h = mm >> 2, e = mm & 3;
+      u32x4 o;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float v = __uint_as_float(raw[j * 2 + h][e]);
+        if (SCALE) v *= s[j];
+        o[j] = __float_as_uint(v);
+      }
+      const int r = m_row0 + mm;
+      lds[r * 8 + swz(r, kg)] = o;
+    }
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ void tile_mfma(const u32x4* __restrict__ Xs, const u32x4* __restrict__ Ys,
+                                          f32x16 (&acc)[4][4], int wm, int wn, int lane) {
+  const int r32 = lane & 31, half = lane >> 5;
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int c = 2 * ks + half;
+    u32x4 xa[4], yb[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rx = wm * 128 + i * 32 + r32, ry = wn * 128 + i * 32 + r32;
+      xa[i] = Xs[rx * 8 + swz(rx, c)];
+      yb[i] = Ys[ry * 8 + swz(ry, c)];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if constexpr (DT == DT_BF16) {
+          acc[i][j] = mfma32_bf16(xa[i], yb[j], acc[i][j]);
+        } else {
+#pragma unroll
+          for (int m = 0; m < 4; ++m)
+            acc[i][j] = mfma32_f32(__uint_as_float(xa[i][m]), __uint_as_float(yb[j][m]), acc[i][j]);
+        }
+      }
+  }
+}
+
+template <int DT, bool VEC, int MODE>
+__global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
+  // Index the layer table in place in the kernel-argument segment.
+  const GemmArgs& a = *(const GemmArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  (void)args;
+  using P = KT<DT>;
+  __shared__ u32x4 Xs[GM_BM * 8];
+  __shared__ u32x4 Ys[GM_BN * 8];
+  __shared__ float red[GM_THREADS / WAVE];
+
+  const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
+  int l = 0;
+  while (l + 1 < a.n_layers && item >= a.L[l + 1].tile_begin) ++l;
+  const GemmLayer& L = a.L[l];
+  uint32_t rel = item - L.tile_begin;
+  const uint32_t ntile = (uint32_t)L.tm * (uint32_t)L.tn;
+  int b = 0;
+  int64_t k_begin = 0, k_end = (int64_t)a.B * a.T;
+  if (MODE == MODE_NORM) {
+    b = (int)(rel / ntile);
+    rel -= (uint32_t)b * ntile;
+    k_begin = (int64_t)b * a.T;
+    k_end = k_begin + a.T;
+  }
+  const int mt = (int)(rel / (uint32_t)L.tn), nt = (int)(rel - (uint32_t)mt * L.tn);
+  const int64_t m0 = (int64_t)L.m_lo + (int64_t)mt * GM_BM;
+  const int64_t n0 = (int64_t)L.n_lo + (int64_t)nt * GM_BN;
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int kg = tid >> 5, mg = tid & 31;
+  const char* Xb = (const char*)L.X;
+  const char* Yb = (const char*)L.Y;
+  const int64_t ldx = L.ldx * P::ES, ldy = L.ldy * P::ES;
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int nS = (int)((k_end - k_begin + P::KS - 1) / P::KS);
+  const double invT = 1.0 / (double)a.T;
+  u32x4 rx[8], ry[8];
+  auto load = [&](int s) {
+    const int64_t k0 = k_begin + (int64_t)s * P::KS + kg * P::RPT;
+    load_block<DT, VEC>(Xb, ldx, k0, k_end, m0 + mg * 8, L.m_hi, rx);
+    load_block<DT, VEC>(Yb, ldy, k0, k_end, n0 + mg * 8, L.n_hi, ry);
+  };
+  load(0);
+  for (int s = 0; s < nS; ++s) {
+    float sc[8];
+    if (MODE == MODE_SUM) {
+      const int64_t k0 = k_begin + (int64_t)s * P::KS + kg * P::RPT;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int64_t k = k0 + j;
+        int64_t e = (int64_t)(((double)k + 0.5) * invT);
+        if (e >= a.B) e = a.B - 1;
+        sc[j] = (j < P::RPT) ? a.c[e] : 0.f;
+      }
+    }
+    __syncthreads();
+    store_block_t<DT, MODE == MODE_SUM>(Xs, rx, sc, mg * 8, kg);
+    store_block_t<DT, false>(Ys, ry, sc, mg * 8, kg);
+    __syncthreads();
+    if (s + 1 < nS) load(s + 1);
+    tile_mfma<DT>(Xs, Ys, acc, wm, wn, lane);
+  }
+
+  if constexpr (MODE == MODE_SUM) {
+    // 32x32 block (i,j): lane l holds column l%32 and, for accumulator e,
+    // row (e/4)*8 + (l/32)*4 + e%4.
+    float* out = L.out;
+    const int64_t ldo = L.ldo;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t n = n0 + wn * 128 + j * 32 + (lane & 31);
+        if (n >= L.n_hi) continue;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int64_t m = m0 + wm * 128 + i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+          if (m < L.m_hi) {
+            const int64_t idx = L.transpose ? n * ldo + m : m * ldo + n;
+            out[idx] = L.accumulate ? out[idx] + acc[i][j][e] : acc[i][j][e];
+          }
+        }
+      }
+  } else {
+    float part = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) part += acc[i][j][e] * acc[i][j][e];
+    part = wave_sum(part);
+    if (lane == 0) red[w] = part;
+    __syncthreads();
+    if (tid == 0)
+      a.ws[(int64_t)b * a.slots + L.slot_begin + rel] = (red[0] + red[1]) + (red[2] + red[3]);
+  }
+}
+
+template <int MODE>
+static hipError_t launch_kt(const GemmArgs& a, int dt, bool vec, hipStream_t s) {
+  if (a.n_items == 0) return hipSuccess;
+  const dim3 g(a.n_items), blk(GM_THREADS);
+  if (dt == DT_BF16) {
+    if (vec) hipLaunchKernelGGL((kt_gemm_kernel<DT_BF16, true, MODE>), g, blk, 0, s, a);
+    else hipLaunchKernelGGL((kt_gemm_kernel<DT_BF16, false, MODE>), g, blk, 0, s, a);
+  } else {
+    if (vec) hipLaunchKernelGGL((kt_gemm_kernel<DT_F32, true, MODE>), g, blk, 0, s, a);
+    else hipLaunchKernelGGL((kt_gemm_kernel<DT_F32, false, MODE>), g, blk, 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_clipped_sum(const GemmArgs& a, int dt, bool vec, hipStream_t s) {
+  return launch_kt<MODE_SUM>(a, dt, vec, s);
+}
+
+hipError_t launch_direct_norm(const GemmArgs& a, int dt, bool vec, hipStream_t s) {
+  return launch_kt<MODE_NORM>(a, dt, vec, s);
+}
+
+}  // namespace dpg

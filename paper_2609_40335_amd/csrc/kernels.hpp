@@ -1,0 +1,130 @@
+// Internal launch interface between the C ABI (api.cpp) and the HIP kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dpg {
+
+enum { DT_F32 = 0, DT_BF16 = 1 };  // element type of the float operands
+
+// ----------------------------------------------------------------- Gram norm
+constexpr int GR_TM = 128;          // rows of one T-tile
+constexpr int GR_MAX_LAYERS = 24;   // layers per launch (kernel-argument budget)
+
+struct GramLayer {
+  const void* A;        // [B*T rows, lda] activations
+  const void* G;        // [B*T rows, ldg] output grads
+  int64_t lda, ldg;
+  int32_t d_in;         // A features
+  int32_t g0, g1;       // G feature range of this entry
+  int32_t kg;           // G features per chunk
+  int32_t nc;           // number of G chunks
+  uint32_t item_begin;  // first work item of this layer
+  int32_t slot_begin;   // first partial slot of this layer in an example's row
+};
+
+struct GramArgs {
+  GramLayer L[GR_MAX_LAYERS];
+  int32_t n_layers;
+  int32_t B, T, n_t, P;   // T-tiles per side, upper-triangle tile pairs
+  int32_t slots;          // partial slots per example
+  uint32_t n_items;
+  float* ws;              // [B, slots]
+};
+
+hipError_t launch_gram_norm(const GramArgs& a, int dt, bool vec, hipStream_t s);
+
+// Tied cross term: sum_{t,s} Gz[s, ids[t]] <dE_t, H_s>, all T-tile pairs.
+struct CrossArgs {
+  const int32_t* ids;   // [B,T]
+  const void* E;        // dE [B*T, lde]
+  const void* H;        // [B*T, ldh]
+  const void* Gz;       // [B*T, ldz]
+  int64_t lde, ldh, ldz;
+  int32_t B, T, V, d, n_t;
+  int32_t slots;        // n_t * n_t
+  float* ws;            // [B, slots]
+};
+hipError_t launch_tied_cross(const CrossArgs& a, int dt, bool vec, hipStream_t s);
+
+// out[b] = (acc ? out[b] : 0) + scale * sum_j ws[b*slots + j], fixed order.
+hipError_t launch_finish_rows(const float* ws, int B, int slots, float* out, int accumulate,
+                              float scale, hipStream_t s);
+
+// ------------------------------------------------------- K-major GEMM family
+constexpr int GM_BM = 256, GM_BN = 256;
+constexpr int GM_MAX_LAYERS = 24;
+
+struct GemmLayer {
+  const void* X;        // [K rows, ldx]
+  const void* Y;        // [K rows, ldy]
+  int64_t ldx, ldy;     // row strides in elements
+  int32_t m_lo, m_hi;   // X columns (output rows) covered by this entry
+  int32_t n_lo, n_hi;   // Y columns (output columns) covered by this entry
+  int32_t tm, tn;       // 256-wide tiles along M and N
+  uint32_t tile_begin;  // first work item of this entry
+  int32_t slot_begin;   // direct norm: first partial slot in an example's row
+  float* out;           // clipped sum: [M, ldo] or transposed [N, ldo]
+  int64_t ldo;
+  int32_t transpose, accumulate;
+};
+
+struct GemmArgs {
+  GemmLayer L[GM_MAX_LAYERS];
+  int32_t n_layers;
+  int32_t B, T;
+  uint32_t n_items;
+  const float* c;       // clipped sum: per-example scale [B]
+  float* ws;            // direct norm: [B, slots]
+  int32_t slots;
+};
+
+// Clipped sum: out (+)= sum_i c_i X_i^T Y_i over all B*T rows (K = B*T).
+hipError_t launch_clipped_sum(const GemmArgs& a, int dt, bool vec, hipStream_t s);
+// Direct norm: ws[b, slot] = ||tile of X_b^T Y_b||_F^2 for every output tile.
+hipError_t launch_direct_norm(const GemmArgs& a, int dt, bool vec, hipStream_t s);
+
+// --------------------------------------------------------- embedding / ids
+struct EmbedNormArgs {
+  const int32_t* ids;   // [B,T]
+  const void* E;        // dE [B*T, lde]
+  int64_t lde;
+  int32_t B, T, V, d;
+  int32_t pbits;        // bits for a position in a sort key
+  int32_t n_chunks;     // feature chunks of 64
+  int32_t* seg_id;      // nullable [B,T]
+  int32_t* n_unique;    // nullable [B]
+  float* ws;            // [B, n_chunks]
+};
+hipError_t launch_embed_norm(const EmbedNormArgs& a, int dt, hipStream_t s);
+
+constexpr int EN_MAX_T = 4096;   // tokens per example sorted in LDS (bucketing)
+constexpr int ES_MAX_K = 16384;  // tokens per batch sorted in LDS (embedding sum)
+constexpr int ES_BLOCK = 32;     // sorted tokens per reduction block
+
+struct EmbedSumArgs {
+  const int32_t* ids;   // [K] flattened B*T
+  const void* E;        // [K, lde]
+  int64_t lde;
+  const float* c;       // [B]
+  int32_t B, K, T, V, d;
+  int32_t pbits;        // bits for a token index in a sort key
+  uint32_t* keys;       // workspace [K] sorted keys
+  int32_t* rank;        // workspace [K] bucket of each sorted position
+  int32_t* seg;         // workspace [K+1] first sorted position of each bucket
+  int32_t* nseg;        // workspace [1]
+  float* head;          // workspace [n_blocks, d] partial of the run a block starts inside
+  float* tail;          // workspace [n_blocks, d] partial of the run a block ends inside
+  float* out;           // [V, ldo] or transposed [d, ldo]; accumulated into
+  int64_t ldo;
+  int32_t transpose;
+};
+hipError_t launch_embed_sum(const EmbedSumArgs& a, int dt, hipStream_t s);
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
+
+// ----------------------------------------------------------- clip and noise
+hipError_t launch_clip_factors(const float* norm2, int B, float C, float* c, hipStream_t s);
+hipError_t launch_add_noise(float* g, int64_t n, float sigma_c, int divide, float b_norm,
+                            uint64_t seed, uint32_t tensor_id, uint32_t step, hipStream_t s);
+
+}  // namespace dpg

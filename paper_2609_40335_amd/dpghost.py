@@ -1,0 +1,270 @@
+"""Python binding of libdpghost: argument marshalling only.
+
+Each function has the name of the C entry point it calls and forwards torch
+device tensors as raw pointers plus their row strides; every step of the
+computation runs in the HIP kernels of libdpghost.so. Workspaces come from
+torch's caching allocator; kernels run on torch's current stream unless a
+stream is passed. Errors from the library raise DPError. There is no
+fallback: if the library is not built, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+__all__ = [
+    "DPError", "DP_F32", "DP_BF16", "DP_NORM_AUTO", "DP_NORM_GRAM", "DP_NORM_DIRECT",
+    "lib", "library_path", "dp_abi_version",
+    "dp_ghost_norm_linear", "dp_ghost_norm_linear_grouped", "dp_ghost_norm_embedding",
+    "dp_tied_cross_term", "dp_clip_factors", "dp_clipped_grad_sum",
+    "dp_clipped_grad_sum_grouped", "dp_add_noise",
+]
+
+DP_F32, DP_BF16 = 0, 1
+DP_NORM_AUTO, DP_NORM_GRAM, DP_NORM_DIRECT = 0, 1, 2
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB: Optional[ctypes.CDLL] = None
+
+
+class DPError(RuntimeError):
+    pass
+
+
+class dp_linear_t(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_void_p), ("lda", ctypes.c_int64), ("d_in", ctypes.c_int32),
+                ("G", ctypes.c_void_p), ("ldg", ctypes.c_int64), ("d_out", ctypes.c_int32),
+                ("algo", ctypes.c_int32)]
+
+
+def library_path() -> str:
+    return os.path.join(_HERE, "libdpghost.so")
+
+
+_VP, _I, _I64, _U64, _F, _SZ = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_uint64,
+                                ctypes.c_float, ctypes.c_size_t)
+_SIGS = {
+    "dp_abi_version": ([], _I),
+    "dp_status_string": ([_I], ctypes.c_char_p),
+    "dp_last_error": ([], ctypes.c_char_p),
+    "dp_ghost_norm_linear_workspace": ([ctypes.POINTER(dp_linear_t), _I, _I, _I, _I], _SZ),
+    "dp_ghost_norm_linear_grouped": ([ctypes.POINTER(dp_linear_t), _I, _I, _I, _I, _VP, _I,
+                                      _VP, _SZ, _VP], _I),
+    "dp_ghost_norm_linear": ([_VP, _I64, _VP, _I64, _I, _I, _I, _I, _I, _I, _VP, _I, _VP, _SZ,
+                              _VP], _I),
+    "dp_ghost_norm_embedding_workspace": ([_I, _I, _I], _SZ),
+    "dp_ghost_norm_embedding": ([_VP, _VP, _I64, _I, _I, _I, _I, _I, _VP, _I, _VP, _VP, _VP,
+                                 _SZ, _VP], _I),
+    "dp_tied_cross_term_workspace": ([_I, _I], _SZ),
+    "dp_tied_cross_term": ([_VP, _VP, _I64, _VP, _I64, _VP, _I64, _I, _I, _I, _I, _I, _F, _VP,
+                            _I, _VP, _SZ, _VP], _I),
+    "dp_clip_factors": ([_VP, _I, _F, _VP, _VP], _I),
+    "dp_clipped_grad_sum_workspace": ([_I, _I, _I, _I], _SZ),
+    "dp_clipped_grad_sum": ([_VP, _I64, _VP, _I64, _VP, _VP, _I, _I, _I, _I, _I, _I, _VP, _I,
+                             _VP, _SZ, _VP], _I),
+    "dp_clipped_grad_sum_grouped": ([ctypes.POINTER(dp_linear_t), ctypes.POINTER(_VP), _I, _VP,
+                                     _I, _I, _I, _I, _I, _VP], _I),
+    "dp_add_noise": ([_VP, _I64, _F, _F, _I, _U64, _U64, _U64, _VP], _I),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """Loads libdpghost.so from the package directory (it must be built)."""
+    global _LIB
+    if _LIB is None:
+        path = library_path()
+        if not os.path.exists(path):
+            raise DPError(f"{path} is not built; run `python -m paper_2609_40335_amd.build`")
+        L = ctypes.CDLL(path)
+        for name, (args, res) in _SIGS.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _LIB = L
+    return _LIB
+
+
+def _check(status: int, name: str) -> None:
+    if status != 0:
+        L = lib()
+        raise DPError(f"{name}: {L.dp_status_string(status).decode()}: "
+                      f"{L.dp_last_error().decode()}")
+
+
+def _dtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return DP_BF16
+    if t.dtype == torch.float32:
+        return DP_F32
+    raise DPError(f"unsupported dtype {t.dtype}")
+
+
+def _rows(t: torch.Tensor, name: str):
+    """(pointer, B, T, width, row stride) of a token-major [B, T, w] tensor."""
+    if t.dim() != 3:
+        raise DPError(f"{name} must be [B, T, w]")
+    B, T, w = t.shape
+    if t.stride(2) != 1 or (B > 1 and t.stride(0) != T * t.stride(1)):
+        raise DPError(f"{name} must have unit feature stride and uniformly spaced token rows")
+    return t.data_ptr(), B, T, w, t.stride(1)
+
+
+def _dev(t: torch.Tensor, name: str) -> None:
+    if not t.is_cuda:
+        raise DPError(f"{name} must be a device tensor")
+
+
+def _stream(stream) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _ws(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def dp_abi_version() -> int:
+    return lib().dp_abi_version()
+
+
+def _layer(A, G, algo=DP_NORM_AUTO) -> dp_linear_t:
+    _dev(A, "A"); _dev(G, "G")
+    pa, B, T, d_in, lda = _rows(A, "A")
+    pg, B2, T2, d_out, ldg = _rows(G, "G")
+    if (B, T) != (B2, T2):
+        raise DPError("A and G must share B and T")
+    if A.dtype != G.dtype:
+        raise DPError("A and G must share a dtype")
+    return dp_linear_t(pa, lda, d_in, pg, ldg, d_out, algo)
+
+
+def dp_ghost_norm_linear_grouped(layers: Sequence, norm2: torch.Tensor, accumulate: bool = False,
+                                 stream=None) -> torch.Tensor:
+    """layers: sequence of (A, G) or (A, G, algo); norm2: fp32 [B]."""
+    L = lib()
+    descs = [_layer(*l) for l in layers]
+    A0 = layers[0][0]
+    B, T = A0.shape[0], A0.shape[1]
+    for l in layers:
+        if tuple(l[0].shape[:2]) != (B, T) or l[0].dtype != A0.dtype:
+            raise DPError("all layers of a group share B, T and dtype")
+    arr = (dp_linear_t * len(descs))(*descs)
+    dt = _dtype(A0)
+    nbytes = L.dp_ghost_norm_linear_workspace(arr, len(descs), B, T, dt)
+    ws = _ws(nbytes, A0.device)
+    _check(L.dp_ghost_norm_linear_grouped(arr, len(descs), B, T, dt, norm2.data_ptr(),
+                                          int(accumulate), ws.data_ptr(), ws.numel(),
+                                          _stream(stream)), "dp_ghost_norm_linear_grouped")
+    return norm2
+
+
+def dp_ghost_norm_linear(A, G, norm2, accumulate: bool = False, algo: int = DP_NORM_AUTO,
+                         stream=None) -> torch.Tensor:
+    L = lib()
+    d = _layer(A, G, algo)
+    B, T = A.shape[0], A.shape[1]
+    dt = _dtype(A)
+    nbytes = L.dp_ghost_norm_linear_workspace(ctypes.byref(d), 1, B, T, dt)
+    ws = _ws(nbytes, A.device)
+    _check(L.dp_ghost_norm_linear(d.A, d.lda, d.G, d.ldg, B, T, d.d_in, d.d_out, dt, algo,
+                                  norm2.data_ptr(), int(accumulate), ws.data_ptr(), ws.numel(),
+                                  _stream(stream)), "dp_ghost_norm_linear")
+    return norm2
+
+
+def dp_ghost_norm_embedding(ids, dE, V: int, norm2, accumulate: bool = False, seg_id=None,
+                            n_unique=None, stream=None) -> torch.Tensor:
+    L = lib()
+    _dev(ids, "ids"); _dev(dE, "dE")
+    pe, B, T, d, lde = _rows(dE, "dE")
+    if ids.dtype != torch.int32 or tuple(ids.shape) != (B, T) or not ids.is_contiguous():
+        raise DPError("ids must be contiguous int32 [B, T]")
+    ws = _ws(L.dp_ghost_norm_embedding_workspace(B, T, d), dE.device)
+    _check(L.dp_ghost_norm_embedding(ids.data_ptr(), pe, lde, B, T, V, d, _dtype(dE),
+                                     norm2.data_ptr(), int(accumulate),
+                                     None if seg_id is None else seg_id.data_ptr(),
+                                     None if n_unique is None else n_unique.data_ptr(),
+                                     ws.data_ptr(), ws.numel(), _stream(stream)),
+           "dp_ghost_norm_embedding")
+    return norm2
+
+
+def dp_tied_cross_term(ids, dE, H, Gz, V: int, out, scale: float = 1.0,
+                       accumulate: bool = False, stream=None) -> torch.Tensor:
+    """Gz: [B, T, V] (may be a column slice of a row-padded tensor)."""
+    L = lib()
+    for t, n in ((ids, "ids"), (dE, "dE"), (H, "H"), (Gz, "Gz")):
+        _dev(t, n)
+    pe, B, T, d, lde = _rows(dE, "dE")
+    ph, _, _, _, ldh = _rows(H, "H")
+    pz, _, _, Vz, ldz = _rows(Gz, "Gz")
+    if Vz < V:
+        raise DPError("Gz must have at least V columns")
+    if ids.dtype != torch.int32 or tuple(ids.shape) != (B, T) or not ids.is_contiguous():
+        raise DPError("ids must be contiguous int32 [B, T]")
+    ws = _ws(L.dp_tied_cross_term_workspace(B, T), dE.device)
+    _check(L.dp_tied_cross_term(ids.data_ptr(), pe, lde, ph, ldh, pz, ldz, B, T, V, d,
+                                _dtype(dE), float(scale), out.data_ptr(), int(accumulate),
+                                ws.data_ptr(), ws.numel(), _stream(stream)),
+           "dp_tied_cross_term")
+    return out
+
+
+def dp_clip_factors(norm2, C: float, c, stream=None) -> torch.Tensor:
+    _check(lib().dp_clip_factors(norm2.data_ptr(), norm2.numel(), float(C), c.data_ptr(),
+                                 _stream(stream)), "dp_clip_factors")
+    return c
+
+
+def dp_clipped_grad_sum(A, G, c, out, ids=None, V: Optional[int] = None,
+                        transpose_out: bool = False, accumulate: bool = False,
+                        stream=None) -> torch.Tensor:
+    """Linear form: A [B,T,d_in], G [B,T,d_out]; embedding form: A None, ids [B,T], V."""
+    L = lib()
+    _dev(G, "G")
+    pg, B, T, d_out, ldg = _rows(G, "G")
+    dt = _dtype(G)
+    if ids is None:
+        _dev(A, "A")
+        pa, _, _, d_in, lda = _rows(A, "A")
+        _check(L.dp_clipped_grad_sum(pa, lda, pg, ldg, None, c.data_ptr(), B, T, d_in, d_out, dt,
+                                     int(transpose_out), out.data_ptr(), int(accumulate), None,
+                                     0, _stream(stream)), "dp_clipped_grad_sum")
+        return out
+    if A is not None or V is None:
+        raise DPError("embedding form takes ids and V, not A")
+    if ids.dtype != torch.int32 or tuple(ids.shape) != (B, T) or not ids.is_contiguous():
+        raise DPError("ids must be contiguous int32 [B, T]")
+    ws = _ws(L.dp_clipped_grad_sum_workspace(B, T, d_out, 1), G.device)
+    _check(L.dp_clipped_grad_sum(None, 0, pg, ldg, ids.data_ptr(), c.data_ptr(), B, T, V, d_out,
+                                 dt, int(transpose_out), out.data_ptr(), int(accumulate),
+                                 ws.data_ptr(), ws.numel(), _stream(stream)),
+           "dp_clipped_grad_sum")
+    return out
+
+
+def dp_clipped_grad_sum_grouped(layers: Sequence, outs: Sequence[torch.Tensor], c,
+                                transpose_out: bool = False, accumulate: bool = False,
+                                stream=None) -> None:
+    L = lib()
+    descs = [_layer(l[0], l[1]) for l in layers]
+    arr = (dp_linear_t * len(descs))(*descs)
+    optrs = (ctypes.c_void_p * len(outs))(*[o.data_ptr() for o in outs])
+    A0 = layers[0][0]
+    _check(L.dp_clipped_grad_sum_grouped(arr, optrs, len(descs), c.data_ptr(), A0.shape[0],
+                                         A0.shape[1], _dtype(A0), int(transpose_out),
+                                         int(accumulate), _stream(stream)),
+           "dp_clipped_grad_sum_grouped")
+
+
+def dp_add_noise(grad, sigma: float, C: float, B_norm: int, seed: int, tensor_id: int,
+                 step: int, stream=None) -> torch.Tensor:
+    if grad.dtype != torch.float32 or not grad.is_contiguous():
+        raise DPError("grad must be contiguous fp32")
+    _check(lib().dp_add_noise(grad.data_ptr(), grad.numel(), float(sigma), float(C), int(B_norm),
+                              int(seed), int(tensor_id), int(step), _stream(stream)),
+           "dp_add_noise")
+    return grad

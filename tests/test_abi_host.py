@@ -1,0 +1,172 @@
+"""The C ABI on a host without a GPU: exports, workspace sizes, validation.
+
+Only invalid arguments are passed to entry points that launch kernels: they
+must be rejected on the host before any HIP call, so these run anywhere.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_40335_amd import build as B
+from paper_2609_40335_amd import dpghost as D
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dpghost.h")
+EINVAL, EUNSUP = 1, 2
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(D.library_path()):
+        B.build()
+    return D.lib()
+
+
+def _declared():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(dp_[a-z0-9_]+)\s*\(", txt)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _declared()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(n for n in names) >= {
+        "dp_ghost_norm_linear", "dp_ghost_norm_embedding", "dp_tied_cross_term",
+        "dp_clip_factors", "dp_clipped_grad_sum", "dp_add_noise"}
+
+
+def test_binding_covers_every_entry_point():
+    for n in _declared():
+        assert n in D._SIGS, n
+
+
+def test_version_and_strings(L):
+    assert L.dp_abi_version() == 1
+    assert L.dp_status_string(0) == b"ok"
+    assert L.dp_status_string(1) == b"invalid argument"
+
+
+def _lin(A=1 << 20, lda=64, d_in=64, G=1 << 21, ldg=64, d_out=64, algo=0):
+    return D.dp_linear_t(A, lda, d_in, G, ldg, d_out, algo)
+
+
+def test_norm_workspace_sizes(L):
+    one = (D.dp_linear_t * 1)(_lin(algo=D.DP_NORM_GRAM))
+    # T = 16: one T-tile pair per example, one G chunk -> 4 bytes per example
+    assert L.dp_ghost_norm_linear_workspace(one, 1, 4, 16, D.DP_F32) == 256
+    # T = 300 -> 3 T-tiles -> 6 pairs
+    assert L.dp_ghost_norm_linear_workspace(one, 1, 100, 300, D.DP_F32) == 2560
+    head = (D.dp_linear_t * 1)(_lin(d_in=768, lda=768, d_out=50257, ldg=50304))
+    # bf16: 16-byte rows -> features [0, 50256) in chunks of 2048 (25) + a 1-wide tail
+    assert L.dp_ghost_norm_linear_workspace(head, 1, 1, 128, D.DP_BF16) == 256
+    ws = L.dp_ghost_norm_linear_workspace(head, 1, 1000, 128, D.DP_BF16)
+    assert ws == ((1000 * 26 * 4 + 255) // 256) * 256
+    # AUTO picks the direct form once T + 1 > 2 d_in d_out / (d_in + d_out) = 64:
+    # one 256x256 output tile per example
+    auto = (D.dp_linear_t * 1)(_lin())
+    assert L.dp_ghost_norm_linear_workspace(auto, 1, 100, 300, D.DP_F32) == 512
+    assert L.dp_ghost_norm_linear_workspace(None, 1, 4, 16, D.DP_F32) == 0
+
+
+def test_linear_norm_rejects_bad_arguments(L):
+    n2 = ctypes.c_void_p(1 << 22)
+    ws = ctypes.c_void_p(1 << 23)
+    f = L.dp_ghost_norm_linear
+    assert f(None, 64, 1 << 21, 64, 4, 16, 64, 64, 0, 0, n2, 0, ws, 1 << 20, None) == EINVAL
+    assert b"NULL" in L.dp_last_error()
+    assert f(1 << 20, 32, 1 << 21, 64, 4, 16, 64, 64, 0, 0, n2, 0, ws, 1 << 20, None) == EINVAL
+    assert f(1 << 20, 64, 1 << 21, 64, 0, 16, 64, 64, 0, 0, n2, 0, ws, 1 << 20, None) == EINVAL
+    assert f(1 << 20, 64, 1 << 21, 64, 4, 16, 64, 64, 7, 0, n2, 0, ws, 1 << 20, None) == EINVAL
+    assert f(1 << 20, 64, 1 << 21, 64, 4, 16, 64, 64, 0, 9, n2, 0, ws, 1 << 20, None) == EINVAL
+    assert f(1 << 20, 64, 1 << 21, 64, 4, 16, 64, 64, 0, 0, None, 0, ws, 1 << 20, None) == EINVAL
+    # workspace too small / missing
+    assert f(1 << 20, 64, 1 << 21, 64, 4, 16, 64, 64, 0, 0, n2, 0, ws, 8, None) == EINVAL
+    assert b"workspace" in L.dp_last_error()
+    assert f(1 << 20, 64, 1 << 21, 64, 4, 16, 64, 64, 0, 0, n2, 0, None, 0, None) == EINVAL
+    assert f(1 << 20, 64, 1 << 21, 64, 4, 70000, 64, 64, 0, 0, n2, 0, ws, 1 << 30,
+             None) == EUNSUP
+
+
+def test_grouped_rejects_bad_layers(L):
+    arr = (D.dp_linear_t * 2)(_lin(), _lin(G=0))
+    assert L.dp_ghost_norm_linear_grouped(arr, 2, 4, 16, 0, 1 << 22, 0, 1 << 23, 1 << 20,
+                                          None) == EINVAL
+    assert b"layer 1" in L.dp_last_error()
+    assert L.dp_ghost_norm_linear_grouped(arr, 0, 4, 16, 0, 1 << 22, 0, 1 << 23, 1 << 20,
+                                          None) == EINVAL
+
+
+def test_embedding_rejects_bad_arguments(L):
+    f = L.dp_ghost_norm_embedding
+    args = dict(ids=1 << 20, dE=1 << 21, lde=64, B=4, T=16, V=512, d=64, dt=0, norm2=1 << 22,
+                acc=0, seg=None, nu=None, ws=1 << 23, wsb=1 << 20, s=None)
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(*a.values())
+    assert call(ids=None) == EINVAL
+    assert call(lde=32) == EINVAL
+    assert call(V=0) == EINVAL
+    assert call(wsb=0) == EINVAL
+    assert call(T=5000) == EUNSUP
+    assert call(V=1 << 30, T=64) == EUNSUP     # 30 + 6 bits > 32
+    assert L.dp_ghost_norm_embedding_workspace(4, 16, 64) == 256
+    assert L.dp_ghost_norm_embedding_workspace(64, 256, 768) == 64 * 12 * 4
+
+
+def test_cross_and_clip_reject_bad_arguments(L):
+    f = L.dp_tied_cross_term
+    ok = [1 << 20, 1 << 21, 64, 1 << 22, 64, 1 << 23, 512, 4, 16, 512, 64, 0, 2.0, 1 << 24, 1,
+          1 << 25, 1 << 20, None]
+    bad_ldz = list(ok); bad_ldz[6] = 100
+    assert f(*bad_ldz) == EINVAL
+    bad_scale = list(ok); bad_scale[12] = float("inf")
+    assert f(*bad_scale) == EINVAL
+    no_ws = list(ok); no_ws[16] = 0
+    assert f(*no_ws) == EINVAL
+    assert L.dp_tied_cross_term_workspace(4, 300) == 256
+    assert L.dp_clip_factors(1 << 20, 4, 0.0, 1 << 21, None) == EINVAL
+    assert L.dp_clip_factors(1 << 20, 4, float("nan"), 1 << 21, None) == EINVAL
+    assert L.dp_clip_factors(1 << 20, 0, 1.0, 1 << 21, None) == EINVAL
+
+
+def test_clipped_sum_rejects_bad_arguments(L):
+    f = L.dp_clipped_grad_sum
+    # both A and ids
+    assert f(1 << 20, 64, 1 << 21, 64, 1 << 22, 1 << 23, 4, 16, 512, 64, 0, 0, 1 << 24, 0,
+             1 << 25, 1 << 20, None) == EINVAL
+    # embedding form without workspace
+    assert f(None, 0, 1 << 21, 64, 1 << 22, 1 << 23, 4, 16, 512, 64, 0, 0, 1 << 24, 0,
+             None, 0, None) == EINVAL
+    # batch too large for the in-LDS sort
+    assert f(None, 0, 1 << 21, 64, 1 << 22, 1 << 23, 64, 512, 512, 64, 0, 0, 1 << 24, 0,
+             1 << 25, 1 << 30, None) == EUNSUP
+    assert L.dp_clipped_grad_sum_workspace(4, 16, 64, 0) == 0
+    assert L.dp_clipped_grad_sum_workspace(64, 256, 768, 1) > 2 * 512 * 768 * 4
+    outs = (ctypes.c_void_p * 1)(None)
+    arr = (D.dp_linear_t * 1)(_lin())
+    assert L.dp_clipped_grad_sum_grouped(arr, outs, 1, 1 << 20, 4, 16, 0, 0, 0, None) == EINVAL
+
+
+def test_noise_rejects_bad_arguments(L):
+    f = L.dp_add_noise
+    assert f(1 << 20, -1, 1.0, 1.0, 4, 0, 0, 0, None) == EINVAL
+    assert f(None, 10, 1.0, 1.0, 4, 0, 0, 0, None) == EINVAL
+    assert f(1 << 20, 10, -1.0, 1.0, 4, 0, 0, 0, None) == EINVAL
+    assert f(1 << 20, 10, 1.0, 0.0, 4, 0, 0, 0, None) == EINVAL
+    assert f(1 << 20, 10, 1.0, 1.0, -4, 0, 0, 0, None) == EINVAL
+    assert f(1 << 20, 10, 1.0, 1.0, 4, 0, 1 << 32, 0, None) == EINVAL
+    assert f(1 << 20, 10, 1.0, 1.0, 4, 0, 0, 1 << 32, None) == EINVAL
+    # n = 0 is a no-op that launches nothing
+    assert f(None, 0, 1.0, 1.0, 4, 0, 0, 0, None) == 0
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(D, "_LIB", None)
+    monkeypatch.setattr(D, "_HERE", str(tmp_path))
+    with pytest.raises(D.DPError, match="not built"):
+        D.lib()

@@ -38,7 +38,7 @@ __all__ = [
     "f32_to_bf16_bits", "bf16_bits_to_f32",
     "block_linears", "model_linears", "gpt2_param_count",
     "LinearInputs", "HeadInputs", "Workload", "CONFIG_NAMES", "make_workload",
-    "zipf_ids", "logit_grads",
+    "zipf_ids", "logit_grads", "draw", "draw_ids",
 ]
 
 GPT2_VOCAB = 50257
@@ -133,6 +133,28 @@ def logit_grads(z: np.ndarray, ids: np.ndarray) -> np.ndarray:
     z[:, T - 1, :] = 0.0
     z /= np.float32(T)
     return z
+
+
+def draw(seed: int, tag: int, shape, std: float = 1.0, dtype: str = "bf16") -> np.ndarray:
+    """One seeded N(0, std) tensor, encoded as bf16 bits or fp32."""
+    x = _normal(seed, tag, shape, std)
+    return f32_to_bf16_bits(x) if dtype == "bf16" else x
+
+
+def draw_ids(seed: int, tag: int, shape, V: int, kind: str = "zipf") -> np.ndarray:
+    """Seeded token ids: "zipf" (s = 1.1), "uniform", "same" (all one id) or
+    "distinct" (a random injection into [0, V); needs the last axis <= V)."""
+    rng = _rng(seed, tag)
+    if kind == "zipf":
+        return zipf_ids(rng, shape, V, 1.1)
+    if kind == "uniform":
+        return rng.integers(0, V, size=shape, dtype=np.int64).astype(np.int32)
+    if kind == "same":
+        return np.full(shape, int(rng.integers(0, V)), dtype=np.int32)
+    if kind == "distinct":
+        flat = np.stack([rng.permutation(V)[: shape[-1]] for _ in range(int(np.prod(shape[:-1])))])
+        return flat.reshape(shape).astype(np.int32)
+    raise ValueError(kind)
 
 
 # --------------------------------------------------------------------------
