@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""DP-SGD ghost-clipping step on one MI355X: examples/s, roofline, CPU baseline.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload gpt2-step]
+
+One step is the whole hot path on one batch, through the C ABI:
+  1. squared per-example norms of every linear layer and of the output head
+     (grouped T x T Gram kernel; eq. 4-6)
+  2. input-embedding norm and token buckets
+  3. tied cross term folded in as + 2 <g_in, g_out> (eq. 11, eq. 13)
+  4. clip factors (eq. 2, eq. 7)
+  5. clipped sums of all linears and of the head, the head landing in the
+     tied embedding gradient (one grouped GEMM, K = B*T)
+  6. the input-embedding part of the tied gradient (sorted segment sums)
+  7. Gaussian noise and division by B over the flat gradient vector (eq. 3)
+Inputs are resident in HBM before the timed region starts. Prints one JSON
+line; per-phase times go to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "examples/sec for ghost-norm + clipped grad sum (GPT-2-small shapes); % MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gpt2-step",
+                    choices=["gpt2-step", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--ldz-multiple", type=int, default=64,
+                    help="pad logit-gradient rows to a multiple of this many columns")
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle work for the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args(argv)
+
+
+def round_up(x, m):
+    return (x + m - 1) // m * m
+
+
+class Step:
+    """Device inputs, outputs and the prepared calls of one DP-SGD step."""
+
+    def __init__(self, wl, dp, torch):
+        self.wl, self.dp, self.torch = wl, dp, torch
+        B, T = wl.B, wl.T
+        dev = lambda a: torch.from_numpy(a.view("int16")).view(torch.bfloat16).cuda()
+        self.lin = [(dev(l.A), dev(l.G)) for l in wl.linears]
+        h = wl.head
+        self.h = h
+        # one flat fp32 gradient vector; every parameter tensor is a view of it
+        n_lin = sum(l.d_in * l.d_out for l in wl.linears)
+        n_head = 0 if h is None or h.H is None else h.V * h.d * (1 if h.tied else 1)
+        n_emb = 0 if h is None else (h.V * h.d if (h.H is None or not h.tied) else 0)
+        self.n_coords = n_lin + n_head + n_emb
+        self.flat = torch.zeros(self.n_coords, device="cuda")
+        off = 0
+        self.outs = []
+        for l in wl.linears:
+            self.outs.append(self.flat[off:off + l.d_in * l.d_out].view(l.d_in, l.d_out))
+            off += l.d_in * l.d_out
+        norm_layers = list(self.lin)
+        sum_layers, sum_outs = list(self.lin), list(self.outs)
+        if h is not None:
+            self.ids = torch.from_numpy(h.ids).cuda()
+            self.dE = dev(h.dE)
+            if h.H is not None:
+                self.H = dev(h.H)
+                self.Gz = dev(h.Gz)[:, :, :h.V]
+                self.W = self.flat[off:off + h.V * h.d].view(h.V, h.d)   # W_out (= E if tied)
+                off += h.V * h.d
+                norm_layers.append((self.H, self.Gz))
+                sum_layers.append((self.Gz, self.H))                    # Gz^T H -> [V, d]
+                sum_outs.append(self.W)
+            if h.H is None or not h.tied:
+                self.E = self.flat[off:off + h.V * h.d].view(h.V, h.d)
+                off += h.V * h.d
+            else:
+                self.E = self.W
+            self.seg = torch.empty((B, T), dtype=torch.int32, device="cuda")
+            self.nu = torch.empty(B, dtype=torch.int32, device="cuda")
+        assert off == self.n_coords
+        self.norm_group = dp.LinearGroup(norm_layers)
+        self.sum_group = dp.LinearGroup(sum_layers, sum_outs) if sum_layers else None
+        self.n2 = torch.zeros(B, device="cuda")
+        self.c = torch.zeros(B, device="cuda")
+        # algorithmic work of the grouped clipped-sum GEMM (the dominant kernel)
+        K = B * T
+        self.gemm_flops = 2.0 * K * sum(a.shape[2] * g.shape[2] for a, g in sum_layers)
+        # algorithmic bytes of the grouped norm kernel: every A and G element once
+        self.norm_bytes = 2.0 * K * sum(a.shape[2] + g.shape[2] for a, g in norm_layers)
+        self.step_id = 0
+
+    def run(self, marks=None):
+        """One step; marks(name) records an event after each phase if given."""
+        dp, wl, h = self.dp, self.wl, self.h
+        mark = marks or (lambda name: None)
+        self.norm_group.ghost_norm(self.n2, accumulate=False)
+        mark("norms")
+        if h is not None:
+            dp.dp_ghost_norm_embedding(self.ids, self.dE, h.V, self.n2, accumulate=True,
+                                       seg_id=self.seg, n_unique=self.nu)
+            mark("embedding_norm")
+            if h.H is not None and h.tied:
+                dp.dp_tied_cross_term(self.ids, self.dE, self.H, self.Gz, h.V, self.n2,
+                                      scale=2.0, accumulate=True)
+                mark("cross_term")
+        dp.dp_clip_factors(self.n2, wl.C, self.c)
+        mark("clip")
+        if self.sum_group is not None:
+            self.sum_group.clipped_sum(self.c)
+        mark("clipped_sum")
+        if h is not None:
+            tied = h.H is not None and h.tied
+            dp.dp_clipped_grad_sum(None, self.dE, self.c, self.E, ids=self.ids, V=h.V,
+                                   accumulate=tied)
+            mark("embedding_sum")
+        dp.dp_add_noise(self.flat, wl.sigma, wl.C, wl.B, seed=1234, tensor_id=0,
+                        step=self.step_id)
+        mark("noise")
+        self.step_id += 1
+
+
+def cpu_baseline(wl, n_coords, budget):
+    """The fp64 oracle on the host: per-example work on a sample of examples,
+    noise on a slice of coordinates, extrapolated to one full step."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()
+                       if p.get("user_api") == "blas"] or [os.cpu_count() or 1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    oracle.step(wl, examples=[0], noise=False)
+    per_ex = time.perf_counter() - t0
+    n_ex = int(max(1, min(wl.B - 1, budget * 0.7 / max(per_ex, 1e-9))))
+    if n_ex > 1:
+        t0 = time.perf_counter()
+        oracle.step(wl, examples=list(range(1, 1 + n_ex)), noise=False)
+        per_ex = (time.perf_counter() - t0) / n_ex
+    n_slice = 1 << 22
+    S = np.zeros(n_slice)
+    t0 = time.perf_counter()
+    oracle.add_noise(S, wl.sigma, wl.C, wl.B, 1234, 0, 0)
+    per_coord = (time.perf_counter() - t0) / n_slice
+    t_step = wl.B * per_ex + n_coords * per_coord
+    return {
+        "value": wl.B / t_step, "unit": "examples/s", "cores": int(threads), "kind": "oracle",
+        "sample": (f"fp64 oracle (materialised per-example gradients): norms, clip factors and "
+                   f"clipped sums on {1 + n_ex} example(s) of this workload, noise on "
+                   f"{n_slice} coordinates; extrapolated to B={wl.B} examples and "
+                   f"{n_coords} coordinates per step"),
+        "seconds_per_example": per_ex, "seconds_noise_per_step": n_coords * per_coord,
+    }
+
+
+def main(argv=None) -> int:
+    args = parse(argv)
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
+              f"multi-GPU path. Run with --gpus 1.", file=sys.stderr)
+        return 2
+    import numpy as np  # noqa: F401
+    import torch
+
+    from paper_2609_40335_amd import dpghost as dp
+    from workloads import gen
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    dp.lib()
+    t0 = time.perf_counter()
+    V = gen.GPT2_VOCAB
+    wl = gen.make_workload(args.workload, seed=args.seed, ldz=round_up(V, args.ldz_multiple))
+    log(f"[bench] generated {args.workload}: {wl.description} in {time.perf_counter() - t0:.1f}s")
+    st = Step(wl, dp, torch)
+    log(f"[bench] {len(wl.linears)} linear layers, head={'none' if wl.head is None else ('tied' if wl.head.tied else 'untied')}, "
+        f"{st.n_coords} gradient coordinates")
+
+    for _ in range(args.warmup):
+        st.run()
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    ev = []
+
+    def marks(name):
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        ev[-1].append((name, e))
+
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        ev.append([("start", e0)])
+        st.run(marks)
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms = total_ms / args.steps
+
+    phases = {}
+    for step_ev in ev:
+        for (n0, a), (n1, b) in zip(step_ev[:-1], step_ev[1:]):
+            phases.setdefault(n1, []).append(a.elapsed_time(b))
+    phase_ms = {k: sum(v) / len(v) for k, v in phases.items()}
+    for k, v in phase_ms.items():
+        log(f"[bench]   {k:16s} {v * 1e3:9.1f} us")
+    gemm_s = phase_ms["clipped_sum"] / 1e3
+    norm_s = phase_ms["norms"] / 1e3
+    achieved = st.gemm_flops / gemm_s / 1e12
+    log(f"[bench] clipped-sum GEMM {st.gemm_flops / 1e9:.1f} GFLOP in {gemm_s * 1e6:.1f} us = "
+        f"{achieved:.1f} TFLOP/s; grouped norm {st.norm_bytes / 1e9:.3f} GB in "
+        f"{norm_s * 1e6:.1f} us = {st.norm_bytes / norm_s / 1e9:.0f} GB/s")
+
+    h = wl.head
+    config = {"workload": f"{args.workload}: {wl.description}", "B": wl.B, "T": wl.T,
+              "linear_layers": len(wl.linears),
+              "head": None if h is None else ("tied" if h.tied else ("untied" if h.H is not None
+                                                                   else "embedding-only")),
+              "V": None if h is None else h.V, "ldz": None if h is None else h.ldz,
+              "gradient_coordinates": st.n_coords, "C": wl.C, "sigma": wl.sigma,
+              "phase_us": {k: round(v * 1e3, 1) for k, v in phase_ms.items()}}
+    out = {
+        "metric": METRIC, "value": wl.B / (ms / 1e3), "unit": "examples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic", "config": config,
+        "roofline": {"bound": "mfma", "kernel": "kt_gemm_kernel (clipped sum, bf16)",
+                     "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "algorithmic_flop_per_launch": st.gemm_flops},
+    }
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        out["cpu_baseline"] = cpu_baseline(wl, st.n_coords, args.cpu_budget)
+        log(f"[bench] cpu baseline took {time.perf_counter() - t0:.1f}s")
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

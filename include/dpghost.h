@@ -11,6 +11,11 @@
  *  - Tensor pointers are DEVICE pointers, row-major. A token-major matrix
  *    [B, T, w] with row stride ld (elements, ld >= w) holds token t of
  *    example b at row b*T + t. bf16 data is passed as its 16-bit patterns.
+ *  - A matrix given with row stride ld > its width occupies ld elements in
+ *    every row, the last one included (as a [rows, ld] buffer viewed to
+ *    fewer columns does). When its rows are 16-byte aligned and ld is a
+ *    whole number of 16-byte chunks, kernels may read, but never use, the
+ *    elements between the width and the next 16-byte boundary of a row.
  *  - Outputs are fp32. Squared norms add across calls ("accumulate" = 1
  *    means +=, 0 means overwrite), which is eq. 6 / eq. 10.
  *  - `stream` is a hipStream_t (NULL = the default stream). Calls are

@@ -65,7 +65,7 @@ struct GemmEntry {
   const void* X;
   const void* Y;
   int64_t ldx, ldy;
-  int m_lo, m_hi, n_lo, n_hi, tm, tn;
+  int M, N, tm, tn;
   int slot_begin;
   float* out;
   int64_t ldo;
@@ -86,61 +86,36 @@ bool use_direct(const dp_linear_t& L, int T) {
   return (double)T + 1.0 > crossover;
 }
 
-// Splits the output region [0,M) x [0,N) of a GEMM into an entry whose every
-// column bound is a multiple of the 16-byte chunk (16-byte loads) and
-// element-wise entries for the ragged edges.
+// One GEMM entry over the output region [0,M) x [0,N); 16-byte loads when
+// both operands have aligned rows whose stride is a whole number of chunks.
 void plan_gemm(const void* X, int64_t ldx, int M, const void* Y, int64_t ldy, int N,
                dp_dtype_t dt, float* out, int64_t ldo, std::vector<GemmEntry>& v,
                int64_t* slots, int64_t slot_mult) {
-  auto add = [&](int m_lo, int m_hi, int n_lo, int n_hi, bool vec) {
-    if (m_hi <= m_lo || n_hi <= n_lo) return;
-    GemmEntry e{X, Y, ldx, ldy, m_lo, m_hi, n_lo, n_hi,
-                (int)ceil_div(m_hi - m_lo, dpg::GM_BM), (int)ceil_div(n_hi - n_lo, dpg::GM_BN),
-                0, out, ldo, vec};
-    if (slots) {
-      e.slot_begin = (int)*slots;
-      *slots += (int64_t)e.tm * e.tn * slot_mult;
-    }
-    v.push_back(e);
-  };
-  const int q = elems_per_chunk(dt);
-  if (vec_ok(X, ldx, dt) && vec_ok(Y, ldy, dt)) {
-    const int Ma = M / q * q, Na = N / q * q;
-    add(0, Ma, 0, Na, true);
-    add(Ma, M, 0, N, false);
-    add(0, Ma, Na, N, false);
-  } else {
-    add(0, M, 0, N, false);
+  GemmEntry e{X, Y, ldx, ldy, M, N, (int)ceil_div(M, dpg::GM_BM), (int)ceil_div(N, dpg::GM_BN),
+              0, out, ldo, vec_ok(X, ldx, dt) && vec_ok(Y, ldy, dt)};
+  if (slots) {
+    e.slot_begin = (int)*slots;
+    *slots += (int64_t)e.tm * e.tn * slot_mult;
   }
+  v.push_back(e);
 }
 
 NormPlan plan_norm(const dp_linear_t* layers, int n, int T, dp_dtype_t dt) {
   NormPlan p;
   p.n_t = (int)ceil_div(T, dpg::GR_TM);
   p.P = p.n_t * (p.n_t + 1) / 2;
-  const int q = elems_per_chunk(dt), ks = stage_features(dt);
+  const int ks = stage_features(dt);
   for (int i = 0; i < n; ++i) {
     const dp_linear_t& L = layers[i];
     if (use_direct(L, T)) {
       plan_gemm(L.A, L.lda, L.d_in, L.G, L.ldg, L.d_out, dt, nullptr, 0, p.direct, &p.slots, 1);
       continue;
     }
-    auto add = [&](int g0, int g1, bool vec) {
-      if (g1 <= g0) return;
-      const int len = g1 - g0;
-      const int kg = len > KG_SPLIT ? KG_CHUNK : (int)(ceil_div(len, ks) * ks);
-      GramEntry e{L.A, L.G, L.lda, L.ldg, L.d_in, g0, g1, kg, (int)ceil_div(len, kg),
-                  (int)p.slots, vec};
-      p.slots += (int64_t)p.P * e.nc;
-      p.gram.push_back(e);
-    };
-    if (vec_ok(L.A, L.lda, dt) && vec_ok(L.G, L.ldg, dt) && L.d_in % q == 0) {
-      const int ga = L.d_out / q * q;
-      add(0, ga, true);
-      add(ga, L.d_out, false);
-    } else {
-      add(0, L.d_out, false);
-    }
+    const int kg = L.d_out > KG_SPLIT ? KG_CHUNK : (int)(ceil_div(L.d_out, ks) * ks);
+    GramEntry e{L.A, L.G, L.lda, L.ldg, L.d_in, 0, L.d_out, kg, (int)ceil_div(L.d_out, kg),
+                (int)p.slots, vec_ok(L.A, L.lda, dt) && vec_ok(L.G, L.ldg, dt)};
+    p.slots += (int64_t)p.P * e.nc;
+    p.gram.push_back(e);
   }
   return p;
 }
@@ -210,18 +185,18 @@ dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int
     for (size_t i0 = 0; i0 < sel.size(); i0 += dpg::GM_MAX_LAYERS) {
       dpg::GemmArgs a{};
       a.B = B; a.T = T; a.c = c; a.ws = ws; a.slots = (int32_t)slots;
+      a.transpose = transpose; a.accumulate = accumulate;
       uint64_t items = 0;
       const size_t n = std::min(sel.size() - i0, (size_t)dpg::GM_MAX_LAYERS);
       for (size_t j = 0; j < n; ++j) {
         const GemmEntry& e = *sel[i0 + j];
         dpg::GemmLayer& L = a.L[j];
         L.X = e.X; L.Y = e.Y; L.ldx = e.ldx; L.ldy = e.ldy;
-        L.m_lo = e.m_lo; L.m_hi = e.m_hi; L.n_lo = e.n_lo; L.n_hi = e.n_hi;
+        L.M = e.M; L.N = e.N;
         L.tm = e.tm; L.tn = e.tn;
         L.tile_begin = (uint32_t)items;
         L.slot_begin = e.slot_begin;
         L.out = e.out; L.ldo = e.ldo;
-        L.transpose = transpose; L.accumulate = accumulate;
         items += (uint64_t)e.tm * e.tn * (mode == 1 ? (uint64_t)B : 1ull);
       }
       if (items > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many work items");
@@ -374,7 +349,7 @@ dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, 
   a.n_t = (int)ceil_div(T, dpg::GR_TM);
   a.slots = a.n_t * a.n_t;
   a.ws = static_cast<float*>(workspace);
-  const bool vec = vec_ok(dE, lde, dt) && vec_ok(H, ldh, dt) && d % elems_per_chunk(dt) == 0;
+  const bool vec = vec_ok(dE, lde, dt) && vec_ok(H, ldh, dt);
   hipStream_t s = as_stream(stream);
   dp_status_t st = hip_status(dpg::launch_tied_cross(a, kdt(dt), vec, s), "tied_cross launch");
   if (st != DP_OK) return st;

@@ -89,6 +89,27 @@ __device__ __forceinline__ u32x4 load_chunk16(const void* row, int64_t col, int 
   return *(const u32x4*)((const char*)row + col * es);
 }
 
+// 16-byte chunk at `col` (< ncol) of a 16-byte aligned row whose stride
+// covers the whole chunk; elements at or past ncol are zeroed in registers.
+template <int DT>
+__device__ __forceinline__ u32x4 load_chunk16_masked(const void* row, int64_t col, int64_t ncol) {
+  constexpr int EPC = (DT == DT_BF16) ? 8 : 4;
+  u32x4 v = load_chunk16(row, col, DT == DT_BF16 ? 2 : 4);
+  const int64_t nv = ncol - col;  // valid elements in this chunk, >= 1
+  if (nv < EPC) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if constexpr (DT == DT_BF16) {
+        const int e = 2 * q;  // elements e, e+1 live in dword q
+        v[q] = e + 1 < nv ? v[q] : (e < nv ? (v[q] & 0xFFFFu) : 0u);
+      } else {
+        v[q] = q < nv ? v[q] : 0u;
+      }
+    }
+  }
+  return v;
+}
+
 // How a thread's chunk [col, col + EPC) of a row relates to the valid columns.
 enum ChunkKind { CHUNK_FULL = 0, CHUNK_PART = 1, CHUNK_NONE = 2 };
 template <int DT>

@@ -62,7 +62,7 @@ __device__ __forceinline__ void load_block(const char* base, int64_t ld, int64_t
       u32x4 v = {0u, 0u, 0u, 0u};
       if (k < k_end && cc < ncol) {
         const char* row = base + k * ld;
-        v = VEC ? load_chunk16(row, cc, P::ES) : load_chunk_elems<DT>(row, cc, ncol);
+        v = VEC ? load_chunk16_masked<DT>(row, cc, ncol) : load_chunk_elems<DT>(row, cc, ncol);
       }
       raw[j * CPR + h] = v;
     }
@@ -163,8 +163,8 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
     k_end = k_begin + a.T;
   }
   const int mt = (int)(rel / (uint32_t)L.tn), nt = (int)(rel - (uint32_t)mt * L.tn);
-  const int64_t m0 = (int64_t)L.m_lo + (int64_t)mt * GM_BM;
-  const int64_t n0 = (int64_t)L.n_lo + (int64_t)nt * GM_BN;
+  const int64_t m0 = (int64_t)mt * GM_BM;
+  const int64_t n0 = (int64_t)nt * GM_BN;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wm = w >> 1, wn = w & 1;
@@ -186,8 +186,8 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
   u32x4 rx[8], ry[8];
   auto load = [&](int s) {
     const int64_t k0 = k_begin + (int64_t)s * P::KS + kg * P::RPT;
-    load_block<DT, VEC>(Xb, ldx, k0, k_end, m0 + mg * 8, L.m_hi, rx);
-    load_block<DT, VEC>(Yb, ldy, k0, k_end, n0 + mg * 8, L.n_hi, ry);
+    load_block<DT, VEC>(Xb, ldx, k0, k_end, m0 + mg * 8, L.M, rx);
+    load_block<DT, VEC>(Yb, ldy, k0, k_end, n0 + mg * 8, L.N, ry);
   };
   load(0);
   for (int s = 0; s < nS; ++s) {
@@ -220,13 +220,13 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int64_t n = n0 + wn * 128 + j * 32 + (lane & 31);
-        if (n >= L.n_hi) continue;
+        if (n >= L.N) continue;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int64_t m = m0 + wm * 128 + i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-          if (m < L.m_hi) {
-            const int64_t idx = L.transpose ? n * ldo + m : m * ldo + n;
-            out[idx] = L.accumulate ? out[idx] + acc[i][j][e] : acc[i][j][e];
+          if (m < L.M) {
+            const int64_t idx = a.transpose ? n * ldo + m : m * ldo + n;
+            out[idx] = a.accumulate ? out[idx] + acc[i][j][e] : acc[i][j][e];
           }
         }
       }

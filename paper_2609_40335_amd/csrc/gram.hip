@@ -109,9 +109,10 @@ struct TileStream {
   int nX;
   int64_t x1, y0, y1;
 
-  // VEC: rows are 16-byte aligned and every column bound is a multiple of
-  // the chunk width, so a chunk is one 16-byte load or all zero. Otherwise
-  // elements are loaded one at a time.
+  // VEC: rows are 16-byte aligned and their stride is a whole number of
+  // chunks, so every chunk is one 16-byte load (elements past the valid
+  // columns are zeroed in registers). Otherwise elements are loaded one at a
+  // time.
   __device__ __forceinline__ void prefetch(int s, u32x4 (&pre)[8], int nent) const {
     const bool inX = s < nX;
     const char* base = inX ? X : Y;
@@ -125,7 +126,7 @@ struct TileStream {
       u32x4 v = {0u, 0u, 0u, 0u};
       if (i < nent && 32 * k < (lo ? T_end_i : T_end_j) && col < ncol) {
         const char* row = base + ((lo ? row_i : row_j) + 32 * k) * ld;
-        v = VEC ? load_chunk16(row, col, ES) : load_chunk_elems<DT>(row, col, ncol);
+        v = VEC ? load_chunk16_masked<DT>(row, col, ncol) : load_chunk_elems<DT>(row, col, ncol);
       }
       pre[i] = v;
     }
@@ -287,7 +288,7 @@ __global__ __launch_bounds__(GR_THREADS) void tied_cross_kernel(CrossArgs a) {
       const int k = lo ? i : i - 4;
       if (col < a.d && 32 * k < (lo ? end_i : end_j)) {
         const char* row = lo ? Eb + (row_i + 32 * k) * lde : Hb + (row_j + 32 * k) * ldh;
-        v = VEC ? load_chunk16(row, col, ES) : load_chunk_elems<DT>(row, col, a.d);
+        v = VEC ? load_chunk16_masked<DT>(row, col, a.d) : load_chunk_elems<DT>(row, col, a.d);
       }
       pre[i] = v;
     }

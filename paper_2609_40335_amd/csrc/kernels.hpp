@@ -9,7 +9,7 @@ enum { DT_F32 = 0, DT_BF16 = 1 };  // element type of the float operands
 
 // ----------------------------------------------------------------- Gram norm
 constexpr int GR_TM = 128;          // rows of one T-tile
-constexpr int GR_MAX_LAYERS = 24;   // layers per launch (kernel-argument budget)
+constexpr int GR_MAX_LAYERS = 52;   // layers per launch (kernel arguments stay < 4 KiB)
 
 struct GramLayer {
   const void* A;        // [B*T rows, lda] activations
@@ -32,6 +32,7 @@ struct GramArgs {
   float* ws;              // [B, slots]
 };
 
+static_assert(sizeof(GramArgs) <= 4096, "kernel arguments must stay within 4 KiB");
 hipError_t launch_gram_norm(const GramArgs& a, int dt, bool vec, hipStream_t s);
 
 // Tied cross term: sum_{t,s} Gz[s, ids[t]] <dE_t, H_s>, all T-tile pairs.
@@ -53,20 +54,17 @@ hipError_t launch_finish_rows(const float* ws, int B, int slots, float* out, int
 
 // ------------------------------------------------------- K-major GEMM family
 constexpr int GM_BM = 256, GM_BN = 256;
-constexpr int GM_MAX_LAYERS = 24;
+constexpr int GM_MAX_LAYERS = 52;   // layers per launch (kernel arguments stay < 4 KiB)
 
 struct GemmLayer {
   const void* X;        // [K rows, ldx]
   const void* Y;        // [K rows, ldy]
-  int64_t ldx, ldy;     // row strides in elements
-  int32_t m_lo, m_hi;   // X columns (output rows) covered by this entry
-  int32_t n_lo, n_hi;   // Y columns (output columns) covered by this entry
+  float* out;           // clipped sum: [M, ldo] or transposed [N, ldo]
+  int64_t ldx, ldy, ldo;  // row strides in elements
+  int32_t M, N;         // X columns (output rows) and Y columns (output columns)
   int32_t tm, tn;       // 256-wide tiles along M and N
   uint32_t tile_begin;  // first work item of this entry
   int32_t slot_begin;   // direct norm: first partial slot in an example's row
-  float* out;           // clipped sum: [M, ldo] or transposed [N, ldo]
-  int64_t ldo;
-  int32_t transpose, accumulate;
 };
 
 struct GemmArgs {
@@ -74,10 +72,13 @@ struct GemmArgs {
   int32_t n_layers;
   int32_t B, T;
   uint32_t n_items;
+  int32_t transpose, accumulate;  // clipped sum: output layout and +=
   const float* c;       // clipped sum: per-example scale [B]
   float* ws;            // direct norm: [B, slots]
   int32_t slots;
 };
+
+static_assert(sizeof(GemmArgs) <= 4096, "kernel arguments must stay within 4 KiB");
 
 // Clipped sum: out (+)= sum_i c_i X_i^T Y_i over all B*T rows (K = B*T).
 hipError_t launch_clipped_sum(const GemmArgs& a, int dt, bool vec, hipStream_t s);

@@ -20,7 +20,7 @@ __all__ = [
     "lib", "library_path", "dp_abi_version",
     "dp_ghost_norm_linear", "dp_ghost_norm_linear_grouped", "dp_ghost_norm_embedding",
     "dp_tied_cross_term", "dp_clip_factors", "dp_clipped_grad_sum",
-    "dp_clipped_grad_sum_grouped", "dp_add_noise",
+    "dp_clipped_grad_sum_grouped", "dp_add_noise", "LinearGroup",
 ]
 
 DP_F32, DP_BF16 = 0, 1
@@ -268,3 +268,51 @@ def dp_add_noise(grad, sigma: float, C: float, B_norm: int, seed: int, tensor_id
                               int(seed), int(tensor_id), int(step), _stream(stream)),
            "dp_add_noise")
     return grad
+
+
+class LinearGroup:
+    """Descriptors of many linear layers of one batch, prepared once.
+
+    Holds the ctypes descriptor array, the output-pointer array and the norm
+    workspace so that repeated steps only pass pointers. ``layers`` is a
+    sequence of (A, G) or (A, G, algo) with a common B, T and dtype.
+    """
+
+    def __init__(self, layers: Sequence, outs: Optional[Sequence[torch.Tensor]] = None):
+        L = lib()
+        self._tensors = [t for l in layers for t in l[:2]]
+        self.n = len(layers)
+        self.descs = (dp_linear_t * self.n)(*[_layer(*l) for l in layers])
+        A0 = layers[0][0]
+        self.B, self.T, self.dt = A0.shape[0], A0.shape[1], _dtype(A0)
+        for l in layers:
+            if tuple(l[0].shape[:2]) != (self.B, self.T) or _dtype(l[0]) != self.dt:
+                raise DPError("all layers of a group share B, T and dtype")
+        nbytes = L.dp_ghost_norm_linear_workspace(self.descs, self.n, self.B, self.T, self.dt)
+        self.ws = _ws(nbytes, A0.device)
+        self.outs = None
+        if outs is not None:
+            self.set_outputs(outs)
+
+    def set_outputs(self, outs: Sequence[torch.Tensor]) -> None:
+        if len(outs) != self.n:
+            raise DPError("one output per layer")
+        self._outs = list(outs)
+        self.outs = (ctypes.c_void_p * self.n)(*[o.data_ptr() for o in outs])
+
+    def ghost_norm(self, norm2: torch.Tensor, accumulate: bool = False, stream=None):
+        _check(lib().dp_ghost_norm_linear_grouped(self.descs, self.n, self.B, self.T, self.dt,
+                                                  norm2.data_ptr(), int(accumulate),
+                                                  self.ws.data_ptr(), self.ws.numel(),
+                                                  _stream(stream)),
+               "dp_ghost_norm_linear_grouped")
+        return norm2
+
+    def clipped_sum(self, c: torch.Tensor, transpose_out: bool = False,
+                    accumulate: bool = False, stream=None) -> None:
+        if self.outs is None:
+            raise DPError("set_outputs() first")
+        _check(lib().dp_clipped_grad_sum_grouped(self.descs, self.outs, self.n, c.data_ptr(),
+                                                 self.B, self.T, self.dt, int(transpose_out),
+                                                 int(accumulate), _stream(stream)),
+               "dp_clipped_grad_sum_grouped")
