@@ -62,6 +62,61 @@ __device__ __forceinline__ f32x16 mfma32_f32(float a, float b, const f32x16& c) 
   return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
 }
 
+// Buffer resources: loads through them need no bounds branches, because the
+// hardware returns 0 for any dword at or past num_records bytes.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int RSRC_WORD3 = 0x00020000;  // raw (untyped) buffer, gfx9 family
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t nbytes) {
+  const uint32_t n = nbytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)nbytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, RSRC_WORD3);
+}
+__device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ uint32_t buf_load4(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+__device__ __forceinline__ uint32_t buf_load2(rsrc_t r, uint32_t off) {
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+}
+
+// 16-byte chunk of elements [col, col+EPC) of the row starting at byte
+// offset `row_off`, through a buffer resource. VEC: one 16-byte load (the row
+// is 16-byte aligned); otherwise one load per element. Elements at or past
+// `ncol` are zeroed when MASK is set.
+template <int DT, bool VEC, bool MASK>
+__device__ __forceinline__ u32x4 buf_chunk(rsrc_t r, uint32_t row_off, int64_t col, int64_t ncol) {
+  constexpr int EPC = (DT == DT_BF16) ? 8 : 4;
+  constexpr int ES = (DT == DT_BF16) ? 2 : 4;
+  u32x4 v;
+  if constexpr (VEC) {
+    v = buf_load16(r, row_off + (uint32_t)(col * ES));
+  } else if constexpr (DT == DT_BF16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      v[q] = buf_load2(r, row_off + (uint32_t)((col + 2 * q) * ES)) |
+             (buf_load2(r, row_off + (uint32_t)((col + 2 * q + 1) * ES)) << 16);
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = buf_load4(r, row_off + (uint32_t)((col + q) * ES));
+  }
+  if constexpr (MASK) {
+    const int64_t nv = ncol - col;  // valid elements in the chunk (may be <= 0)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if constexpr (DT == DT_BF16) {
+        const int e = 2 * q;
+        v[q] = e + 1 < nv ? v[q] : (e < nv ? (v[q] & 0xFFFFu) : 0u);
+      } else {
+        v[q] = q < nv ? v[q] : 0u;
+      }
+    }
+  }
+  (void)EPC;
+  return v;
+}
+
 // Chunk loaders: 16 bytes = 8 bf16 or 4 fp32 starting at element `col` of a
 // row. Elements at or past `ncol` read as zero.
 template <int DT>

@@ -14,17 +14,19 @@
 // when T exceeds about 2 d_in d_out / (d_in + d_out).
 //
 // MFMA wants 8 consecutive k per lane, but both operands are contiguous along
-// M/N. Each thread loads an 8(k) x 8(m) block with 16-byte loads, scales it
-// (bf16: exact widening, fp32 multiply, v_cvt_pk_bf16_f32 rounding), and
-// transposes it in registers into 8 k-contiguous chunks written to LDS.
-// Tile 256x256x64 (bf16) or 256x256x32 (fp32); 4 waves, each a 128x128
-// quadrant of 4x4 32x32 blocks.
+// M/N. Each staging thread loads an 8(k) x 8(m) block with 16-byte buffer
+// loads, scales it (X only: exact widening, fp32 multiply,
+// v_cvt_pk_bf16_f32 rounding) and transposes it in registers into 8
+// k-contiguous chunks written to LDS. Waves 0-3 stage X, waves 4-7 stage Y.
+// Tile 256x256, 64 (bf16) or 32 (fp32) k per stage, LDS double-buffered with
+// one barrier per stage; each of the 8 waves owns a 128x64 quadrant of 4x2
+// 32x32 MFMA blocks, so two waves share every SIMD.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace dpg {
 
-constexpr int GM_THREADS = 256;
+constexpr int GM_THREADS = 512;
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -44,33 +46,31 @@ struct KT {
   static constexpr int KS = 8 * RPT;                   // k rows per stage
   static constexpr int ES = (DT == DT_BF16) ? 2 : 4;
   static constexpr int EPC = 16 / ES;                  // elements per 16-byte chunk
+  static constexpr int CPR = 8 / RPT;                  // chunks per 8-column segment
 };
 
-// Loads this thread's block of one operand for the stage starting at row k0:
-// rows k0 + kg*RPT + j, columns col .. col+7. raw[j*CPR + h] is 16 bytes.
-template <int DT, bool VEC>
-__device__ __forceinline__ void load_block(const char* base, int64_t ld, int64_t k0, int64_t k_end,
+// This thread's block of one operand for the stage whose first row is k0:
+// rows k0 .. k0+RPT-1, columns col .. col+7. Rows at or past k_end read as
+// zero (they belong to another example or lie past the matrix).
+template <int DT, bool VEC, bool MASKC>
+__device__ __forceinline__ void load_block(rsrc_t r, int64_t ld_bytes, int64_t k0, int64_t k_end,
                                            int64_t col, int64_t ncol, u32x4 (&raw)[8]) {
   using P = KT<DT>;
-  constexpr int CPR = 8 / P::RPT;  // 16-byte chunks per 8-column segment: 1 (bf16) or 2 (fp32)
 #pragma unroll
   for (int j = 0; j < P::RPT; ++j) {
     const int64_t k = k0 + j;
+    const uint32_t row_off = (uint32_t)(k * ld_bytes);
 #pragma unroll
-    for (int h = 0; h < CPR; ++h) {
-      const int64_t cc = col + h * P::EPC;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (k < k_end && cc < ncol) {
-        const char* row = base + k * ld;
-        v = VEC ? load_chunk16_masked<DT>(row, cc, ncol) : load_chunk_elems<DT>(row, cc, ncol);
-      }
-      raw[j * CPR + h] = v;
+    for (int h = 0; h < P::CPR; ++h) {
+      u32x4 v = buf_chunk<DT, VEC, MASKC>(r, row_off, col + h * P::EPC, ncol);
+      if (k >= k_end) v = u32x4{0u, 0u, 0u, 0u};
+      raw[j * P::CPR + h] = v;
     }
   }
 }
 
-// Scales row j of the block by s[j], transposes to 8 column chunks of RPT
-// consecutive k, and writes them to LDS rows m_row0 .. m_row0+7, chunk kg.
+// Scales row j of the block by s[j], transposes it into 8 column chunks of
+// RPT consecutive k, and writes them to LDS rows m_row0 .. m_row0+7, chunk kg.
 template <int DT, bool SCALE>
 __device__ __forceinline__ void store_block_t(u32x4* lds, u32x4 (&raw)[8], const float (&s)[8],
                                               int m_row0, int kg) {
@@ -109,24 +109,30 @@ __device__ __forceinline__ void store_block_t(u32x4* lds, u32x4 (&raw)[8], const
   }
 }
 
+// One LDS stage into this wave's 4x2 blocks: X rows wm*128 + i*32, Y rows
+// wn*64 + j*32. Lane l supplies row l%32 and 16-byte chunk 2*ks + l/32.
 template <int DT>
 __device__ __forceinline__ void tile_mfma(const u32x4* __restrict__ Xs, const u32x4* __restrict__ Ys,
-                                          f32x16 (&acc)[4][4], int wm, int wn, int lane) {
+                                          f32x16 (&acc)[4][2], int wm, int wn, int lane) {
   const int r32 = lane & 31, half = lane >> 5;
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
     const int c = 2 * ks + half;
-    u32x4 xa[4], yb[4];
+    u32x4 xa[4], yb[2];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int rx = wm * 128 + i * 32 + r32, ry = wn * 128 + i * 32 + r32;
+      const int rx = wm * 128 + i * 32 + r32;
       xa[i] = Xs[rx * 8 + swz(rx, c)];
-      yb[i] = Ys[ry * 8 + swz(ry, c)];
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int ry = wn * 64 + j * 32 + r32;
+      yb[j] = Ys[ry * 8 + swz(ry, c)];
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < 2; ++j) {
         if constexpr (DT == DT_BF16) {
           acc[i][j] = mfma32_bf16(xa[i], yb[j], acc[i][j]);
         } else {
@@ -144,8 +150,8 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
   const GemmArgs& a = *(const GemmArgs*)__builtin_amdgcn_kernarg_segment_ptr();
   (void)args;
   using P = KT<DT>;
-  __shared__ u32x4 Xs[GM_BM * 8];
-  __shared__ u32x4 Ys[GM_BN * 8];
+  __shared__ u32x4 Xs[2][GM_BM * 8];
+  __shared__ u32x4 Ys[2][GM_BN * 8];
   __shared__ float red[GM_THREADS / WAVE];
 
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
@@ -154,8 +160,9 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
   const GemmLayer& L = a.L[l];
   uint32_t rel = item - L.tile_begin;
   const uint32_t ntile = (uint32_t)L.tm * (uint32_t)L.tn;
+  const int64_t K = (int64_t)a.B * a.T;
   int b = 0;
-  int64_t k_begin = 0, k_end = (int64_t)a.B * a.T;
+  int64_t k_begin = 0, k_end = K;
   if (MODE == MODE_NORM) {
     b = (int)(rel / ntile);
     rel -= (uint32_t)b * ntile;
@@ -166,48 +173,65 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
   const int64_t m0 = (int64_t)mt * GM_BM;
   const int64_t n0 = (int64_t)nt * GM_BN;
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w >> 1, wn = w & 1;
-  const int kg = tid >> 5, mg = tid & 31;
-  const char* Xb = (const char*)L.X;
-  const char* Yb = (const char*)L.Y;
-  const int64_t ldx = L.ldx * P::ES, ldy = L.ldy * P::ES;
+  // The wave index goes through readfirstlane so that everything derived
+  // from it (staging role, buffer resource) is known to be wave-uniform.
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = w & 1, wn = w >> 1;
+  // staging role: waves 0..3 stage X, waves 4..7 stage Y
+  const bool stage_x = w < 4;
+  const int st = tid & 255, kg = st >> 5, mg = st & 31;
+  const int64_t ld_bytes = (stage_x ? L.ldx : L.ldy) * P::ES;
+  const rsrc_t rsrc = make_rsrc(stage_x ? L.X : L.Y, (uint64_t)K * ld_bytes);
+  const int64_t col = (stage_x ? m0 : n0) + mg * 8;
+  const int64_t ncol = stage_x ? L.M : L.N;
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
   const int nS = (int)((k_end - k_begin + P::KS - 1) / P::KS);
   const double invT = 1.0 / (double)a.T;
-  u32x4 rx[8], ry[8];
+  u32x4 raw[8];
+  float sc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) sc[j] = 1.f;
+  // Issues the global loads of stage s (and, for X in the clipped sum, the
+  // clip factors of its rows); they complete while the MFMAs of stage s-1 run.
   auto load = [&](int s) {
     const int64_t k0 = k_begin + (int64_t)s * P::KS + kg * P::RPT;
-    load_block<DT, VEC>(Xb, ldx, k0, k_end, m0 + mg * 8, L.M, rx);
-    load_block<DT, VEC>(Yb, ldy, k0, k_end, n0 + mg * 8, L.N, ry);
-  };
-  load(0);
-  for (int s = 0; s < nS; ++s) {
-    float sc[8];
-    if (MODE == MODE_SUM) {
-      const int64_t k0 = k_begin + (int64_t)s * P::KS + kg * P::RPT;
+    // Columns past M/N only feed output rows that are never stored, except in
+    // the direct norm, whose tile sum must not see them.
+    load_block<DT, VEC, MODE == MODE_NORM>(rsrc, ld_bytes, k0, k_end, col, ncol, raw);
+    if (MODE == MODE_SUM && stage_x) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int64_t k = k0 + j;
-        int64_t e = (int64_t)(((double)k + 0.5) * invT);
-        if (e >= a.B) e = a.B - 1;
-        sc[j] = (j < P::RPT) ? a.c[e] : 0.f;
+      for (int j = 0; j < P::RPT; ++j) {
+        int64_t e = (int64_t)(((double)(k0 + j) + 0.5) * invT);
+        e = e < a.B ? e : a.B - 1;
+        sc[j] = a.c[e];
       }
     }
-    __syncthreads();
-    store_block_t<DT, MODE == MODE_SUM>(Xs, rx, sc, mg * 8, kg);
-    store_block_t<DT, false>(Ys, ry, sc, mg * 8, kg);
-    __syncthreads();
+  };
+  auto stage = [&](int buf) {
+    if (stage_x)
+      store_block_t<DT, MODE == MODE_SUM>(Xs[buf], raw, sc, mg * 8, kg);
+    else
+      store_block_t<DT, false>(Ys[buf], raw, sc, mg * 8, kg);
+  };
+
+  load(0);
+  stage(0);
+  __syncthreads();
+  for (int s = 0; s < nS; ++s) {
+    const int buf = s & 1;
     if (s + 1 < nS) load(s + 1);
-    tile_mfma<DT>(Xs, Ys, acc, wm, wn, lane);
+    tile_mfma<DT>(Xs[buf], Ys[buf], acc, wm, wn, lane);
+    if (s + 1 < nS) stage(buf ^ 1);
+    __syncthreads();
   }
 
   if constexpr (MODE == MODE_SUM) {
@@ -218,8 +242,8 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int64_t n = n0 + wn * 128 + j * 32 + (lane & 31);
+      for (int j = 0; j < 2; ++j) {
+        const int64_t n = n0 + wn * 64 + j * 32 + (lane & 31);
         if (n >= L.N) continue;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
@@ -235,14 +259,18 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int e = 0; e < 16; ++e) part += acc[i][j][e] * acc[i][j][e];
     part = wave_sum(part);
     if (lane == 0) red[w] = part;
     __syncthreads();
-    if (tid == 0)
-      a.ws[(int64_t)b * a.slots + L.slot_begin + rel] = (red[0] + red[1]) + (red[2] + red[3]);
+    if (tid == 0) {
+      float t = 0.f;
+#pragma unroll
+      for (int q = 0; q < GM_THREADS / WAVE; ++q) t += red[q];
+      a.ws[(int64_t)b * a.slots + L.slot_begin + rel] = t;
+    }
   }
 }
 
