@@ -179,6 +179,7 @@ dp_status_t dp_clipped_grad_sum_grouped(const dp_linear_t* layers, float* const*
  * high word, tensor_id, step); the four outputs x become uniforms
  * (x + 1/2) 2^-32 and the pairs (0,1), (2,3) give r cos(2 pi u_odd),
  * r sin(2 pi u_odd) with r = sqrt(-2 ln u_even); element j takes output j%4.
+ * The device evaluates the transform in fp32 (relative error ~1e-7 on z).
  * The same (seed, tensor_id, step) reproduces the same noise, so the
  * generator position is the only state to checkpoint. tensor_id and step
  * must be < 2^32. grad is fp32.

@@ -71,35 +71,36 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t nbytes) {
   const uint32_t n = nbytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)nbytes;
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, RSRC_WORD3);
 }
-__device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+// voff: per-lane byte offset; soff: wave-uniform byte offset (an SGPR).
+__device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t voff, uint32_t soff = 0) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
-__device__ __forceinline__ uint32_t buf_load4(rsrc_t r, uint32_t off) {
-  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+__device__ __forceinline__ uint32_t buf_load4(rsrc_t r, uint32_t voff, uint32_t soff = 0) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
 }
-__device__ __forceinline__ uint32_t buf_load2(rsrc_t r, uint32_t off) {
-  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+__device__ __forceinline__ uint32_t buf_load2(rsrc_t r, uint32_t voff, uint32_t soff = 0) {
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
 }
 
-// 16-byte chunk of elements [col, col+EPC) of the row starting at byte
-// offset `row_off`, through a buffer resource. VEC: one 16-byte load (the row
-// is 16-byte aligned); otherwise one load per element. Elements at or past
+// 16-byte chunk of elements [col, col+EPC) of a row, through a buffer
+// resource; the chunk starts at byte voff + soff. VEC: one 16-byte load (the
+// row is 16-byte aligned); otherwise one load per element. Elements at or past
 // `ncol` are zeroed when MASK is set.
 template <int DT, bool VEC, bool MASK>
-__device__ __forceinline__ u32x4 buf_chunk(rsrc_t r, uint32_t row_off, int64_t col, int64_t ncol) {
-  constexpr int EPC = (DT == DT_BF16) ? 8 : 4;
+__device__ __forceinline__ u32x4 buf_chunk(rsrc_t r, uint32_t voff, uint32_t soff, int64_t col,
+                                           int64_t ncol) {
   constexpr int ES = (DT == DT_BF16) ? 2 : 4;
   u32x4 v;
   if constexpr (VEC) {
-    v = buf_load16(r, row_off + (uint32_t)(col * ES));
+    v = buf_load16(r, voff, soff);
   } else if constexpr (DT == DT_BF16) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      v[q] = buf_load2(r, row_off + (uint32_t)((col + 2 * q) * ES)) |
-             (buf_load2(r, row_off + (uint32_t)((col + 2 * q + 1) * ES)) << 16);
+      v[q] = buf_load2(r, voff + (2 * q) * ES, soff) |
+             (buf_load2(r, voff + (2 * q + 1) * ES, soff) << 16);
   } else {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = buf_load4(r, row_off + (uint32_t)((col + q) * ES));
+    for (int q = 0; q < 4; ++q) v[q] = buf_load4(r, voff + q * ES, soff);
   }
   if constexpr (MASK) {
     const int64_t nv = ncol - col;  // valid elements in the chunk (may be <= 0)
@@ -113,7 +114,6 @@ __device__ __forceinline__ u32x4 buf_chunk(rsrc_t r, uint32_t row_off, int64_t c
       }
     }
   }
-  (void)EPC;
   return v;
 }
 

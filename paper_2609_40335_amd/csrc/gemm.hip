@@ -49,21 +49,23 @@ struct KT {
   static constexpr int CPR = 8 / RPT;                  // chunks per 8-column segment
 };
 
-// This thread's block of one operand for the stage whose first row is k0:
-// rows k0 .. k0+RPT-1, columns col .. col+7. Rows at or past k_end read as
-// zero (they belong to another example or lie past the matrix).
-template <int DT, bool VEC, bool MASKC>
-__device__ __forceinline__ void load_block(rsrc_t r, int64_t ld_bytes, int64_t k0, int64_t k_end,
+// This thread's block of one operand: rows r0 .. r0+RPT-1 (r0 relative to
+// the stage) at columns col .. col+7. voff is this lane's byte offset of
+// (r0, col) and soff the wave-uniform byte offset of the stage's first row.
+// ROWMASK: rows at or past `rows_left` (counted from the stage start) read
+// as zero (they belong to the next example).
+template <int DT, bool VEC, bool MASKC, bool ROWMASK>
+__device__ __forceinline__ void load_block(rsrc_t r, uint32_t voff, uint32_t soff,
+                                           uint32_t ld_bytes, int r0, int64_t rows_left,
                                            int64_t col, int64_t ncol, u32x4 (&raw)[8]) {
   using P = KT<DT>;
 #pragma unroll
   for (int j = 0; j < P::RPT; ++j) {
-    const int64_t k = k0 + j;
-    const uint32_t row_off = (uint32_t)(k * ld_bytes);
 #pragma unroll
     for (int h = 0; h < P::CPR; ++h) {
-      u32x4 v = buf_chunk<DT, VEC, MASKC>(r, row_off, col + h * P::EPC, ncol);
-      if (k >= k_end) v = u32x4{0u, 0u, 0u, 0u};
+      u32x4 v = buf_chunk<DT, VEC, MASKC>(r, voff + h * 16, soff + j * ld_bytes,
+                                          col + h * P::EPC, ncol);
+      if (ROWMASK && r0 + j >= rows_left) v = u32x4{0u, 0u, 0u, 0u};
       raw[j * P::CPR + h] = v;
     }
   }
@@ -144,7 +146,13 @@ __device__ __forceinline__ void tile_mfma(const u32x4* __restrict__ Xs, const u3
   }
 }
 
-template <int DT, bool VEC, int MODE>
+// Scaling of the clipped sum: SC_NONE (direct norm), SC_STAGE (rows scaled
+// while staged, any T), SC_ACC (every stage lies inside one example, so the
+// fp32 accumulators are rescaled by c_prev / c_next at example boundaries and
+// by the last factor at the end; examples with c = 0 are skipped).
+enum { SC_NONE = 0, SC_STAGE = 1, SC_ACC = 2 };
+
+template <int DT, bool VEC, int MODE, int SC>
 __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
   // Index the layer table in place in the kernel-argument segment.
   const GemmArgs& a = *(const GemmArgs*)__builtin_amdgcn_kernarg_segment_ptr();
@@ -181,11 +189,12 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
   // staging role: waves 0..3 stage X, waves 4..7 stage Y
   const bool stage_x = w < 4;
   const int st = tid & 255, kg = st >> 5, mg = st & 31;
-  const int64_t ld_bytes = (stage_x ? L.ldx : L.ldy) * P::ES;
+  const uint32_t ld_bytes = (uint32_t)((stage_x ? L.ldx : L.ldy) * P::ES);
   const rsrc_t rsrc = make_rsrc(stage_x ? L.X : L.Y, (uint64_t)K * ld_bytes);
   const int64_t col = (stage_x ? m0 : n0) + mg * 8;
   const int64_t ncol = stage_x ? L.M : L.N;
-
+  const int r0 = kg * P::RPT;                       // this thread's first row in a stage
+  const uint32_t voff = (uint32_t)(r0 * ld_bytes + col * P::ES);
   f32x16 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -196,42 +205,104 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
 
   const int nS = (int)((k_end - k_begin + P::KS - 1) / P::KS);
   const double invT = 1.0 / (double)a.T;
-  u32x4 raw[8];
   float sc[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) sc[j] = 1.f;
-  // Issues the global loads of stage s (and, for X in the clipped sum, the
-  // clip factors of its rows); they complete while the MFMAs of stage s-1 run.
-  auto load = [&](int s) {
-    const int64_t k0 = k_begin + (int64_t)s * P::KS + kg * P::RPT;
-    // Columns past M/N only feed output rows that are never stored, except in
-    // the direct norm, whose tile sum must not see them.
-    load_block<DT, VEC, MODE == MODE_NORM>(rsrc, ld_bytes, k0, k_end, col, ncol, raw);
-    if (MODE == MODE_SUM && stage_x) {
+  // Issues the global loads of stage s into r; with SC_STAGE also fetches
+  // the clip factors of this thread's rows.
+  auto load = [&](int s, u32x4 (&r)[8]) {
+    const int64_t ks0 = k_begin + (int64_t)s * P::KS;   // first row of the stage
+    // Rows past the matrix read as zero through the buffer bounds; columns
+    // past M/N only feed output rows that are never stored, except in the
+    // direct norm, whose tile sum must not see them (nor the next example).
+    load_block<DT, VEC, MODE == MODE_NORM, MODE == MODE_NORM>(
+        rsrc, voff, (uint32_t)(ks0 * ld_bytes), ld_bytes, r0, k_end - ks0, col, ncol, r);
+    if (SC == SC_STAGE && stage_x) {
 #pragma unroll
       for (int j = 0; j < P::RPT; ++j) {
-        int64_t e = (int64_t)(((double)(k0 + j) + 0.5) * invT);
+        int64_t e = (int64_t)(((double)(ks0 + r0 + j) + 0.5) * invT);
         e = e < a.B ? e : a.B - 1;
         sc[j] = a.c[e];
       }
     }
   };
-  auto stage = [&](int buf) {
+  auto stage = [&](int buf, u32x4 (&r)[8]) {
     if (stage_x)
-      store_block_t<DT, MODE == MODE_SUM>(Xs[buf], raw, sc, mg * 8, kg);
+      store_block_t<DT, SC == SC_STAGE>(Xs[buf], r, sc, mg * 8, kg);
     else
-      store_block_t<DT, false>(Ys[buf], raw, sc, mg * 8, kg);
+      store_block_t<DT, false>(Ys[buf], r, sc, mg * 8, kg);
   };
 
-  load(0);
-  stage(0);
-  __syncthreads();
-  for (int s = 0; s < nS; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nS) load(s + 1);
+  // SC_ACC bookkeeping (wave-uniform): factor of the accumulated examples.
+  const int spe = (SC == SC_ACC) ? a.T / P::KS : 1;  // stages per example
+  float c_acc = 0.f;                                  // 0: nothing accumulated yet
+  bool skip = false;
+  auto compute = [&](int s, int buf) {
+    if constexpr (SC == SC_ACC) {
+      if (s % spe == 0) {
+        const float ce = a.c[s / spe];
+        skip = !(ce != 0.f);
+        if (!skip) {
+          if (c_acc != 0.f) {
+            const float f = c_acc / ce;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+              for (int j = 0; j < 2; ++j) acc[i][j] *= f;
+          }
+          c_acc = ce;
+        }
+      }
+      if (skip) return;
+    }
     tile_mfma<DT>(Xs[buf], Ys[buf], acc, wm, wn, lane);
-    if (s + 1 < nS) stage(buf ^ 1);
+  };
+
+  if constexpr (SC == SC_ACC) {
+    // Two register sets: the loads of stage s+2 are in flight while stage s
+    // is multiplied and stage s+1 is transposed into the other LDS buffer.
+    // The scheduling fences keep each phase's instructions in place so that
+    // the compiler does not hoist loads across phases (which costs registers).
+    u32x4 rA[8], rB[8];
+    load(0, rA);
+    if (nS > 1) load(1, rB);
+    stage(0, rA);
     __syncthreads();
+    for (int s = 0; s < nS; s += 2) {
+      if (s + 2 < nS) load(s + 2, rA);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(s, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (s + 1 < nS) stage(1, rB);
+      __syncthreads();
+      if (s + 1 >= nS) break;
+      if (s + 3 < nS) load(s + 3, rB);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(s + 1, 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (s + 2 < nS) stage(0, rA);
+      __syncthreads();
+    }
+  } else {
+    // One register set (these variants need more registers per stage): the
+    // loads of stage s+1 are in flight while stage s is multiplied.
+    u32x4 rA[8];
+    load(0, rA);
+    stage(0, rA);
+    __syncthreads();
+    for (int s = 0; s < nS; ++s) {
+      const int buf = s & 1;
+      if (s + 1 < nS) load(s + 1, rA);
+      compute(s, buf);
+      if (s + 1 < nS) stage(buf ^ 1, rA);
+      __syncthreads();
+    }
+  }
+  if constexpr (SC == SC_ACC) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] *= c_acc;
   }
 
   if constexpr (MODE == MODE_SUM) {
@@ -274,16 +345,31 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
   }
 }
 
+template <int DT, bool VEC, int MODE>
+static void launch_sc(const GemmArgs& a, int sc, hipStream_t s) {
+  const dim3 g(a.n_items), blk(GM_THREADS);
+  if constexpr (MODE == MODE_NORM) {
+    hipLaunchKernelGGL((kt_gemm_kernel<DT, VEC, MODE, SC_NONE>), g, blk, 0, s, a);
+  } else {
+    if (sc == SC_ACC)
+      hipLaunchKernelGGL((kt_gemm_kernel<DT, VEC, MODE, SC_ACC>), g, blk, 0, s, a);
+    else
+      hipLaunchKernelGGL((kt_gemm_kernel<DT, VEC, MODE, SC_STAGE>), g, blk, 0, s, a);
+  }
+}
+
 template <int MODE>
 static hipError_t launch_kt(const GemmArgs& a, int dt, bool vec, hipStream_t s) {
   if (a.n_items == 0) return hipSuccess;
-  const dim3 g(a.n_items), blk(GM_THREADS);
+  // The accumulator form needs every K-stage inside one example.
+  const int ks = dt == DT_BF16 ? KT<DT_BF16>::KS : KT<DT_F32>::KS;
+  const int sc = MODE == MODE_NORM ? SC_NONE : (a.T % ks == 0 ? SC_ACC : SC_STAGE);
   if (dt == DT_BF16) {
-    if (vec) hipLaunchKernelGGL((kt_gemm_kernel<DT_BF16, true, MODE>), g, blk, 0, s, a);
-    else hipLaunchKernelGGL((kt_gemm_kernel<DT_BF16, false, MODE>), g, blk, 0, s, a);
+    if (vec) launch_sc<DT_BF16, true, MODE>(a, sc, s);
+    else launch_sc<DT_BF16, false, MODE>(a, sc, s);
   } else {
-    if (vec) hipLaunchKernelGGL((kt_gemm_kernel<DT_F32, true, MODE>), g, blk, 0, s, a);
-    else hipLaunchKernelGGL((kt_gemm_kernel<DT_F32, false, MODE>), g, blk, 0, s, a);
+    if (vec) launch_sc<DT_F32, true, MODE>(a, sc, s);
+    else launch_sc<DT_F32, false, MODE>(a, sc, s);
   }
   return hipGetLastError();
 }

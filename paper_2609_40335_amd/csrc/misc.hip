@@ -37,17 +37,19 @@ __device__ __forceinline__ void philox4x32_10(uint32_t (&c)[4], uint32_t k0, uin
 
 // Four standard normals of Philox block `blk` of one tensor. Uniforms are
 // u = (x + 1/2) 2^-32; Box-Muller pairs (u0,u1) and (u2,u3) give
-// r cos(2 pi u_odd), r sin(2 pi u_odd) with r = sqrt(-2 ln u_even). The
-// radius is evaluated in double (u is exact there), the angle in float.
+// r cos(2 pi u_odd), r sin(2 pi u_odd) with r = sqrt(-2 ln u_even). In fp32
+// the conversion of x is exact below 2^24 (the far tail, small u) and rounds x
+// to 24 bits above, which moves ln u by at most 2^-24; the angle uses
+// sincospi on 2u.
 __device__ __forceinline__ void gauss4(uint64_t blk, uint64_t seed, uint32_t tensor_id,
                                        uint32_t step, float (&z)[4]) {
   uint32_t c[4] = {(uint32_t)blk, (uint32_t)(blk >> 32), tensor_id, step};
   philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
-    const double u = ((double)c[2 * p] + 0.5) * 0x1p-32;
-    const float r = (float)sqrt(-2.0 * log(u));
-    const float twice_u = (float)(((double)c[2 * p + 1] + 0.5) * 0x1p-31);
+    const float u = ((float)c[2 * p] + 0.5f) * 0x1p-32f;
+    const float r = sqrtf(-2.f * logf(u));
+    const float twice_u = ((float)c[2 * p + 1] + 0.5f) * 0x1p-31f;
     float sn, cs;
     sincospif(twice_u, &sn, &cs);
     z[2 * p] = r * cs;
