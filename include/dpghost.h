@@ -26,6 +26,9 @@
  *    *_workspace() function; its contents need no initialisation and are
  *    dead after the call's kernels finish. Two calls in flight at once must
  *    not share a workspace.
+ *  - Operands are addressed with 32-bit byte offsets: every operand matrix
+ *    (rows x row stride x element size) must span less than 4 GiB, else
+ *    DP_EUNSUPPORTED.
  *  - Errors: arguments are validated on the host before any HIP call. A
  *    NULL required pointer, a non-positive size, a stride smaller than its
  *    row width, an unknown dtype or a too-small workspace returns DP_EINVAL;
@@ -131,7 +134,7 @@ dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t 
  * H [B,T,d] (ldh) are the hidden states entering the head; Gz [B,T,V]
  * (row stride ldz >= V) the logit gradients.
  * ------------------------------------------------------------------- */
-size_t dp_tied_cross_term_workspace(int B, int T);
+size_t dp_tied_cross_term_workspace(int B, int T, int d);
 dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, const void* H,
                                int64_t ldh, const void* Gz, int64_t ldz, int B, int T, int V,
                                int d, dp_dtype_t dt, float scale, float* out, int accumulate,

@@ -47,6 +47,11 @@ inline int bits_for(int64_t n_values) {  // bits to index n_values distinct valu
   return b;
 }
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+inline int esize(dp_dtype_t dt) { return dt == DP_BF16 ? 2 : 4; }
+// Kernels address operands through buffer resources with 32-bit byte offsets.
+inline bool span_ok(int64_t rows, int64_t ld, dp_dtype_t dt) {
+  return rows * ld * esize(dt) < (int64_t(1) << 32);
+}
 
 // ------------------------------------------------------------------ planning
 constexpr int KG_SPLIT = 4096;  // G feature ranges longer than this are chunked
@@ -135,6 +140,8 @@ dp_status_t check_layers(const dp_linear_t* layers, int n, int B, int T, dp_dtyp
       return fail(DP_EINVAL, "layer %d: row stride smaller than row width", i);
     if (L.algo < DP_NORM_AUTO || L.algo > DP_NORM_DIRECT)
       return fail(DP_EINVAL, "layer %d: unknown algo %d", i, L.algo);
+    if (!span_ok((int64_t)B * T, L.lda, dt) || !span_ok((int64_t)B * T, L.ldg, dt))
+      return fail(DP_EUNSUPPORTED, "layer %d: an operand spans 4 GiB or more", i);
   }
   return DP_OK;
 }
@@ -322,10 +329,10 @@ dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t 
                     "finish launch");
 }
 
-size_t dp_tied_cross_term_workspace(int B, int T) {
-  if (B <= 0 || T <= 0) return 0;
+size_t dp_tied_cross_term_workspace(int B, int T, int d) {
+  if (B <= 0 || T <= 0 || d <= 0) return 0;
   const int64_t nt = ceil_div(T, dpg::GR_TM);
-  return align_up((size_t)B * nt * nt * 4);
+  return align_up((size_t)B * nt * nt * ceil_div(d, dpg::CR_FCHUNK) * 4);
 }
 
 dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, const void* H,
@@ -339,7 +346,9 @@ dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, 
   if (!dtype_ok(dt)) return fail(DP_EINVAL, "unknown dtype %d", (int)dt);
   if (!std::isfinite(scale)) return fail(DP_EINVAL, "scale must be finite");
   if (T > 65536) return fail(DP_EUNSUPPORTED, "T = %d exceeds 65536", T);
-  const size_t need = dp_tied_cross_term_workspace(B, T);
+  if (!span_ok(T, lde, dt) || !span_ok(T, ldh, dt) || !span_ok(T, ldz, dt))
+    return fail(DP_EUNSUPPORTED, "one example's rows of an operand span 4 GiB or more");
+  const size_t need = dp_tied_cross_term_workspace(B, T, d);
   if (!workspace || workspace_bytes < need)
     return fail(DP_EINVAL, "workspace of %zu bytes needed", need);
   dpg::CrossArgs a{};
@@ -347,7 +356,8 @@ dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, 
   a.lde = lde; a.ldh = ldh; a.ldz = ldz;
   a.B = B; a.T = T; a.V = V; a.d = d;
   a.n_t = (int)ceil_div(T, dpg::GR_TM);
-  a.slots = a.n_t * a.n_t;
+  a.n_fc = (int)ceil_div(d, dpg::CR_FCHUNK);
+  a.slots = a.n_t * a.n_t * a.n_fc;
   a.ws = static_cast<float*>(workspace);
   const bool vec = vec_ok(dE, lde, dt) && vec_ok(H, ldh, dt);
   hipStream_t s = as_stream(stream);

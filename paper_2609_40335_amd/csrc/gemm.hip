@@ -234,13 +234,18 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
   };
 
   // SC_ACC bookkeeping (wave-uniform): factor of the accumulated examples.
+  // The factor of the next example is fetched one example ahead so that no
+  // stage waits on it.
   const int spe = (SC == SC_ACC) ? a.T / P::KS : 1;  // stages per example
   float c_acc = 0.f;                                  // 0: nothing accumulated yet
+  float c_next = (SC == SC_ACC) ? a.c[0] : 0.f;
   bool skip = false;
   auto compute = [&](int s, int buf) {
     if constexpr (SC == SC_ACC) {
       if (s % spe == 0) {
-        const float ce = a.c[s / spe];
+        const int e = s / spe;
+        const float ce = c_next;
+        if (e + 1 < a.B) c_next = a.c[e + 1];
         skip = !(ce != 0.f);
         if (!skip) {
           if (c_acc != 0.f) {
@@ -307,24 +312,57 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
 
   if constexpr (MODE == MODE_SUM) {
     // 32x32 block (i,j): lane l holds column l%32 and, for accumulator e,
-    // row (e/4)*8 + (l/32)*4 + e%4.
+    // row (e/4)*8 + (l/32)*4 + e%4. Stores bypass L2 residency (the output
+    // is written once) so that they do not evict operand rows.
     float* out = L.out;
     const int64_t ldo = L.ldo;
+    const int mw = (int)m0 + wm * 128 + (lane >> 5) * 4;  // row of e = 0 in block i = 0
+    const int nw = (int)n0 + wn * 64 + (lane & 31);         // column in block j = 0
+    const bool full = m0 + GM_BM <= L.M && n0 + GM_BN <= L.N;
+    if (a.transpose) {
+      // out[n][m]: the 4 accumulators e = 4g..4g+3 are 4 consecutive rows m.
+      const bool vec4 = full && (ldo & 3) == 0 && (((uintptr_t)out) & 15) == 0;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int64_t n = n0 + wn * 64 + j * 32 + (lane & 31);
-        if (n >= L.N) continue;
+        for (int j = 0; j < 2; ++j) {
+          const int n = nw + j * 32;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int64_t m = m0 + wm * 128 + i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-          if (m < L.M) {
-            const int64_t idx = a.transpose ? n * ldo + m : m * ldo + n;
-            out[idx] = a.accumulate ? out[idx] + acc[i][j][e] : acc[i][j][e];
+          for (int g = 0; g < 4; ++g) {
+            const int m = mw + i * 32 + g * 8;
+            float* p = out + (int64_t)n * ldo + m;
+            if (vec4) {
+              f32x4 v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                         acc[i][j][4 * g + 3]};
+              if (a.accumulate) v += *(const f32x4*)p;
+              __builtin_nontemporal_store(v, (f32x4*)p);
+            } else if (n < L.N) {
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (m + r < L.M) p[r] = a.accumulate ? p[r] + acc[i][j][4 * g + r]
+                                                     : acc[i][j][4 * g + r];
+            }
           }
         }
-      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int n = nw + j * 32;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int m = mw + i * 32 + (e >> 2) * 8 + (e & 3);
+            float* p = out + (int64_t)m * ldo + n;
+            if (full) {
+              const float v = a.accumulate ? *p + acc[i][j][e] : acc[i][j][e];
+              __builtin_nontemporal_store(v, p);
+            } else if (m < L.M && n < L.N) {
+              *p = a.accumulate ? *p + acc[i][j][e] : acc[i][j][e];
+            }
+          }
+        }
+    }
   } else {
     float part = 0.f;
 #pragma unroll

@@ -69,7 +69,7 @@ __device__ __forceinline__ void block_rows(int w, int (&ra)[4], int (&rb)[4], fl
 // both operands carry the same features in the same MFMA k-slots.
 template <int DT, int NB>
 __device__ __forceinline__ void stage_mfma(const u32x4* __restrict__ lds, const int (&ra)[4],
-                                           const int (&rb)[4], f32x16 (&acc)[4], int lane) {
+                                           const int (&rb)[4], f32x16 (&acc)[NB], int lane) {
   const int r32 = lane & 31, half = lane >> 5;
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
@@ -94,107 +94,132 @@ __device__ __forceinline__ void stage_mfma(const u32x4* __restrict__ lds, const 
 // Entry i (0..7) of a thread is LDS row (tid/8) + 32*i, chunk tid%8; entries
 // 0..3 are rows of T-tile ti, entries 4..7 rows of T-tile tj. Stage s < nX
 // reads features [s*KS, ...) of X up to column x1; later stages read features
-// [y0 + (s-nX)*KS, ...) of Y up to column y1.
+// [y0 + (s-nX)*KS, ...) of Y up to column y1. The buffer resources span one
+// example's T rows, so rows past T read as zero; per-row offsets are
+// wave-uniform (SGPR) and only the lane's own (row, chunk) offset is a VGPR.
 template <int DT, bool VEC>
 struct TileStream {
   static constexpr int EPC = (DT == DT_BF16) ? 8 : 4;
   static constexpr int KS = 8 * EPC;
   static constexpr int ES = (DT == DT_BF16) ? 2 : 4;
-  const char* X;
-  const char* Y;
-  int64_t ldx, ldy;           // row strides in bytes
-  int64_t row_i, row_j;       // global row of entry 0 (tile ti) and entry 4 (tile tj)
-  int T_end_i, T_end_j;       // entries i with 32*i (+ first row) below these are valid
-  int c;                      // this thread's chunk within a row
+  rsrc_t rx, ry;
+  uint32_t ldx, ldy;           // row strides in bytes
+  uint32_t vxi, vxj, vyi, vyj; // lane offsets of entry 0 / entry 4 in X and Y
+  int c;                       // this thread's chunk within a row
   int nX;
   int64_t x1, y0, y1;
 
-  // VEC: rows are 16-byte aligned and their stride is a whole number of
-  // chunks, so every chunk is one 16-byte load (elements past the valid
-  // columns are zeroed in registers). Otherwise elements are loaded one at a
-  // time.
-  __device__ __forceinline__ void prefetch(int s, u32x4 (&pre)[8], int nent) const {
+  template <int NENT>
+  __device__ __forceinline__ void prefetch(int s, u32x4 (&pre)[NENT]) const {
     const bool inX = s < nX;
-    const char* base = inX ? X : Y;
-    const int64_t ld = inX ? ldx : ldy;
-    const int64_t col = inX ? (int64_t)s * KS + c * EPC : y0 + (int64_t)(s - nX) * KS + c * EPC;
+    const rsrc_t r = inX ? rx : ry;
+    const uint32_t ld = inX ? ldx : ldy;
+    const int64_t c0 = inX ? (int64_t)s * KS : y0 + (int64_t)(s - nX) * KS;  // stage column
     const int64_t ncol = inX ? x1 : y1;
+    const uint32_t vi = inX ? vxi : vyi, vj = inX ? vxj : vyj;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const bool lo = i < 4;
-      const int k = lo ? i : i - 4;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (i < nent && 32 * k < (lo ? T_end_i : T_end_j) && col < ncol) {
-        const char* row = base + ((lo ? row_i : row_j) + 32 * k) * ld;
-        v = VEC ? load_chunk16_masked<DT>(row, col, ncol) : load_chunk_elems<DT>(row, col, ncol);
-      }
-      pre[i] = v;
+    for (int i = 0; i < NENT; ++i) {
+      const uint32_t soff = (uint32_t)(c0 * ES) + (uint32_t)(32 * (i & 3)) * ld;
+      pre[i] = buf_chunk<DT, VEC, true>(r, i < 4 ? vi : vj, soff, c0 + c * EPC, ncol);
     }
   }
 };
 
-__device__ __forceinline__ void store_stage(u32x4* lds, const u32x4 (&pre)[8], int tid, int nent) {
+template <int NENT>
+__device__ __forceinline__ void store_stage(u32x4* lds, const u32x4 (&pre)[NENT], int tid) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    if (i < nent) {
-      const int r = (tid >> 3) + 32 * i, c = tid & 7;
-      lds[r * 8 + swz(r, c)] = pre[i];
-    }
+  for (int i = 0; i < NENT; ++i) {
+    const int r = (tid >> 3) + 32 * i, c = tid & 7;
+    lds[r * 8 + swz(r, c)] = pre[i];
   }
 }
 
-template <int DT, bool VEC, int PAT>
-__device__ float gram_item(const GramLayer& L, int b, int T, int ti, int tj, int chunk,
+// LDS of one stage: a diagonal pair streams 128 rows, an off-diagonal 256.
+template <int PAT> struct PatRows { static constexpr int ROWS = PAT == PAT_OFF ? 2 * GR_TM : GR_TM; };
+
+template <int DT, bool VEC, int PAT, int PF>
+__device__ __forceinline__ float gram_item(const GramLayer& L, int b, int T, int ti, int tj, int chunk,
                            u32x4* lds) {
   constexpr int NB = PatNB<PAT>::NB;
+  constexpr int ROWS = PatRows<PAT>::ROWS;
+  constexpr int NENT = ROWS / 32;  // 16-byte chunks per thread per stage
   using TS = TileStream<DT, VEC>;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int nent = (ti == tj) ? 4 : 8;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   TS ts;
-  ts.X = (const char*)L.A;
-  ts.Y = (const char*)L.G;
-  ts.ldx = L.lda * TS::ES;
-  ts.ldy = L.ldg * TS::ES;
+  const uint64_t ex_rows = (uint64_t)b * T;
+  ts.ldx = (uint32_t)(L.lda * TS::ES);
+  ts.ldy = (uint32_t)(L.ldg * TS::ES);
+  ts.rx = make_rsrc((const char*)L.A + ex_rows * ts.ldx, (uint64_t)T * ts.ldx);
+  ts.ry = make_rsrc((const char*)L.G + ex_rows * ts.ldy, (uint64_t)T * ts.ldy);
   ts.c = tid & 7;
   ts.x1 = L.d_in;
   ts.y0 = (int64_t)L.g0 + (int64_t)chunk * L.kg;
   ts.y1 = ts.y0 + L.kg < L.g1 ? ts.y0 + L.kg : L.g1;
-  ts.nX = (L.d_in + TS::KS - 1) / TS::KS;
+  ts.nX = ((L.d_in + TS::KS - 1) / TS::KS + 1) & ~1;  // padded to even
   const int nY = (int)((ts.y1 - ts.y0 + TS::KS - 1) / TS::KS);
-  const int r0 = tid >> 3;
-  ts.row_i = (int64_t)b * T + ti * GR_TM + r0;
-  ts.row_j = (int64_t)b * T + tj * GR_TM + r0;
-  ts.T_end_i = T - (ti * GR_TM + r0);
-  ts.T_end_j = T - (tj * GR_TM + r0);
+  const uint32_t r0 = tid >> 3, cb = (tid & 7) * 16;
+  ts.vxi = (ti * GR_TM + r0) * ts.ldx + cb;
+  ts.vxj = (tj * GR_TM + r0) * ts.ldx + cb;
+  ts.vyi = (ti * GR_TM + r0) * ts.ldy + cb;
+  ts.vyj = (tj * GR_TM + r0) * ts.ldy + cb;
 
   int ra[4], rb[4];
   float wt[4];
   block_rows<PAT>(w, ra, rb, wt);
-  f32x16 accP[4], accQ[4];
+  f32x16 accP[NB], accQ[NB];
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int j = 0; j < NB; ++j)
 #pragma unroll
     for (int e = 0; e < 16; ++e) { accP[j][e] = 0.f; accQ[j][e] = 0.f; }
 
-  // Features of A into P, then this chunk's features of G into Q; the
-  // prefetch of stage s+1 is in flight while stage s is multiplied.
   const int n = ts.nX + nY;
-  u32x4 pre[8];
-  ts.prefetch(0, pre, nent);
-  for (int s = 0; s < ts.nX; ++s) {
+  u32x4* buf0 = lds;
+  u32x4* buf1 = lds + ROWS * 8;
+  if constexpr (PF == 2) {
+    // Two register sets and two LDS buffers: the loads of stage s+2 are in
+    // flight while stage s is multiplied and stage s+1 is stored. Even
+    // stages use set A and buffer 0. The A phase is padded to an even number
+    // of stages (padding stages read masked zeros), so both phases start even
+    // and each keeps its own accumulators in its own loop.
+    u32x4 pA[NENT], pB[NENT];
+    auto phase = [&](int s_begin, int s_end, f32x16 (&acc)[NB]) {
+      for (int s = s_begin; s < s_end; s += 2) {
+        if (s + 2 < n) ts.template prefetch<NENT>(s + 2, pA);
+        stage_mfma<DT, NB>(buf0, ra, rb, acc, lane);
+        if (s + 1 < n) store_stage<NENT>(buf1, pB, tid);
+        __syncthreads();
+        if (s + 1 >= s_end) break;
+        if (s + 3 < n) ts.template prefetch<NENT>(s + 3, pB);
+        stage_mfma<DT, NB>(buf1, ra, rb, acc, lane);
+        if (s + 2 < n) store_stage<NENT>(buf0, pA, tid);
+        __syncthreads();
+      }
+    };
+    ts.template prefetch<NENT>(0, pA);
+    if (n > 1) ts.template prefetch<NENT>(1, pB);
+    store_stage<NENT>(buf0, pA, tid);
     __syncthreads();
-    store_stage(lds, pre, tid, nent);
+    phase(0, ts.nX, accP);
+    phase(ts.nX, n, accQ);
+  } else {
+    // One register set, two LDS buffers: the loads of stage s+1 are in
+    // flight while stage s is multiplied.
+    u32x4 pA[NENT];
+    auto phase = [&](int s_begin, int s_end, f32x16 (&acc)[NB]) {
+      for (int s = s_begin; s < s_end; ++s) {
+        if (s + 1 < n) ts.template prefetch<NENT>(s + 1, pA);
+        stage_mfma<DT, NB>((s & 1) ? buf1 : buf0, ra, rb, acc, lane);
+        if (s + 1 < n) store_stage<NENT>((s & 1) ? buf0 : buf1, pA, tid);
+        __syncthreads();
+      }
+    };
+    ts.template prefetch<NENT>(0, pA);
+    store_stage<NENT>(buf0, pA, tid);
     __syncthreads();
-    if (s + 1 < n) ts.prefetch(s + 1, pre, nent);
-    stage_mfma<DT, NB>(lds, ra, rb, accP, lane);
-  }
-  for (int s = ts.nX; s < n; ++s) {
-    __syncthreads();
-    store_stage(lds, pre, tid, nent);
-    __syncthreads();
-    if (s + 1 < n) ts.prefetch(s + 1, pre, nent);
-    stage_mfma<DT, NB>(lds, ra, rb, accQ, lane);
+    phase(0, ts.nX, accP);
+    phase(ts.nX, n, accQ);
   }
   float part = 0.f;
 #pragma unroll
@@ -207,13 +232,16 @@ __device__ float gram_item(const GramLayer& L, int b, int T, int ti, int tj, int
   return part;
 }
 
-template <int DT, bool VEC>
+// SINGLE: every example fits one T-tile (T <= 128), so only the diagonal
+// patterns exist; fewer registers and a 2 x 16 KB LDS footprint let three
+// workgroups share a CU.
+template <int DT, bool VEC, bool SINGLE>
 __global__ __launch_bounds__(GR_THREADS) void gram_norm_kernel(GramArgs args) {
   // Index the layer table in place in the kernel-argument segment (the only
   // explicit argument sits at offset 0) instead of copying it to the stack.
   const GramArgs& a = *(const GramArgs*)__builtin_amdgcn_kernarg_segment_ptr();
   (void)args;
-  __shared__ u32x4 lds[GR_ROWS * 8];
+  __shared__ u32x4 lds[2 * (SINGLE ? GR_TM : GR_ROWS) * 8];
   __shared__ float red[GR_THREADS / WAVE];
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
   int l = 0;
@@ -228,15 +256,23 @@ __global__ __launch_bounds__(GR_THREADS) void gram_norm_kernel(GramArgs args) {
   int ti = 0, rem = pair;
   while (rem >= a.n_t - ti) { rem -= a.n_t - ti; ++ti; }
   const int tj = ti + rem;
-  const int w = threadIdx.x >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
   float part;
-  if (ti != tj)
-    part = gram_item<DT, VEC, PAT_OFF>(L, b, a.T, ti, tj, chunk, lds);
-  else if (w < 2)
-    part = gram_item<DT, VEC, PAT_D1>(L, b, a.T, ti, tj, chunk, lds);
-  else
-    part = gram_item<DT, VEC, PAT_D2>(L, b, a.T, ti, tj, chunk, lds);
+  // Prefetch depth 2 where registers allow (one 128-row tile), else 1.
+  if constexpr (SINGLE) {
+    if (w < 2)
+      part = gram_item<DT, VEC, PAT_D1, 2>(L, b, a.T, ti, tj, chunk, lds);
+    else
+      part = gram_item<DT, VEC, PAT_D2, 2>(L, b, a.T, ti, tj, chunk, lds);
+  } else {
+    if (ti != tj)
+      part = gram_item<DT, VEC, PAT_OFF, 1>(L, b, a.T, ti, tj, chunk, lds);
+    else if (w < 2)
+      part = gram_item<DT, VEC, PAT_D1, 1>(L, b, a.T, ti, tj, chunk, lds);
+    else
+      part = gram_item<DT, VEC, PAT_D2, 1>(L, b, a.T, ti, tj, chunk, lds);
+  }
   part = wave_sum(part);
   if ((threadIdx.x & 63) == 0) red[w] = part;
   __syncthreads();
@@ -245,29 +281,36 @@ __global__ __launch_bounds__(GR_THREADS) void gram_norm_kernel(GramArgs args) {
         (red[0] + red[1]) + (red[2] + red[3]);
 }
 
+// Work item = (example, T-tile pair (ti, tj), chunk of CR_FCHUNK features).
+// The reduction is linear in the features, so chunks add up exactly.
 template <int DT, bool VEC>
 __global__ __launch_bounds__(GR_THREADS) void tied_cross_kernel(CrossArgs a) {
   __shared__ u32x4 lds[GR_ROWS * 8];
   __shared__ float red[GR_THREADS / WAVE];
   using TS = TileStream<DT, VEC>;
+  constexpr int EPC = TS::EPC, KS = TS::KS, ES = TS::ES;
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
   const int b = (int)(item / (uint32_t)a.slots);
-  const int pair = (int)(item - (uint32_t)b * a.slots);
+  const int slot = (int)(item - (uint32_t)b * a.slots);
+  const int pair = slot / a.n_fc, fc = slot - pair * a.n_fc;
   const int ti = pair / a.n_t, tj = pair - ti * a.n_t;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int T = a.T;
 
-  // LDS rows 0..127: dE rows of tile ti; rows 128..255: H rows of tile tj.
-  // Both come in the same stage: "X" is dE for entries 0..3 and H for 4..7.
-  constexpr int EPC = TS::EPC, KS = TS::KS, ES = TS::ES;
-  const int r0 = tid >> 3, c = tid & 7;
-  const int64_t row_i = (int64_t)b * T + ti * GR_TM + r0;
-  const int64_t row_j = (int64_t)b * T + tj * GR_TM + r0;
-  const int end_i = T - (ti * GR_TM + r0), end_j = T - (tj * GR_TM + r0);
-  const char* Eb = (const char*)a.E;
-  const char* Hb = (const char*)a.H;
-  const int64_t lde = a.lde * ES, ldh = a.ldh * ES;
-  const int nX = (a.d + KS - 1) / KS;
+  // LDS rows 0..127: dE rows of tile ti; rows 128..255: H rows of tile tj,
+  // both loaded in the same stage through per-example buffer resources.
+  const uint64_t ex_rows = (uint64_t)b * T;
+  const uint32_t lde = (uint32_t)(a.lde * ES), ldh = (uint32_t)(a.ldh * ES);
+  const rsrc_t rE = make_rsrc((const char*)a.E + ex_rows * lde, (uint64_t)T * lde);
+  const rsrc_t rH = make_rsrc((const char*)a.H + ex_rows * ldh, (uint64_t)T * ldh);
+  const uint32_t r0 = tid >> 3, c = tid & 7;
+  const uint32_t ve = (ti * GR_TM + r0) * lde + c * 16;
+  const uint32_t vh = (tj * GR_TM + r0) * ldh + c * 16;
+  const int64_t f0 = (int64_t)fc * CR_FCHUNK;
+  const int64_t f1 = f0 + CR_FCHUNK < a.d ? f0 + CR_FCHUNK : a.d;
+  const int n = (int)((f1 - f0 + KS - 1) / KS);
+
   int ra[4], rb[4];
   float wt[4];
   block_rows<PAT_OFF>(w, ra, rb, wt);
@@ -277,52 +320,49 @@ __global__ __launch_bounds__(GR_THREADS) void tied_cross_kernel(CrossArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[j][e] = 0.f;
 
-  const int n = nX;
   u32x4 pre[8];
   auto fetch = [&](int s) {
-    const int64_t col = (int64_t)s * KS + c * EPC;
+    const int64_t c0 = f0 + (int64_t)s * KS;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      u32x4 v = {0u, 0u, 0u, 0u};
       const bool lo = i < 4;
-      const int k = lo ? i : i - 4;
-      if (col < a.d && 32 * k < (lo ? end_i : end_j)) {
-        const char* row = lo ? Eb + (row_i + 32 * k) * lde : Hb + (row_j + 32 * k) * ldh;
-        v = VEC ? load_chunk16_masked<DT>(row, col, a.d) : load_chunk_elems<DT>(row, col, a.d);
-      }
-      pre[i] = v;
+      const uint32_t soff = (uint32_t)(c0 * ES) + (uint32_t)(32 * (i & 3)) * (lo ? lde : ldh);
+      pre[i] = buf_chunk<DT, VEC, true>(lo ? rE : rH, lo ? ve : vh, soff, c0 + c * EPC, f1);
     }
   };
   fetch(0);
   for (int s = 0; s < n; ++s) {
     __syncthreads();
-    store_stage(lds, pre, tid, 8);
+    store_stage<8>(lds, pre, tid);
     __syncthreads();
     if (s + 1 < n) fetch(s + 1);
     stage_mfma<DT, 4>(lds, ra, rb, acc, lane);
   }
 
-  // Block j holds P[t, s] = <dE_t, H_s>: lane l has column s = l%32 and, for
-  // accumulator e, row (e/4)*8 + (l/32)*4 + e%4 of the 32x32 MFMA output.
+  // Block j holds P[t, s] = <dE_t, H_s> (this feature chunk): lane l has
+  // column s = l%32 and, for accumulator e, row (e/4)*8 + (l/32)*4 + e%4 of
+  // the 32x32 MFMA output. Logit gradients are gathered through a buffer
+  // resource spanning this example's rows of Gz.
+  const uint32_t ldz = (uint32_t)(a.ldz * ES);
+  const rsrc_t rZ = make_rsrc((const char*)a.Gz + ex_rows * ldz, (uint64_t)T * ldz);
   float part = 0.f;
-  const int64_t ldz = a.ldz;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int t0 = ti * GR_TM + ra[j] + (lane >> 5) * 4;
     const int s = tj * GR_TM + (rb[j] - GR_TM) + (lane & 31);
     if (s >= T) continue;
-    const int64_t zrow = ((int64_t)b * T + s) * ldz;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const int t = t0 + (e >> 2) * 8 + (e & 3);
       if (t < T) {
-        const uint32_t v = (uint32_t)a.ids[(int64_t)b * T + t];
+        const uint32_t v = (uint32_t)a.ids[ex_rows + t];
         if (v >= (uint32_t)a.V) continue;  // invalid id: contributes nothing
+        const uint32_t off = (uint32_t)s * ldz + v * ES;
         float g;
         if constexpr (DT == DT_BF16)
-          g = bf16_to_f32(((const uint16_t*)a.Gz)[zrow + v]);
+          g = bf16_to_f32((uint16_t)buf_load2(rZ, off));
         else
-          g = ((const float*)a.Gz)[zrow + v];
+          g = __uint_as_float(buf_load4(rZ, off));
         part += acc[j][e] * g;
       }
     }
@@ -330,7 +370,7 @@ __global__ __launch_bounds__(GR_THREADS) void tied_cross_kernel(CrossArgs a) {
   part = wave_sum(part);
   if (lane == 0) red[w] = part;
   __syncthreads();
-  if (tid == 0) a.ws[(int64_t)b * a.slots + pair] = (red[0] + red[1]) + (red[2] + red[3]);
+  if (tid == 0) a.ws[(int64_t)b * a.slots + slot] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
 // out[b] = (accumulate ? out[b] : 0) + scale * sum_j ws[b, j]; each lane sums
@@ -347,16 +387,25 @@ __global__ __launch_bounds__(WAVE) void finish_rows_kernel(const float* __restri
 
 // `vec` selects the 16-byte load path; the caller sets it only when every
 // operand of the launch has 16-byte aligned rows.
+template <int DT>
+static void launch_gram_dt(const GramArgs& a, bool vec, hipStream_t s) {
+  const dim3 g(a.n_items), blk(GR_THREADS);
+  const bool single = a.n_t == 1;
+  if (vec) {
+    if (single) hipLaunchKernelGGL((gram_norm_kernel<DT, true, true>), g, blk, 0, s, a);
+    else hipLaunchKernelGGL((gram_norm_kernel<DT, true, false>), g, blk, 0, s, a);
+  } else {
+    if (single) hipLaunchKernelGGL((gram_norm_kernel<DT, false, true>), g, blk, 0, s, a);
+    else hipLaunchKernelGGL((gram_norm_kernel<DT, false, false>), g, blk, 0, s, a);
+  }
+}
+
 hipError_t launch_gram_norm(const GramArgs& a, int dt, bool vec, hipStream_t s) {
   if (a.n_items == 0) return hipSuccess;
-  const dim3 g(a.n_items), blk(GR_THREADS);
-  if (dt == DT_BF16) {
-    if (vec) hipLaunchKernelGGL((gram_norm_kernel<DT_BF16, true>), g, blk, 0, s, a);
-    else hipLaunchKernelGGL((gram_norm_kernel<DT_BF16, false>), g, blk, 0, s, a);
-  } else {
-    if (vec) hipLaunchKernelGGL((gram_norm_kernel<DT_F32, true>), g, blk, 0, s, a);
-    else hipLaunchKernelGGL((gram_norm_kernel<DT_F32, false>), g, blk, 0, s, a);
-  }
+  if (dt == DT_BF16)
+    launch_gram_dt<DT_BF16>(a, vec, s);
+  else
+    launch_gram_dt<DT_F32>(a, vec, s);
   return hipGetLastError();
 }
 

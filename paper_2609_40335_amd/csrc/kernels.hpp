@@ -36,6 +36,8 @@ static_assert(sizeof(GramArgs) <= 4096, "kernel arguments must stay within 4 KiB
 hipError_t launch_gram_norm(const GramArgs& a, int dt, bool vec, hipStream_t s);
 
 // Tied cross term: sum_{t,s} Gz[s, ids[t]] <dE_t, H_s>, all T-tile pairs.
+constexpr int CR_FCHUNK = 128;  // features per cross-term work item
+
 struct CrossArgs {
   const int32_t* ids;   // [B,T]
   const void* E;        // dE [B*T, lde]
@@ -43,7 +45,8 @@ struct CrossArgs {
   const void* Gz;       // [B*T, ldz]
   int64_t lde, ldh, ldz;
   int32_t B, T, V, d, n_t;
-  int32_t slots;        // n_t * n_t
+  int32_t n_fc;         // feature chunks
+  int32_t slots;        // n_t * n_t * n_fc
   float* ws;            // [B, slots]
 };
 hipError_t launch_tied_cross(const CrossArgs& a, int dt, bool vec, hipStream_t s);

@@ -58,7 +58,7 @@ _SIGS = {
     "dp_ghost_norm_embedding_workspace": ([_I, _I, _I], _SZ),
     "dp_ghost_norm_embedding": ([_VP, _VP, _I64, _I, _I, _I, _I, _I, _VP, _I, _VP, _VP, _VP,
                                  _SZ, _VP], _I),
-    "dp_tied_cross_term_workspace": ([_I, _I], _SZ),
+    "dp_tied_cross_term_workspace": ([_I, _I, _I], _SZ),
     "dp_tied_cross_term": ([_VP, _VP, _I64, _VP, _I64, _VP, _I64, _I, _I, _I, _I, _I, _F, _VP,
                             _I, _VP, _SZ, _VP], _I),
     "dp_clip_factors": ([_VP, _I, _F, _VP, _VP], _I),
@@ -205,7 +205,7 @@ def dp_tied_cross_term(ids, dE, H, Gz, V: int, out, scale: float = 1.0,
         raise DPError("Gz must have at least V columns")
     if ids.dtype != torch.int32 or tuple(ids.shape) != (B, T) or not ids.is_contiguous():
         raise DPError("ids must be contiguous int32 [B, T]")
-    ws = _ws(L.dp_tied_cross_term_workspace(B, T), dE.device)
+    ws = _ws(L.dp_tied_cross_term_workspace(B, T, d), dE.device)
     _check(L.dp_tied_cross_term(ids.data_ptr(), pe, lde, ph, ldh, pz, ldz, B, T, V, d,
                                 _dtype(dE), float(scale), out.data_ptr(), int(accumulate),
                                 ws.data_ptr(), ws.numel(), _stream(stream)),

@@ -62,10 +62,14 @@ def test_norm_workspace_sizes(L):
     # T = 300 -> 3 T-tiles -> 6 pairs
     assert L.dp_ghost_norm_linear_workspace(one, 1, 100, 300, D.DP_F32) == 2560
     head = (D.dp_linear_t * 1)(_lin(d_in=768, lda=768, d_out=50257, ldg=50304))
-    # bf16: 16-byte rows -> features [0, 50256) in chunks of 2048 (25) + a 1-wide tail
+    # bf16 head: V = 50257 features in chunks of 2048 -> 25 partials per example
     assert L.dp_ghost_norm_linear_workspace(head, 1, 1, 128, D.DP_BF16) == 256
-    ws = L.dp_ghost_norm_linear_workspace(head, 1, 1000, 128, D.DP_BF16)
-    assert ws == ((1000 * 26 * 4 + 255) // 256) * 256
+    ws = L.dp_ghost_norm_linear_workspace(head, 1, 100, 128, D.DP_BF16)
+    assert ws == ((100 * 25 * 4 + 255) // 256) * 256
+    # an operand spanning 4 GiB or more is refused (32-bit buffer offsets)
+    assert L.dp_ghost_norm_linear_workspace(head, 1, 1000, 128, D.DP_BF16) == 0
+    assert L.dp_ghost_norm_linear_grouped(head, 1, 1000, 128, D.DP_BF16, 1 << 22, 0, 1 << 23,
+                                          1 << 30, None) == EUNSUP
     # AUTO picks the direct form once T + 1 > 2 d_in d_out / (d_in + d_out) = 64:
     # one 256x256 output tile per example
     auto = (D.dp_linear_t * 1)(_lin())
@@ -128,7 +132,8 @@ def test_cross_and_clip_reject_bad_arguments(L):
     assert f(*bad_scale) == EINVAL
     no_ws = list(ok); no_ws[16] = 0
     assert f(*no_ws) == EINVAL
-    assert L.dp_tied_cross_term_workspace(4, 300) == 256
+    assert L.dp_tied_cross_term_workspace(4, 300, 64) == 256
+    assert L.dp_tied_cross_term_workspace(32, 128, 768) == 32 * 6 * 4
     assert L.dp_clip_factors(1 << 20, 4, 0.0, 1 << 21, None) == EINVAL
     assert L.dp_clip_factors(1 << 20, 4, float("nan"), 1 << 21, None) == EINVAL
     assert L.dp_clip_factors(1 << 20, 0, 1.0, 1 << 21, None) == EINVAL
