@@ -13,6 +13,11 @@
 // squared and summed in registers and never stored. It beats the Gram form
 // when T exceeds about 2 d_in d_out / (d_in + d_out).
 //
+// Two kernels. dl_gemm_kernel (below, the bf16 clipped sum on aligned rows)
+// loads rows straight into LDS and transposes on the way out of LDS. The
+// general kernel kt_gemm_kernel (fp32, unaligned strides, any T, and the
+// direct norm) stages through registers:
+//
 // MFMA wants 8 consecutive k per lane, but both operands are contiguous along
 // M/N. Each staging thread loads an 8(k) x 8(m) block with 16-byte buffer
 // loads, scales it (X only: exact widening, fp32 multiply,
@@ -141,6 +146,65 @@ __device__ __forceinline__ void tile_mfma(const u32x4* __restrict__ Xs, const u3
 #pragma unroll
           for (int m = 0; m < 4; ++m)
             acc[i][j] = mfma32_f32(__uint_as_float(xa[i][m]), __uint_as_float(yb[j][m]), acc[i][j]);
+        }
+      }
+  }
+}
+
+// Writes (or adds) one 256x256 output tile: each wave's 4x2 32x32 blocks at
+// rows m0 + wm*128 + i*32, columns n0 + wn*64 + j*32. In a 32x32 block, lane l
+// holds column l%32 and, for accumulator e, row (e/4)*8 + (l/32)*4 + e%4.
+// Stores bypass L2 residency (the output is written once) so that they do
+// not evict operand rows.
+__device__ __forceinline__ void store_tile(const GemmArgs& a, const GemmLayer& L, int64_t m0,
+                                           int64_t n0, int wm, int wn, int lane,
+                                           f32x16 (&acc)[4][2]) {
+  float* out = L.out;
+  const int64_t ldo = L.ldo;
+  const int mw = (int)m0 + wm * 128 + (lane >> 5) * 4;  // row of e = 0 in block i = 0
+  const int nw = (int)n0 + wn * 64 + (lane & 31);         // column in block j = 0
+  const bool full = m0 + GM_BM <= L.M && n0 + GM_BN <= L.N;
+  if (a.transpose) {
+    // out[n][m]: the 4 accumulators e = 4g..4g+3 are 4 consecutive rows m.
+    const bool vec4 = full && (ldo & 3) == 0 && (((uintptr_t)out) & 15) == 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int n = nw + j * 32;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int m = mw + i * 32 + g * 8;
+          float* p = out + (int64_t)n * ldo + m;
+          if (vec4) {
+            f32x4 v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                       acc[i][j][4 * g + 3]};
+            if (a.accumulate) v += *(const f32x4*)p;
+            __builtin_nontemporal_store(v, (f32x4*)p);
+          } else if (n < L.N) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (m + r < L.M) p[r] = a.accumulate ? p[r] + acc[i][j][4 * g + r]
+                                                   : acc[i][j][4 * g + r];
+          }
+        }
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int n = nw + j * 32;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = mw + i * 32 + (e >> 2) * 8 + (e & 3);
+          float* p = out + (int64_t)m * ldo + n;
+          if (full) {
+            const float v = a.accumulate ? *p + acc[i][j][e] : acc[i][j][e];
+            __builtin_nontemporal_store(v, p);
+          } else if (m < L.M && n < L.N) {
+            *p = a.accumulate ? *p + acc[i][j][e] : acc[i][j][e];
+          }
         }
       }
   }
@@ -311,58 +375,7 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
   }
 
   if constexpr (MODE == MODE_SUM) {
-    // 32x32 block (i,j): lane l holds column l%32 and, for accumulator e,
-    // row (e/4)*8 + (l/32)*4 + e%4. Stores bypass L2 residency (the output
-    // is written once) so that they do not evict operand rows.
-    float* out = L.out;
-    const int64_t ldo = L.ldo;
-    const int mw = (int)m0 + wm * 128 + (lane >> 5) * 4;  // row of e = 0 in block i = 0
-    const int nw = (int)n0 + wn * 64 + (lane & 31);         // column in block j = 0
-    const bool full = m0 + GM_BM <= L.M && n0 + GM_BN <= L.N;
-    if (a.transpose) {
-      // out[n][m]: the 4 accumulators e = 4g..4g+3 are 4 consecutive rows m.
-      const bool vec4 = full && (ldo & 3) == 0 && (((uintptr_t)out) & 15) == 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int n = nw + j * 32;
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int m = mw + i * 32 + g * 8;
-            float* p = out + (int64_t)n * ldo + m;
-            if (vec4) {
-              f32x4 v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
-                         acc[i][j][4 * g + 3]};
-              if (a.accumulate) v += *(const f32x4*)p;
-              __builtin_nontemporal_store(v, (f32x4*)p);
-            } else if (n < L.N) {
-#pragma unroll
-              for (int r = 0; r < 4; ++r)
-                if (m + r < L.M) p[r] = a.accumulate ? p[r] + acc[i][j][4 * g + r]
-                                                     : acc[i][j][4 * g + r];
-            }
-          }
-        }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int n = nw + j * 32;
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int m = mw + i * 32 + (e >> 2) * 8 + (e & 3);
-            float* p = out + (int64_t)m * ldo + n;
-            if (full) {
-              const float v = a.accumulate ? *p + acc[i][j][e] : acc[i][j][e];
-              __builtin_nontemporal_store(v, p);
-            } else if (m < L.M && n < L.N) {
-              *p = a.accumulate ? *p + acc[i][j][e] : acc[i][j][e];
-            }
-          }
-        }
-    }
+    store_tile(a, L, m0, n0, wm, wn, lane, acc);
   } else {
     float part = 0.f;
 #pragma unroll
@@ -381,6 +394,221 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
       a.ws[(int64_t)b * a.slots + L.slot_begin + rel] = t;
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Direct-load kernel for the bf16 clipped sum (16-byte aligned rows, T a
+// multiple of 32, B <= 4096): no staging through VGPRs at all.
+//
+// Global rows go straight into LDS through buffer loads that write LDS
+// (each lane's 16 bytes land at M0 + 16*lane), so LDS keeps the token-major
+// layout: stage row r = token, 256 features = 32 chunks of 16 bytes, chunk c
+// stored at physical chunk c ^ dl_sw(r). The MFMA fragments (8 consecutive k
+// of one column per lane) come out of LDS through the transposing read
+// ds_read_b64_tr_b16, which gathers 4 rows x 4 columns per 16-lane group:
+// two such reads give one 32x32x16 operand. With the swizzle the 16 chunks a
+// half-wave touches fall in 16 distinct bank groups.
+//
+// Ring of 4 stages of 32 k (32 KB each: X then Y). Iteration s: read the
+// second half (k 16..31) of stage s, issue the first half's MFMAs, wait for
+// stage s+1 and barrier, load stage s+4 into stage s's slot, read the first
+// half of stage s+1, issue the second half's MFMAs. The barrier thus
+// certifies both that stage s+1 has landed and that every wave is done with
+// stage s, and the MFMAs issued before it keep the matrix cores busy while
+// the waves synchronise. Every iteration issues the same 4 loads per wave
+// (stages past the end read zeros through the range check into a slot that
+// is never read), so the wait counts are constants.
+//
+// The loads are issued from inline assembly: the compiler would otherwise
+// treat every later LDS read as possibly aliasing an LDS-writing load and
+// drain all of them (vmcnt(0)) before it, serialising the ring. Its wait
+// bookkeeping stays sound: untracked loads only make its own waits stricter.
+// Clip factors are staged in LDS so that the loop issues no other vector
+// memory instruction. Scaling is on the fp32 accumulators as in SC_ACC.
+constexpr int DL_BK = 32;                   // k rows per stage
+constexpr int DL_NS = 4;                    // stages in the ring
+constexpr int DL_ROWB = GM_BM * 2;          // bytes per LDS row (256 bf16)
+constexpr int DL_OPB = DL_BK * DL_ROWB;     // one operand's stage: 16 KB
+constexpr int DL_STB = 2 * DL_OPB;          // one stage: X then Y
+constexpr int DL_MAXB = 4096;               // clip factors held in LDS
+constexpr int DL_LOADS = 4;                 // loads per wave per stage
+static_assert(GM_BM == GM_BN, "square tiles");
+static_assert(DL_STB == (GM_THREADS / WAVE) * DL_LOADS * 1024, "one KB per load");
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) char lds_char_t;
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4_t;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Physical chunk of chunk c in stage row r is c ^ dl_sw(r). The 4 rows read
+// together are r = 4a..4a+3; dl_sw maps them to 0, 6, 12, 10, whose bits 1-2
+// and bits 2-3 are both all distinct, so the reads are conflict-free whether
+// the LDS serves 16 or 32 lanes of a 64-bit read per cycle.
+__device__ __forceinline__ int dl_sw(int r) {
+  const int q = r & 3;
+  return (q << 2) ^ (q << 1);
+}
+
+__device__ __forceinline__ u32x2 lds_read_tr(const lds_char_t* p) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)p));
+}
+
+// 32x32x16 operand: lane l gets column l%32 at k rows 8*(l/32) .. +7 of the
+// 16-row half stage at `off` (two reads of 4 rows each).
+__device__ __forceinline__ u32x4 dl_frag(const lds_char_t* base, uint32_t off) {
+  const u32x2 lo = lds_read_tr(base + off), hi = lds_read_tr(base + off + 4 * DL_ROWB);
+  return u32x4{lo[0], lo[1], hi[0], hi[1]};
+}
+
+// s_waitcnt vmcnt(N) leaving the other counters alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
+  const GemmArgs& a = *(const GemmArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  (void)args;
+  __shared__ __attribute__((aligned(1024))) char ring_raw[DL_NS * DL_STB];
+  __shared__ float cs[DL_MAXB];
+  lds_char_t* ring = (lds_char_t*)(lds_void_t*)ring_raw;
+
+  const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
+  int l = 0;
+  while (l + 1 < a.n_layers && item >= a.L[l + 1].tile_begin) ++l;
+  const GemmLayer& L = a.L[l];
+  const uint32_t rel = item - L.tile_begin;
+  const int64_t K = (int64_t)a.B * a.T;
+  const int mt = (int)(rel / (uint32_t)L.tn), nt = (int)(rel - (uint32_t)mt * L.tn);
+  const int64_t m0 = (int64_t)mt * GM_BM;
+  const int64_t n0 = (int64_t)nt * GM_BN;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = w & 1, wn = w >> 1;
+
+  // Load role: waves 0-3 fill X rows 8w..8w+7 of every stage, waves 4-7 the
+  // same rows of Y. Load t writes rows 2t, 2t+1 of that block: lane l takes
+  // row l/32 and physical chunk l%32, i.e. logical chunk (l%32) ^ dl_sw(row).
+  const bool load_x = w < 4;
+  const int wq = w & 3;
+  const uint32_t ld_bytes = (uint32_t)((load_x ? L.ldx : L.ldy) * 2);
+  const int64_t col0 = load_x ? m0 : n0;
+  uint32_t lvo[2];  // lane offsets of loads with t even / odd
+#pragma unroll
+  for (int par = 0; par < 2; ++par) {
+    const int c = (lane & 31) ^ dl_sw(2 * par + (lane >> 5));
+    lvo[par] = (uint32_t)((lane >> 5) * ld_bytes + (col0 + 8 * c) * 2);
+  }
+  const uint32_t lds_role = (uint32_t)(load_x ? 0 : DL_OPB) + (uint32_t)wq * 8 * DL_ROWB;
+  const uint64_t gbase = (uint64_t)(load_x ? (const void*)L.X : (const void*)L.Y);
+  const uint64_t nrec64 = (uint64_t)K * ld_bytes;
+  const uint32_t nrec = nrec64 > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)nrec64;
+  const u32x4 desc = {(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)gbase),
+                      (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(gbase >> 32)),
+                      (uint32_t)__builtin_amdgcn_readfirstlane((int)nrec), (uint32_t)RSRC_WORD3};
+  const uint32_t ring_base = (uint32_t)(uintptr_t)ring;
+  const int nS = (int)(K / DL_BK);
+  auto issue = [&](int s) {
+    const uint32_t dst = ring_base + (uint32_t)((s % DL_NS) * DL_STB) + lds_role;
+    const int64_t row0 = (int64_t)s * DL_BK + wq * 8;
+    const uint32_t sbase = row0 < K ? (uint32_t)(row0 * ld_bytes) : nrec;
+#pragma unroll
+    for (int t = 0; t < DL_LOADS; ++t) {
+      const uint32_t m0v = (uint32_t)__builtin_amdgcn_readfirstlane((int)(dst + t * 1024));
+      const uint32_t so = (uint32_t)__builtin_amdgcn_readfirstlane((int)(sbase + 2 * t * ld_bytes));
+      // M0 (the LDS destination) is a reserved register that the compiler
+      // sets right before each of its own users; this kernel has none.
+      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                   :: "s"(m0v), "v"(lvo[t & 1]), "s"(desc), "s"(so));
+    }
+  };
+
+  // Transposing-read lane offsets of this wave's 4 X blocks and 2 Y blocks:
+  // within each 16-lane group, lane j addresses row j/4 and columns
+  // 4*(j%4) .. +3 of the group's 16 columns.
+  const int g = lane >> 4, jl = lane & 15;
+  const int rrow = 8 * (g >> 1) + (jl >> 2);
+  const int F = dl_sw(jl >> 2);
+  uint32_t ox[4], oy[2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = wm * 128 + i * 32 + 16 * (g & 1) + 4 * (jl & 3);
+    ox[i] = (uint32_t)(rrow * DL_ROWB + (((m >> 3) ^ F) << 4) + ((m & 7) << 1));
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int n = wn * 64 + j * 32 + 16 * (g & 1) + 4 * (jl & 3);
+    oy[j] = (uint32_t)(DL_OPB + rrow * DL_ROWB + (((n >> 3) ^ F) << 4) + ((n & 7) << 1));
+  }
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  for (int i = tid; i < a.B; i += GM_THREADS) cs[i] = a.c[i];
+  const int spe = a.T / DL_BK;  // stages per example
+  float c_acc = 0.f;            // factor of what is accumulated; 0: nothing yet
+  bool skip = false;
+  auto enter = [&](int s) {
+    if (s % spe == 0) {
+      const float ce = cs[s / spe];
+      skip = !(ce != 0.f);
+      if (!skip) {
+        if (c_acc != 0.f) {
+          const float f = c_acc / ce;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) acc[i][j] *= f;
+        }
+        c_acc = ce;
+      }
+    }
+  };
+  auto rd = [&](int s, int half, u32x4 (&f)[6]) {
+    const lds_char_t* base = ring + (s % DL_NS) * DL_STB;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f[i] = dl_frag(base, ox[i] + half * 16 * DL_ROWB);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) f[4 + j] = dl_frag(base, oy[j] + half * 16 * DL_ROWB);
+  };
+  auto mm = [&](const u32x4 (&f)[6]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = mfma32_bf16(f[i], f[4 + j], acc[i][j]);
+  };
+
+  u32x4 fa[6], fb[6];
+#pragma unroll
+  for (int p = 0; p < DL_NS; ++p) issue(p);
+  wait_vmcnt<DL_LOADS * (DL_NS - 1)>();
+  __syncthreads();
+  rd(0, 0, fa);
+  for (int s = 0; s < nS; ++s) {
+    enter(s);
+    rd(s, 1, fb);
+    if (!skip) mm(fa);
+    wait_vmcnt<DL_LOADS * (DL_NS - 2)>();
+    __syncthreads();
+    issue(s + DL_NS);
+    rd(s + 1, 0, fa);
+    if (!skip) mm(fb);
+  }
+  // No load may still be writing LDS when the workgroup ends.
+  wait_vmcnt<0>();
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] *= c_acc;
+  store_tile(a, L, m0, n0, wm, wn, lane, acc);
 }
 
 template <int DT, bool VEC, int MODE>
@@ -402,6 +630,10 @@ static hipError_t launch_kt(const GemmArgs& a, int dt, bool vec, hipStream_t s) 
   // The accumulator form needs every K-stage inside one example.
   const int ks = dt == DT_BF16 ? KT<DT_BF16>::KS : KT<DT_F32>::KS;
   const int sc = MODE == MODE_NORM ? SC_NONE : (a.T % ks == 0 ? SC_ACC : SC_STAGE);
+  if (MODE == MODE_SUM && dt == DT_BF16 && vec && a.T % DL_BK == 0 && a.B <= DL_MAXB) {
+    hipLaunchKernelGGL(dl_gemm_kernel, dim3(a.n_items), dim3(GM_THREADS), 0, s, a);
+    return hipGetLastError();
+  }
   if (dt == DT_BF16) {
     if (vec) launch_sc<DT_BF16, true, MODE>(a, sc, s);
     else launch_sc<DT_BF16, false, MODE>(a, sc, s);

@@ -246,6 +246,57 @@ def test_clipped_sum_linear(dp, case, transpose):
     assert fro_rel(got2, 2 * ref) <= TOL[dtype]
 
 
+# bf16 sums on 16-byte aligned rows with T % 32 == 0 take the direct-load
+# kernel (rows loaded straight into LDS, 4-stage ring, per-example factors on
+# the accumulators); these cases pin its edges.
+DL_CASES = [
+    # B, T, d_in, d_out, lda, ldg, c
+    (5, 32, 300, 520, 304, 528, [0.0, 1.0, 0.5, 0.0, 0.25]),   # c = 0 first/middle, ragged tiles
+    (1, 32, 64, 64, None, None, [0.7]),                       # one stage (less than the ring)
+    (3, 96, 256, 256, None, None, [1.0, 1.0, 1.0]),            # all c = 1, exact tiles
+    (4, 64, 520, 264, 528, 272, [0.9, 0.1, 0.6, 0.0]),         # last example skipped
+]
+
+
+@pytest.mark.parametrize("transpose", [False, True])
+@pytest.mark.parametrize("case", DL_CASES, ids=lambda c: "-".join(str(x) for x in c[:6]))
+def test_clipped_sum_direct_load(dp, case, transpose):
+    B, T, d_in, d_out, lda, ldg, cl = case
+    _say(f"direct-load sum {case[:6]} transpose={transpose}")
+    A, G = _layer_inputs("bf16", B, T, d_in, d_out, seed=37, lda=lda, ldg=ldg)
+    # Stride padding holds NaN: the kernel loads whole 256-column tile rows,
+    # and what lies past the valid columns may only reach unstored outputs.
+    if lda:
+        A[:, :, d_in:] = 0x7FC0
+    if ldg:
+        G[:, :, d_out:] = 0x7FC0
+    c = np.asarray(cl, np.float32)
+    ref = O.clipped_sum_linear(O.decode(A[:, :, :d_in], "bf16"),
+                               O.decode(G[:, :, :d_out], "bf16"), c.astype(np.float64))
+    shape = (d_out, d_in) if transpose else (d_in, d_out)
+    out = torch.full(shape, 3.0, device="cuda")
+    dp.dp_clipped_grad_sum(dev(A, "bf16")[:, :, :d_in], dev(G, "bf16")[:, :, :d_out], dev(c), out,
+                           transpose_out=transpose)
+    got = host(out)
+    got = got.T if transpose else got
+    assert np.isfinite(got).all()
+    err = fro_rel(got, ref)
+    _say(f"  fro rel err {err:.3e}")
+    assert err <= TOL["bf16"]
+
+
+def test_clipped_sum_many_examples(dp):
+    """B above the direct-load kernel's factor table (4096): general kernel."""
+    B, T, d_in, d_out = 4100, 32, 64, 72
+    A, G = _layer_inputs("bf16", B, T, d_in, d_out, seed=38)
+    c = gen.draw(38, 3, (B,), 1.0, "f32")
+    c = np.abs(c).astype(np.float32)
+    ref = O.clipped_sum_linear(O.decode(A, "bf16"), O.decode(G, "bf16"), c.astype(np.float64))
+    out = torch.zeros((d_in, d_out), device="cuda")
+    dp.dp_clipped_grad_sum(dev(A, "bf16"), dev(G, "bf16"), dev(c), out)
+    assert fro_rel(host(out), ref) <= TOL["bf16"]
+
+
 def test_clipped_sum_grouped(dp):
     B, T = 2, 96
     shapes = [(64, 192), (200, 96), (768, 768)]
@@ -283,16 +334,17 @@ def test_clipped_sum_embedding(dp, dtype, B, T, V, d, kind):
     assert fro_rel(host(outT).T, ref) <= TOL[dtype]
 
 
-def test_tied_clipped_sum_one_buffer(dp):
+@pytest.mark.parametrize("T,ldz", [(100, 1001), (64, 1008)])   # general / direct-load head
+def test_tied_clipped_sum_one_buffer(dp, T, ldz):
     """Tied E: the head sum and the embedding sum land in one [V, d] buffer."""
-    dtype, B, T, V, d = "bf16", 3, 100, 1001, 64
-    ids, dE, H, Gz = _tied_inputs(dtype, B, T, V, d, V, seed=8)
+    dtype, B, V, d = "bf16", 3, 1001, 64
+    ids, dE, H, Gz = _tied_inputs(dtype, B, T, V, d, ldz, seed=8)
     c = np.array([0.3, 1.0, 0.7], np.float32)
     dEd, Hd, Gzd = O.decode(dE, dtype), O.decode(H, dtype), O.decode(Gz, dtype)
     ref = (O.clipped_sum_head(Hd, Gzd, c.astype(np.float64), V)
            + O.clipped_sum_embedding(ids, dEd, c.astype(np.float64), V))
     out = torch.empty((V, d), device="cuda")
-    dp.dp_clipped_grad_sum(dev(Gz, dtype), dev(H, dtype), dev(c), out)   # Gz^T H -> [V, d]
+    dp.dp_clipped_grad_sum(dev(Gz, dtype)[:, :, :V], dev(H, dtype), dev(c), out)   # Gz^T H -> [V, d]
     dp.dp_clipped_grad_sum(None, dev(dE, dtype), dev(c), out, ids=dev(ids), V=V, accumulate=True)
     assert fro_rel(host(out), ref) <= TOL[dtype]
 
