@@ -19,6 +19,7 @@ line; per-phase times go to stderr.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -31,6 +32,11 @@ if ROOT not in sys.path:
 METRIC = "examples/sec for ghost-norm + clipped grad sum (GPT-2-small shapes); % MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+# HBM bytes per launch of the clipped-sum kernel: rocprofv3 FETCH_SIZE x 2 +
+# WRITE_SIZE x 1 (factors from a plain 1 GiB copy), recorded for the kernel
+# source with this SHA-256; any other source reports null.
+GEMM_TRAFFIC = {"gemm.hip sha256": "07988a6d578e152bfba4c175b66835b2c65826b794abf37fafcc95d24f47de81",
+                "bytes": 2818646741}
 
 
 def log(*a):
@@ -51,6 +57,13 @@ def parse(argv=None):
                     help="seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     return ap.parse_args(argv)
+
+
+def gemm_traffic():
+    src = os.path.join(ROOT, "paper_2609_40335_amd", "csrc", "gemm.hip")
+    with open(src, "rb") as f:
+        h = hashlib.sha256(f.read()).hexdigest()
+    return GEMM_TRAFFIC["bytes"] if h == GEMM_TRAFFIC["gemm.hip sha256"] else None
 
 
 def round_up(x, m):
@@ -252,9 +265,9 @@ def main(argv=None) -> int:
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic", "config": config,
-        "roofline": {"bound": "mfma", "kernel": "kt_gemm_kernel (clipped sum, bf16)",
+        "roofline": {"bound": "mfma", "kernel": "dl_gemm_kernel (clipped sum, bf16)",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": gemm_traffic(),
                      "algorithmic_flop_per_launch": st.gemm_flops},
     }
     if not args.no_cpu_baseline:
