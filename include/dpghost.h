@@ -175,14 +175,16 @@ dp_status_t dp_clipped_grad_sum_grouped(const dp_linear_t* layers, float* const*
 
 /* ---------------------------------------------------------------------
  * Gaussian mechanism (eq. 3): grad[j] = (grad[j] + sigma*C*z_j) / B_norm
- * (no division when B_norm = 0), in place, for j < n. z_j is a standard
+ * (no division when B_norm = 0), in place, for j < n; the division is a
+ * multiplication by 1/B_norm rounded to fp32 (within an ulp of dividing). z_j is a standard
  * normal from the counter-based Philox4x32-10 generator (Salmon et al.,
  * SC'11) and the Box-Muller transform: element j uses Philox block j/4 with
  * key (seed low word, seed high word) and counter (block low word, block
  * high word, tensor_id, step); the four outputs x become uniforms
  * (x + 1/2) 2^-32 and the pairs (0,1), (2,3) give r cos(2 pi u_odd),
  * r sin(2 pi u_odd) with r = sqrt(-2 ln u_even); element j takes output j%4.
- * The device evaluates the transform in fp32 (relative error ~1e-7 on z).
+ * The device evaluates the transform in fp32 on the hardware log2, sqrt,
+ * sin and cos units (absolute error on z below 1e-4, tails included).
  * The same (seed, tensor_id, step) reproduces the same noise, so the
  * generator position is the only state to checkpoint. tensor_id and step
  * must be < 2^32. grad is fp32.

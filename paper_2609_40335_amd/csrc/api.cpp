@@ -455,9 +455,9 @@ dp_status_t dp_add_noise(float* grad, int64_t n, float sigma, float C, int B_nor
   if (B_norm < 0) return fail(DP_EINVAL, "B_norm must be >= 0");
   if (tensor_id >> 32 || step >> 32) return fail(DP_EINVAL, "tensor_id and step must be < 2^32");
   const float sigma_c = (float)((double)sigma * (double)C);
-  return hip_status(dpg::launch_add_noise(grad, n, sigma_c, B_norm > 0 ? 1 : 0, (float)B_norm,
-                                          seed, (uint32_t)tensor_id, (uint32_t)step,
-                                          as_stream(stream)),
+  const float inv_b = B_norm > 0 ? (float)(1.0 / (double)B_norm) : 1.f;
+  return hip_status(dpg::launch_add_noise(grad, n, sigma_c, inv_b, seed, (uint32_t)tensor_id,
+                                          (uint32_t)step, as_stream(stream)),
                     "noise launch");
 }
 

@@ -128,7 +128,7 @@ hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 
 // ----------------------------------------------------------- clip and noise
 hipError_t launch_clip_factors(const float* norm2, int B, float C, float* c, hipStream_t s);
-hipError_t launch_add_noise(float* g, int64_t n, float sigma_c, int divide, float b_norm,
-                            uint64_t seed, uint32_t tensor_id, uint32_t step, hipStream_t s);
+hipError_t launch_add_noise(float* g, int64_t n, float sigma_c, float inv_b, uint64_t seed,
+                            uint32_t tensor_id, uint32_t step, hipStream_t s);
 
 }  // namespace dpg

@@ -28,10 +28,11 @@ __device__ __forceinline__ void philox4x32_10(uint32_t (&c)[4], uint32_t k0, uin
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     if (r) { k0 += W0; k1 += W1; }
-    const uint32_t hi0 = __umulhi(M0, c[0]), lo0 = M0 * c[0];
-    const uint32_t hi1 = __umulhi(M1, c[2]), lo1 = M1 * c[2];
-    const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
-    c[0] = n0; c[1] = lo1; c[2] = n2; c[3] = lo0;
+    // Full 64-bit products: one v_mad_u64_u32 each instead of mul_hi + mul_lo.
+    const uint64_t p0 = (uint64_t)M0 * c[0], p1 = (uint64_t)M1 * c[2];
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c[1] ^ k0;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c[3] ^ k1;
+    c[0] = n0; c[1] = (uint32_t)p1; c[2] = n2; c[3] = (uint32_t)p0;
   }
 }
 
@@ -39,28 +40,30 @@ __device__ __forceinline__ void philox4x32_10(uint32_t (&c)[4], uint32_t k0, uin
 // u = (x + 1/2) 2^-32; Box-Muller pairs (u0,u1) and (u2,u3) give
 // r cos(2 pi u_odd), r sin(2 pi u_odd) with r = sqrt(-2 ln u_even). In fp32
 // the conversion of x is exact below 2^24 (the far tail, small u) and rounds x
-// to 24 bits above, which moves ln u by at most 2^-24; the angle uses
-// sincospi on 2u.
+// to 24 bits above, which moves ln u by at most 2^-24. The transcendental
+// steps run on the hardware units: ln u = ln 2 * V_LOG_F32(u) (base 2),
+// V_SQRT_F32, and V_SIN_F32 / V_COS_F32, whose argument is in revolutions,
+// so that sin(2 pi u) is V_SIN_F32(u) with no range reduction for u in (0,1).
 __device__ __forceinline__ void gauss4(uint64_t blk, uint64_t seed, uint32_t tensor_id,
                                        uint32_t step, float (&z)[4]) {
   uint32_t c[4] = {(uint32_t)blk, (uint32_t)(blk >> 32), tensor_id, step};
   philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
+  constexpr float MINUS_2_LN2 = -1.3862943611198906f;
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     const float u = ((float)c[2 * p] + 0.5f) * 0x1p-32f;
-    const float r = sqrtf(-2.f * logf(u));
-    const float twice_u = ((float)c[2 * p + 1] + 0.5f) * 0x1p-31f;
-    float sn, cs;
-    sincospif(twice_u, &sn, &cs);
-    z[2 * p] = r * cs;
-    z[2 * p + 1] = r * sn;
+    const float r = __builtin_amdgcn_sqrtf(MINUS_2_LN2 * __builtin_amdgcn_logf(u));
+    const float v = ((float)c[2 * p + 1] + 0.5f) * 0x1p-32f;
+    z[2 * p] = r * __builtin_amdgcn_cosf(v);
+    z[2 * p + 1] = r * __builtin_amdgcn_sinf(v);
   }
 }
 
-// g[j] = (g[j] + sigma*C*z_j) / B (or without the division). One thread per
-// Philox block of 4 consecutive elements.
-__global__ void add_noise_kernel(float* g, int64_t n, float sigma_c, int divide, float b_norm,
-                                 uint64_t seed, uint32_t tensor_id, uint32_t step) {
+// g[j] = (g[j] + sigma*C*z_j) * inv_b, inv_b = 1/B rounded to fp32 (1 when
+// there is no division). One thread per Philox block of 4 consecutive
+// elements; the gradient is streamed once (non-temporal).
+__global__ void add_noise_kernel(float* g, int64_t n, float sigma_c, float inv_b, uint64_t seed,
+                                 uint32_t tensor_id, uint32_t step) {
   const int64_t nblk = (n + 3) / 4;
   const bool vec = (((uintptr_t)g) & 15) == 0;
   for (int64_t blk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; blk < nblk;
@@ -69,18 +72,12 @@ __global__ void add_noise_kernel(float* g, int64_t n, float sigma_c, int divide,
     gauss4((uint64_t)blk, seed, tensor_id, step, z);
     const int64_t j0 = blk * 4;
     if (vec && j0 + 4 <= n) {
-      f32x4 v = *(const f32x4*)(g + j0);
+      f32x4 v = __builtin_nontemporal_load((const f32x4*)(g + j0));
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float t = v[q] + sigma_c * z[q];
-        v[q] = divide ? t / b_norm : t;
-      }
-      *(f32x4*)(g + j0) = v;
+      for (int q = 0; q < 4; ++q) v[q] = (v[q] + sigma_c * z[q]) * inv_b;
+      __builtin_nontemporal_store(v, (f32x4*)(g + j0));
     } else {
-      for (int q = 0; q < 4 && j0 + q < n; ++q) {
-        const float t = g[j0 + q] + sigma_c * z[q];
-        g[j0 + q] = divide ? t / b_norm : t;
-      }
+      for (int q = 0; q < 4 && j0 + q < n; ++q) g[j0 + q] = (g[j0 + q] + sigma_c * z[q]) * inv_b;
     }
   }
 }
@@ -91,14 +88,14 @@ hipError_t launch_clip_factors(const float* norm2, int B, float C, float* c, hip
   return hipGetLastError();
 }
 
-hipError_t launch_add_noise(float* g, int64_t n, float sigma_c, int divide, float b_norm,
-                            uint64_t seed, uint32_t tensor_id, uint32_t step, hipStream_t s) {
+hipError_t launch_add_noise(float* g, int64_t n, float sigma_c, float inv_b, uint64_t seed,
+                            uint32_t tensor_id, uint32_t step, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int64_t nblk = (n + 3) / 4;
   int64_t grid = (nblk + 255) / 256;
   if (grid > 8192) grid = 8192;
   hipLaunchKernelGGL(add_noise_kernel, dim3((unsigned)grid), dim3(256), 0, s, g, n, sigma_c,
-                     divide, b_norm, seed, tensor_id, step);
+                     inv_b, seed, tensor_id, step);
   return hipGetLastError();
 }
 
