@@ -8,7 +8,8 @@
 // the same kernel with G = the logit gradients.
 //
 // Work item = (layer, example, upper-triangle T-tile pair, chunk of G features).
-// A workgroup streams the rows of its two 128-row T-tiles through LDS, first
+// For bf16 rows that are 16-byte aligned with T <= 128, dl_gram_kernel loads
+// the rows straight into LDS (see there); otherwise a workgroup streams the rows of its two 128-row T-tiles through LDS, first
 // over the features of A (Gram P) then over its chunk of G features (Gram Q),
 // both accumulated by 32x32 MFMA blocks held in registers, and reduces
 // sum w * P o Q in registers. No Gram ever leaves the chip. Splitting the G
@@ -281,6 +282,157 @@ __global__ __launch_bounds__(GR_THREADS) void gram_norm_kernel(GramArgs args) {
         (red[0] + red[1]) + (red[2] + red[3]);
 }
 
+// ---------------------------------------------------------------------------
+// Direct-load Gram kernel: bf16, 16-byte aligned rows, T <= 128 (one T-tile).
+// Rows go straight into LDS through LDS-writing buffer loads (lane l's 16
+// bytes land at M0 + 16*l), four 16 KB stages in a ring, two workgroups per
+// CU. Stage row r holds token r of the example, 64 features as 8 chunks,
+// logical chunk c at physical chunk swz(r, c); the MFMA reads are the same as
+// the register-staged kernel's. Rows past T read zero through the example's
+// buffer range; chunks wholly past the last feature are pointed past the
+// range; a chunk that straddles it is masked in LDS after it lands.
+constexpr int DG_NS = 4;
+constexpr int DG_ROWB = 128;                  // 64 bf16 per LDS row
+constexpr int DG_STB = GR_TM * DG_ROWB;       // 16 KB per stage
+constexpr int DG_LOADS = 4;                   // 1 KB loads per wave per stage
+static_assert(DG_STB == (GR_THREADS / WAVE) * DG_LOADS * 1024, "one KB per load");
+
+typedef __attribute__((address_space(3))) void lds_void_g;
+
+template <int N>
+__device__ __forceinline__ void dg_wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int PAT>
+__device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int chunk, u32x4* ring) {
+  constexpr int NB = PatNB<PAT>::NB;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint64_t ex_rows = (uint64_t)b * T;
+  const uint32_t ldx = (uint32_t)(L.lda * 2), ldy = (uint32_t)(L.ldg * 2);
+  const uint64_t xb = (uint64_t)L.A + ex_rows * ldx, yb = (uint64_t)L.G + ex_rows * ldy;
+  const uint32_t nrx = T * ldx, nry = T * ldy;
+  auto desc_of = [](uint64_t base, uint32_t nrec) {
+    return u32x4{(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)base),
+                 (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(base >> 32)),
+                 (uint32_t)__builtin_amdgcn_readfirstlane((int)nrec), (uint32_t)RSRC_WORD3};
+  };
+  const u32x4 dx = desc_of(xb, nrx), dy = desc_of(yb, nry);
+  const int64_t x1 = L.d_in;
+  const int64_t y0 = (int64_t)L.g0 + (int64_t)chunk * L.kg;
+  const int64_t y1 = y0 + L.kg < L.g1 ? y0 + L.kg : L.g1;
+  const int nX = (int)((x1 + 63) / 64);
+  const int nY = (int)((y1 - y0 + 63) / 64);
+  const int n = nX + nY;
+  const uint32_t ring_base = (uint32_t)(uintptr_t)(lds_void_g*)ring;
+
+  // Load t of wave w writes stage rows r = 32w + 8t + l/8, physical chunk l%8.
+  const int lr = lane >> 3;
+  auto issue = [&](int s) {
+    const bool inX = s < nX;
+    const u32x4 d = inX ? dx : dy;
+    const uint32_t ld = inX ? ldx : ldy, nrec = inX ? nrx : nry;
+    const int64_t c0 = inX ? (int64_t)s * 64 : y0 + (int64_t)(s - nX) * 64;
+    const int64_t c1 = inX ? x1 : y1;
+    const bool live = s < n;
+    const uint32_t dst = ring_base + (uint32_t)((s % DG_NS) * DG_STB) + (uint32_t)w * 32 * DG_ROWB;
+#pragma unroll
+    for (int t = 0; t < DG_LOADS; ++t) {
+      const int r = 32 * w + 8 * t + lr;
+      const int c = (lane & 7) ^ ((r ^ (r >> 3)) & 7);
+      const int64_t col = c0 + 8 * c;
+      const uint32_t voff = (live && col < c1) ? (uint32_t)(lr * ld + col * 2) : nrec;
+      const uint32_t m0v = (uint32_t)__builtin_amdgcn_readfirstlane((int)(dst + t * 1024));
+      const uint32_t so = (uint32_t)__builtin_amdgcn_readfirstlane((int)((32 * w + 8 * t) * ld));
+      // Issued from asm so that the compiler does not drain all of them before
+      // every LDS read; M0 has no other user in this kernel.
+      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                   :: "s"(m0v), "v"(voff), "s"(d), "s"(so));
+    }
+  };
+  // Zero the features at or past c1 inside the chunk that straddles c1.
+  auto fix = [&](int s) {
+    const bool inX = s < nX;
+    const int64_t c0 = inX ? (int64_t)s * 64 : y0 + (int64_t)(s - nX) * 64;
+    const int64_t c1 = inX ? x1 : y1;
+    const int64_t nv = c1 - c0;  // valid features in this stage
+    if (nv >= 64 || (nv & 7) == 0) return;
+    if (tid < GR_TM) {
+      const int cp = (int)(nv >> 3), keep = (int)(nv & 7);
+      u32x4* p = ring + (s % DG_NS) * (DG_STB / 16) + tid * 8 + swz(tid, cp);
+      u32x4 v = *p;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = 2 * q;
+        v[q] = e + 1 < keep ? v[q] : (e < keep ? (v[q] & 0xFFFFu) : 0u);
+      }
+      *p = v;
+    }
+    __syncthreads();
+  };
+
+  int ra[4], rb[4];
+  float wt[4];
+  block_rows<PAT>(w, ra, rb, wt);
+  f32x16 accP[NB], accQ[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) { accP[j][e] = 0.f; accQ[j][e] = 0.f; }
+
+#pragma unroll
+  for (int p = 0; p < DG_NS - 1; ++p) issue(p);
+  auto phase = [&](int s_begin, int s_end, f32x16 (&acc)[NB]) {
+    for (int s = s_begin; s < s_end; ++s) {
+      dg_wait_vmcnt<DG_LOADS * (DG_NS - 2)>();
+      __syncthreads();
+      fix(s);
+      issue(s + DG_NS - 1);
+      stage_mfma<DT_BF16, NB>(ring + (s % DG_NS) * (DG_STB / 16), ra, rb, acc, lane);
+    }
+  };
+  phase(0, nX, accP);
+  phase(nX, n, accQ);
+  dg_wait_vmcnt<0>();
+  float part = 0.f;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s += accP[j][e] * accQ[j][e];
+    part += wt[j] * s;
+  }
+  return part;
+}
+
+__global__ __launch_bounds__(GR_THREADS, 2) void dl_gram_kernel(GramArgs args) {
+  const GramArgs& a = *(const GramArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  (void)args;
+  __shared__ __attribute__((aligned(1024))) u32x4 ring[DG_NS * DG_STB / 16];
+  __shared__ float red[GR_THREADS / WAVE];
+  const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
+  int l = 0;
+  while (l + 1 < a.n_layers && item >= a.L[l + 1].item_begin) ++l;
+  const GramLayer& L = a.L[l];
+  uint32_t rel = item - L.item_begin;
+  const uint32_t per_b = (uint32_t)L.nc;
+  const int b = (int)(rel / per_b);
+  const int chunk = (int)(rel - (uint32_t)b * per_b);
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  float part;
+  if (w < 2)
+    part = dg_item<PAT_D1>(L, b, a.T, chunk, ring);
+  else
+    part = dg_item<PAT_D2>(L, b, a.T, chunk, ring);
+  part = wave_sum(part);
+  if ((threadIdx.x & 63) == 0) red[w] = part;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    a.ws[(int64_t)b * a.slots + L.slot_begin + chunk] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
 // Work item = (example, T-tile pair (ti, tj), chunk of CR_FCHUNK features).
 // The reduction is linear in the features, so chunks add up exactly.
 template <int DT, bool VEC>
@@ -391,6 +543,12 @@ template <int DT>
 static void launch_gram_dt(const GramArgs& a, bool vec, hipStream_t s) {
   const dim3 g(a.n_items), blk(GR_THREADS);
   const bool single = a.n_t == 1;
+  if constexpr (DT == DT_BF16) {
+    if (vec && single) {
+      hipLaunchKernelGGL(dl_gram_kernel, g, blk, 0, s, a);
+      return;
+    }
+  }
   if (vec) {
     if (single) hipLaunchKernelGGL((gram_norm_kernel<DT, true, true>), g, blk, 0, s, a);
     else hipLaunchKernelGGL((gram_norm_kernel<DT, true, false>), g, blk, 0, s, a);

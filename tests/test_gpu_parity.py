@@ -56,6 +56,7 @@ NORM_CASES = [
     ("bf16", 2, 50, 64, 40, 72, 48),           # padded aligned strides
     ("bf16", 2, 17, 24, 5000, None, 5008),     # G chunked (> 4096 features) + ragged tail
     ("bf16", 1, 1, 8, 8, None, None),          # T = 1
+    ("bf16", 3, 96, 100, 77, 104, 80),         # last chunk straddles d, aligned strides
 ]
 
 
@@ -65,6 +66,10 @@ def test_linear_norm(dp, case, algo):
     dtype, B, T, d_in, d_out, lda, ldg = case
     _say(f"linear norm {algo} {case}")
     A, G = _layer_inputs(dtype, B, T, d_in, d_out, seed=11, lda=lda, ldg=ldg)
+    # Stride padding holds NaN: no kernel may let features past d reach a sum.
+    nan = np.uint16(0x7FC0) if dtype == "bf16" else np.float32("nan")
+    A[:, :, d_in:] = nan
+    G[:, :, d_out:] = nan
     ref = _oracle_linear_norm2(A, G, d_in, d_out, dtype)
     At = dev(A, dtype)[:, :, :d_in]
     Gt = dev(G, dtype)[:, :, :d_out]
