@@ -95,7 +95,10 @@ const char* dp_last_error(void);
  *   norm2[b] (+)= sum over layers of ||A_b^T G_b||_F^2.
  * The grouped form evaluates many layers of one batch in one launch (all
  * share B, T and dtype). Limits: T <= 65536, d_in, d_out <= 2^31 - 1.
- * Workspace: dp_ghost_norm_linear_workspace() bytes (fp32 partials).
+ * Workspace: dp_ghost_norm_linear_workspace() bytes (fp32 partials). The
+ * size depends on the layer table, pointers included (their alignment picks
+ * the kernel and so the number of partials): query it with the same table
+ * the call gets; a smaller workspace is rejected with DP_EINVAL.
  * ------------------------------------------------------------------- */
 size_t dp_ghost_norm_linear_workspace(const dp_linear_t* layers, int n_layers, int B, int T,
                                       dp_dtype_t dt);

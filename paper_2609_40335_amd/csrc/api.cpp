@@ -105,6 +105,12 @@ void plan_gemm(const void* X, int64_t ldx, int M, const void* Y, int64_t ldy, in
   v.push_back(e);
 }
 
+// Work items per (example, G chunk): one per T-tile pair, or one in all when
+// the whole-example Gram applies.
+int gram_pairs(const NormPlan& p, dp_dtype_t dt, bool vec, int T) {
+  return dpg::gram_whole(kdt(dt), vec, T) ? 1 : p.P;
+}
+
 NormPlan plan_norm(const dp_linear_t* layers, int n, int T, dp_dtype_t dt) {
   NormPlan p;
   p.n_t = (int)ceil_div(T, dpg::GR_TM);
@@ -119,7 +125,7 @@ NormPlan plan_norm(const dp_linear_t* layers, int n, int T, dp_dtype_t dt) {
     const int kg = L.d_out > KG_SPLIT ? KG_CHUNK : (int)(ceil_div(L.d_out, ks) * ks);
     GramEntry e{L.A, L.G, L.lda, L.ldg, L.d_in, 0, L.d_out, kg, (int)ceil_div(L.d_out, kg),
                 (int)p.slots, vec_ok(L.A, L.lda, dt) && vec_ok(L.G, L.ldg, dt)};
-    p.slots += (int64_t)p.P * e.nc;
+    p.slots += (int64_t)gram_pairs(p, dt, e.vec, T) * e.nc;
     p.gram.push_back(e);
   }
   return p;
@@ -155,7 +161,7 @@ dp_status_t run_gram(const NormPlan& p, int B, int T, dp_dtype_t dt, float* ws, 
       if (e.vec == vec) sel.push_back(&e);
     for (size_t i0 = 0; i0 < sel.size(); i0 += dpg::GR_MAX_LAYERS) {
       dpg::GramArgs a{};
-      a.B = B; a.T = T; a.n_t = p.n_t; a.P = p.P;
+      a.B = B; a.T = T; a.n_t = p.n_t; a.P = gram_pairs(p, dt, vec, T);
       a.slots = (int32_t)p.slots;
       a.ws = ws;
       uint64_t items = 0;
@@ -167,7 +173,7 @@ dp_status_t run_gram(const NormPlan& p, int B, int T, dp_dtype_t dt, float* ws, 
         L.d_in = e.d_in; L.g0 = e.g0; L.g1 = e.g1; L.kg = e.kg; L.nc = e.nc;
         L.item_begin = (uint32_t)items;
         L.slot_begin = e.slot_begin;
-        items += (uint64_t)B * p.P * e.nc;
+        items += (uint64_t)B * a.P * e.nc;
       }
       if (items > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many work items (%llu)",
                                              (unsigned long long)items);

@@ -8,8 +8,8 @@
 // the same kernel with G = the logit gradients.
 //
 // Work item = (layer, example, upper-triangle T-tile pair, chunk of G features).
-// For bf16 rows that are 16-byte aligned with T <= 128, dl_gram_kernel loads
-// the rows straight into LDS (see there); otherwise a workgroup streams the rows of its two 128-row T-tiles through LDS, first
+// For bf16 rows that are 16-byte aligned, dl_gram_kernel loads the rows
+// straight into LDS (see there); otherwise a workgroup streams the rows of its two 128-row T-tiles through LDS, first
 // over the features of A (Gram P) then over its chunk of G features (Gram Q),
 // both accumulated by 32x32 MFMA blocks held in registers, and reduces
 // sum w * P o Q in registers. No Gram ever leaves the chip. Splitting the G
@@ -68,9 +68,10 @@ __device__ __forceinline__ void block_rows(int w, int (&ra)[4], int (&rb)[4], fl
 // One LDS stage (64 bf16 or 32 fp32 features per row) into the NB blocks.
 // Lane l supplies row l%32 of each operand and 16-byte chunk 2*ks + l/32, so
 // both operands carry the same features in the same MFMA k-slots.
-template <int DT, int NB>
-__device__ __forceinline__ void stage_mfma(const u32x4* __restrict__ lds, const int (&ra)[4],
-                                           const int (&rb)[4], f32x16 (&acc)[NB], int lane) {
+template <int DT, int NB, int NA>
+__device__ __forceinline__ void stage_mfma(const u32x4* __restrict__ lds, const int (&ra)[NA],
+                                           const int (&rb)[NA], f32x16 (&acc)[NB], int lane) {
+  static_assert(NB <= NA, "block list");
   const int r32 = lane & 31, half = lane >> 5;
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
@@ -283,19 +284,19 @@ __global__ __launch_bounds__(GR_THREADS) void gram_norm_kernel(GramArgs args) {
 }
 
 // ---------------------------------------------------------------------------
-// Direct-load Gram kernel: bf16, 16-byte aligned rows, T <= 128 (one T-tile).
+// Direct-load Gram kernel: bf16, 16-byte aligned rows.
 // Rows go straight into LDS through LDS-writing buffer loads (lane l's 16
-// bytes land at M0 + 16*l), four 16 KB stages in a ring, two workgroups per
-// CU. Stage row r holds token r of the example, 64 features as 8 chunks,
-// logical chunk c at physical chunk swz(r, c); the MFMA reads are the same as
-// the register-staged kernel's. Rows past T read zero through the example's
-// buffer range; chunks wholly past the last feature are pointed past the
-// range; a chunk that straddles it is masked in LDS after it lands.
+// bytes land at M0 + 16*l), four stages in a ring. A stage holds 64 features
+// of the rows of the item's T-tile pair: 128 rows for a diagonal pair, 256
+// (tile ti then tile tj) for an off-diagonal one; row r holds its 8 chunks
+// with logical chunk c at physical chunk swz(r, c), so the MFMA reads are the
+// same as the register-staged kernel's. Rows past T read zero through the
+// example's buffer range; chunks wholly past the last feature are pointed
+// past the range; a chunk that straddles it is masked in LDS after it lands.
+// SINGLE (T <= 128): 16 KB stages, two workgroups per CU; otherwise 32 KB
+// stages and one workgroup per CU.
 constexpr int DG_NS = 4;
 constexpr int DG_ROWB = 128;                  // 64 bf16 per LDS row
-constexpr int DG_STB = GR_TM * DG_ROWB;       // 16 KB per stage
-constexpr int DG_LOADS = 4;                   // 1 KB loads per wave per stage
-static_assert(DG_STB == (GR_THREADS / WAVE) * DG_LOADS * 1024, "one KB per load");
 
 typedef __attribute__((address_space(3))) void lds_void_g;
 
@@ -306,8 +307,13 @@ __device__ __forceinline__ void dg_wait_vmcnt() {
 }
 
 template <int PAT>
-__device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int chunk, u32x4* ring) {
+__device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int ti, int tj,
+                                         int chunk, u32x4* ring) {
   constexpr int NB = PatNB<PAT>::NB;
+  constexpr int ROWS = PatRows<PAT>::ROWS;        // 128 or 256
+  constexpr int STB = ROWS * DG_ROWB;             // bytes per stage
+  constexpr int LOADS = STB / 1024 / (GR_THREADS / WAVE);  // 1 KB loads per wave per stage
+  constexpr int WROWS = ROWS / (GR_THREADS / WAVE);        // stage rows per wave
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const uint64_t ex_rows = (uint64_t)b * T;
@@ -328,8 +334,12 @@ __device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int c
   const int n = nX + nY;
   const uint32_t ring_base = (uint32_t)(uintptr_t)(lds_void_g*)ring;
 
-  // Load t of wave w writes stage rows r = 32w + 8t + l/8, physical chunk l%8.
+  // Wave w fills stage rows WROWS*w ..: load t writes rows r = WROWS*w + 8t +
+  // l/8 at physical chunk l%8. Stage rows 0..127 are rows of tile ti, rows
+  // 128..255 (off-diagonal pairs) rows of tile tj.
   const int lr = lane >> 3;
+  const int wr0 = WROWS * w;                               // first stage row of this wave
+  const int ex_row0 = (wr0 < GR_TM ? ti : tj) * GR_TM + (wr0 & (GR_TM - 1));
   auto issue = [&](int s) {
     const bool inX = s < nX;
     const u32x4 d = inX ? dx : dy;
@@ -337,15 +347,16 @@ __device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int c
     const int64_t c0 = inX ? (int64_t)s * 64 : y0 + (int64_t)(s - nX) * 64;
     const int64_t c1 = inX ? x1 : y1;
     const bool live = s < n;
-    const uint32_t dst = ring_base + (uint32_t)((s % DG_NS) * DG_STB) + (uint32_t)w * 32 * DG_ROWB;
+    const uint32_t dst = ring_base + (uint32_t)((s % DG_NS) * STB) + (uint32_t)wr0 * DG_ROWB;
 #pragma unroll
-    for (int t = 0; t < DG_LOADS; ++t) {
-      const int r = 32 * w + 8 * t + lr;
+    for (int t = 0; t < LOADS; ++t) {
+      const int r = wr0 + 8 * t + lr;
       const int c = (lane & 7) ^ ((r ^ (r >> 3)) & 7);
       const int64_t col = c0 + 8 * c;
       const uint32_t voff = (live && col < c1) ? (uint32_t)(lr * ld + col * 2) : nrec;
       const uint32_t m0v = (uint32_t)__builtin_amdgcn_readfirstlane((int)(dst + t * 1024));
-      const uint32_t so = (uint32_t)__builtin_amdgcn_readfirstlane((int)((32 * w + 8 * t) * ld));
+      const uint32_t so =
+          (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)(ex_row0 + 8 * t) * ld));
       // Issued from asm so that the compiler does not drain all of them before
       // every LDS read; M0 has no other user in this kernel.
       asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
@@ -359,9 +370,9 @@ __device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int c
     const int64_t c1 = inX ? x1 : y1;
     const int64_t nv = c1 - c0;  // valid features in this stage
     if (nv >= 64 || (nv & 7) == 0) return;
-    if (tid < GR_TM) {
+    if (tid < ROWS) {
       const int cp = (int)(nv >> 3), keep = (int)(nv & 7);
-      u32x4* p = ring + (s % DG_NS) * (DG_STB / 16) + tid * 8 + swz(tid, cp);
+      u32x4* p = ring + (s % DG_NS) * (STB / 16) + tid * 8 + swz(tid, cp);
       u32x4 v = *p;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -382,15 +393,177 @@ __device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int c
 #pragma unroll
     for (int e = 0; e < 16; ++e) { accP[j][e] = 0.f; accQ[j][e] = 0.f; }
 
+  // Every iteration issues one stage's loads (past the end they read zeros into
+  // a slot nobody reads), so the wait count is a constant.
 #pragma unroll
   for (int p = 0; p < DG_NS - 1; ++p) issue(p);
   auto phase = [&](int s_begin, int s_end, f32x16 (&acc)[NB]) {
     for (int s = s_begin; s < s_end; ++s) {
-      dg_wait_vmcnt<DG_LOADS * (DG_NS - 2)>();
+      dg_wait_vmcnt<LOADS * (DG_NS - 2)>();
       __syncthreads();
       fix(s);
       issue(s + DG_NS - 1);
-      stage_mfma<DT_BF16, NB>(ring + (s % DG_NS) * (DG_STB / 16), ra, rb, acc, lane);
+      stage_mfma<DT_BF16, NB>(ring + (s % DG_NS) * (STB / 16), ra, rb, acc, lane);
+    }
+  };
+  phase(0, nX, accP);
+  phase(nX, n, accQ);
+  // No load may still be writing LDS when the workgroup moves on.
+  dg_wait_vmcnt<0>();
+  float part = 0.f;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s += accP[j][e] * accQ[j][e];
+    part += wt[j] * s;
+  }
+  return part;
+}
+
+template <bool SINGLE>
+__global__ __launch_bounds__(GR_THREADS, SINGLE ? 2 : 1) void dl_gram_kernel(GramArgs args) {
+  const GramArgs& a = *(const GramArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  (void)args;
+  __shared__ __attribute__((aligned(1024))) u32x4 ring[DG_NS * (SINGLE ? GR_TM : GR_ROWS) * 8];
+  __shared__ float red[GR_THREADS / WAVE];
+  const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
+  int l = 0;
+  while (l + 1 < a.n_layers && item >= a.L[l + 1].item_begin) ++l;
+  const GramLayer& L = a.L[l];
+  uint32_t rel = item - L.item_begin;
+  const uint32_t per_b = (uint32_t)a.P * (uint32_t)L.nc;
+  const int b = (int)(rel / per_b);
+  rel -= (uint32_t)b * per_b;
+  const int pair = (int)(rel / (uint32_t)L.nc);
+  const int chunk = (int)(rel - (uint32_t)pair * L.nc);
+  int ti = 0, rem = pair;
+  while (rem >= a.n_t - ti) { rem -= a.n_t - ti; ++ti; }
+  const int tj = ti + rem;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  float part;
+  if (!SINGLE && ti != tj)
+    part = dg_item<PAT_OFF>(L, b, a.T, ti, tj, chunk, ring);
+  else if (w < 2)
+    part = dg_item<PAT_D1>(L, b, a.T, ti, tj, chunk, ring);
+  else
+    part = dg_item<PAT_D2>(L, b, a.T, ti, tj, chunk, ring);
+  part = wave_sum(part);
+  if ((threadIdx.x & 63) == 0) red[w] = part;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    a.ws[(int64_t)b * a.slots + L.slot_begin + pair * L.nc + chunk] =
+        (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// Whole-example variant for 128 < T <= 256 (bf16, aligned rows): 8 waves
+// reduce all 36 upper 32x32 blocks of the 256 x 256 Gram, so every row is
+// read once (pair items would read each T-tile twice). The blocks of row
+// pair {g, 7-g} (9 of them) go to waves g (5 blocks) and g+4 (4 blocks), so
+// each SIMD carries 9. Stages are 256 rows x 64 features (32 KB), four in a
+// ring, one workgroup per CU.
+constexpr int DW_NS = 4;
+constexpr int DW_THREADS = 512;
+constexpr int DW_ROWS = 2 * GR_TM;
+constexpr int DW_STB = DW_ROWS * DG_ROWB;
+constexpr int DW_LOADS = DW_STB / 1024 / (DW_THREADS / WAVE);
+static_assert(DW_LOADS * 8 * (DW_THREADS / WAVE) == DW_ROWS, "rows per load");
+
+template <int NB>
+__device__ __forceinline__ float dw_item(const GramLayer& L, int b, int T, int chunk, u32x4* ring) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint64_t ex_rows = (uint64_t)b * T;
+  const uint32_t ldx = (uint32_t)(L.lda * 2), ldy = (uint32_t)(L.ldg * 2);
+  const uint64_t xb = (uint64_t)L.A + ex_rows * ldx, yb = (uint64_t)L.G + ex_rows * ldy;
+  const uint32_t nrx = T * ldx, nry = T * ldy;
+  auto desc_of = [](uint64_t base, uint32_t nrec) {
+    return u32x4{(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)base),
+                 (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(base >> 32)),
+                 (uint32_t)__builtin_amdgcn_readfirstlane((int)nrec), (uint32_t)RSRC_WORD3};
+  };
+  const u32x4 dx = desc_of(xb, nrx), dy = desc_of(yb, nry);
+  const int64_t x1 = L.d_in;
+  const int64_t y0 = (int64_t)L.g0 + (int64_t)chunk * L.kg;
+  const int64_t y1 = y0 + L.kg < L.g1 ? y0 + L.kg : L.g1;
+  const int nX = (int)((x1 + 63) / 64);
+  const int nY = (int)((y1 - y0 + 63) / 64);
+  const int n = nX + nY;
+  const uint32_t ring_base = (uint32_t)(uintptr_t)(lds_void_g*)ring;
+
+  // Wave w fills stage rows 32w .. 32w+31 (example rows; past T they read 0).
+  const int lr = lane >> 3;
+  const int wr0 = 32 * w;
+  auto issue = [&](int s) {
+    const bool inX = s < nX;
+    const u32x4 d = inX ? dx : dy;
+    const uint32_t ld = inX ? ldx : ldy, nrec = inX ? nrx : nry;
+    const int64_t c0 = inX ? (int64_t)s * 64 : y0 + (int64_t)(s - nX) * 64;
+    const int64_t c1 = inX ? x1 : y1;
+    const bool live = s < n;
+    const uint32_t dst = ring_base + (uint32_t)((s % DW_NS) * DW_STB) + (uint32_t)wr0 * DG_ROWB;
+#pragma unroll
+    for (int t = 0; t < DW_LOADS; ++t) {
+      const int r = wr0 + 8 * t + lr;
+      const int c = (lane & 7) ^ ((r ^ (r >> 3)) & 7);
+      const int64_t col = c0 + 8 * c;
+      const uint32_t voff = (live && col < c1) ? (uint32_t)(lr * ld + col * 2) : nrec;
+      const uint32_t m0v = (uint32_t)__builtin_amdgcn_readfirstlane((int)(dst + t * 1024));
+      const uint32_t so =
+          (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)(wr0 + 8 * t) * ld));
+      // Issued from asm so that the compiler does not drain all of them before
+      // every LDS read; M0 has no other user in this kernel.
+      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                   :: "s"(m0v), "v"(voff), "s"(d), "s"(so));
+    }
+  };
+  auto fix = [&](int s) {
+    const bool inX = s < nX;
+    const int64_t c0 = inX ? (int64_t)s * 64 : y0 + (int64_t)(s - nX) * 64;
+    const int64_t c1 = inX ? x1 : y1;
+    const int64_t nv = c1 - c0;
+    if (nv >= 64 || (nv & 7) == 0) return;
+    if (tid < DW_ROWS) {
+      const int cp = (int)(nv >> 3), keep = (int)(nv & 7);
+      u32x4* p = ring + (s % DW_NS) * (DW_STB / 16) + tid * 8 + swz(tid, cp);
+      u32x4 v = *p;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = 2 * q;
+        v[q] = e + 1 < keep ? v[q] : (e < keep ? (v[q] & 0xFFFFu) : 0u);
+      }
+      *p = v;
+    }
+    __syncthreads();
+  };
+
+  // Block list: entry k of row pair g is (g, g+k) for k < 8-g, else
+  // (7-g, 7-g + k-(8-g)); wave g takes entries 0..4, wave g+4 entries 5..8.
+  const int g = w & 3, k0 = (w >> 2) * 5;
+  int ra[NB], rb[NB];
+  float wt[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int k = k0 + j;
+    const int bi = k < 8 - g ? g : 7 - g;
+    const int bj = k < 8 - g ? g + k : 7 - g + (k - (8 - g));
+    ra[j] = 32 * bi; rb[j] = 32 * bj; wt[j] = bi == bj ? 1.f : 2.f;
+  }
+  f32x16 accP[NB], accQ[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) { accP[j][e] = 0.f; accQ[j][e] = 0.f; }
+
+#pragma unroll
+  for (int p = 0; p < DW_NS - 1; ++p) issue(p);
+  auto phase = [&](int s_begin, int s_end, f32x16 (&acc)[NB]) {
+    for (int s = s_begin; s < s_end; ++s) {
+      dg_wait_vmcnt<DW_LOADS * (DW_NS - 2)>();
+      __syncthreads();
+      fix(s);
+      issue(s + DW_NS - 1);
+      stage_mfma<DT_BF16, NB>(ring + (s % DW_NS) * (DW_STB / 16), ra, rb, acc, lane);
     }
   };
   phase(0, nX, accP);
@@ -407,30 +580,31 @@ __device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int c
   return part;
 }
 
-__global__ __launch_bounds__(GR_THREADS, 2) void dl_gram_kernel(GramArgs args) {
+__global__ __launch_bounds__(DW_THREADS) void dl_gram_whole_kernel(GramArgs args) {
   const GramArgs& a = *(const GramArgs*)__builtin_amdgcn_kernarg_segment_ptr();
   (void)args;
-  __shared__ __attribute__((aligned(1024))) u32x4 ring[DG_NS * DG_STB / 16];
-  __shared__ float red[GR_THREADS / WAVE];
+  __shared__ __attribute__((aligned(1024))) u32x4 ring[DW_NS * DW_STB / 16];
+  // The partial sums reuse the ring: every load has landed by then.
+  float* red = (float*)ring;
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
   int l = 0;
   while (l + 1 < a.n_layers && item >= a.L[l + 1].item_begin) ++l;
   const GramLayer& L = a.L[l];
-  uint32_t rel = item - L.item_begin;
-  const uint32_t per_b = (uint32_t)L.nc;
-  const int b = (int)(rel / per_b);
-  const int chunk = (int)(rel - (uint32_t)b * per_b);
+  const uint32_t rel = item - L.item_begin;
+  const int b = (int)(rel / (uint32_t)L.nc);
+  const int chunk = (int)(rel - (uint32_t)b * L.nc);
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  float part;
-  if (w < 2)
-    part = dg_item<PAT_D1>(L, b, a.T, chunk, ring);
-  else
-    part = dg_item<PAT_D2>(L, b, a.T, chunk, ring);
+  float part = w < 4 ? dw_item<5>(L, b, a.T, chunk, ring) : dw_item<4>(L, b, a.T, chunk, ring);
   part = wave_sum(part);
+  __syncthreads();  // every wave is done reading the ring
   if ((threadIdx.x & 63) == 0) red[w] = part;
   __syncthreads();
-  if (threadIdx.x == 0)
-    a.ws[(int64_t)b * a.slots + L.slot_begin + chunk] = (red[0] + red[1]) + (red[2] + red[3]);
+  if (threadIdx.x == 0) {
+    float t = 0.f;
+#pragma unroll
+    for (int q = 0; q < DW_THREADS / WAVE; ++q) t += red[q];
+    a.ws[(int64_t)b * a.slots + L.slot_begin + chunk] = t;
+  }
 }
 
 // Work item = (example, T-tile pair (ti, tj), chunk of CR_FCHUNK features).
@@ -544,8 +718,11 @@ static void launch_gram_dt(const GramArgs& a, bool vec, hipStream_t s) {
   const dim3 g(a.n_items), blk(GR_THREADS);
   const bool single = a.n_t == 1;
   if constexpr (DT == DT_BF16) {
-    if (vec && single) {
-      hipLaunchKernelGGL(dl_gram_kernel, g, blk, 0, s, a);
+    if (vec) {
+      if (single) hipLaunchKernelGGL(dl_gram_kernel<true>, g, blk, 0, s, a);
+      else if (gram_whole(DT, vec, a.T))
+        hipLaunchKernelGGL(dl_gram_whole_kernel, g, dim3(DW_THREADS), 0, s, a);
+      else hipLaunchKernelGGL(dl_gram_kernel<false>, g, blk, 0, s, a);
       return;
     }
   }

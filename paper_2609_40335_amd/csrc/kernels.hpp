@@ -10,6 +10,12 @@ enum { DT_F32 = 0, DT_BF16 = 1 };  // element type of the float operands
 // ----------------------------------------------------------------- Gram norm
 constexpr int GR_TM = 128;          // rows of one T-tile
 constexpr int GR_MAX_LAYERS = 52;   // layers per launch (kernel arguments stay < 4 KiB)
+// bf16 launches with aligned rows and 128 < T <= 256 reduce each example's
+// whole 256 x 256 Gram in one work item (one partial slot per chunk) instead
+// of one item per T-tile pair.
+inline bool gram_whole(int dt, bool vec, int T) {
+  return dt == DT_BF16 && vec && T > GR_TM && T <= 2 * GR_TM;
+}
 
 struct GramLayer {
   const void* A;        // [B*T rows, lda] activations

@@ -57,6 +57,7 @@ NORM_CASES = [
     ("bf16", 2, 17, 24, 5000, None, 5008),     # G chunked (> 4096 features) + ragged tail
     ("bf16", 1, 1, 8, 8, None, None),          # T = 1
     ("bf16", 3, 96, 100, 77, 104, 80),         # last chunk straddles d, aligned strides
+    ("bf16", 2, 200, 64, 4500, None, 4504),    # two T-tiles (off-diagonal pair) + G chunks
 ]
 
 
