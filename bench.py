@@ -56,6 +56,9 @@ def parse(argv=None):
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--crossover", action="store_true",
+                    help="instead of the step: time each distinct layer shape's grouped norm "
+                         "with the Gram kernel and with the direct kernel (one JSON line)")
     return ap.parse_args(argv)
 
 
@@ -112,6 +115,7 @@ class Step:
             self.seg = torch.empty((B, T), dtype=torch.int32, device="cuda")
             self.nu = torch.empty(B, dtype=torch.int32, device="cuda")
         assert off == self.n_coords
+        self.norm_layers = norm_layers
         self.norm_group = dp.LinearGroup(norm_layers)
         self.sum_group = dp.LinearGroup(sum_layers, sum_outs) if sum_layers else None
         self.n2 = torch.zeros(B, device="cuda")
@@ -153,6 +157,44 @@ class Step:
         self.step_id += 1
 
 
+def crossover(st, dp, torch, reps=10):
+    """Row a10: per distinct (d_in, d_out) of the workload, the grouped norm of
+    all layers of that shape with the T x T Gram kernel and with the direct
+    per-example GEMM, next to the flop-count rule T + 1 > 2 d_in d_out / (d_in + d_out)."""
+    B, T = st.wl.B, st.wl.T
+    by_shape = {}
+    for A, G in st.norm_layers:
+        by_shape.setdefault((A.shape[2], G.shape[2]), []).append((A, G))
+    rows = []
+    for (d_in, d_out), layers in by_shape.items():
+        us = {}
+        for name, algo in (("gram", dp.DP_NORM_GRAM), ("direct", dp.DP_NORM_DIRECT)):
+            grp = dp.LinearGroup([(a, g, algo) for a, g in layers])
+            n2 = torch.zeros(B, device="cuda")
+            for _ in range(2):
+                grp.ghost_norm(n2)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                grp.ghost_norm(n2)
+            e1.record()
+            torch.cuda.synchronize()
+            us[name] = e0.elapsed_time(e1) / reps * 1e3
+        rule = "direct" if T + 1 > 2.0 * d_in * d_out / (d_in + d_out) else "gram"
+        gram_flop = float(len(layers)) * B * T * (T + 1) * (d_in + d_out)
+        direct_flop = float(len(layers)) * B * 2.0 * T * d_in * d_out
+        rows.append({"d_in": d_in, "d_out": d_out, "layers": len(layers),
+                     "gram_us": round(us["gram"], 1), "direct_us": round(us["direct"], 1),
+                     "gram_tflops": round(gram_flop / us["gram"] / 1e6, 1),
+                     "direct_tflops": round(direct_flop / us["direct"] / 1e6, 1),
+                     "flop_rule": rule,
+                     "faster": "direct" if us["direct"] < us["gram"] else "gram"})
+        log(f"[bench] crossover d_in={d_in} d_out={d_out} x{len(layers)}: gram {us['gram']:.1f} us, "
+            f"direct {us['direct']:.1f} us (rule: {rule})")
+    return rows
+
+
 def cpu_baseline(wl, n_coords, budget):
     """The fp64 oracle on the host: per-example work on a sample of examples,
     noise on a slice of coordinates, extrapolated to one full step."""
@@ -191,7 +233,7 @@ def cpu_baseline(wl, n_coords, budget):
 def main(argv=None) -> int:
     args = parse(argv)
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the library has no "
               f"multi-GPU path. Run with --gpus 1.", file=sys.stderr)
         return 2
     import numpy as np  # noqa: F401
@@ -211,6 +253,12 @@ def main(argv=None) -> int:
     st = Step(wl, dp, torch)
     log(f"[bench] {len(wl.linears)} linear layers, head={'none' if wl.head is None else ('tied' if wl.head.tied else 'untied')}, "
         f"{st.n_coords} gradient coordinates")
+
+    if args.crossover:
+        rows = crossover(st, dp, torch)
+        print(json.dumps({"crossover": rows, "workload": args.workload, "B": wl.B, "T": wl.T}),
+              flush=True)
+        return 0
 
     for _ in range(args.warmup):
         st.run()

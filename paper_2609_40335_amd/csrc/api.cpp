@@ -84,11 +84,14 @@ struct NormPlan {
   int64_t slots = 0;
 };
 
+// Gram flops T(T+1)(d_in+d_out) against direct flops 2 T d_in d_out, the
+// Gram's weighted by the measured ratio of the two kernels' throughputs.
+constexpr double GRAM_VS_DIRECT_THROUGHPUT = 0.57;
 bool use_direct(const dp_linear_t& L, int T) {
   if (L.algo == DP_NORM_DIRECT) return true;
   if (L.algo == DP_NORM_GRAM) return false;
   const double crossover = 2.0 * (double)L.d_in * L.d_out / ((double)L.d_in + L.d_out);
-  return (double)T + 1.0 > crossover;
+  return (double)T + 1.0 > GRAM_VS_DIRECT_THROUGHPUT * crossover;
 }
 
 // One GEMM entry over the output region [0,M) x [0,N); 16-byte loads when

@@ -468,6 +468,10 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// MODE_SUM: the clipped sum over all K = B*T rows. MODE_NORM (the direct
+// norm): K restricted to example b's T rows, no factors, and the tile's
+// in-range elements squared and summed in registers.
+template <int MODE>
 __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
   const GemmArgs& a = *(const GemmArgs*)__builtin_amdgcn_kernarg_segment_ptr();
   (void)args;
@@ -479,8 +483,17 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
   int l = 0;
   while (l + 1 < a.n_layers && item >= a.L[l + 1].tile_begin) ++l;
   const GemmLayer& L = a.L[l];
-  const uint32_t rel = item - L.tile_begin;
+  uint32_t rel = item - L.tile_begin;
   const int64_t K = (int64_t)a.B * a.T;
+  int b = 0;
+  int64_t k_begin = 0, k_end = K;
+  if constexpr (MODE == MODE_NORM) {
+    const uint32_t ntile = (uint32_t)L.tm * (uint32_t)L.tn;
+    b = (int)(rel / ntile);
+    rel -= (uint32_t)b * ntile;
+    k_begin = (int64_t)b * a.T;
+    k_end = k_begin + a.T;
+  }
   const int mt = (int)(rel / (uint32_t)L.tn), nt = (int)(rel - (uint32_t)mt * L.tn);
   const int64_t m0 = (int64_t)mt * GM_BM;
   const int64_t n0 = (int64_t)nt * GM_BN;
@@ -510,11 +523,11 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
                       (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(gbase >> 32)),
                       (uint32_t)__builtin_amdgcn_readfirstlane((int)nrec), (uint32_t)RSRC_WORD3};
   const uint32_t ring_base = (uint32_t)(uintptr_t)ring;
-  const int nS = (int)(K / DL_BK);
+  const int nS = (int)((k_end - k_begin) / DL_BK);
   auto issue = [&](int s) {
     const uint32_t dst = ring_base + (uint32_t)((s % DL_NS) * DL_STB) + lds_role;
-    const int64_t row0 = (int64_t)s * DL_BK + wq * 8;
-    const uint32_t sbase = row0 < K ? (uint32_t)(row0 * ld_bytes) : nrec;
+    const int64_t row0 = k_begin + (int64_t)s * DL_BK + wq * 8;
+    const uint32_t sbase = s < nS ? (uint32_t)(row0 * ld_bytes) : nrec;
 #pragma unroll
     for (int t = 0; t < DL_LOADS; ++t) {
       const uint32_t m0v = (uint32_t)__builtin_amdgcn_readfirstlane((int)(dst + t * 1024));
@@ -552,12 +565,13 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  for (int i = tid; i < a.B; i += GM_THREADS) cs[i] = a.c[i];
+  if constexpr (MODE == MODE_SUM)
+    for (int i = tid; i < a.B; i += GM_THREADS) cs[i] = a.c[i];
   const int spe = a.T / DL_BK;  // stages per example
   float c_acc = 0.f;            // factor of what is accumulated; 0: nothing yet
   bool skip = false;
   auto enter = [&](int s) {
-    if (s % spe == 0) {
+    if (MODE == MODE_SUM && s % spe == 0) {
       const float ce = cs[s / spe];
       skip = !(ce != 0.f);
       if (!skip) {
@@ -604,11 +618,41 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
   }
   // No load may still be writing LDS when the workgroup ends.
   wait_vmcnt<0>();
+  if constexpr (MODE == MODE_SUM) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] *= c_acc;
-  store_tile(a, L, m0, n0, wm, wn, lane, acc);
+      for (int j = 0; j < 2; ++j) acc[i][j] *= c_acc;
+    store_tile(a, L, m0, n0, wm, wn, lane, acc);
+  } else {
+    // Columns past M or N were loaded from beyond the rows' valid width and
+    // only reach out-of-range elements, which the sum leaves out.
+    const int mw = (int)m0 + wm * 128 + (lane >> 5) * 4;
+    const int nw = (int)n0 + wn * 64 + (lane & 31);
+    float part = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const bool nin = nw + j * 32 < L.N;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = mw + i * 32 + (e >> 2) * 8 + (e & 3);
+          const float v = acc[i][j][e];
+          part += (nin && m < L.M) ? v * v : 0.f;
+        }
+      }
+    part = wave_sum(part);
+    float* red = cs;  // the factor table is unused in this mode
+    if (lane == 0) red[w] = part;
+    __syncthreads();
+    if (tid == 0) {
+      float t = 0.f;
+#pragma unroll
+      for (int q = 0; q < GM_THREADS / WAVE; ++q) t += red[q];
+      a.ws[(int64_t)b * a.slots + L.slot_begin + rel] = t;
+    }
+  }
 }
 
 template <int DT, bool VEC, int MODE>
@@ -630,8 +674,8 @@ static hipError_t launch_kt(const GemmArgs& a, int dt, bool vec, hipStream_t s) 
   // The accumulator form needs every K-stage inside one example.
   const int ks = dt == DT_BF16 ? KT<DT_BF16>::KS : KT<DT_F32>::KS;
   const int sc = MODE == MODE_NORM ? SC_NONE : (a.T % ks == 0 ? SC_ACC : SC_STAGE);
-  if (MODE == MODE_SUM && dt == DT_BF16 && vec && a.T % DL_BK == 0 && a.B <= DL_MAXB) {
-    hipLaunchKernelGGL(dl_gemm_kernel, dim3(a.n_items), dim3(GM_THREADS), 0, s, a);
+  if (dt == DT_BF16 && vec && a.T % DL_BK == 0 && (MODE == MODE_NORM || a.B <= DL_MAXB)) {
+    hipLaunchKernelGGL(dl_gemm_kernel<MODE>, dim3(a.n_items), dim3(GM_THREADS), 0, s, a);
     return hipGetLastError();
   }
   if (dt == DT_BF16) {

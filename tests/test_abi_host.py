@@ -70,10 +70,15 @@ def test_norm_workspace_sizes(L):
     assert L.dp_ghost_norm_linear_workspace(head, 1, 1000, 128, D.DP_BF16) == 0
     assert L.dp_ghost_norm_linear_grouped(head, 1, 1000, 128, D.DP_BF16, 1 << 22, 0, 1 << 23,
                                           1 << 30, None) == EUNSUP
-    # AUTO picks the direct form once T + 1 > 2 d_in d_out / (d_in + d_out) = 64:
-    # one 256x256 output tile per example
+    # AUTO picks the direct form once T + 1 > 0.57 * 2 d_in d_out / (d_in + d_out)
+    # (0.57 * 64 here): one 256x256 output tile per example
     auto = (D.dp_linear_t * 1)(_lin())
     assert L.dp_ghost_norm_linear_workspace(auto, 1, 100, 300, D.DP_F32) == 512
+    # at d_in = d_out = 512 the switch sits at T + 1 > 291.84: T = 290 keeps the
+    # Gram (3 T-tiles, 6 pairs per example), T = 291 goes direct (2 x 2 tiles)
+    sq = (D.dp_linear_t * 1)(_lin(d_in=512, lda=512, d_out=512, ldg=512))
+    assert L.dp_ghost_norm_linear_workspace(sq, 1, 100, 290, D.DP_F32) == 2560
+    assert L.dp_ghost_norm_linear_workspace(sq, 1, 100, 291, D.DP_F32) == 1792
     assert L.dp_ghost_norm_linear_workspace(None, 1, 4, 16, D.DP_F32) == 0
 
 

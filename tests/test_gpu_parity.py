@@ -58,6 +58,7 @@ NORM_CASES = [
     ("bf16", 1, 1, 8, 8, None, None),          # T = 1
     ("bf16", 3, 96, 100, 77, 104, 80),         # last chunk straddles d, aligned strides
     ("bf16", 2, 200, 64, 4500, None, 4504),    # two T-tiles (off-diagonal pair) + G chunks
+    ("bf16", 3, 64, 300, 520, None, None),     # 2 x 3 ragged output tiles for the direct norm
 ]
 
 
