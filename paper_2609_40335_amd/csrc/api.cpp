@@ -229,18 +229,15 @@ dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int
 
 size_t norm_ws_bytes(const NormPlan& p, int B) { return align_up((size_t)B * p.slots * 4); }
 
-// Embedding-sum workspace layout (bytes): keys, rank, seg, nseg, head, tail.
+// Embedding-sum workspace layout (bytes): sorted keys, block head/tail partials.
 struct EsLayout {
-  size_t keys, rank, seg, nseg, head, tail, total;
+  size_t keys, head, tail, total;
 };
 EsLayout es_layout(int64_t K, int d) {
   EsLayout l{};
   const int64_t nb = ceil_div(K, dpg::ES_BLOCK);
   size_t off = 0;
   l.keys = off; off = align_up(off + (size_t)K * 4);
-  l.rank = off; off = align_up(off + (size_t)K * 4);
-  l.seg = off; off = align_up(off + (size_t)(K + 1) * 4);
-  l.nseg = off; off = align_up(off + 4);
   l.head = off; off = align_up(off + (size_t)nb * d * 4);
   l.tail = off; off = align_up(off + (size_t)nb * d * 4);
   l.total = off;
@@ -428,7 +425,7 @@ dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64
   if (K > dpg::ES_MAX_K)
     return fail(DP_EUNSUPPORTED, "B*T = %lld exceeds %d", (long long)K, dpg::ES_MAX_K);
   const int pbits = std::max(1, bits_for(K));
-  if (bits_for(d_in) + pbits > 32)
+  if (bits_for((int64_t)d_in + 1) + pbits > 32)  // ids are clamped to V, so V + 1 values
     return fail(DP_EUNSUPPORTED, "V and B*T do not fit a 32-bit sort key");
   const EsLayout l = es_layout(K, d_out);
   if (!workspace || workspace_bytes < l.total)
@@ -444,9 +441,6 @@ dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64
   a.B = B; a.K = (int32_t)K; a.T = T; a.V = d_in; a.d = d_out;
   a.pbits = pbits;
   a.keys = reinterpret_cast<uint32_t*>(w + l.keys);
-  a.rank = reinterpret_cast<int32_t*>(w + l.rank);
-  a.seg = reinterpret_cast<int32_t*>(w + l.seg);
-  a.nseg = reinterpret_cast<int32_t*>(w + l.nseg);
   a.head = reinterpret_cast<float*>(w + l.head);
   a.tail = reinterpret_cast<float*>(w + l.tail);
   a.out = out;

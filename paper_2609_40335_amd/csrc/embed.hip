@@ -10,8 +10,8 @@
 // LDS (bitonic), marks the first token of each run of equal ids, and turns the
 // marks into dense ranks with a wavefront-shuffle prefix scan. The norm then
 // sums each bucket's rows (lanes = 64 features, coalesced row reads) and
-// squares. The clipped sum sorts all B*T tokens of the batch the same way and
-// reduces runs of equal ids in fixed 32-token blocks; a run that crosses a
+// squares. The clipped sum sorts all B*T tokens of the batch (radix sort on
+// the ids, below) and reduces runs of equal ids in fixed 32-token blocks; a run that crosses a
 // block boundary is closed by a fix-up pass that adds the block partials in
 // order. Every output row is written by exactly one wave: no atomics, and
 // results are bitwise reproducible.
@@ -144,19 +144,73 @@ __global__ __launch_bounds__(EN_THREADS) void embed_norm_kernel(EmbedNormArgs a)
 // Batch-wide clipped sum of the input embedding:
 // out[v, f] (+)= sum over tokens k with ids[k] = v of c[k / T] * E[k, f].
 // ---------------------------------------------------------------------------
+// Sorts the batch's keys (id << pbits | position) by id with a stable LSD
+// radix sort on the id bits, 8 bits per pass, in one workgroup: the keys
+// arrive in position order, so a stable sort on the id alone yields the
+// (id, position) order. Wave w owns a contiguous segment of the keys. A pass
+// counts digits per wave, turns the (digit, wave) counts into offsets in
+// digit-major, wave-minor order, and scatters each wave's keys 64 at a time:
+// lanes with equal digits are found with eight ballots, ranked by lane, and
+// the group's lowest lane advances the wave's running count. Ids at or past V
+// are clamped to V, so they sort last and every valid id stays one run.
+constexpr int RS_WAVES = ES_THREADS / WAVE;
+constexpr int RS_RADIX = 256;
+
 __global__ __launch_bounds__(ES_THREADS) void embed_sort_kernel(EmbedSumArgs a) {
-  __shared__ uint32_t keys[ES_MAX_K];
+  __shared__ uint32_t buf[2][ES_MAX_K];
+  __shared__ int cnt[RS_WAVES][RS_RADIX];
   __shared__ int wave_tot[ES_THREADS / WAVE];
-  const int tid = threadIdx.x, K = a.K;
-  int n2 = 1;
-  while (n2 < K) n2 <<= 1;
-  for (int p = tid; p < n2; p += ES_THREADS)
-    keys[p] = p < K ? ((((uint32_t)a.ids[p]) << a.pbits) | (uint32_t)p) : 0xFFFFFFFFu;
-  __syncthreads();
-  bitonic_sort(keys, n2, tid, ES_THREADS);
-  for (int p = tid; p < K; p += ES_THREADS) a.keys[p] = keys[p];
-  const int nseg = rank_sorted(keys, K, a.pbits, a.rank, a.seg, wave_tot, tid, ES_THREADS);
-  if (tid == 0) *a.nseg = nseg;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, K = a.K, pb = a.pbits;
+  const uint32_t V = (uint32_t)a.V;
+  for (int p = tid; p < K; p += ES_THREADS) {
+    const uint32_t id = (uint32_t)a.ids[p];
+    buf[0][p] = ((id < V ? id : V) << pb) | (uint32_t)p;
+  }
+  int idbits = 0;  // bits of the values 0..V
+  while ((1u << idbits) <= V) ++idbits;
+  const int seg_len = ((K + RS_WAVES - 1) / RS_WAVES + WAVE - 1) / WAVE * WAVE;
+  const int s0 = min(w * seg_len, K), s1 = min(s0 + seg_len, K);
+  const uint64_t lt = (1ull << lane) - 1ull;
+  int src = 0;
+  for (int shift = 0; shift < idbits; shift += 8, src ^= 1) {
+    const int sh = pb + shift;
+    for (int i = tid; i < RS_WAVES * RS_RADIX; i += ES_THREADS) (&cnt[0][0])[i] = 0;
+    __syncthreads();
+    for (int p = s0 + lane; p < s1; p += WAVE) atomicAdd(&cnt[w][(buf[src][p] >> sh) & 255], 1);
+    __syncthreads();
+    // Exclusive offsets in (digit, wave) order; thread t holds entries
+    // 4t .. 4t+3 of that order, i.e. digit t/4, waves 4(t%4) .. +3.
+    {
+      const int d = tid >> 2, w0 = (tid & 3) * 4;
+      int v[4], loc = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { v[q] = cnt[w0 + q][d]; loc += v[q]; }
+      int total;
+      const int incl = block_inclusive_scan(loc, wave_tot, tid, ES_THREADS, &total);
+      int run = incl - loc;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { cnt[w0 + q][d] = run; run += v[q]; }
+    }
+    __syncthreads();
+    for (int base = s0; base < s1; base += WAVE) {
+      const int p = base + lane;
+      const bool valid = p < s1;
+      const uint32_t key = valid ? buf[src][p] : 0u;
+      const int dg = (int)((key >> sh) & 255);
+      uint64_t m = __ballot(valid);
+#pragma unroll
+      for (int bit = 0; bit < 8; ++bit) {
+        const uint64_t mb = __ballot(valid && ((dg >> bit) & 1));
+        m &= ((dg >> bit) & 1) ? mb : ~mb;
+      }
+      const int rank = __popcll(m & lt);
+      const int off = valid ? cnt[w][dg] : 0;
+      if (valid) buf[src ^ 1][off + rank] = key;
+      if (valid && rank == 0) cnt[w][dg] = off + __popcll(m);
+    }
+    __syncthreads();
+  }
+  for (int p = tid; p < K; p += ES_THREADS) a.keys[p] = buf[src][p];
 }
 
 __device__ __forceinline__ float example_scale(const float* c, int64_t k, double invT, int B) {
@@ -229,7 +283,7 @@ __global__ __launch_bounds__(ES_WAVES * WAVE) void embed_fixup_kernel(EmbedSumAr
   if (p1 >= K) return;
   const uint32_t id = a.keys[p1 - 1] >> pb;
   if ((a.keys[p1] >> pb) != id) return;             // last run ends in this block
-  if (a.seg[a.rank[p1 - 1]] < p0) return;           // it started in an earlier block
+  if (p0 > 0 && (a.keys[p0 - 1] >> pb) == id) return;  // it started in an earlier block
   if (f >= a.d) return;
   float acc = a.tail[(int64_t)q * a.d + f];
   for (int qq = q + 1; qq < n_blocks; ++qq) {

@@ -120,9 +120,6 @@ struct EmbedSumArgs {
   int32_t B, K, T, V, d;
   int32_t pbits;        // bits for a token index in a sort key
   uint32_t* keys;       // workspace [K] sorted keys
-  int32_t* rank;        // workspace [K] bucket of each sorted position
-  int32_t* seg;         // workspace [K+1] first sorted position of each bucket
-  int32_t* nseg;        // workspace [1]
   float* head;          // workspace [n_blocks, d] partial of the run a block starts inside
   float* tail;          // workspace [n_blocks, d] partial of the run a block ends inside
   float* out;           // [V, ldo] or transposed [d, ldo]; accumulated into

@@ -341,6 +341,26 @@ def test_clipped_sum_embedding(dp, dtype, B, T, V, d, kind):
     assert fro_rel(host(outT).T, ref) <= TOL[dtype]
 
 
+def test_clipped_sum_embedding_invalid_ids(dp):
+    """Ids outside [0, V) contribute nothing (header contract); they sort after
+    every valid id, so each valid id still forms one run."""
+    B, T, V, d = 4, 96, 300, 72
+    ids = gen.draw_ids(12, 1, (B, T), V, "zipf")
+    bad = np.zeros((B, T), bool)
+    bad[:, ::7] = True
+    ids = ids.copy()
+    ids[bad] = np.where(np.arange(bad.sum()) % 2 == 0, -1, V + 7)
+    dE = gen.draw(12, 2, (B, T, d), 1e-2, "bf16")
+    c = np.linspace(0.4, 1.0, B).astype(np.float32)
+    ids_ref = np.where(bad, 0, ids)
+    dE_ref = O.decode(dE, "bf16").copy()
+    dE_ref[bad] = 0.0
+    ref = O.clipped_sum_embedding(ids_ref, dE_ref, c.astype(np.float64), V)
+    out = torch.full((V, d), 2.0, device="cuda")
+    dp.dp_clipped_grad_sum(None, dev(dE, "bf16"), dev(c), out, ids=dev(ids), V=V)
+    assert fro_rel(host(out), ref) <= TOL["bf16"]
+
+
 @pytest.mark.parametrize("T,ldz", [(100, 1001), (64, 1008)])   # general / direct-load head
 def test_tied_clipped_sum_one_buffer(dp, T, ldz):
     """Tied E: the head sum and the embedding sum land in one [V, d] buffer."""
