@@ -335,10 +335,21 @@ dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t 
                     "finish launch");
 }
 
+// Partials per example: (128-row tile pair, 128-feature chunk) for the
+// register-staged kernel, (64-row block pair) for the direct-load one. The
+// size query cannot know which kernel a call takes, so it covers both.
+int64_t cross_slots(int T, int d, bool direct) {
+  if (direct) {
+    const int64_t nq = ceil_div(T, dpg::CR_DL_ROWS);
+    return nq * nq;
+  }
+  const int64_t nt = ceil_div(T, dpg::GR_TM);
+  return nt * nt * ceil_div(d, dpg::CR_FCHUNK);
+}
+
 size_t dp_tied_cross_term_workspace(int B, int T, int d) {
   if (B <= 0 || T <= 0 || d <= 0) return 0;
-  const int64_t nt = ceil_div(T, dpg::GR_TM);
-  return align_up((size_t)B * nt * nt * ceil_div(d, dpg::CR_FCHUNK) * 4);
+  return align_up((size_t)B * std::max(cross_slots(T, d, true), cross_slots(T, d, false)) * 4);
 }
 
 dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, const void* H,
@@ -361,11 +372,12 @@ dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, 
   a.ids = ids; a.E = dE; a.H = H; a.Gz = Gz;
   a.lde = lde; a.ldh = ldh; a.ldz = ldz;
   a.B = B; a.T = T; a.V = V; a.d = d;
-  a.n_t = (int)ceil_div(T, dpg::GR_TM);
-  a.n_fc = (int)ceil_div(d, dpg::CR_FCHUNK);
-  a.slots = a.n_t * a.n_t * a.n_fc;
-  a.ws = static_cast<float*>(workspace);
   const bool vec = vec_ok(dE, lde, dt) && vec_ok(H, ldh, dt);
+  const bool direct = dpg::cross_direct(kdt(dt), vec);
+  a.n_t = (int)ceil_div(T, direct ? dpg::CR_DL_ROWS : dpg::GR_TM);
+  a.n_fc = direct ? 1 : (int)ceil_div(d, dpg::CR_FCHUNK);
+  a.slots = (int32_t)cross_slots(T, d, direct);
+  a.ws = static_cast<float*>(workspace);
   hipStream_t s = as_stream(stream);
   dp_status_t st = hip_status(dpg::launch_tied_cross(a, kdt(dt), vec, s), "tied_cross launch");
   if (st != DP_OK) return st;

@@ -213,19 +213,18 @@ __global__ __launch_bounds__(ES_THREADS) void embed_sort_kernel(EmbedSumArgs a) 
   for (int p = tid; p < K; p += ES_THREADS) a.keys[p] = buf[src][p];
 }
 
-__device__ __forceinline__ float example_scale(const float* c, int64_t k, double invT, int B) {
-  int64_t e = (int64_t)(((double)k + 0.5) * invT);
-  if (e >= B) e = B - 1;
-  return c[e];
-}
-
 __device__ __forceinline__ void out_add(const EmbedSumArgs& a, uint32_t v, int f, float val) {
   if (v >= (uint32_t)a.V) return;  // invalid id: contributes nothing
   float* o = a.transpose ? a.out + (int64_t)f * a.ldo + v : a.out + (int64_t)v * a.ldo + f;
   *o += val;
 }
 
-// One wave per (block of ES_BLOCK sorted tokens, 64-feature chunk).
+// One wave per (block of ES_BLOCK sorted tokens, 64-feature chunk). Lanes
+// 0..ES_BLOCK-1 first fetch the block's keys and the tokens' clip factors;
+// then every lane (one feature) issues the loads of all ES_BLOCK rows back to
+// back, and the runs of equal ids are closed in order with the keys broadcast
+// from the lanes that hold them.
+static_assert(ES_BLOCK <= WAVE, "one key per lane");
 template <int DT>
 __global__ __launch_bounds__(ES_WAVES * WAVE) void embed_block_kernel(EmbedSumArgs a) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -238,33 +237,43 @@ __global__ __launch_bounds__(ES_WAVES * WAVE) void embed_block_kernel(EmbedSumAr
   const bool fok = f < a.d;
   const int K = a.K, pb = a.pbits;
   const uint32_t pmask = (1u << pb) - 1u;
-  const int p0 = q * ES_BLOCK, p1 = min(p0 + ES_BLOCK, K);
-  const double invT = 1.0 / (double)a.T;
-  const bool starts_before = p0 > 0 && (a.keys[p0 - 1] >> pb) == (a.keys[p0] >> pb);
-  const bool ends_after = p1 < K && (a.keys[p1] >> pb) == (a.keys[p1 - 1] >> pb);
+  const int p0 = q * ES_BLOCK, n = min(ES_BLOCK, K - p0);
+  // Keys of this block (lane j < n holds key p0 + j) and their factors.
+  const uint32_t mykey = lane < n ? a.keys[p0 + lane] : 0xFFFFFFFFu;
+  const float myc = lane < n ? a.c[(int)((mykey & pmask) / (uint32_t)a.T)] : 0.f;
+  const uint32_t id_before = p0 > 0 ? (a.keys[p0 - 1] >> pb) : 0xFFFFFFFFu;
+  const uint32_t id_after = p0 + n < K ? (a.keys[p0 + n] >> pb) : 0xFFFFFFFFu;
+  float ev[ES_BLOCK];
+#pragma unroll
+  for (int j = 0; j < ES_BLOCK; ++j) {
+    const uint32_t kj = (uint32_t)__builtin_amdgcn_readlane((int)mykey, j);
+    const float cj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, myc), j));
+    ev[j] = (j < n && fok) ? cj * load_elem<DT>(a.E, (int64_t)(kj & pmask) * a.lde + f) : 0.f;
+  }
   float acc = 0.f;
-  int run_start = p0;
-  uint32_t key = a.keys[p0];
-  for (int p = p0; p < p1; ++p) {
-    const uint32_t next = (p + 1 < K) ? a.keys[p + 1] : 0xFFFFFFFFu;
-    const int64_t k = key & pmask;
-    if (fok) acc += example_scale(a.c, k, invT, a.B) * load_elem<DT>(a.E, k * a.lde + f);
-    const bool last = (p + 1 == p1) || ((next >> pb) != (key >> pb));
+  int run_start = 0;
+#pragma unroll
+  for (int j = 0; j < ES_BLOCK; ++j) {
+    if (j >= n) break;
+    const uint32_t id = (uint32_t)__builtin_amdgcn_readlane((int)mykey, j) >> pb;
+    const uint32_t nid = j + 1 < n ? ((uint32_t)__builtin_amdgcn_readlane((int)mykey, j + 1) >> pb)
+                                   : id_after;
+    acc += ev[j];
+    const bool last = (j + 1 == n) || (nid != id);
     if (last) {
-      const bool open_head = (run_start == p0) && starts_before;
-      const bool open_tail = (p + 1 == p1) && ends_after;
+      const bool open_head = run_start == 0 && id_before == id;
+      const bool open_tail = j + 1 == n && id_after == id;
       if (fok) {
         if (open_head)
           a.head[(int64_t)q * a.d + f] = acc;
         else if (open_tail)
           a.tail[(int64_t)q * a.d + f] = acc;
         else
-          out_add(a, key >> pb, f, acc);
+          out_add(a, id, f, acc);
       }
       acc = 0.f;
-      run_start = p + 1;
+      run_start = j + 1;
     }
-    key = next;
   }
 }
 

@@ -607,6 +607,119 @@ __global__ __launch_bounds__(DW_THREADS) void dl_gram_whole_kernel(GramArgs args
   }
 }
 
+// Direct-load cross term (bf16, aligned rows). Work item = (example b,
+// 64-row block qi of dE, 64-row block qj of H), over all d features, so the
+// logit gradients are gathered once per product element. A stage holds 64
+// features of the 64 dE rows (stage rows 0..63) and the 64 H rows (64..127),
+// four stages in a ring, two workgroups per CU; wave w owns the 32x32 block
+// (dE rows 32*(w&1), H rows 32*(w>>1)) of the 64x64 product.
+constexpr int DC_ROWS = 128;
+constexpr int DC_STB = DC_ROWS * DG_ROWB;     // 16 KB
+constexpr int DC_LOADS = DC_STB / 1024 / (GR_THREADS / WAVE);
+
+__global__ __launch_bounds__(GR_THREADS, 2) void dl_cross_kernel(CrossArgs a) {
+  __shared__ __attribute__((aligned(1024))) u32x4 ring[DG_NS * DC_STB / 16];
+  __shared__ float red[GR_THREADS / WAVE];
+  const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
+  const int b = (int)(item / (uint32_t)a.slots);
+  const int slot = (int)(item - (uint32_t)b * a.slots);
+  const int nq = a.n_t;  // 64-row blocks per example in this kernel
+  const int qi = slot / nq, qj = slot - qi * nq;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int T = a.T;
+  const uint64_t ex_rows = (uint64_t)b * T;
+  const uint32_t lde = (uint32_t)(a.lde * 2), ldh = (uint32_t)(a.ldh * 2);
+  auto desc_of = [](uint64_t base, uint32_t nrec) {
+    return u32x4{(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)base),
+                 (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(base >> 32)),
+                 (uint32_t)__builtin_amdgcn_readfirstlane((int)nrec), (uint32_t)RSRC_WORD3};
+  };
+  const bool load_e = w < 2;  // waves 0-1 load dE rows, 2-3 H rows
+  const uint32_t ld = load_e ? lde : ldh;
+  const uint32_t nrec = (uint32_t)T * ld;
+  const u32x4 d = desc_of((uint64_t)(load_e ? a.E : a.H) + ex_rows * ld, nrec);
+  const int wr0 = 32 * w;                                   // first stage row of this wave
+  const int ex_row0 = (load_e ? qi : qj) * 64 + (wr0 & 63); // its example row
+  const int n = (a.d + 63) / 64;
+  const uint32_t ring_base = (uint32_t)(uintptr_t)(lds_void_g*)ring;
+  const int lr = lane >> 3;
+  auto issue = [&](int s) {
+    const int64_t c0 = (int64_t)s * 64;
+    const bool live = s < n;
+    const uint32_t dst = ring_base + (uint32_t)((s % DG_NS) * DC_STB) + (uint32_t)wr0 * DG_ROWB;
+#pragma unroll
+    for (int t = 0; t < DC_LOADS; ++t) {
+      const int r = wr0 + 8 * t + lr;
+      const int c = (lane & 7) ^ ((r ^ (r >> 3)) & 7);
+      const int64_t col = c0 + 8 * c;
+      const uint32_t voff = (live && col < a.d) ? (uint32_t)(lr * ld + col * 2) : nrec;
+      const uint32_t m0v = (uint32_t)__builtin_amdgcn_readfirstlane((int)(dst + t * 1024));
+      const uint32_t so =
+          (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)(ex_row0 + 8 * t) * ld));
+      // Issued from asm so that the compiler does not drain all of them before
+      // every LDS read; M0 has no other user in this kernel.
+      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                   :: "s"(m0v), "v"(voff), "s"(d), "s"(so));
+    }
+  };
+  auto fix = [&](int s) {
+    const int64_t nv = (int64_t)a.d - (int64_t)s * 64;
+    if (nv >= 64 || (nv & 7) == 0) return;
+    if (tid < DC_ROWS) {
+      const int cp = (int)(nv >> 3), keep = (int)(nv & 7);
+      u32x4* p = ring + (s % DG_NS) * (DC_STB / 16) + tid * 8 + swz(tid, cp);
+      u32x4 v = *p;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = 2 * q;
+        v[q] = e + 1 < keep ? v[q] : (e < keep ? (v[q] & 0xFFFFu) : 0u);
+      }
+      *p = v;
+    }
+    __syncthreads();
+  };
+
+  int ra[1] = {32 * (w & 1)}, rb[1] = {64 + 32 * (w >> 1)};
+  f32x16 acc[1];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[0][e] = 0.f;
+#pragma unroll
+  for (int p = 0; p < DG_NS - 1; ++p) issue(p);
+  for (int s = 0; s < n; ++s) {
+    dg_wait_vmcnt<DC_LOADS * (DG_NS - 2)>();
+    __syncthreads();
+    fix(s);
+    issue(s + DG_NS - 1);
+    stage_mfma<DT_BF16, 1>(ring + (s % DG_NS) * (DC_STB / 16), ra, rb, acc, lane);
+  }
+  dg_wait_vmcnt<0>();
+
+  // acc holds P[t, s] = <dE_t, H_s>: lane l has s = l%32 of the block and,
+  // for accumulator e, t = (e/4)*8 + (l/32)*4 + e%4. Logit gradients are
+  // gathered through a range-checked buffer over this example's rows of Gz.
+  const uint32_t ldz = (uint32_t)(a.ldz * 2);
+  const rsrc_t rZ = make_rsrc((const char*)a.Gz + ex_rows * ldz, (uint64_t)T * ldz);
+  const int s_row = qj * 64 + 32 * (w >> 1) + (lane & 31);
+  const int t0 = qi * 64 + 32 * (w & 1) + (lane >> 5) * 4;
+  float part = 0.f;
+  if (s_row < T) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int t = t0 + (e >> 2) * 8 + (e & 3);
+      if (t < T) {
+        const uint32_t v = (uint32_t)a.ids[ex_rows + t];
+        if (v < (uint32_t)a.V)  // an invalid id contributes nothing
+          part += acc[0][e] * bf16_to_f32((uint16_t)buf_load2(rZ, (uint32_t)s_row * ldz + v * 2));
+      }
+    }
+  }
+  part = wave_sum(part);
+  if (lane == 0) red[w] = part;
+  __syncthreads();
+  if (tid == 0) a.ws[(int64_t)b * a.slots + slot] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
 // Work item = (example, T-tile pair (ti, tj), chunk of CR_FCHUNK features).
 // The reduction is linear in the features, so chunks add up exactly.
 template <int DT, bool VEC>
@@ -749,7 +862,7 @@ hipError_t launch_tied_cross(const CrossArgs& a, int dt, bool vec, hipStream_t s
   if (n == 0) return hipSuccess;
   const dim3 g(n), blk(GR_THREADS);
   if (dt == DT_BF16) {
-    if (vec) hipLaunchKernelGGL((tied_cross_kernel<DT_BF16, true>), g, blk, 0, s, a);
+    if (vec) hipLaunchKernelGGL(dl_cross_kernel, g, blk, 0, s, a);
     else hipLaunchKernelGGL((tied_cross_kernel<DT_BF16, false>), g, blk, 0, s, a);
   } else {
     if (vec) hipLaunchKernelGGL((tied_cross_kernel<DT_F32, true>), g, blk, 0, s, a);

@@ -43,6 +43,8 @@ hipError_t launch_gram_norm(const GramArgs& a, int dt, bool vec, hipStream_t s);
 
 // Tied cross term: sum_{t,s} Gz[s, ids[t]] <dE_t, H_s>, all T-tile pairs.
 constexpr int CR_FCHUNK = 128;  // features per cross-term work item
+constexpr int CR_DL_ROWS = 64;  // row block of the direct-load cross kernel
+inline bool cross_direct(int dt, bool vec) { return dt == DT_BF16 && vec; }
 
 struct CrossArgs {
   const int32_t* ids;   // [B,T]
@@ -50,8 +52,8 @@ struct CrossArgs {
   const void* H;        // [B*T, ldh]
   const void* Gz;       // [B*T, ldz]
   int64_t lde, ldh, ldz;
-  int32_t B, T, V, d, n_t;
-  int32_t n_fc;         // feature chunks
+  int32_t B, T, V, d, n_t;  // n_t: row blocks per example (128 rows, 64 for bf16 aligned)
+  int32_t n_fc;         // feature chunks (1 for bf16 aligned: all features per item)
   int32_t slots;        // n_t * n_t * n_fc
   float* ws;            // [B, slots]
 };

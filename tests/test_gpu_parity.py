@@ -201,6 +201,25 @@ def test_tied_cross_term(dp, dtype, B, T, V, d, ldz):
     assert rel(host(n2), tied_ref).max() <= TOL[dtype]
 
 
+def test_tied_cross_term_padded_rows(dp):
+    """dE and H on 16-byte aligned strides wider than d (NaN in the padding):
+    the direct-load kernel's last feature chunk straddles d."""
+    B, T, V, d, ld = 2, 200, 900, 100, 104
+    ids, dE, H, Gz = _tied_inputs("bf16", B, T, V, d, V, seed=23)
+    dEp = np.full((B, T, ld), 0x7FC0, np.uint16)
+    Hp = np.full((B, T, ld), 0x7FC0, np.uint16)
+    dEp[:, :, :d], Hp[:, :, :d] = dE, H
+    dEd, Hd, Gzd = O.decode(dE, "bf16"), O.decode(H, "bf16"), O.decode(Gz, "bf16")
+    cross = O.tied_cross(ids, dEd, Hd, Gzd, V)
+    n_in = O.embedding_norm2(ids, dEd, V)
+    n_out = O.head_norm2(Hd, Gzd, V)
+    out = torch.zeros(B, device="cuda")
+    dp.dp_tied_cross_term(dev(ids), dev(dEp, "bf16")[:, :, :d], dev(Hp, "bf16")[:, :, :d],
+                          dev(Gz, "bf16"), V, out)
+    got = host(out)
+    assert np.all(np.abs(got - cross) <= TOL["bf16"] * np.sqrt(n_in * n_out))
+
+
 # ---------------------------------------------------------------------------
 # a6: clip factors
 # ---------------------------------------------------------------------------
