@@ -123,7 +123,8 @@ dp_status_t dp_ghost_norm_linear(const void* A, int64_t lda, const void* G, int6
  *   seg_id[b,t]  = rank of ids[b,t] among the sorted distinct ids of b
  *   n_unique[b]  = number of distinct ids of b
  * seg_id and n_unique may be NULL. Exact (integer) outputs.
- * Limits: T <= 4096 and ceil(log2 V) + ceil(log2 T) <= 32.
+ * Limits: T <= 4096 and ceil(log2(V + 1)) + ceil(log2 T) <= 32 (a sort key
+ * holds an id clamped to V and a position).
  * ------------------------------------------------------------------- */
 size_t dp_ghost_norm_embedding_workspace(int B, int T, int d);
 dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t lde, int B, int T,
@@ -167,7 +168,7 @@ dp_status_t dp_clip_factors(const float* norm2, int B, float C, float* c, void* 
  * accumulate = 1.
  * Workspace: only the embedding form needs one,
  * dp_clipped_grad_sum_workspace(B, T, d_out, 1) bytes; limits for it:
- * B*T <= 16384 and ceil(log2 V) + ceil(log2(B*T)) <= 32.
+ * B*T <= 16384 and ceil(log2(V + 1)) + ceil(log2(B*T)) <= 32.
  * ------------------------------------------------------------------- */
 size_t dp_clipped_grad_sum_workspace(int B, int T, int d_out, int with_ids);
 dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64_t ldg,

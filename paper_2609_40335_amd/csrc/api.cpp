@@ -316,7 +316,7 @@ dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t 
   if (!dtype_ok(dt)) return fail(DP_EINVAL, "unknown dtype %d", (int)dt);
   if (T > dpg::EN_MAX_T) return fail(DP_EUNSUPPORTED, "T = %d exceeds %d", T, dpg::EN_MAX_T);
   const int pbits = std::max(1, bits_for(T));
-  if (bits_for(V) + pbits > 32)
+  if (bits_for((int64_t)V + 1) + pbits > 32)  // ids are clamped to V, so V + 1 values
     return fail(DP_EUNSUPPORTED, "V = %d and T = %d do not fit a 32-bit sort key", V, T);
   const size_t need = dp_ghost_norm_embedding_workspace(B, T, d);
   if (!workspace || workspace_bytes < need)

@@ -7,8 +7,9 @@
 // with x_t = v. Its squared norm is sum_v ||sum_{t: x_t = v} dE_t||^2.
 //
 // Bucketing sorts the packed keys (id << pbits | position) of one example in
-// LDS (bitonic), marks the first token of each run of equal ids, and turns the
-// marks into dense ranks with a wavefront-shuffle prefix scan. The norm then
+// LDS (a stable radix sort on the id bits), marks the first token of each run
+// of equal ids, and turns the marks into dense ranks with a wavefront-shuffle
+// prefix scan. The norm then
 // sums each bucket's rows (lanes = 64 features, coalesced row reads) and
 // squares. The clipped sum sorts all B*T tokens of the batch (radix sort on
 // the ids, below) and reduces runs of equal ids in fixed 32-token blocks; a run that crosses a
@@ -23,23 +24,6 @@ namespace dpg {
 constexpr int EN_THREADS = 256;
 constexpr int ES_THREADS = 1024;
 constexpr int ES_WAVES = 4;  // waves per workgroup of the block and fix-up passes
-
-// Ascending bitonic sort of n (a power of two) keys in LDS.
-__device__ void bitonic_sort(uint32_t* keys, int n, int tid, int nthreads) {
-  for (int k = 2; k <= n; k <<= 1) {
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = tid; i < n; i += nthreads) {
-        const int p = i ^ j;
-        if (p > i) {
-          const uint32_t x = keys[i], y = keys[p];
-          const bool up = (i & k) == 0;
-          if ((x > y) == up) { keys[i] = y; keys[p] = x; }
-        }
-      }
-      __syncthreads();
-    }
-  }
-}
 
 // Inclusive prefix sum of one value per thread across the workgroup:
 // shuffles within each wavefront, then the wave totals through LDS.
@@ -84,6 +68,69 @@ __device__ int rank_sorted(const uint32_t* keys, int n, int pbits, int32_t* rank
   return total;
 }
 
+// Stable LSD radix sort, 8 bits per pass, of n keys (id << pb | position)
+// held in LDS buffer buf0, over the bits of the ids 0..V (ids at or past V
+// must already be clamped to V). The keys arrive in position order, so the
+// result is the (id, position) order. NW waves; wave w owns a contiguous
+// segment of the keys. A pass counts digits per wave (cnt[w][digit]), turns
+// the counts into offsets in digit-major, wave-minor order, and scatters each
+// wave's keys 64 at a time: lanes with equal digits are found with eight
+// ballots and ranked by lane; the group's lowest lane advances the wave's
+// running offset. Returns the index of the buffer that holds the result.
+template <int NW>
+__device__ int lds_radix_sort(uint32_t* buf0, uint32_t* buf1, int n, int pb, uint32_t V, int* cnt,
+                              int* wave_tot) {
+  static_assert(NW % 4 == 0, "4 (digit, wave) entries per thread");
+  constexpr int NT = NW * WAVE;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int idbits = 0;  // bits of the values 0..V
+  while ((1u << idbits) <= V) ++idbits;
+  const int seg_len = ((n + NW - 1) / NW + WAVE - 1) / WAVE * WAVE;
+  const int s0 = min(w * seg_len, n), s1 = min(s0 + seg_len, n);
+  const uint64_t lt = (1ull << lane) - 1ull;
+  int src = 0;
+  for (int shift = 0; shift < idbits; shift += 8, src ^= 1) {
+    const int sh = pb + shift;
+    const uint32_t* in = src ? buf1 : buf0;
+    uint32_t* out = src ? buf0 : buf1;
+    for (int i = tid; i < NW * 256; i += NT) cnt[i] = 0;
+    __syncthreads();
+    for (int p = s0 + lane; p < s1; p += WAVE) atomicAdd(&cnt[w * 256 + ((in[p] >> sh) & 255)], 1);
+    __syncthreads();
+    {
+      // thread t holds entries 4t .. 4t+3 of the (digit, wave) order
+      const int d = (4 * tid) / NW, w0 = (4 * tid) % NW;
+      int v[4], loc = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { v[q] = cnt[(w0 + q) * 256 + d]; loc += v[q]; }
+      int total;
+      const int incl = block_inclusive_scan(loc, wave_tot, tid, NT, &total);
+      int run = incl - loc;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { cnt[(w0 + q) * 256 + d] = run; run += v[q]; }
+    }
+    __syncthreads();
+    for (int base = s0; base < s1; base += WAVE) {
+      const int p = base + lane;
+      const bool valid = p < s1;
+      const uint32_t key = valid ? in[p] : 0u;
+      const int dg = (int)((key >> sh) & 255);
+      uint64_t m = __ballot(valid);
+#pragma unroll
+      for (int bit = 0; bit < 8; ++bit) {
+        const uint64_t mb = __ballot(valid && ((dg >> bit) & 1));
+        m &= ((dg >> bit) & 1) ? mb : ~mb;
+      }
+      const int rank = __popcll(m & lt);
+      const int off = valid ? cnt[w * 256 + dg] : 0;
+      if (valid) out[off + rank] = key;
+      if (valid && rank == 0) cnt[w * 256 + dg] = off + __popcll(m);
+    }
+    __syncthreads();
+  }
+  return src;
+}
+
 template <int DT>
 __device__ __forceinline__ float load_elem(const void* base, int64_t idx) {
   if constexpr (DT == DT_BF16)
@@ -97,21 +144,24 @@ __device__ __forceinline__ float load_elem(const void* base, int64_t idx) {
 // ---------------------------------------------------------------------------
 template <int DT>
 __global__ __launch_bounds__(EN_THREADS) void embed_norm_kernel(EmbedNormArgs a) {
-  __shared__ uint32_t keys[EN_MAX_T];
+  __shared__ uint32_t kbuf[2][EN_MAX_T];
   __shared__ int32_t rank[EN_MAX_T];
   __shared__ int32_t seg[EN_MAX_T + 1];
+  __shared__ int cnt[(EN_THREADS / WAVE) * 256];
   __shared__ int wave_tot[EN_THREADS / WAVE];
   __shared__ float red[EN_THREADS / WAVE];
   const int b = blockIdx.x, chunk = blockIdx.y, tid = threadIdx.x;
   const int T = a.T;
-  int n2 = 1;
-  while (n2 < T) n2 <<= 1;
   const uint32_t pmask = (1u << a.pbits) - 1u;
+  const uint32_t V = (uint32_t)a.V;
   const int32_t* ids = a.ids + (int64_t)b * T;
-  for (int p = tid; p < n2; p += EN_THREADS)
-    keys[p] = p < T ? ((((uint32_t)ids[p]) << a.pbits) | (uint32_t)p) : 0xFFFFFFFFu;
+  for (int p = tid; p < T; p += EN_THREADS) {
+    const uint32_t id = (uint32_t)ids[p];
+    kbuf[0][p] = ((id < V ? id : V) << a.pbits) | (uint32_t)p;
+  }
   __syncthreads();
-  bitonic_sort(keys, n2, tid, EN_THREADS);
+  const uint32_t* keys =
+      kbuf[lds_radix_sort<EN_THREADS / WAVE>(kbuf[0], kbuf[1], T, a.pbits, V, cnt, wave_tot)];
   const int nseg = rank_sorted(keys, T, a.pbits, rank, seg, wave_tot, tid, EN_THREADS);
   if (chunk == 0) {
     if (a.seg_id)
@@ -119,19 +169,69 @@ __global__ __launch_bounds__(EN_THREADS) void embed_norm_kernel(EmbedNormArgs a)
         a.seg_id[(int64_t)b * T + (keys[p] & pmask)] = rank[p];
     if (a.n_unique && tid == 0) a.n_unique[b] = nseg;
   }
+  // Bucket sums: wave w walks sorted positions [s_w, e_w) 32 rows at a time
+  // (lane = feature), squaring each run of equal ids that closes inside its
+  // range. A run that crosses a range boundary leaves partials: hp (the run
+  // open at s_w, closing here or, if `through`, passing on) and tp (a run that
+  // starts here and stays open at e_w). Wave 0 then chains them in order.
+  constexpr int NW = EN_THREADS / WAVE;
   const int lane = tid & 63, w = tid >> 6;
   const int f = chunk * WAVE + lane;
-  const int nw = EN_THREADS / WAVE;
-  float sq = 0.f;
-  if (f < a.d) {
-    const int64_t row0 = (int64_t)b * T;
-    for (int r = w; r < nseg; r += nw) {
-      float acc = 0.f;
-      const int e = seg[r + 1];
-#pragma unroll 4
-      for (int p = seg[r]; p < e; ++p)
-        acc += load_elem<DT>(a.E, (row0 + (keys[p] & pmask)) * a.lde + f);
-      sq += acc * acc;
+  const bool fok = f < a.d;
+  const int fs = fok ? f : a.d - 1;  // a feature index that is always in the row
+  const int pb = a.pbits;
+  const int64_t row0 = (int64_t)b * T;
+  const int per = (T + NW - 1) / NW;
+  const int s_w = min(w * per, T), e_w = min(s_w + per, T);
+  bool h_open = false, t_open = false, through = false;
+  float sq = 0.f, hp = 0.f, tp = 0.f;
+  if (s_w < e_w) {
+    h_open = s_w > 0 && (keys[s_w - 1] >> pb) == (keys[s_w] >> pb);
+    bool in_head = h_open;  // the current run started before s_w
+    float acc = 0.f;
+    for (int base = s_w; base < e_w; base += 32) {
+      const int nb = min(32, e_w - base);
+      // Clamped indices keep every address valid, so the 32 loads issue back
+      // to back; the values past the range or past d are masked afterwards.
+      float ev[32];
+#pragma unroll
+      for (int j = 0; j < 32; ++j) {
+        const int jj = j < nb ? j : nb - 1;
+        const float v = load_elem<DT>(a.E, (row0 + (keys[base + jj] & pmask)) * a.lde + fs);
+        ev[j] = (j < nb && fok) ? v : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < 32; ++j) {
+        if (j >= nb) break;
+        const int p = base + j;
+        acc += ev[j];
+        const bool run_end = p + 1 == T || (keys[p + 1] >> pb) != (keys[p] >> pb);
+        if (run_end) {
+          if (in_head) hp = acc; else sq += acc * acc;
+          in_head = false;
+          acc = 0.f;
+        } else if (p + 1 == e_w) {  // the run stays open past this range
+          t_open = true;
+          if (in_head) { hp = acc; through = true; } else tp = acc;
+        }
+      }
+    }
+  }
+  __shared__ float bh[NW][WAVE], bt[NW][WAVE];
+  __shared__ int bflag[NW];
+  bh[w][lane] = hp;
+  bt[w][lane] = tp;
+  if (lane == 0) bflag[w] = (h_open ? 1 : 0) | (t_open ? 2 : 0) | (through ? 4 : 0);
+  __syncthreads();
+  if (w == 0) {
+    float carry = 0.f;
+    for (int q = 0; q < NW; ++q) {
+      const int fl = bflag[q];
+      if (fl & 1) {
+        carry += bh[q][lane];
+        if (!(fl & 4)) { sq += carry * carry; carry = 0.f; }
+      }
+      if ((fl & 2) && !(fl & 4)) carry = bt[q][lane];
     }
   }
   sq = wave_sum(sq);
@@ -144,73 +244,24 @@ __global__ __launch_bounds__(EN_THREADS) void embed_norm_kernel(EmbedNormArgs a)
 // Batch-wide clipped sum of the input embedding:
 // out[v, f] (+)= sum over tokens k with ids[k] = v of c[k / T] * E[k, f].
 // ---------------------------------------------------------------------------
-// Sorts the batch's keys (id << pbits | position) by id with a stable LSD
-// radix sort on the id bits, 8 bits per pass, in one workgroup: the keys
-// arrive in position order, so a stable sort on the id alone yields the
-// (id, position) order. Wave w owns a contiguous segment of the keys. A pass
-// counts digits per wave, turns the (digit, wave) counts into offsets in
-// digit-major, wave-minor order, and scatters each wave's keys 64 at a time:
-// lanes with equal digits are found with eight ballots, ranked by lane, and
-// the group's lowest lane advances the wave's running count. Ids at or past V
-// are clamped to V, so they sort last and every valid id stays one run.
+// Sorts all B*T keys (id << pbits | position) of the batch by id in one
+// workgroup (lds_radix_sort); ids at or past V are clamped to V, so they
+// sort last and every valid id stays one run.
 constexpr int RS_WAVES = ES_THREADS / WAVE;
-constexpr int RS_RADIX = 256;
 
 __global__ __launch_bounds__(ES_THREADS) void embed_sort_kernel(EmbedSumArgs a) {
-  __shared__ uint32_t buf[2][ES_MAX_K];
-  __shared__ int cnt[RS_WAVES][RS_RADIX];
+  __shared__ uint32_t kbuf[2][ES_MAX_K];
+  __shared__ int cnt[RS_WAVES * 256];
   __shared__ int wave_tot[ES_THREADS / WAVE];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, K = a.K, pb = a.pbits;
+  const int tid = threadIdx.x, K = a.K, pb = a.pbits;
   const uint32_t V = (uint32_t)a.V;
   for (int p = tid; p < K; p += ES_THREADS) {
     const uint32_t id = (uint32_t)a.ids[p];
-    buf[0][p] = ((id < V ? id : V) << pb) | (uint32_t)p;
+    kbuf[0][p] = ((id < V ? id : V) << pb) | (uint32_t)p;
   }
-  int idbits = 0;  // bits of the values 0..V
-  while ((1u << idbits) <= V) ++idbits;
-  const int seg_len = ((K + RS_WAVES - 1) / RS_WAVES + WAVE - 1) / WAVE * WAVE;
-  const int s0 = min(w * seg_len, K), s1 = min(s0 + seg_len, K);
-  const uint64_t lt = (1ull << lane) - 1ull;
-  int src = 0;
-  for (int shift = 0; shift < idbits; shift += 8, src ^= 1) {
-    const int sh = pb + shift;
-    for (int i = tid; i < RS_WAVES * RS_RADIX; i += ES_THREADS) (&cnt[0][0])[i] = 0;
-    __syncthreads();
-    for (int p = s0 + lane; p < s1; p += WAVE) atomicAdd(&cnt[w][(buf[src][p] >> sh) & 255], 1);
-    __syncthreads();
-    // Exclusive offsets in (digit, wave) order; thread t holds entries
-    // 4t .. 4t+3 of that order, i.e. digit t/4, waves 4(t%4) .. +3.
-    {
-      const int d = tid >> 2, w0 = (tid & 3) * 4;
-      int v[4], loc = 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) { v[q] = cnt[w0 + q][d]; loc += v[q]; }
-      int total;
-      const int incl = block_inclusive_scan(loc, wave_tot, tid, ES_THREADS, &total);
-      int run = incl - loc;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) { cnt[w0 + q][d] = run; run += v[q]; }
-    }
-    __syncthreads();
-    for (int base = s0; base < s1; base += WAVE) {
-      const int p = base + lane;
-      const bool valid = p < s1;
-      const uint32_t key = valid ? buf[src][p] : 0u;
-      const int dg = (int)((key >> sh) & 255);
-      uint64_t m = __ballot(valid);
-#pragma unroll
-      for (int bit = 0; bit < 8; ++bit) {
-        const uint64_t mb = __ballot(valid && ((dg >> bit) & 1));
-        m &= ((dg >> bit) & 1) ? mb : ~mb;
-      }
-      const int rank = __popcll(m & lt);
-      const int off = valid ? cnt[w][dg] : 0;
-      if (valid) buf[src ^ 1][off + rank] = key;
-      if (valid && rank == 0) cnt[w][dg] = off + __popcll(m);
-    }
-    __syncthreads();
-  }
-  for (int p = tid; p < K; p += ES_THREADS) a.keys[p] = buf[src][p];
+  __syncthreads();
+  const int r = lds_radix_sort<RS_WAVES>(kbuf[0], kbuf[1], K, pb, V, cnt, wave_tot);
+  for (int p = tid; p < K; p += ES_THREADS) a.keys[p] = kbuf[r][p];
 }
 
 __device__ __forceinline__ void out_add(const EmbedSumArgs& a, uint32_t v, int f, float val) {
@@ -243,12 +294,17 @@ __global__ __launch_bounds__(ES_WAVES * WAVE) void embed_block_kernel(EmbedSumAr
   const float myc = lane < n ? a.c[(int)((mykey & pmask) / (uint32_t)a.T)] : 0.f;
   const uint32_t id_before = p0 > 0 ? (a.keys[p0 - 1] >> pb) : 0xFFFFFFFFu;
   const uint32_t id_after = p0 + n < K ? (a.keys[p0 + n] >> pb) : 0xFFFFFFFFu;
+  // Every load has a valid address (the last key repeats past the block, the
+  // feature is clamped into the row), so all ES_BLOCK loads issue back to back.
+  const uint32_t lastkey = (uint32_t)__builtin_amdgcn_readlane((int)mykey, n - 1);
+  const int fs = fok ? f : a.d - 1;
   float ev[ES_BLOCK];
 #pragma unroll
   for (int j = 0; j < ES_BLOCK; ++j) {
-    const uint32_t kj = (uint32_t)__builtin_amdgcn_readlane((int)mykey, j);
+    const uint32_t kj = j < n ? (uint32_t)__builtin_amdgcn_readlane((int)mykey, j) : lastkey;
     const float cj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, myc), j));
-    ev[j] = (j < n && fok) ? cj * load_elem<DT>(a.E, (int64_t)(kj & pmask) * a.lde + f) : 0.f;
+    const float v = load_elem<DT>(a.E, (int64_t)(kj & pmask) * a.lde + fs);
+    ev[j] = (j < n && fok) ? cj * v : 0.f;
   }
   float acc = 0.f;
   int run_start = 0;
