@@ -500,6 +500,26 @@ def test_full_size_gpt2_body_sampled(dp):
         assert fro_rel(host(o)[rows], ref) <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("algo", ["gram", "direct"])
+def test_full_size_long_sequence(dp, algo):
+    """T = 1024 at GPT-2 widths (the long-sequence config's shapes): the
+    multi-tile Gram and the direct norm, for a body layer and the head."""
+    a = dp.DP_NORM_GRAM if algo == "gram" else dp.DP_NORM_DIRECT
+    B, T = 2, 1024
+    A, G = _layer_inputs("bf16", B, T, 768, 2304, seed=51, g_std=1e-3)
+    n2 = torch.zeros(B, device="cuda")
+    dp.dp_ghost_norm_linear(dev(A, "bf16"), dev(G, "bf16"), n2, algo=a)
+    ref = _oracle_linear_norm2(A, G, 768, 2304, "bf16")
+    _say(f"  long-T {algo} body max rel err {rel(host(n2), ref).max():.3e}")
+    assert rel(host(n2), ref).max() <= TOL["bf16"]
+    V, d = 50257, 768
+    ids, dE, H, Gz = _tied_inputs("bf16", 1, T, V, d, 50304, seed=52)
+    n_out = torch.zeros(1, device="cuda")
+    dp.dp_ghost_norm_linear(dev(H, "bf16"), dev(Gz, "bf16")[:, :, :V], n_out, algo=a)
+    ref_out = O.sqnorm(O.head_grad(O.decode(H[0], "bf16"), O.decode(Gz[0], "bf16"), V))
+    assert rel(host(n_out)[0], ref_out) <= TOL["bf16"]
+
+
 def test_full_size_gpt2_head_sampled(dp):
     wl = gen.make_workload("c3")
     h = wl.head
