@@ -35,8 +35,8 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 # HBM bytes per launch of the clipped-sum kernel: rocprofv3 FETCH_SIZE x 2 +
 # WRITE_SIZE x 1 (factors from a plain 1 GiB copy), recorded for the kernel
 # source with this SHA-256; any other source reports null.
-GEMM_TRAFFIC = {"gemm.hip sha256": "07988a6d578e152bfba4c175b66835b2c65826b794abf37fafcc95d24f47de81",
-                "bytes": 2818646741}
+GEMM_TRAFFIC = {"gemm.hip sha256": "59a50bb18e8577c27deb406b2bfd475d3c8a82eb88c7b8f8cd4de0a620e21b4c",
+                "bytes": 2816417088}
 
 
 def log(*a):
