@@ -9,10 +9,11 @@ One step is the whole hot path on one batch, through the C ABI:
   2. input-embedding norm and token buckets
   3. tied cross term folded in as + 2 <g_in, g_out> (eq. 11, eq. 13)
   4. clip factors (eq. 2, eq. 7)
-  5. clipped sums of all linears and of the head, the head landing in the
-     tied embedding gradient (one grouped GEMM, K = B*T)
-  6. the input-embedding part of the tied gradient (sorted segment sums)
-  7. Gaussian noise and division by B over the flat gradient vector (eq. 3)
+  5. the input-embedding part of the tied gradient (sorted segment sums)
+  6. clipped sums of all linears and of the head (one grouped GEMM, K = B*T),
+     the head accumulating onto the tied embedding gradient, with Gaussian
+     noise and the division by B fused into the GEMM's store (eq. 3); one
+     generator stream per parameter tensor
 Inputs are resident in HBM before the timed region starts. Prints one JSON
 line; per-phase times go to stderr.
 """
@@ -118,6 +119,18 @@ class Step:
         self.norm_layers = norm_layers
         self.norm_group = dp.LinearGroup(norm_layers)
         self.sum_group = dp.LinearGroup(sum_layers, sum_outs) if sum_layers else None
+        # Noise generator ids per parameter tensor, as in the oracle's step:
+        # linear l -> l, the input embedding (or tied matrix) -> L, an untied
+        # head -> L + 1. The tied matrix receives the embedding sum first and
+        # the head GEMM accumulates onto it, so it is noised once.
+        L = len(wl.linears)
+        self.sum_tids = list(range(L))
+        self.sum_acc = [False] * L
+        self.tied = h is not None and h.H is not None and h.tied
+        if h is not None and h.H is not None:
+            self.sum_tids.append(L if h.tied else L + 1)
+            self.sum_acc.append(self.tied)
+        self.e_tid = L
         self.n2 = torch.zeros(B, device="cuda")
         self.c = torch.zeros(B, device="cuda")
         # algorithmic work of the grouped clipped-sum GEMM (the dominant kernel)
@@ -143,17 +156,20 @@ class Step:
                 mark("cross_term")
         dp.dp_clip_factors(self.n2, wl.C, self.c)
         mark("clip")
-        if self.sum_group is not None:
-            self.sum_group.clipped_sum(self.c)
-        mark("clipped_sum")
         if h is not None:
-            tied = h.H is not None and h.tied
-            dp.dp_clipped_grad_sum(None, self.dE, self.c, self.E, ids=self.ids, V=h.V,
-                                   accumulate=tied)
+            dp.dp_clipped_grad_sum(None, self.dE, self.c, self.E, ids=self.ids, V=h.V)
             mark("embedding_sum")
-        dp.dp_add_noise(self.flat, wl.sigma, wl.C, wl.B, seed=1234, tensor_id=0,
-                        step=self.step_id)
-        mark("noise")
+        # clipped sums of every GEMM-shaped tensor with the Gaussian mechanism
+        # fused into their store (eq. 3): (S + sigma C z) / B
+        if self.sum_group is not None:
+            self.sum_group.clipped_sum_noised(self.c, self.sum_tids, wl.sigma, wl.C, wl.B,
+                                              seed=1234, step=self.step_id,
+                                              accumulate=self.sum_acc)
+            mark("clipped_sum_noise")
+        if h is not None and not self.tied:
+            dp.dp_add_noise(self.E, wl.sigma, wl.C, wl.B, seed=1234, tensor_id=self.e_tid,
+                            step=self.step_id)
+            mark("embedding_noise")
         self.step_id += 1
 
 
@@ -293,7 +309,7 @@ def main(argv=None) -> int:
     phase_ms = {k: sum(v) / len(v) for k, v in phases.items()}
     for k, v in phase_ms.items():
         log(f"[bench]   {k:16s} {v * 1e3:9.1f} us")
-    gemm_s = phase_ms["clipped_sum"] / 1e3
+    gemm_s = phase_ms["clipped_sum_noise"] / 1e3
     norm_s = phase_ms["norms"] / 1e3
     achieved = st.gemm_flops / gemm_s / 1e12
     log(f"[bench] clipped-sum GEMM {st.gemm_flops / 1e9:.1f} GFLOP in {gemm_s * 1e6:.1f} us = "
@@ -313,7 +329,8 @@ def main(argv=None) -> int:
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic", "config": config,
-        "roofline": {"bound": "mfma", "kernel": "dl_gemm_kernel (clipped sum, bf16)",
+        "roofline": {"bound": "mfma",
+                     "kernel": "dl_gemm_kernel (clipped sum with fused noise, bf16)",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": gemm_traffic(),
                      "algorithmic_flop_per_launch": st.gemm_flops},

@@ -183,6 +183,29 @@ dp_status_t dp_clipped_grad_sum_grouped(const dp_linear_t* layers, float* const*
                                         void* stream);
 
 /* ---------------------------------------------------------------------
+ * Clipped sum and Gaussian mechanism in one pass (eq. 3): for each layer l
+ *   outs[l] = (prior + sum_i c_i A_i^T G_i + sigma*C*z) / B_norm
+ * where prior is outs[l]'s content if accumulate[l] != 0 (else 0), and z is
+ * the standard normal that dp_add_noise(outs[l], rows*cols, sigma, C, B_norm,
+ * seed, tensor_ids[l], step) would add to the same element: the element at
+ * row r, column k of the output ([d_in, d_out], or [d_out, d_in] with
+ * transpose_out) takes index r*cols + k of the tensor's Philox stream. The
+ * result equals dp_clipped_grad_sum_grouped followed by dp_add_noise on each
+ * output, without a second pass over the gradients. B_norm = 0: no
+ * division. A tied matrix is noised once: write its other contribution first
+ * (e.g. the embedding-form clipped sum) and pass accumulate[l] = 1.
+ * tensor_ids[l] and step must be < 2^32; accumulate may be NULL (all 0).
+ * tensor_ids and accumulate are host arrays of n_layers entries.
+ * ------------------------------------------------------------------- */
+dp_status_t dp_clipped_grad_sum_noised_grouped(const dp_linear_t* layers, float* const* outs,
+                                               const uint64_t* tensor_ids,
+                                               const int32_t* accumulate, int n_layers,
+                                               const float* c, int B, int T, dp_dtype_t dt,
+                                               int transpose_out, float sigma, float C,
+                                               int B_norm, uint64_t seed, uint64_t step,
+                                               void* stream);
+
+/* ---------------------------------------------------------------------
  * Gaussian mechanism (eq. 3): grad[j] = (grad[j] + sigma*C*z_j) / B_norm
  * (no division when B_norm = 0), in place, for j < n; the division is a
  * multiplication by 1/B_norm rounded to fp32 (within an ulp of dividing). z_j is a standard

@@ -75,6 +75,16 @@ struct GemmEntry {
   float* out;
   int64_t ldo;
   bool vec;
+  int acc = 0;             // clipped sum: out += (else out =)
+  uint32_t tensor_id = 0;  // clipped sum with noise: generator id of the tensor
+};
+
+// The Gaussian mechanism fused into a clipped-sum launch.
+struct NoiseCfg {
+  bool on = false;
+  float sigma_c = 0.f, inv_b = 1.f;
+  uint32_t step = 0;
+  uint64_t seed = 0;
 };
 
 struct NormPlan {
@@ -114,6 +124,18 @@ int gram_pairs(const NormPlan& p, dp_dtype_t dt, bool vec, int T) {
   return dpg::gram_whole(kdt(dt), vec, T) ? 1 : p.P;
 }
 
+// A clipped-sum entry whose kernel rows are the output's rows: X is the
+// operand indexing the output's rows (A for [d_in, d_out], G for the
+// transposed [d_out, d_in]), so the kernel always stores row-major and the
+// caller's layout only decides the operand order.
+void plan_sum(const dp_linear_t& L, int transpose_out, dp_dtype_t dt, float* out,
+              std::vector<GemmEntry>& v) {
+  if (transpose_out)
+    plan_gemm(L.G, L.ldg, L.d_out, L.A, L.lda, L.d_in, dt, out, L.d_in, v, nullptr, 0);
+  else
+    plan_gemm(L.A, L.lda, L.d_in, L.G, L.ldg, L.d_out, dt, out, L.d_out, v, nullptr, 0);
+}
+
 NormPlan plan_norm(const dp_linear_t* layers, int n, int T, dp_dtype_t dt) {
   NormPlan p;
   p.n_t = (int)ceil_div(T, dpg::GR_TM);
@@ -151,6 +173,8 @@ dp_status_t check_layers(const dp_linear_t* layers, int n, int B, int T, dp_dtyp
       return fail(DP_EINVAL, "layer %d: unknown algo %d", i, L.algo);
     if (!span_ok((int64_t)B * T, L.lda, dt) || !span_ok((int64_t)B * T, L.ldg, dt))
       return fail(DP_EUNSUPPORTED, "layer %d: an operand spans 4 GiB or more", i);
+    if (ceil_div(L.d_in, dpg::GM_BM) > 65535 || ceil_div(L.d_out, dpg::GM_BN) > 65535)
+      return fail(DP_EUNSUPPORTED, "layer %d: a width exceeds 65535 tiles of 256", i);
   }
   return DP_OK;
 }
@@ -191,7 +215,7 @@ dp_status_t run_gram(const NormPlan& p, int B, int T, dp_dtype_t dt, float* ws, 
 
 // mode 0: clipped sum (c, out); mode 1: direct norm (ws, slots)
 dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int T, dp_dtype_t dt,
-                     const float* c, float* ws, int64_t slots, int transpose, int accumulate,
+                     const float* c, float* ws, int64_t slots, int transpose, const NoiseCfg& nz,
                      hipStream_t s) {
   for (int pass = 0; pass < 2; ++pass) {
     const bool vec = pass == 0;
@@ -201,7 +225,9 @@ dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int
     for (size_t i0 = 0; i0 < sel.size(); i0 += dpg::GM_MAX_LAYERS) {
       dpg::GemmArgs a{};
       a.B = B; a.T = T; a.c = c; a.ws = ws; a.slots = (int32_t)slots;
-      a.transpose = transpose; a.accumulate = accumulate;
+      a.transpose = transpose;
+      a.noise = nz.on ? 1 : 0;
+      a.sigma_c = nz.sigma_c; a.inv_b = nz.inv_b; a.step = nz.step; a.seed = nz.seed;
       uint64_t items = 0;
       const size_t n = std::min(sel.size() - i0, (size_t)dpg::GM_MAX_LAYERS);
       for (size_t j = 0; j < n; ++j) {
@@ -209,9 +235,11 @@ dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int
         dpg::GemmLayer& L = a.L[j];
         L.X = e.X; L.Y = e.Y; L.ldx = e.ldx; L.ldy = e.ldy;
         L.M = e.M; L.N = e.N;
-        L.tm = e.tm; L.tn = e.tn;
+        L.tm = (uint16_t)e.tm; L.tn = (uint16_t)e.tn;
         L.tile_begin = (uint32_t)items;
-        L.slot_begin = e.slot_begin;
+        if (mode == 0) L.tensor_id = e.tensor_id;
+        else L.slot_begin = e.slot_begin;
+        L.accumulate = e.acc;
         L.out = e.out; L.ldo = e.ldo;
         items += (uint64_t)e.tm * e.tn * (mode == 1 ? (uint64_t)B : 1ull);
       }
@@ -285,7 +313,7 @@ dp_status_t dp_ghost_norm_linear_grouped(const dp_linear_t* layers, int n_layers
   float* ws = static_cast<float*>(workspace);
   st = run_gram(p, B, T, dt, ws, s);
   if (st != DP_OK) return st;
-  st = run_gemm(p.direct, 1, B, T, dt, nullptr, ws, p.slots, 0, 0, s);
+  st = run_gemm(p.direct, 1, B, T, dt, nullptr, ws, p.slots, 0, NoiseCfg{}, s);
   if (st != DP_OK) return st;
   return hip_status(dpg::launch_finish_rows(ws, B, (int)p.slots, norm2, accumulate, 1.f, s),
                     "finish launch");
@@ -407,13 +435,43 @@ dp_status_t dp_clipped_grad_sum_grouped(const dp_linear_t* layers, float* const*
   if ((int64_t)B * T > (int64_t(1) << 40)) return fail(DP_EUNSUPPORTED, "B*T too large");
   std::vector<GemmEntry> entries;
   for (int i = 0; i < n_layers; ++i) {
-    const dp_linear_t& L = layers[i];
     if (!outs[i]) return fail(DP_EINVAL, "outs[%d] is NULL", i);
-    const int64_t ldo = transpose_out ? L.d_in : L.d_out;
-    plan_gemm(L.A, L.lda, L.d_in, L.G, L.ldg, L.d_out, dt, outs[i], ldo, entries, nullptr, 0);
+    plan_sum(layers[i], transpose_out, dt, outs[i], entries);
+    entries.back().acc = accumulate ? 1 : 0;
   }
-  return run_gemm(entries, 0, B, T, dt, c, nullptr, 0, transpose_out ? 1 : 0,
-                  accumulate ? 1 : 0, as_stream(stream));
+  return run_gemm(entries, 0, B, T, dt, c, nullptr, 0, 0, NoiseCfg{}, as_stream(stream));
+}
+
+dp_status_t dp_clipped_grad_sum_noised_grouped(const dp_linear_t* layers, float* const* outs,
+                                               const uint64_t* tensor_ids,
+                                               const int32_t* accumulate, int n_layers,
+                                               const float* c, int B, int T, dp_dtype_t dt,
+                                               int transpose_out, float sigma, float C,
+                                               int B_norm, uint64_t seed, uint64_t step,
+                                               void* stream) {
+  dp_status_t st = check_layers(layers, n_layers, B, T, dt);
+  if (st != DP_OK) return st;
+  if (!outs || !c || !tensor_ids) return fail(DP_EINVAL, "outs, c or tensor_ids is NULL");
+  if ((int64_t)B * T > (int64_t(1) << 40)) return fail(DP_EUNSUPPORTED, "B*T too large");
+  if (!(sigma >= 0.f) || !std::isfinite(sigma)) return fail(DP_EINVAL, "sigma must be >= 0");
+  if (!(C > 0.f) || !std::isfinite(C)) return fail(DP_EINVAL, "C must be positive and finite");
+  if (B_norm < 0) return fail(DP_EINVAL, "B_norm must be >= 0");
+  if (step >> 32) return fail(DP_EINVAL, "step must be < 2^32");
+  std::vector<GemmEntry> entries;
+  for (int i = 0; i < n_layers; ++i) {
+    if (!outs[i]) return fail(DP_EINVAL, "outs[%d] is NULL", i);
+    if (tensor_ids[i] >> 32) return fail(DP_EINVAL, "tensor_ids[%d] must be < 2^32", i);
+    plan_sum(layers[i], transpose_out, dt, outs[i], entries);
+    entries.back().acc = accumulate && accumulate[i] ? 1 : 0;
+    entries.back().tensor_id = (uint32_t)tensor_ids[i];
+  }
+  NoiseCfg nz;
+  nz.on = true;
+  nz.sigma_c = (float)((double)sigma * (double)C);
+  nz.inv_b = B_norm > 0 ? (float)(1.0 / (double)B_norm) : 1.f;
+  nz.seed = seed;
+  nz.step = (uint32_t)step;
+  return run_gemm(entries, 0, B, T, dt, c, nullptr, 0, 0, nz, as_stream(stream));
 }
 
 dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64_t ldg,

@@ -151,22 +151,54 @@ __device__ __forceinline__ void tile_mfma(const u32x4* __restrict__ Xs, const u3
   }
 }
 
+// Tile (mt, nt) of work item rel within a layer: the direction with fewer
+// tiles varies fastest, so consecutive items (which run side by side on one
+// XCD) share a tile of the operand that has more of them in L2.
+__device__ __forceinline__ void tile_of(const GemmLayer& L, uint32_t rel, int& mt, int& nt) {
+  if (L.tn <= L.tm) {
+    mt = (int)(rel / (uint32_t)L.tn);
+    nt = (int)(rel - (uint32_t)mt * L.tn);
+  } else {
+    nt = (int)(rel / (uint32_t)L.tm);
+    mt = (int)(rel - (uint32_t)nt * L.tm);
+  }
+}
+
 // Writes (or adds) one 256x256 output tile: each wave's 4x2 32x32 blocks at
 // rows m0 + wm*128 + i*32, columns n0 + wn*64 + j*32. In a 32x32 block, lane l
 // holds column l%32 and, for accumulator e, row (e/4)*8 + (l/32)*4 + e%4.
 // Stores bypass L2 residency (the output is written once) so that they do
 // not evict operand rows.
+//
+// With the Gaussian mechanism fused (a.noise): value = (prior + sum +
+// sigma_c * z) * inv_b, where z is the standard normal the noise generator
+// assigns to the element's row-major index in the output tensor (row length
+// M when transposed, N otherwise), i.e. the draw dp_add_noise would add to
+// that element. In the transposed layout a lane's 4 accumulators e = 4g..4g+3
+// are 4 consecutive elements of one output row starting at a multiple of 4,
+// so one Philox block serves them when the row length is a multiple of 4.
+__device__ __forceinline__ float noise_at(const GemmArgs& a, uint32_t tid, uint64_t j) {
+  float z[4];
+  gauss4(j >> 2, a.seed, tid, a.step, z);
+  const int q = (int)(j & 3);
+  return q == 0 ? z[0] : q == 1 ? z[1] : q == 2 ? z[2] : z[3];
+}
+
 __device__ __forceinline__ void store_tile(const GemmArgs& a, const GemmLayer& L, int64_t m0,
                                            int64_t n0, int wm, int wn, int lane,
                                            f32x16 (&acc)[4][2]) {
   float* out = L.out;
   const int64_t ldo = L.ldo;
+  const bool accum = L.accumulate != 0;
+  const bool noise = a.noise != 0;
+  const uint32_t tid = L.tensor_id;
   const int mw = (int)m0 + wm * 128 + (lane >> 5) * 4;  // row of e = 0 in block i = 0
   const int nw = (int)n0 + wn * 64 + (lane & 31);         // column in block j = 0
   const bool full = m0 + GM_BM <= L.M && n0 + GM_BN <= L.N;
   if (a.transpose) {
     // out[n][m]: the 4 accumulators e = 4g..4g+3 are 4 consecutive rows m.
-    const bool vec4 = full && (ldo & 3) == 0 && (((uintptr_t)out) & 15) == 0;
+    const bool vec4 = full && (ldo & 3) == 0 && (((uintptr_t)out) & 15) == 0 &&
+                      (!noise || (L.M & 3) == 0);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -179,13 +211,24 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const GemmLayer& L
           if (vec4) {
             f32x4 v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
                        acc[i][j][4 * g + 3]};
-            if (a.accumulate) v += *(const f32x4*)p;
+            if (accum) v += *(const f32x4*)p;
+            if (noise) {
+              float z[4];
+              gauss4(((uint64_t)n * (uint64_t)L.M + (uint64_t)m) >> 2, a.seed, tid, a.step, z);
+#pragma unroll
+              for (int r = 0; r < 4; ++r) v[r] = (v[r] + a.sigma_c * z[r]) * a.inv_b;
+            }
             __builtin_nontemporal_store(v, (f32x4*)p);
           } else if (n < L.N) {
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-              if (m + r < L.M) p[r] = a.accumulate ? p[r] + acc[i][j][4 * g + r]
-                                                   : acc[i][j][4 * g + r];
+              if (m + r < L.M) {
+                float v = (accum ? p[r] : 0.f) + acc[i][j][4 * g + r];
+                if (noise)
+                  v = (v + a.sigma_c * noise_at(a, tid, (uint64_t)n * (uint64_t)L.M + m + r)) *
+                      a.inv_b;
+                p[r] = v;
+              }
           }
         }
       }
@@ -199,15 +242,99 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const GemmLayer& L
         for (int e = 0; e < 16; ++e) {
           const int m = mw + i * 32 + (e >> 2) * 8 + (e & 3);
           float* p = out + (int64_t)m * ldo + n;
-          if (full) {
-            const float v = a.accumulate ? *p + acc[i][j][e] : acc[i][j][e];
-            __builtin_nontemporal_store(v, p);
-          } else if (m < L.M && n < L.N) {
-            *p = a.accumulate ? *p + acc[i][j][e] : acc[i][j][e];
+          if (full || (m < L.M && n < L.N)) {
+            float v = (accum ? *p : 0.f) + acc[i][j][e];
+            if (noise)
+              v = (v + a.sigma_c * noise_at(a, tid, (uint64_t)m * (uint64_t)L.N + n)) * a.inv_b;
+            if (full) __builtin_nontemporal_store(v, p);
+            else *p = v;
           }
         }
       }
   }
+}
+
+// Row-major store of one tile through LDS, for the non-transposed layout
+// (the host orders every launch so that the kernel's rows are the output's
+// rows). Each wave copies one 32x32 block at a time into its own 32 x 36
+// float slice of LDS (MFMA layout in: lane l writes column l%32 of its 16
+// rows), then reads it back as float4s of 4 consecutive columns: lane l takes
+// row l/8 + 8*it, columns 4*(l%8) .. +3, so 8 lanes store 128 contiguous bytes
+// of a row and every float4 is one Philox block of the output tensor (when
+// the row length is a multiple of 4) for the fused Gaussian mechanism.
+constexpr int EP_LD = 36;  // floats per LDS row of a block (16-byte aligned rows, fewer conflicts)
+
+__device__ __forceinline__ void store_tile_rows(const GemmArgs& a, const GemmLayer& L, int64_t m0,
+                                                int64_t n0, int wm, int wn, int lane,
+                                                f32x16 (&acc)[4][2], float* slice) {
+  float* out = L.out;
+  const int64_t ldo = L.ldo;
+  const bool accum = L.accumulate != 0;
+  const bool noise = a.noise != 0;
+  const uint32_t tid = L.tensor_id;
+  const bool full = m0 + GM_BM <= L.M && n0 + GM_BN <= L.N;
+  const bool vec = full && (ldo & 3) == 0 && (((uintptr_t)out) & 15) == 0 && (L.N & 3) == 0;
+  const int rw = (lane >> 5) * 4;  // row of e = 0 within a block
+  const int cw = lane & 31;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) slice[(rw + (e >> 2) * 8 + (e & 3)) * EP_LD + cw] = acc[i][j][e];
+      const int64_t mb = m0 + wm * 128 + i * 32, nb = n0 + wn * 64 + j * 32;
+      // The block's 4 float4s per lane: prior values (when accumulating) are
+      // requested first and the noise is drawn while they are in flight.
+      const int c4 = 4 * (lane & 7);
+      const int64_t n = nb + c4;
+      f32x4 v[4], prior[4];
+#pragma unroll
+      for (int it = 0; it < 4; ++it) {
+        const int r = (lane >> 3) + 8 * it;
+        v[it] = *(const f32x4*)(slice + r * EP_LD + c4);
+      }
+      if (vec) {
+        if (accum) {
+#pragma unroll
+          for (int it = 0; it < 4; ++it)
+            prior[it] = *(const f32x4*)(out + (mb + (lane >> 3) + 8 * it) * ldo + n);
+        }
+        if (noise) {
+#pragma unroll
+          for (int it = 0; it < 4; ++it) {
+            const int64_t m = mb + (lane >> 3) + 8 * it;
+            float z[4];
+            gauss4(((uint64_t)m * (uint64_t)L.N + (uint64_t)n) >> 2, a.seed, tid, a.step, z);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[it][q] += a.sigma_c * z[q];
+          }
+        }
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+          const int64_t m = mb + (lane >> 3) + 8 * it;
+          f32x4 x = v[it];
+          if (accum) x += prior[it];
+          if (noise) x *= a.inv_b;
+          __builtin_nontemporal_store(x, (f32x4*)(out + m * ldo + n));
+        }
+      } else {
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+          const int64_t m = mb + (lane >> 3) + 8 * it;
+          if (m >= L.M) continue;
+          float* p = out + m * ldo + n;
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (n + q < L.N) {
+              float x = (accum ? p[q] : 0.f) + v[it][q];
+              if (noise)
+                x = (x + a.sigma_c * noise_at(a, tid, (uint64_t)m * (uint64_t)L.N + n + q)) *
+                    a.inv_b;
+              p[q] = x;
+            }
+        }
+      }
+    }
 }
 
 // Scaling of the clipped sum: SC_NONE (direct norm), SC_STAGE (rows scaled
@@ -241,7 +368,8 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
     k_begin = (int64_t)b * a.T;
     k_end = k_begin + a.T;
   }
-  const int mt = (int)(rel / (uint32_t)L.tn), nt = (int)(rel - (uint32_t)mt * L.tn);
+  int mt, nt;
+  tile_of(L, rel, mt, nt);
   const int64_t m0 = (int64_t)mt * GM_BM;
   const int64_t n0 = (int64_t)nt * GM_BN;
 
@@ -434,6 +562,7 @@ constexpr int DL_MAXB = 4096;               // clip factors held in LDS
 constexpr int DL_LOADS = 4;                 // loads per wave per stage
 static_assert(GM_BM == GM_BN, "square tiles");
 static_assert(DL_STB == (GM_THREADS / WAVE) * DL_LOADS * 1024, "one KB per load");
+static_assert((GM_THREADS / WAVE) * 32 * EP_LD * 4 <= DL_NS * DL_STB, "epilogue slices fit the ring");
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(3))) char lds_char_t;
@@ -494,7 +623,8 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
     k_begin = (int64_t)b * a.T;
     k_end = k_begin + a.T;
   }
-  const int mt = (int)(rel / (uint32_t)L.tn), nt = (int)(rel - (uint32_t)mt * L.tn);
+  int mt, nt;
+  tile_of(L, rel, mt, nt);
   const int64_t m0 = (int64_t)mt * GM_BM;
   const int64_t n0 = (int64_t)nt * GM_BN;
 
@@ -623,7 +753,14 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[i][j] *= c_acc;
-    store_tile(a, L, m0, n0, wm, wn, lane, acc);
+    if (a.transpose) {
+      store_tile(a, L, m0, n0, wm, wn, lane, acc);
+    } else {
+      // The ring is free once every wave is past its last read of it.
+      __syncthreads();
+      float* slice = (float*)ring_raw + w * 32 * EP_LD;
+      store_tile_rows(a, L, m0, n0, wm, wn, lane, acc, slice);
+    }
   } else {
     // Columns past M or N were loaded from beyond the rows' valid width and
     // only reach out-of-range elements, which the sum leaves out.

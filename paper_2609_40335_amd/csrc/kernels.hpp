@@ -73,9 +73,13 @@ struct GemmLayer {
   float* out;           // clipped sum: [M, ldo] or transposed [N, ldo]
   int64_t ldx, ldy, ldo;  // row strides in elements
   int32_t M, N;         // X columns (output rows) and Y columns (output columns)
-  int32_t tm, tn;       // 256-wide tiles along M and N
+  uint16_t tm, tn;      // 256-wide tiles along M and N
   uint32_t tile_begin;  // first work item of this entry
-  int32_t slot_begin;   // direct norm: first partial slot in an example's row
+  union {
+    int32_t slot_begin;   // direct norm: first partial slot in an example's row
+    uint32_t tensor_id;   // clipped sum with noise: the tensor's generator id
+  };
+  int32_t accumulate;   // clipped sum: out += (else out =)
 };
 
 struct GemmArgs {
@@ -83,10 +87,17 @@ struct GemmArgs {
   int32_t n_layers;
   int32_t B, T;
   uint32_t n_items;
-  int32_t transpose, accumulate;  // clipped sum: output layout and +=
+  int32_t transpose;    // clipped sum: output layout
   const float* c;       // clipped sum: per-example scale [B]
   float* ws;            // direct norm: [B, slots]
   int32_t slots;
+  // Gaussian mechanism fused into the clipped sum's store (noise != 0):
+  // out = (prior + sum + sigma_c * z) * inv_b, z from Philox (seed, tensor_id,
+  // step) at the element's row-major index in the output tensor.
+  int32_t noise;
+  float sigma_c, inv_b;
+  uint32_t step;
+  uint64_t seed;
 };
 
 static_assert(sizeof(GemmArgs) <= 4096, "kernel arguments must stay within 4 KiB");

@@ -18,47 +18,6 @@ __global__ void clip_factors_kernel(const float* __restrict__ norm2, int B, floa
   c[i] = (float)r;
 }
 
-// Philox4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC'11): each round
-// multiplies counter words 0 and 2 by the round constants, keeps both halves
-// of the 64-bit products and mixes them with words 1 and 3 and the key; the
-// key advances by the Weyl increments between rounds.
-__device__ __forceinline__ void philox4x32_10(uint32_t (&c)[4], uint32_t k0, uint32_t k1) {
-  constexpr uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
-  constexpr uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
-#pragma unroll
-  for (int r = 0; r < 10; ++r) {
-    if (r) { k0 += W0; k1 += W1; }
-    // Full 64-bit products: one v_mad_u64_u32 each instead of mul_hi + mul_lo.
-    const uint64_t p0 = (uint64_t)M0 * c[0], p1 = (uint64_t)M1 * c[2];
-    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c[1] ^ k0;
-    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c[3] ^ k1;
-    c[0] = n0; c[1] = (uint32_t)p1; c[2] = n2; c[3] = (uint32_t)p0;
-  }
-}
-
-// Four standard normals of Philox block `blk` of one tensor. Uniforms are
-// u = (x + 1/2) 2^-32; Box-Muller pairs (u0,u1) and (u2,u3) give
-// r cos(2 pi u_odd), r sin(2 pi u_odd) with r = sqrt(-2 ln u_even). In fp32
-// the conversion of x is exact below 2^24 (the far tail, small u) and rounds x
-// to 24 bits above, which moves ln u by at most 2^-24. The transcendental
-// steps run on the hardware units: ln u = ln 2 * V_LOG_F32(u) (base 2),
-// V_SQRT_F32, and V_SIN_F32 / V_COS_F32, whose argument is in revolutions,
-// so that sin(2 pi u) is V_SIN_F32(u) with no range reduction for u in (0,1).
-__device__ __forceinline__ void gauss4(uint64_t blk, uint64_t seed, uint32_t tensor_id,
-                                       uint32_t step, float (&z)[4]) {
-  uint32_t c[4] = {(uint32_t)blk, (uint32_t)(blk >> 32), tensor_id, step};
-  philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
-  constexpr float MINUS_2_LN2 = -1.3862943611198906f;
-#pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const float u = ((float)c[2 * p] + 0.5f) * 0x1p-32f;
-    const float r = __builtin_amdgcn_sqrtf(MINUS_2_LN2 * __builtin_amdgcn_logf(u));
-    const float v = ((float)c[2 * p + 1] + 0.5f) * 0x1p-32f;
-    z[2 * p] = r * __builtin_amdgcn_cosf(v);
-    z[2 * p + 1] = r * __builtin_amdgcn_sinf(v);
-  }
-}
-
 // g[j] = (g[j] + sigma*C*z_j) * inv_b, inv_b = 1/B rounded to fp32 (1 when
 // there is no division). One thread per Philox block of 4 consecutive
 // elements; the gradient is streamed once (non-temporal).

@@ -20,7 +20,8 @@ __all__ = [
     "lib", "library_path", "dp_abi_version",
     "dp_ghost_norm_linear", "dp_ghost_norm_linear_grouped", "dp_ghost_norm_embedding",
     "dp_tied_cross_term", "dp_clip_factors", "dp_clipped_grad_sum",
-    "dp_clipped_grad_sum_grouped", "dp_add_noise", "LinearGroup",
+    "dp_clipped_grad_sum_grouped", "dp_clipped_grad_sum_noised_grouped", "dp_add_noise",
+    "LinearGroup",
 ]
 
 DP_F32, DP_BF16 = 0, 1
@@ -67,6 +68,10 @@ _SIGS = {
                              _VP, _SZ, _VP], _I),
     "dp_clipped_grad_sum_grouped": ([ctypes.POINTER(dp_linear_t), ctypes.POINTER(_VP), _I, _VP,
                                      _I, _I, _I, _I, _I, _VP], _I),
+    "dp_clipped_grad_sum_noised_grouped": ([ctypes.POINTER(dp_linear_t), ctypes.POINTER(_VP),
+                                            ctypes.POINTER(_U64), ctypes.POINTER(ctypes.c_int32),
+                                            _I, _VP, _I, _I, _I, _I, _F, _F, _I, _U64, _U64, _VP],
+                                           _I),
     "dp_add_noise": ([_VP, _I64, _F, _F, _I, _U64, _U64, _U64, _VP], _I),
 }
 
@@ -260,6 +265,40 @@ def dp_clipped_grad_sum_grouped(layers: Sequence, outs: Sequence[torch.Tensor], 
            "dp_clipped_grad_sum_grouped")
 
 
+def _noise_arrays(n: int, tensor_ids: Sequence[int], accumulate):
+    if len(tensor_ids) != n:
+        raise DPError("one tensor id per layer")
+    tids = (ctypes.c_uint64 * n)(*[int(t) for t in tensor_ids])
+    if accumulate is None or isinstance(accumulate, (bool, int)):
+        acc = (ctypes.c_int32 * n)(*([int(bool(accumulate))] * n))
+    else:
+        if len(accumulate) != n:
+            raise DPError("one accumulate flag per layer")
+        acc = (ctypes.c_int32 * n)(*[int(bool(a)) for a in accumulate])
+    return tids, acc
+
+
+def dp_clipped_grad_sum_noised_grouped(layers: Sequence, outs: Sequence[torch.Tensor], c,
+                                       tensor_ids: Sequence[int], sigma: float, C: float,
+                                       B_norm: int, seed: int, step: int, accumulate=None,
+                                       transpose_out: bool = False, stream=None) -> None:
+    """Clipped sums with the Gaussian mechanism fused into their store; the
+    noise each output gets is the one dp_add_noise(outs[l], ..., tensor_ids[l],
+    step) would add. ``accumulate`` is a bool or one bool per layer."""
+    L = lib()
+    descs = [_layer(l[0], l[1]) for l in layers]
+    arr = (dp_linear_t * len(descs))(*descs)
+    optrs = (ctypes.c_void_p * len(outs))(*[o.data_ptr() for o in outs])
+    tids, acc = _noise_arrays(len(descs), tensor_ids, accumulate)
+    A0 = layers[0][0]
+    _check(L.dp_clipped_grad_sum_noised_grouped(arr, optrs, tids, acc, len(descs), c.data_ptr(),
+                                                A0.shape[0], A0.shape[1], _dtype(A0),
+                                                int(transpose_out), float(sigma), float(C),
+                                                int(B_norm), int(seed), int(step),
+                                                _stream(stream)),
+           "dp_clipped_grad_sum_noised_grouped")
+
+
 def dp_add_noise(grad, sigma: float, C: float, B_norm: int, seed: int, tensor_id: int,
                  step: int, stream=None) -> torch.Tensor:
     if grad.dtype != torch.float32 or not grad.is_contiguous():
@@ -316,3 +355,24 @@ class LinearGroup:
                                                  self.B, self.T, self.dt, int(transpose_out),
                                                  int(accumulate), _stream(stream)),
                "dp_clipped_grad_sum_grouped")
+
+    def clipped_sum_noised(self, c: torch.Tensor, tensor_ids: Sequence[int], sigma: float,
+                           C: float, B_norm: int, seed: int, step: int, accumulate=None,
+                           transpose_out: bool = False, stream=None) -> None:
+        """clipped_sum with the Gaussian mechanism fused (see
+        dp_clipped_grad_sum_noised_grouped)."""
+        if self.outs is None:
+            raise DPError("set_outputs() first")
+        key = (tuple(int(t) for t in tensor_ids),
+               accumulate if isinstance(accumulate, (bool, int, type(None)))
+               else tuple(bool(a) for a in accumulate))
+        if getattr(self, "_noise_key", None) != key:
+            self._noise_key = key
+            self._noise_arr = _noise_arrays(self.n, tensor_ids, accumulate)
+        tids, acc = self._noise_arr
+        _check(lib().dp_clipped_grad_sum_noised_grouped(self.descs, self.outs, tids, acc, self.n,
+                                                        c.data_ptr(), self.B, self.T, self.dt,
+                                                        int(transpose_out), float(sigma),
+                                                        float(C), int(B_norm), int(seed),
+                                                        int(step), _stream(stream)),
+               "dp_clipped_grad_sum_noised_grouped")
