@@ -163,6 +163,34 @@ def test_clipped_sum_rejects_bad_arguments(L):
     assert L.dp_clipped_grad_sum_grouped(arr, outs, 1, 1 << 20, 4, 16, 0, 0, 0, None) == EINVAL
 
 
+def test_noised_sum_rejects_bad_arguments(L):
+    """The fused clipped sum + noise validates everything on the host (no launch)."""
+    f = L.dp_clipped_grad_sum_noised_grouped
+    arr = (D.dp_linear_t * 1)(_lin())
+    outs = (ctypes.c_void_p * 1)(1 << 24)
+    tids = (ctypes.c_uint64 * 1)(3)
+    acc = (ctypes.c_int32 * 1)(0)
+    ok = dict(c=1 << 20, B=4, T=16, dt=D.DP_F32, tr=0, sigma=1.0, C=1.0, Bn=4, seed=1, step=2)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(arr, outs, kw.get("tids", tids), acc, 1, a["c"], a["B"], a["T"], a["dt"], a["tr"],
+                 a["sigma"], a["C"], a["Bn"], a["seed"], a["step"], None)
+
+    assert call(tids=None) == EINVAL
+    assert call(tids=(ctypes.c_uint64 * 1)(1 << 32)) == EINVAL
+    assert b"tensor_ids" in L.dp_last_error()
+    assert call(sigma=-1.0) == EINVAL
+    assert call(sigma=float("nan")) == EINVAL
+    assert call(C=0.0) == EINVAL
+    assert call(Bn=-1) == EINVAL
+    assert call(step=1 << 32) == EINVAL
+    assert call(c=None) == EINVAL
+    assert f(arr, (ctypes.c_void_p * 1)(None), tids, acc, 1, 1 << 20, 4, 16, D.DP_F32, 0, 1.0,
+             1.0, 4, 1, 2, None) == EINVAL
+    assert call(B=0) == EINVAL
+
+
 def test_noise_rejects_bad_arguments(L):
     f = L.dp_add_noise
     assert f(1 << 20, -1, 1.0, 1.0, 4, 0, 0, 0, None) == EINVAL
