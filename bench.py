@@ -36,8 +36,8 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 # HBM bytes per launch of the clipped-sum kernel: rocprofv3 FETCH_SIZE x 2 +
 # WRITE_SIZE x 1 (factors from a plain 1 GiB copy), recorded for the kernel
 # source with this SHA-256; any other source reports null.
-GEMM_TRAFFIC = {"gemm.hip sha256": "59a50bb18e8577c27deb406b2bfd475d3c8a82eb88c7b8f8cd4de0a620e21b4c",
-                "bytes": 2816417088}
+GEMM_TRAFFIC = {"gemm.hip sha256": "e9250bc390301fc0ab68c7a2dddf700b251067a36bd0ffd2f528ec20303ada9d",
+                "bytes": 2575342231}
 
 
 def log(*a):
@@ -60,6 +60,9 @@ def parse(argv=None):
     ap.add_argument("--crossover", action="store_true",
                     help="instead of the step: time each distinct layer shape's grouped norm "
                          "with the Gram kernel and with the direct kernel (one JSON line)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="instead of the step: three plain 1 GiB device copies, the reference "
+                         "for scaling the FETCH_SIZE / WRITE_SIZE counters to bytes")
     return ap.parse_args(argv)
 
 
@@ -121,18 +124,19 @@ class Step:
         self.sum_group = dp.LinearGroup(sum_layers, sum_outs) if sum_layers else None
         # Noise generator ids per parameter tensor, as in the oracle's step:
         # linear l -> l, the input embedding (or tied matrix) -> L, an untied
-        # head -> L + 1. The tied matrix receives the embedding sum first and
-        # the head GEMM accumulates onto it, so it is noised once.
+        # head -> L + 1. Every GEMM-shaped output is written once with its
+        # noise; the embedding part is then added onto the (tied or untied)
+        # embedding matrix with the factors c/B, so that matrix is noised once
+        # and never zero-filled.
         L = len(wl.linears)
         self.sum_tids = list(range(L))
-        self.sum_acc = [False] * L
         self.tied = h is not None and h.H is not None and h.tied
         if h is not None and h.H is not None:
             self.sum_tids.append(L if h.tied else L + 1)
-            self.sum_acc.append(self.tied)
         self.e_tid = L
         self.n2 = torch.zeros(B, device="cuda")
         self.c = torch.zeros(B, device="cuda")
+        self.c_b = torch.zeros(B, device="cuda")   # c / B
         # algorithmic work of the grouped clipped-sum GEMM (the dominant kernel)
         K = B * T
         self.gemm_flops = 2.0 * K * sum(a.shape[2] * g.shape[2] for a, g in sum_layers)
@@ -154,22 +158,22 @@ class Step:
                 dp.dp_tied_cross_term(self.ids, self.dE, self.H, self.Gz, h.V, self.n2,
                                       scale=2.0, accumulate=True)
                 mark("cross_term")
-        dp.dp_clip_factors(self.n2, wl.C, self.c)
+        dp.dp_clip_factors_scaled(self.n2, wl.C, 1.0 / wl.B, self.c_b, c=self.c)
         mark("clip")
-        if h is not None:
-            dp.dp_clipped_grad_sum(None, self.dE, self.c, self.E, ids=self.ids, V=h.V)
-            mark("embedding_sum")
         # clipped sums of every GEMM-shaped tensor with the Gaussian mechanism
         # fused into their store (eq. 3): (S + sigma C z) / B
         if self.sum_group is not None:
             self.sum_group.clipped_sum_noised(self.c, self.sum_tids, wl.sigma, wl.C, wl.B,
-                                              seed=1234, step=self.step_id,
-                                              accumulate=self.sum_acc)
+                                              seed=1234, step=self.step_id)
             mark("clipped_sum_noise")
-        if h is not None and not self.tied:
-            dp.dp_add_noise(self.E, wl.sigma, wl.C, wl.B, seed=1234, tensor_id=self.e_tid,
-                            step=self.step_id)
-            mark("embedding_noise")
+        if h is not None:
+            if not self.tied:
+                dp.dp_noise_fill(self.E, wl.sigma, wl.C, wl.B, seed=1234, tensor_id=self.e_tid,
+                                 step=self.step_id)
+                mark("embedding_noise")
+            dp.dp_clipped_grad_sum(None, self.dE, self.c_b, self.E, ids=self.ids, V=h.V,
+                                   accumulate=True)
+            mark("embedding_sum")
         self.step_id += 1
 
 
@@ -261,6 +265,15 @@ def main(argv=None) -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
+    if args.copy_calibration:
+        n = 256 << 20  # 256 Mi floats = 1 GiB
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": src.numel() * 4, "copies": 3}), flush=True)
+        return 0
     dp.lib()
     t0 = time.perf_counter()
     V = gen.GPT2_VOCAB

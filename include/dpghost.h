@@ -156,6 +156,20 @@ dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, 
 dp_status_t dp_clip_factors(const float* norm2, int B, float C, float* c, void* stream);
 
 /* ---------------------------------------------------------------------
+ * Scaled clip factors (eq. 2, eq. 7 and the 1/B of eq. 3):
+ *   c_scaled[b] = scale * min(1, C / sqrt(norm2[b]))   (1 when norm2 <= 0)
+ * evaluated in double and rounded once to fp32; c (may be NULL) receives
+ * the unscaled factors of dp_clip_factors in the same launch. With scale =
+ * 1/B these factors let an embedding-form clipped sum add its part of eq. 3
+ * directly onto an output that already holds (S + sigma*C*z)/B (written by
+ * dp_clipped_grad_sum_noised_grouped or dp_noise_fill), so the output is
+ * written once. norm2, c and c_scaled are device arrays of B floats; scale
+ * must be finite.
+ * ------------------------------------------------------------------- */
+dp_status_t dp_clip_factors_scaled(const float* norm2, int B, float C, float scale, float* c,
+                                   float* c_scaled, void* stream);
+
+/* ---------------------------------------------------------------------
  * Clipped gradient sum (the bracket of eq. 3 without noise): the gradient
  * of the loss reweighted by the clip factors, as one GEMM over the B*T
  * tokens (K = B*T) with token k of example b scaled by c[b]:
@@ -192,8 +206,10 @@ dp_status_t dp_clipped_grad_sum_grouped(const dp_linear_t* layers, float* const*
  * transpose_out) takes index r*cols + k of the tensor's Philox stream. The
  * result equals dp_clipped_grad_sum_grouped followed by dp_add_noise on each
  * output, without a second pass over the gradients. B_norm = 0: no
- * division. A tied matrix is noised once: write its other contribution first
- * (e.g. the embedding-form clipped sum) and pass accumulate[l] = 1.
+ * division. A tied matrix is noised once: either write the head's part here
+ * (accumulate[l] = 0) and then add the embedding-form clipped sum with the
+ * factors c/B_norm from dp_clip_factors_scaled (the matrix is written once),
+ * or write the embedding part first and pass accumulate[l] = 1.
  * tensor_ids[l] and step must be < 2^32; accumulate may be NULL (all 0).
  * tensor_ids and accumulate are host arrays of n_layers entries.
  * ------------------------------------------------------------------- */
@@ -223,6 +239,13 @@ dp_status_t dp_clipped_grad_sum_noised_grouped(const dp_linear_t* layers, float*
  * ------------------------------------------------------------------- */
 dp_status_t dp_add_noise(float* grad, int64_t n, float sigma, float C, int B_norm, uint64_t seed,
                          uint64_t tensor_id, uint64_t step, void* stream);
+
+/* Noise alone (eq. 3 with a zero sum): out[j] = sigma*C*z_j / B_norm with
+ * the z_j of dp_add_noise for the same (seed, tensor_id, step), bit-identical
+ * to dp_add_noise on zeros; out is written without being read. Arguments
+ * and limits as for dp_add_noise. */
+dp_status_t dp_noise_fill(float* out, int64_t n, float sigma, float C, int B_norm, uint64_t seed,
+                          uint64_t tensor_id, uint64_t step, void* stream);
 
 #ifdef __cplusplus
 }

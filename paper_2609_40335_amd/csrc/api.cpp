@@ -417,7 +417,18 @@ dp_status_t dp_clip_factors(const float* norm2, int B, float C, float* c, void* 
   if (!norm2 || !c) return fail(DP_EINVAL, "norm2 or c is NULL");
   if (B <= 0) return fail(DP_EINVAL, "B must be positive");
   if (!(C > 0.f) || !std::isfinite(C)) return fail(DP_EINVAL, "C must be positive and finite");
-  return hip_status(dpg::launch_clip_factors(norm2, B, C, c, as_stream(stream)), "clip launch");
+  return hip_status(dpg::launch_clip_factors(norm2, B, C, 1.f, c, nullptr, as_stream(stream)),
+                    "clip launch");
+}
+
+dp_status_t dp_clip_factors_scaled(const float* norm2, int B, float C, float scale, float* c,
+                                   float* c_scaled, void* stream) {
+  if (!norm2 || !c_scaled) return fail(DP_EINVAL, "norm2 or c_scaled is NULL");
+  if (B <= 0) return fail(DP_EINVAL, "B must be positive");
+  if (!(C > 0.f) || !std::isfinite(C)) return fail(DP_EINVAL, "C must be positive and finite");
+  if (!std::isfinite(scale)) return fail(DP_EINVAL, "scale must be finite");
+  return hip_status(dpg::launch_clip_factors(norm2, B, C, scale, c, c_scaled, as_stream(stream)),
+                    "clip launch");
 }
 
 size_t dp_clipped_grad_sum_workspace(int B, int T, int d_out, int with_ids) {
@@ -519,8 +530,9 @@ dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64
   return hip_status(dpg::launch_embed_sum(a, kdt(dt), s), "embed_sum launch");
 }
 
-dp_status_t dp_add_noise(float* grad, int64_t n, float sigma, float C, int B_norm, uint64_t seed,
-                         uint64_t tensor_id, uint64_t step, void* stream) {
+static dp_status_t noise_call(float* grad, int64_t n, float sigma, float C, int B_norm,
+                              uint64_t seed, uint64_t tensor_id, uint64_t step, bool accumulate,
+                              void* stream) {
   if (n < 0) return fail(DP_EINVAL, "n must be >= 0");
   if (n > 0 && !grad) return fail(DP_EINVAL, "grad is NULL");
   if (!(sigma >= 0.f) || !std::isfinite(sigma)) return fail(DP_EINVAL, "sigma must be >= 0");
@@ -530,8 +542,18 @@ dp_status_t dp_add_noise(float* grad, int64_t n, float sigma, float C, int B_nor
   const float sigma_c = (float)((double)sigma * (double)C);
   const float inv_b = B_norm > 0 ? (float)(1.0 / (double)B_norm) : 1.f;
   return hip_status(dpg::launch_add_noise(grad, n, sigma_c, inv_b, seed, (uint32_t)tensor_id,
-                                          (uint32_t)step, as_stream(stream)),
+                                          (uint32_t)step, accumulate, as_stream(stream)),
                     "noise launch");
+}
+
+dp_status_t dp_add_noise(float* grad, int64_t n, float sigma, float C, int B_norm, uint64_t seed,
+                         uint64_t tensor_id, uint64_t step, void* stream) {
+  return noise_call(grad, n, sigma, C, B_norm, seed, tensor_id, step, true, stream);
+}
+
+dp_status_t dp_noise_fill(float* out, int64_t n, float sigma, float C, int B_norm, uint64_t seed,
+                          uint64_t tensor_id, uint64_t step, void* stream) {
+  return noise_call(out, n, sigma, C, B_norm, seed, tensor_id, step, false, stream);
 }
 
 }  // extern "C"

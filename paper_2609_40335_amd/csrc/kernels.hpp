@@ -143,8 +143,11 @@ hipError_t launch_embed_sum(const EmbedSumArgs& a, int dt, hipStream_t s);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 
 // ----------------------------------------------------------- clip and noise
-hipError_t launch_clip_factors(const float* norm2, int B, float C, float* c, hipStream_t s);
+// c (nullable) = clip factors; cs (nullable) = scale * clip factors.
+hipError_t launch_clip_factors(const float* norm2, int B, float C, float scale, float* c,
+                               float* cs, hipStream_t s);
+// accumulate: g = (g + sigma_c z) inv_b; else g = sigma_c z inv_b (g not read).
 hipError_t launch_add_noise(float* g, int64_t n, float sigma_c, float inv_b, uint64_t seed,
-                            uint32_t tensor_id, uint32_t step, hipStream_t s);
+                            uint32_t tensor_id, uint32_t step, bool accumulate, hipStream_t s);
 
 }  // namespace dpg

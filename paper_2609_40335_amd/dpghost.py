@@ -19,8 +19,9 @@ __all__ = [
     "DPError", "DP_F32", "DP_BF16", "DP_NORM_AUTO", "DP_NORM_GRAM", "DP_NORM_DIRECT",
     "lib", "library_path", "dp_abi_version",
     "dp_ghost_norm_linear", "dp_ghost_norm_linear_grouped", "dp_ghost_norm_embedding",
-    "dp_tied_cross_term", "dp_clip_factors", "dp_clipped_grad_sum",
+    "dp_tied_cross_term", "dp_clip_factors", "dp_clip_factors_scaled", "dp_clipped_grad_sum",
     "dp_clipped_grad_sum_grouped", "dp_clipped_grad_sum_noised_grouped", "dp_add_noise",
+    "dp_noise_fill",
     "LinearGroup",
 ]
 
@@ -73,6 +74,8 @@ _SIGS = {
                                             _I, _VP, _I, _I, _I, _I, _F, _F, _I, _U64, _U64, _VP],
                                            _I),
     "dp_add_noise": ([_VP, _I64, _F, _F, _I, _U64, _U64, _U64, _VP], _I),
+    "dp_clip_factors_scaled": ([_VP, _I, _F, _F, _VP, _VP, _VP], _I),
+    "dp_noise_fill": ([_VP, _I64, _F, _F, _I, _U64, _U64, _U64, _VP], _I),
 }
 
 
@@ -224,6 +227,16 @@ def dp_clip_factors(norm2, C: float, c, stream=None) -> torch.Tensor:
     return c
 
 
+def dp_clip_factors_scaled(norm2, C: float, scale: float, c_scaled, c=None,
+                           stream=None) -> torch.Tensor:
+    """c_scaled = scale * clip factors (and the factors into c when given)."""
+    _check(lib().dp_clip_factors_scaled(norm2.data_ptr(), norm2.numel(), float(C), float(scale),
+                                        None if c is None else c.data_ptr(),
+                                        c_scaled.data_ptr(), _stream(stream)),
+           "dp_clip_factors_scaled")
+    return c_scaled
+
+
 def dp_clipped_grad_sum(A, G, c, out, ids=None, V: Optional[int] = None,
                         transpose_out: bool = False, accumulate: bool = False,
                         stream=None) -> torch.Tensor:
@@ -307,6 +320,17 @@ def dp_add_noise(grad, sigma: float, C: float, B_norm: int, seed: int, tensor_id
                               int(seed), int(tensor_id), int(step), _stream(stream)),
            "dp_add_noise")
     return grad
+
+
+def dp_noise_fill(out, sigma: float, C: float, B_norm: int, seed: int, tensor_id: int,
+                  step: int, stream=None) -> torch.Tensor:
+    """out = sigma*C*z / B_norm: dp_add_noise on zeros, without reading out."""
+    if out.dtype != torch.float32 or not out.is_contiguous():
+        raise DPError("out must be contiguous fp32")
+    _check(lib().dp_noise_fill(out.data_ptr(), out.numel(), float(sigma), float(C), int(B_norm),
+                               int(seed), int(tensor_id), int(step), _stream(stream)),
+           "dp_noise_fill")
+    return out
 
 
 class LinearGroup:

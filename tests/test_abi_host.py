@@ -143,6 +143,12 @@ def test_cross_and_clip_reject_bad_arguments(L):
     assert L.dp_clip_factors(1 << 20, 4, 0.0, 1 << 21, None) == EINVAL
     assert L.dp_clip_factors(1 << 20, 4, float("nan"), 1 << 21, None) == EINVAL
     assert L.dp_clip_factors(1 << 20, 0, 1.0, 1 << 21, None) == EINVAL
+    g = L.dp_clip_factors_scaled
+    assert g(1 << 20, 4, 1.0, 0.5, None, None, None) == EINVAL       # no c_scaled
+    assert g(None, 4, 1.0, 0.5, None, 1 << 21, None) == EINVAL       # no norm2
+    assert g(1 << 20, 0, 1.0, 0.5, None, 1 << 21, None) == EINVAL
+    assert g(1 << 20, 4, -1.0, 0.5, None, 1 << 21, None) == EINVAL
+    assert g(1 << 20, 4, 1.0, float("inf"), None, 1 << 21, None) == EINVAL
 
 
 def test_clipped_sum_rejects_bad_arguments(L):
@@ -202,6 +208,12 @@ def test_noise_rejects_bad_arguments(L):
     assert f(1 << 20, 10, 1.0, 1.0, 4, 0, 0, 1 << 32, None) == EINVAL
     # n = 0 is a no-op that launches nothing
     assert f(None, 0, 1.0, 1.0, 4, 0, 0, 0, None) == 0
+    # the write-only form validates the same way
+    g = L.dp_noise_fill
+    assert g(None, 10, 1.0, 1.0, 4, 0, 0, 0, None) == EINVAL
+    assert g(1 << 20, 10, float("nan"), 1.0, 4, 0, 0, 0, None) == EINVAL
+    assert g(1 << 20, 10, 1.0, 1.0, 4, 0, 0, 1 << 32, None) == EINVAL
+    assert g(None, 0, 1.0, 1.0, 4, 0, 0, 0, None) == 0
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

@@ -235,6 +235,22 @@ def test_clip_factors(dp):
         assert np.all(got * np.sqrt(n2.astype(np.float64)) <= C * (1 + 1e-5))
 
 
+def test_clip_factors_scaled(dp):
+    n2 = np.array([0.0, 1e-12, 0.25, 1.0, 1.0000001, 4.0, 1e6, 3.3e-3, 17.0], np.float32)
+    for C, scale in ((1.0, 1 / 32), (0.05, 1 / 24), (0.5, 3.0)):
+        ref = O.clip_factors(n2.astype(np.float64), C)
+        c = torch.full((len(n2),), -1.0, device="cuda")
+        cs = torch.empty(len(n2), device="cuda")
+        dp.dp_clip_factors_scaled(dev(n2), C, scale, cs, c=c)
+        assert rel(host(cs), np.float32(scale) * ref).max() <= 1e-6
+        plain = torch.empty(len(n2), device="cuda")
+        dp.dp_clip_factors(dev(n2), C, plain)
+        assert torch.equal(c, plain)
+        cs2 = torch.empty(len(n2), device="cuda")
+        dp.dp_clip_factors_scaled(dev(n2), C, scale, cs2)   # without c
+        assert torch.equal(cs, cs2)
+
+
 # ---------------------------------------------------------------------------
 # a7 / a8: clipped sums
 # ---------------------------------------------------------------------------
@@ -482,6 +498,21 @@ def test_noise_sigma_zero_and_unaligned(dp):
     assert fro_rel(host(sub), ref) <= TOL["f32"]
 
 
+@pytest.mark.parametrize("n,offset", [(1_000_003, 0), (1001, 1), (4, 0), (3, 2)])
+def test_noise_fill(dp, n, offset):
+    """Noise alone equals dp_add_noise on zeros bit for bit, without reading
+    the output (it starts as NaN), aligned or not, with a ragged tail."""
+    sigma, C, B = 1.3, 0.5, 24
+    buf = torch.full((n + offset,), float("nan"), device="cuda")
+    out = buf[offset:]
+    dp.dp_noise_fill(out, sigma, C, B, seed=99, tensor_id=4, step=11)
+    zeros = torch.zeros(n, device="cuda")
+    dp.dp_add_noise(zeros, sigma, C, B, seed=99, tensor_id=4, step=11)
+    assert torch.equal(out, zeros)
+    ref = O.add_noise(np.zeros(n), sigma, C, B, seed=99, tensor_id=4, step=11)
+    assert fro_rel(host(out), ref) <= TOL["f32"]
+
+
 # ---------------------------------------------------------------------------
 # The whole step on the tiny configs, against oracle.step
 # ---------------------------------------------------------------------------
@@ -519,17 +550,21 @@ def test_tiny_step(dp, name):
     dp.dp_add_noise(E, wl.sigma, wl.C, B, 3, 1, 5)
     assert fro_rel(host(S), ref["noisy"]["linear"]) <= TOL[dt]
     assert fro_rel(host(E), ref["noisy"]["wte"]) <= TOL[dt]
-    # The same step with the noise fused into the GEMM store (the benchmark's
-    # order): the embedding sum first, the tied head accumulating onto it.
+    # The same step in the benchmark's order: the noise fused into the GEMM
+    # store (the tied head written first), then the embedding part added with
+    # the factors c/B; an embedding without a tied head starts from noise alone.
     S2 = torch.empty(lin.d_in, lin.d_out, device="cuda")
-    E2 = torch.empty(h.V, h.d, device="cuda")
-    dp.dp_clipped_grad_sum(None, dE, c, E2, ids=ids, V=h.V)
+    E2 = torch.full((h.V, h.d), float("nan"), device="cuda")
+    c2, c_b = torch.empty(B, device="cuda"), torch.empty(B, device="cuda")
+    dp.dp_clip_factors_scaled(n2, wl.C, 1.0 / B, c_b, c=c2)
+    assert torch.equal(c2, c)
     if h.H is not None:
         dp.dp_clipped_grad_sum_noised_grouped([(A, G), (Gzd, Hd)], [S2, E2], c, [0, 1],
-                                              wl.sigma, wl.C, B, 3, 5, accumulate=[False, True])
+                                              wl.sigma, wl.C, B, 3, 5)
     else:
         dp.dp_clipped_grad_sum_noised_grouped([(A, G)], [S2], c, [0], wl.sigma, wl.C, B, 3, 5)
-        dp.dp_add_noise(E2, wl.sigma, wl.C, B, 3, 1, 5)
+        dp.dp_noise_fill(E2, wl.sigma, wl.C, B, 3, 1, 5)
+    dp.dp_clipped_grad_sum(None, dE, c_b, E2, ids=ids, V=h.V, accumulate=True)
     assert fro_rel(host(S2), ref["noisy"]["linear"]) <= TOL[dt]
     assert fro_rel(host(E2), ref["noisy"]["wte"]) <= TOL[dt]
 
