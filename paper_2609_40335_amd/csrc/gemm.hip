@@ -537,22 +537,32 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
 // two such reads give one 32x32x16 operand. With the swizzle the 16 chunks a
 // half-wave touches fall in 16 distinct bank groups.
 //
-// Ring of 4 stages of 32 k (32 KB each: X then Y). Iteration s: read the
-// second half (k 16..31) of stage s, issue the first half's MFMAs, wait for
-// stage s+1 and barrier, load stage s+4 into stage s's slot, read the first
-// half of stage s+1, issue the second half's MFMAs. The barrier thus
-// certifies both that stage s+1 has landed and that every wave is done with
-// stage s, and the MFMAs issued before it keep the matrix cores busy while
-// the waves synchronise. Every iteration issues the same 4 loads per wave
+// Ring of 4 stages of 32 k (32 KB each: X then Y), worked in ping-pong by
+// two groups of four waves, one wave of each group per SIMD: while one group
+// issues a stage's 16 MFMAs (at raised wave priority), the other reads the
+// next stage's fragments out of LDS, issues its share of a later stage's
+// loads and, at an example boundary, rescales its accumulators; a barrier
+// swaps the roles. So each SIMD always has one wave feeding its matrix core
+// and one wave doing everything else, and the VALU work of the rescale runs
+// beside the other group's MFMAs. Group 0 (waves 0-3, the X loaders)
+// computes stage s in phase 2s and reads stage s+1 in phase 2s+1; group 1
+// (waves 4-7, the Y loaders) reads stage s in phase 2s and computes it in
+// phase 2s+1. Stage s's slot is free once phase 2s ends: group 0 refills it
+// with stage s+4 in phase 2s+1, and group 1 refills the slot of stage s-1
+// with stage s+3 in phase 2s. Every wave waits for its own loads of stage
+// s+1 at the end of phase 2s, so the barrier that ends the phase certifies
+// that stage s+1 has landed. Every phase issues the same 4 loads per wave
 // (stages past the end read zeros through the range check into a slot that
-// is never read), so the wait counts are constants.
+// is never read again), so the wait counts are constants.
 //
 // The loads are issued from inline assembly: the compiler would otherwise
 // treat every later LDS read as possibly aliasing an LDS-writing load and
 // drain all of them (vmcnt(0)) before it, serialising the ring. Its wait
 // bookkeeping stays sound: untracked loads only make its own waits stricter.
 // Clip factors are staged in LDS so that the loop issues no other vector
-// memory instruction. Scaling is on the fp32 accumulators as in SC_ACC.
+// memory instruction; each is read one example ahead, so that a rescale never
+// waits behind the fragment reads. Scaling is on the fp32 accumulators as in
+// SC_ACC.
 constexpr int DL_BK = 32;                   // k rows per stage
 constexpr int DL_NS = 4;                    // stages in the ring
 constexpr int DL_ROWB = GM_BM * 2;          // bytes per LDS row (256 bf16)
@@ -699,10 +709,18 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
     for (int i = tid; i < a.B; i += GM_THREADS) cs[i] = a.c[i];
   const int spe = a.T / DL_BK;  // stages per example
   float c_acc = 0.f;            // factor of what is accumulated; 0: nothing yet
+  float c_nx = 0.f;             // factor of the example that starts at stage s_nx
   bool skip = false;
+  int s_nx = 0, e_nx = 0;       // next example boundary (a stage) and its example
+  // Called once per stage, in increasing order, in the memory phase before
+  // that stage's MFMAs: at an example boundary, rescales the accumulators by
+  // c_prev / c_next and fetches the factor of the example after.
   auto enter = [&](int s) {
-    if (MODE == MODE_SUM && s % spe == 0) {
-      const float ce = cs[s / spe];
+    if (MODE == MODE_SUM && s == s_nx) {
+      const float ce = c_nx;
+      ++e_nx;
+      s_nx += spe;
+      if (e_nx < a.B) c_nx = cs[e_nx];
       skip = !(ce != 0.f);
       if (!skip) {
         if (c_acc != 0.f) {
@@ -716,35 +734,72 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
       }
     }
   };
-  auto rd = [&](int s, int half, u32x4 (&f)[6]) {
+  // Both halves (k 0..15 and 16..31) of stage s: 4 X and 2 Y fragments each.
+  auto rd = [&](int s, u32x4 (&f)[12]) {
     const lds_char_t* base = ring + (s % DL_NS) * DL_STB;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) f[i] = dl_frag(base, ox[i] + half * 16 * DL_ROWB);
+    for (int h = 0; h < 2; ++h) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) f[4 + j] = dl_frag(base, oy[j] + half * 16 * DL_ROWB);
+      for (int i = 0; i < 4; ++i) f[6 * h + i] = dl_frag(base, ox[i] + h * 16 * DL_ROWB);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) f[6 * h + 4 + j] = dl_frag(base, oy[j] + h * 16 * DL_ROWB);
+    }
   };
-  auto mm = [&](const u32x4 (&f)[6]) {
+  auto compute = [&](const u32x4 (&f)[12]) {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(1);
+    if (!skip) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = mfma32_bf16(f[i], f[4 + j], acc[i][j]);
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = mfma32_bf16(f[6 * h + i], f[6 * h + 4 + j], acc[i][j]);
+    }
+    __builtin_amdgcn_s_setprio(0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // Phase boundary; nothing is scheduled across it.
+  auto bar = [&]() {
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
   };
 
-  u32x4 fa[6], fb[6];
+  u32x4 fr[12];
+  if (w < 4) {
 #pragma unroll
-  for (int p = 0; p < DL_NS; ++p) issue(p);
-  wait_vmcnt<DL_LOADS * (DL_NS - 1)>();
-  __syncthreads();
-  rd(0, 0, fa);
-  for (int s = 0; s < nS; ++s) {
-    enter(s);
-    rd(s, 1, fb);
-    if (!skip) mm(fa);
+    for (int p = 0; p < DL_NS; ++p) issue(p);
+    wait_vmcnt<DL_LOADS * (DL_NS - 1)>();
+    bar();  // stage 0 has landed, the factor table is filled
+    if constexpr (MODE == MODE_SUM) c_nx = cs[0];
+    rd(0, fr);
+    enter(0);
+    for (int s = 0; s < nS; ++s) {
+      compute(fr);
+      wait_vmcnt<DL_LOADS * (DL_NS - 2)>();
+      bar();
+      issue(s + DL_NS);
+      rd(s + 1, fr);  // past the last stage: a harmless read of an unused slot
+      if (s + 1 < nS) enter(s + 1);
+      bar();
+    }
+  } else {
+#pragma unroll
+    for (int p = 0; p < DL_NS - 1; ++p) issue(p);
     wait_vmcnt<DL_LOADS * (DL_NS - 2)>();
-    __syncthreads();
-    issue(s + DL_NS);
-    rd(s + 1, 0, fa);
-    if (!skip) mm(fb);
+    bar();
+    if constexpr (MODE == MODE_SUM) c_nx = cs[0];
+    for (int s = 0; s < nS; ++s) {
+      issue(s + DL_NS - 1);
+      rd(s, fr);
+      enter(s);
+      wait_vmcnt<DL_LOADS * (DL_NS - 2)>();
+      bar();
+      compute(fr);
+      bar();
+    }
   }
   // No load may still be writing LDS when the workgroup ends.
   wait_vmcnt<0>();
