@@ -36,8 +36,8 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 # HBM bytes per launch of the clipped-sum kernel: rocprofv3 FETCH_SIZE x 2 +
 # WRITE_SIZE x 1 (factors from a plain 1 GiB copy), recorded for the kernel
 # source with this SHA-256; any other source reports null.
-GEMM_TRAFFIC = {"gemm.hip sha256": "e9250bc390301fc0ab68c7a2dddf700b251067a36bd0ffd2f528ec20303ada9d",
-                "bytes": 2575342231}
+GEMM_TRAFFIC = {"gemm.hip sha256": "6ae185e5967dbd6850dd579285b26884d314b5296fc147d6dc07e8a618dcada6",
+                "bytes": 2575286961}
 
 
 def log(*a):
@@ -54,7 +54,7 @@ def parse(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--ldz-multiple", type=int, default=64,
                     help="pad logit-gradient rows to a multiple of this many columns")
-    ap.add_argument("--cpu-budget", type=float, default=15.0,
+    ap.add_argument("--cpu-budget", type=float, default=25.0,
                     help="seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--crossover", action="store_true",
