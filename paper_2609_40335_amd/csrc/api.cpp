@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -55,7 +56,22 @@ inline bool span_ok(int64_t rows, int64_t ld, dp_dtype_t dt) {
 
 // ------------------------------------------------------------------ planning
 constexpr int KG_SPLIT = 4096;  // G feature ranges longer than this are chunked
-constexpr int KG_CHUNK = 2048;  // chunk width (a multiple of both stage widths)
+constexpr int KG_MIN = 1024;    // narrowest chunk considered
+
+// Compute units of the current device (256 on MI355X), read once per device.
+int device_cus() {
+  static thread_local int cached_dev = -1, cached_cus = 256;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return cached_cus;
+  if (dev != cached_dev) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        cus > 0)
+      cached_cus = cus;
+    cached_dev = dev;
+  }
+  return cached_cus;
+}
 
 struct GramEntry {
   const void* A;
@@ -136,20 +152,56 @@ void plan_sum(const dp_linear_t& L, int transpose_out, dp_dtype_t dt, float* out
     plan_gemm(L.A, L.lda, L.d_in, L.G, L.ldg, L.d_out, dt, out, L.d_out, v, nullptr, 0);
 }
 
-NormPlan plan_norm(const dp_linear_t* layers, int n, int T, dp_dtype_t dt) {
+// Chunk count of a G range longer than KG_SPLIT features. Chunks are at most
+// KG_SPLIT and at least KG_MIN features wide (whole stages); among those
+// counts, the one whose launch (this layer's items plus `other` items of the
+// same kernel) fills the last round of `slots` concurrent workgroups best,
+// the fewest chunks on a tie (each chunk re-reads A).
+int pick_chunks(int64_t width, int ks, int64_t items_per_chunk, int64_t other, int64_t slots) {
+  const int64_t nc_lo = ceil_div(width, KG_SPLIT);
+  const int64_t nc_hi = std::max(nc_lo, ceil_div(width, KG_MIN));
+  int64_t best = nc_lo;
+  double best_idle = 2.0;
+  for (int64_t nc = nc_lo; nc <= nc_hi; ++nc) {
+    const int64_t kg = ceil_div(ceil_div(width, nc), ks) * ks;
+    const int64_t eff = ceil_div(width, kg);
+    const int64_t total = other + items_per_chunk * eff;
+    const double idle = (double)(ceil_div(total, slots) * slots - total) / (double)total;
+    if (idle < best_idle - 1e-9) { best_idle = idle; best = eff; }
+  }
+  return (int)best;
+}
+
+NormPlan plan_norm(const dp_linear_t* layers, int n, int B, int T, dp_dtype_t dt) {
   NormPlan p;
   p.n_t = (int)ceil_div(T, dpg::GR_TM);
   p.P = p.n_t * (p.n_t + 1) / 2;
   const int ks = stage_features(dt);
+  // Items of the unchunked Gram layers, per kernel (16-byte rows or not).
+  int64_t plain_items[2] = {0, 0};
+  for (int i = 0; i < n; ++i) {
+    const dp_linear_t& L = layers[i];
+    if (use_direct(L, T) || L.d_out > KG_SPLIT) continue;
+    const bool vec = vec_ok(L.A, L.lda, dt) && vec_ok(L.G, L.ldg, dt);
+    plain_items[vec] += (int64_t)B * gram_pairs(p, dt, vec, T);
+  }
   for (int i = 0; i < n; ++i) {
     const dp_linear_t& L = layers[i];
     if (use_direct(L, T)) {
       plan_gemm(L.A, L.lda, L.d_in, L.G, L.ldg, L.d_out, dt, nullptr, 0, p.direct, &p.slots, 1);
       continue;
     }
-    const int kg = L.d_out > KG_SPLIT ? KG_CHUNK : (int)(ceil_div(L.d_out, ks) * ks);
+    const bool vec = vec_ok(L.A, L.lda, dt) && vec_ok(L.G, L.ldg, dt);
+    int kg = (int)(ceil_div(L.d_out, ks) * ks);
+    if (L.d_out > KG_SPLIT) {
+      const int64_t per_chunk = (int64_t)B * gram_pairs(p, dt, vec, T);
+      const int64_t slots = (int64_t)device_cus() * dpg::gram_groups_per_cu(kdt(dt), vec, T);
+      const int nc = pick_chunks(L.d_out, ks, per_chunk, plain_items[vec], slots);
+      kg = (int)(ceil_div(ceil_div(L.d_out, nc), ks) * ks);
+      plain_items[vec] += per_chunk * ceil_div(L.d_out, kg);
+    }
     GramEntry e{L.A, L.G, L.lda, L.ldg, L.d_in, 0, L.d_out, kg, (int)ceil_div(L.d_out, kg),
-                (int)p.slots, vec_ok(L.A, L.lda, dt) && vec_ok(L.G, L.ldg, dt)};
+                (int)p.slots, vec};
     p.slots += (int64_t)gram_pairs(p, dt, e.vec, T) * e.nc;
     p.gram.push_back(e);
   }
@@ -294,7 +346,7 @@ const char* dp_last_error(void) { return g_last_error.c_str(); }
 size_t dp_ghost_norm_linear_workspace(const dp_linear_t* layers, int n_layers, int B, int T,
                                       dp_dtype_t dt) {
   if (check_layers(layers, n_layers, B, T, dt) != DP_OK) return 0;
-  return norm_ws_bytes(plan_norm(layers, n_layers, T, dt), B);
+  return norm_ws_bytes(plan_norm(layers, n_layers, B, T, dt), B);
 }
 
 dp_status_t dp_ghost_norm_linear_grouped(const dp_linear_t* layers, int n_layers, int B, int T,
@@ -303,7 +355,7 @@ dp_status_t dp_ghost_norm_linear_grouped(const dp_linear_t* layers, int n_layers
   dp_status_t st = check_layers(layers, n_layers, B, T, dt);
   if (st != DP_OK) return st;
   if (!norm2) return fail(DP_EINVAL, "norm2 is NULL");
-  const NormPlan p = plan_norm(layers, n_layers, T, dt);
+  const NormPlan p = plan_norm(layers, n_layers, B, T, dt);
   if ((uint64_t)B * p.slots > 0x7FFFFFFFull) return fail(DP_EUNSUPPORTED, "too many partials");
   const size_t need = norm_ws_bytes(p, B);
   if (!workspace || workspace_bytes < need)

@@ -16,6 +16,11 @@ constexpr int GR_MAX_LAYERS = 52;   // layers per launch (kernel arguments stay 
 inline bool gram_whole(int dt, bool vec, int T) {
   return dt == DT_BF16 && vec && T > GR_TM && T <= 2 * GR_TM;
 }
+// Gram workgroups resident per CU: two for the single-tile direct-load kernel
+// (bf16, 16-byte rows, T <= 128), one for the others.
+inline int gram_groups_per_cu(int dt, bool vec, int T) {
+  return dt == DT_BF16 && vec && T <= GR_TM ? 2 : 1;
+}
 
 struct GramLayer {
   const void* A;        // [B*T rows, lda] activations

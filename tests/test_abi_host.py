@@ -55,6 +55,24 @@ def _lin(A=1 << 20, lda=64, d_in=64, G=1 << 21, ldg=64, d_out=64, algo=0):
     return D.dp_linear_t(A, lda, d_in, G, ldg, d_out, algo)
 
 
+def _head_chunks(width, ks, per_chunk, other, slots):
+    """The planner's chunk count for a long G range: chunks of at most 4096 and at
+    least 1024 features (whole stages of ks) whose launch, with `other` items,
+    leaves the smallest idle fraction of `slots` in its last round."""
+    cdiv = lambda a, b: -(-a // b)
+    lo = cdiv(width, 4096)
+    hi = max(lo, cdiv(width, 1024))
+    best, best_idle = lo, 2.0
+    for nc in range(lo, hi + 1):
+        kg = cdiv(cdiv(width, nc), ks) * ks
+        eff = cdiv(width, kg)
+        total = other + per_chunk * eff
+        idle = (cdiv(total, slots) * slots - total) / total
+        if idle < best_idle - 1e-9:
+            best, best_idle = eff, idle
+    return best
+
+
 def test_norm_workspace_sizes(L):
     one = (D.dp_linear_t * 1)(_lin(algo=D.DP_NORM_GRAM))
     # T = 16: one T-tile pair per example, one G chunk -> 4 bytes per example
@@ -62,10 +80,16 @@ def test_norm_workspace_sizes(L):
     # T = 300 -> 3 T-tiles -> 6 pairs
     assert L.dp_ghost_norm_linear_workspace(one, 1, 100, 300, D.DP_F32) == 2560
     head = (D.dp_linear_t * 1)(_lin(d_in=768, lda=768, d_out=50257, ldg=50304))
-    # bf16 head: V = 50257 features in chunks of 2048 -> 25 partials per example
+    # bf16 head: V = 50257 features in chunks; the chunk count is the one whose
+    # items best fill the last round of 512 workgroups (256 CUs, two per CU)
     assert L.dp_ghost_norm_linear_workspace(head, 1, 1, 128, D.DP_BF16) == 256
-    ws = L.dp_ghost_norm_linear_workspace(head, 1, 100, 128, D.DP_BF16)
-    assert ws == ((100 * 25 * 4 + 255) // 256) * 256
+    for B in (32, 100):
+        nc = _head_chunks(50257, 64, B, 0, 512)
+        assert 50257 / nc <= 4096 and 50257 / nc >= 1024 - 64
+        ws = L.dp_ghost_norm_linear_workspace(head, 1, B, 128, D.DP_BF16)
+        assert ws == ((B * nc * 4 + 255) // 256) * 256
+    assert _head_chunks(50257, 64, 32, 0, 512) == 16          # 512 items: one full round
+    assert _head_chunks(50257, 64, 32, 48 * 32, 512) == 16    # with 48 body layers: 2048 items
     # an operand spanning 4 GiB or more is refused (32-bit buffer offsets)
     assert L.dp_ghost_norm_linear_workspace(head, 1, 1000, 128, D.DP_BF16) == 0
     assert L.dp_ghost_norm_linear_grouped(head, 1, 1000, 128, D.DP_BF16, 1 << 22, 0, 1 << 23,
