@@ -238,25 +238,32 @@ dp_status_t run_gram(const NormPlan& p, int B, int T, dp_dtype_t dt, float* ws, 
     std::vector<const GramEntry*> sel;
     for (const auto& e : p.gram)
       if (e.vec == vec) sel.push_back(&e);
+    // Within an example, the layers with the longest items go first, so that
+    // the last items each XCD runs are short ones (a shorter tail).
+    std::stable_sort(sel.begin(), sel.end(), [](const GramEntry* x, const GramEntry* y) {
+      return x->d_in + x->kg > y->d_in + y->kg;
+    });
     for (size_t i0 = 0; i0 < sel.size(); i0 += dpg::GR_MAX_LAYERS) {
       dpg::GramArgs a{};
       a.B = B; a.T = T; a.n_t = p.n_t; a.P = gram_pairs(p, dt, vec, T);
       a.slots = (int32_t)p.slots;
       a.ws = ws;
-      uint64_t items = 0;
+      uint64_t per_ex = 0;
       const size_t n = std::min(sel.size() - i0, (size_t)dpg::GR_MAX_LAYERS);
       for (size_t j = 0; j < n; ++j) {
         const GramEntry& e = *sel[i0 + j];
         dpg::GramLayer& L = a.L[j];
         L.A = e.A; L.G = e.G; L.lda = e.lda; L.ldg = e.ldg;
         L.d_in = e.d_in; L.g0 = e.g0; L.g1 = e.g1; L.kg = e.kg; L.nc = e.nc;
-        L.item_begin = (uint32_t)items;
+        L.item_begin = (uint32_t)per_ex;
         L.slot_begin = e.slot_begin;
-        items += (uint64_t)B * a.P * e.nc;
+        per_ex += (uint64_t)a.P * e.nc;
       }
+      const uint64_t items = per_ex * (uint64_t)B;
       if (items > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many work items (%llu)",
                                              (unsigned long long)items);
       a.n_layers = (int32_t)n;
+      a.per_ex = (uint32_t)per_ex;
       a.n_items = (uint32_t)items;
       dp_status_t st = hip_status(dpg::launch_gram_norm(a, kdt(dt), vec, s), "gram_norm launch");
       if (st != DP_OK) return st;

@@ -28,6 +28,23 @@
 
 namespace dpg {
 
+// Layer, example and item index within (example, layer) of work item `item`.
+struct GramItem {
+  int l, b;
+  uint32_t rel;
+};
+__device__ __forceinline__ GramItem gram_item(const GramArgs& a, uint32_t item) {
+  GramItem g;
+  g.b = (int)(item / a.per_ex);
+  uint32_t rel = item - (uint32_t)g.b * a.per_ex;
+  int l = 0;
+  while (l + 1 < a.n_layers && rel >= a.L[l + 1].item_begin) ++l;
+  g.l = l;
+  g.rel = rel - a.L[l].item_begin;
+  return g;
+}
+
+
 constexpr int GR_THREADS = 256;
 constexpr int GR_ROWS = 2 * GR_TM;  // LDS rows of one stage (two T-tiles)
 
@@ -246,15 +263,11 @@ __global__ __launch_bounds__(GR_THREADS) void gram_norm_kernel(GramArgs args) {
   __shared__ u32x4 lds[2 * (SINGLE ? GR_TM : GR_ROWS) * 8];
   __shared__ float red[GR_THREADS / WAVE];
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
-  int l = 0;
-  while (l + 1 < a.n_layers && item >= a.L[l + 1].item_begin) ++l;
-  const GramLayer& L = a.L[l];
-  uint32_t rel = item - L.item_begin;
-  const uint32_t per_b = (uint32_t)a.P * (uint32_t)L.nc;
-  const int b = (int)(rel / per_b);
-  rel -= (uint32_t)b * per_b;
-  const int pair = (int)(rel / (uint32_t)L.nc);
-  const int chunk = (int)(rel - (uint32_t)pair * L.nc);
+  const GramItem gi = gram_item(a, item);
+  const GramLayer& L = a.L[gi.l];
+  const int b = gi.b;
+  const int pair = (int)(gi.rel / (uint32_t)L.nc);
+  const int chunk = (int)(gi.rel - (uint32_t)pair * L.nc);
   int ti = 0, rem = pair;
   while (rem >= a.n_t - ti) { rem -= a.n_t - ti; ++ti; }
   const int tj = ti + rem;
@@ -428,15 +441,11 @@ __global__ __launch_bounds__(GR_THREADS, SINGLE ? 2 : 1) void dl_gram_kernel(Gra
   __shared__ __attribute__((aligned(1024))) u32x4 ring[DG_NS * (SINGLE ? GR_TM : GR_ROWS) * 8];
   __shared__ float red[GR_THREADS / WAVE];
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
-  int l = 0;
-  while (l + 1 < a.n_layers && item >= a.L[l + 1].item_begin) ++l;
-  const GramLayer& L = a.L[l];
-  uint32_t rel = item - L.item_begin;
-  const uint32_t per_b = (uint32_t)a.P * (uint32_t)L.nc;
-  const int b = (int)(rel / per_b);
-  rel -= (uint32_t)b * per_b;
-  const int pair = (int)(rel / (uint32_t)L.nc);
-  const int chunk = (int)(rel - (uint32_t)pair * L.nc);
+  const GramItem gi = gram_item(a, item);
+  const GramLayer& L = a.L[gi.l];
+  const int b = gi.b;
+  const int pair = (int)(gi.rel / (uint32_t)L.nc);
+  const int chunk = (int)(gi.rel - (uint32_t)pair * L.nc);
   int ti = 0, rem = pair;
   while (rem >= a.n_t - ti) { rem -= a.n_t - ti; ++ti; }
   const int tj = ti + rem;
@@ -587,12 +596,10 @@ __global__ __launch_bounds__(DW_THREADS) void dl_gram_whole_kernel(GramArgs args
   // The partial sums reuse the ring: every load has landed by then.
   float* red = (float*)ring;
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
-  int l = 0;
-  while (l + 1 < a.n_layers && item >= a.L[l + 1].item_begin) ++l;
-  const GramLayer& L = a.L[l];
-  const uint32_t rel = item - L.item_begin;
-  const int b = (int)(rel / (uint32_t)L.nc);
-  const int chunk = (int)(rel - (uint32_t)b * L.nc);
+  const GramItem gi = gram_item(a, item);
+  const GramLayer& L = a.L[gi.l];
+  const int b = gi.b;
+  const int chunk = (int)gi.rel;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   float part = w < 4 ? dw_item<5>(L, b, a.T, chunk, ring) : dw_item<4>(L, b, a.T, chunk, ring);
   part = wave_sum(part);

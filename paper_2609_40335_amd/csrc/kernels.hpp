@@ -30,15 +30,20 @@ struct GramLayer {
   int32_t g0, g1;       // G feature range of this entry
   int32_t kg;           // G features per chunk
   int32_t nc;           // number of G chunks
-  uint32_t item_begin;  // first work item of this layer
+  uint32_t item_begin;  // first work item of this layer among an example's items
   int32_t slot_begin;   // first partial slot of this layer in an example's row
 };
 
+// Work items are numbered example-major: example b owns items
+// [b * per_ex, (b + 1) * per_ex), one per (layer, T-tile pair, G chunk), so
+// that the contiguous item range each XCD walks holds whole examples (equal
+// work per XCD, and an example's G chunks share its A rows in one L2).
 struct GramArgs {
   GramLayer L[GR_MAX_LAYERS];
   int32_t n_layers;
   int32_t B, T, n_t, P;   // T-tiles per side, upper-triangle tile pairs
   int32_t slots;          // partial slots per example
+  uint32_t per_ex;        // work items per example
   uint32_t n_items;
   float* ws;              // [B, slots]
 };
