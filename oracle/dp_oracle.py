@@ -32,6 +32,11 @@ Readings taken where the paper is silent (each is also listed in the design doc):
     (seed, tensor_id, step); see ``gaussian``.
   * Gradient layout is [d_in, d_out] (activations on the rows); norms do not
     depend on it.
+  * The parameters the paper counts besides the weight matrices (its table of
+    trainable-parameter counts: biases, LayerNorm gains and biases, position
+    embeddings) enter the flat norm of eq. 6 like every other parameter; their
+    per-example gradients follow from the chain rule (``vector_grad``,
+    ``positional_grad``).
 """
 from __future__ import annotations
 
@@ -43,7 +48,8 @@ __all__ = [
     "decode", "linear_grad", "embedding_grad", "head_grad", "sqnorm",
     "linear_norm2", "embedding_norm2", "head_norm2", "tied_cross", "tied_norm2",
     "buckets", "clip_factors", "clipped_sum_linear", "clipped_sum_embedding",
-    "clipped_sum_head", "philox4x32_10", "gaussian", "add_noise",
+    "clipped_sum_head", "vector_grad", "positional_grad", "vector_norm2", "positional_norm2",
+    "clipped_sum_vector", "clipped_sum_positional", "philox4x32_10", "gaussian", "add_noise",
     "per_example_norms", "step",
 ]
 
@@ -95,6 +101,28 @@ def head_grad(H_i: np.ndarray, Gz_i: np.ndarray, V: int) -> np.ndarray:
     return Gz_i[:, :V].T @ H_i
 
 
+def vector_grad(X_i: Optional[np.ndarray], G_i: np.ndarray) -> np.ndarray:
+    """Per-example gradient of a vector parameter applied to every token, [d].
+
+    A bias b enters every token's output as y_t = ... + b, so its gradient is
+    the sum over tokens of the output grads G_t (X_i is None). A LayerNorm gain
+    enters as y_t = gamma * xhat_t + beta, so its gradient is the sum over tokens
+    of xhat_t * G_t (X_i = xhat), and the LayerNorm bias is again the plain sum.
+    """
+    return G_i.sum(axis=0) if X_i is None else (X_i * G_i).sum(axis=0)
+
+
+def positional_grad(dE_i: np.ndarray, n_pos: int) -> np.ndarray:
+    """Per-example gradient of a learned position table, [n_pos, d].
+
+    Token t adds row t of the table to its input embedding, so row t receives
+    that token's embedding-output grad dE_t; rows at or past T receive nothing.
+    """
+    g = np.zeros((n_pos, dE_i.shape[1]), dtype=np.float64)
+    g[: dE_i.shape[0]] = dE_i
+    return g
+
+
 def sqnorm(g: np.ndarray) -> float:
     return float(np.sum(g * g))
 
@@ -113,6 +141,15 @@ def embedding_norm2(ids: np.ndarray, dE: np.ndarray, V: int) -> np.ndarray:
 
 def head_norm2(H: np.ndarray, Gz: np.ndarray, V: int) -> np.ndarray:
     return np.array([sqnorm(head_grad(H[i], Gz[i], V)) for i in range(H.shape[0])])
+
+
+def vector_norm2(X: Optional[np.ndarray], G: np.ndarray) -> np.ndarray:
+    return np.array([sqnorm(vector_grad(None if X is None else X[i], G[i]))
+                     for i in range(G.shape[0])])
+
+
+def positional_norm2(dE: np.ndarray, n_pos: int) -> np.ndarray:
+    return np.array([sqnorm(positional_grad(dE[i], n_pos)) for i in range(dE.shape[0])])
 
 
 def tied_cross(ids, dE, H, Gz, V) -> np.ndarray:
@@ -179,6 +216,20 @@ def clipped_sum_head(H, Gz, c, V) -> np.ndarray:
     S = np.zeros((V, H.shape[2]))
     for i in range(H.shape[0]):
         S += c[i] * head_grad(H[i], Gz[i], V)
+    return S
+
+
+def clipped_sum_vector(X: Optional[np.ndarray], G: np.ndarray, c) -> np.ndarray:
+    S = np.zeros(G.shape[2])
+    for i in range(G.shape[0]):
+        S += c[i] * vector_grad(None if X is None else X[i], G[i])
+    return S
+
+
+def clipped_sum_positional(dE: np.ndarray, c, n_pos: int) -> np.ndarray:
+    S = np.zeros((n_pos, dE.shape[2]))
+    for i in range(dE.shape[0]):
+        S += c[i] * positional_grad(dE[i], n_pos)
     return S
 
 
@@ -286,6 +337,19 @@ def per_example_norms(wl, examples: Optional[List[int]] = None) -> Dict[str, np.
             total = total + tied
         else:
             total = total + n_in + n_out
+    vecs = getattr(wl, "vectors", [])
+    if vecs:
+        vn = np.zeros((len(vecs), len(ex)))
+        for v, vec in enumerate(vecs):
+            for k, i in enumerate(ex):
+                X = None if vec.X is None else decode(vec.X[i], dt)
+                vn[v, k] = sqnorm(vector_grad(X, decode(vec.G[i], dt)))
+        out["vector"] = vn
+        total = total + vn.sum(axis=0)
+    if getattr(wl, "n_pos", 0):
+        pos = np.array([sqnorm(positional_grad(decode(h.dE[i], dt), wl.n_pos)) for i in ex])
+        out["pos"] = pos
+        total = total + pos
     out["total"] = total
     return out
 
@@ -295,7 +359,8 @@ def step(wl, seed: int = 0, step_id: int = 0, examples: Optional[List[int]] = No
     """One DP-SGD aggregation on the listed examples: norms, clip, sums, noise.
 
     Tensor ids for the noise: linear layer l uses l; then the input embedding
-    (or the tied matrix) uses L, and an untied output head uses L+1.
+    (or the tied matrix) uses L, and an untied output head uses L+1; the vector
+    parameters follow in their order, then the position table.
     """
     ex = list(range(wl.B)) if examples is None else list(examples)
     dt = wl.dtype
@@ -323,9 +388,22 @@ def step(wl, seed: int = 0, step_id: int = 0, examples: Optional[List[int]] = No
                 sums["wte"], sums["lm_head"] = SE, SW
         else:
             sums["wte"] = SE
+    for vec in getattr(wl, "vectors", []):
+        S = np.zeros(vec.d)
+        for k, i in enumerate(ex):
+            X = None if vec.X is None else decode(vec.X[i], dt)
+            S += c[k] * vector_grad(X, decode(vec.G[i], dt))
+        sums[vec.name] = S
+    if getattr(wl, "n_pos", 0):
+        SP = np.zeros((wl.n_pos, h.d))
+        for k, i in enumerate(ex):
+            SP += c[k] * positional_grad(decode(h.dE[i], dt), wl.n_pos)
+        sums["wpe"] = SP
     noisy: Dict[str, np.ndarray] = {}
     if noise:
         names = [lay.name for lay in wl.linears] + [n for n in ("wte", "lm_head") if n in sums]
+        names += [vec.name for vec in getattr(wl, "vectors", [])]
+        names += ["wpe"] if "wpe" in sums else []
         for tid, name in enumerate(names):
             noisy[name] = add_noise(sums[name], wl.sigma, wl.C, len(ex), seed, tid, step_id)
     return {"norms": norms, "c": c, "sums": sums, "noisy": noisy}

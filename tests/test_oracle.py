@@ -392,6 +392,127 @@ def test_step_tiny_tied_consistency():
 
 
 # ---------------------------------------------------------------------------
+# Pin: biases, LayerNorm gain/bias and the position table (the parameters the
+# paper's parameter-count table includes besides the weight matrices)
+# ---------------------------------------------------------------------------
+def check_vector_and_position_grads_autograd(o, B=3, T=5, d=6, d_out=4, n_pos=8):
+    """Per-example grads of a block h0 = tok + wpe[t], h1 = LayerNorm(h0) with
+    gain and bias, y = h1 W + b, loss_i = sum(y * R_i), from fp64 autograd;
+    the upstream grads the oracle takes (dL/dy, dL/dh1, dL/dh0) come from
+    autograd too."""
+    g = torch.Generator().manual_seed(7)
+    f64 = dict(dtype=torch.float64)
+    wpe = torch.randn(n_pos, d, generator=g, **f64).requires_grad_()
+    gamma = (1 + 0.3 * torch.randn(d, generator=g, **f64)).requires_grad_()
+    beta = (0.3 * torch.randn(d, generator=g, **f64)).requires_grad_()
+    W = torch.randn(d, d_out, generator=g, **f64).requires_grad_()
+    b = torch.randn(d_out, generator=g, **f64).requires_grad_()
+    for i in range(B):
+        for p in (wpe, gamma, beta, W, b):
+            p.grad = None
+        tok = torch.randn(T, d, generator=g, **f64).requires_grad_()
+        R = torch.randn(T, d_out, generator=g, **f64)
+        h0 = tok + wpe[torch.arange(T)]
+        h1 = torch.nn.functional.layer_norm(h0, (d,), gamma, beta)
+        y = h1 @ W + b
+        h1.retain_grad(); y.retain_grad()
+        (y * R).sum().backward()
+        xhat = torch.nn.functional.layer_norm(h0.detach(), (d,))
+        dE, G1, Gy = tok.grad.numpy(), h1.grad.numpy(), y.grad.numpy()
+        np.testing.assert_allclose(o.vector_grad(None, Gy), b.grad.numpy(), rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(o.vector_grad(xhat.numpy(), G1), gamma.grad.numpy(),
+                                   rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(o.vector_grad(None, G1), beta.grad.numpy(), rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(o.positional_grad(dE, n_pos), wpe.grad.numpy(),
+                                   rtol=1e-12, atol=1e-12)
+        # the flat norm of eq. 6 over every parameter of the block
+        flat = torch.cat([p.grad.reshape(-1) for p in (wpe, gamma, beta, W, b)])
+        ours = (o.sqnorm(o.positional_grad(dE, n_pos)) + o.sqnorm(o.vector_grad(xhat.numpy(), G1))
+                + o.sqnorm(o.vector_grad(None, G1)) + o.sqnorm(o.linear_grad(h1.detach().numpy(), Gy))
+                + o.sqnorm(o.vector_grad(None, Gy)))
+        np.testing.assert_allclose(ours, float(flat @ flat), rtol=1e-12)
+
+
+def test_vector_and_position_grads_match_autograd():
+    check_vector_and_position_grads_autograd(O)
+
+
+def test_position_grad_is_embedding_grad_of_distinct_positions():
+    T, d, n_pos = 7, 5, 12
+    dE = _rand(T, d)
+    np.testing.assert_array_equal(O.positional_grad(dE, n_pos),
+                                  O.embedding_grad(np.arange(T), dE, n_pos))
+    # distinct rows: the squared norm is the sum of the rows' squared norms
+    np.testing.assert_allclose(O.positional_norm2(dE[None], n_pos), [np.sum(dE * dE)], rtol=1e-13)
+
+
+def test_vector_norm_special_cases():
+    G = _rand(2, 1, 6)
+    X = _rand(2, 1, 6)
+    # one token: the gain's gradient is x * g, the bias's g
+    np.testing.assert_allclose(O.vector_norm2(X, G), np.sum((X * G) ** 2, axis=(1, 2)), rtol=1e-13)
+    np.testing.assert_allclose(O.vector_norm2(None, G), np.sum(G * G, axis=(1, 2)), rtol=1e-13)
+    # the bias gradient is the Gram form with A a column of ones: 1^T (G G^T) 1
+    G = _rand(3, 9, 5)
+    gram = np.array([np.sum(G[i] @ G[i].T) for i in range(3)])
+    np.testing.assert_allclose(O.vector_norm2(None, G), gram, rtol=1e-12)
+    np.testing.assert_allclose(O.vector_norm2(None, G),
+                               O.linear_norm2(np.ones((3, 9, 1)), G), rtol=1e-12)
+
+
+def test_full_param_workloads_cover_the_paper_counts():
+    with open(os.path.join(GOLDEN, "gpt2_param_counts.txt")) as f:
+        rows = {(int(r[1]), int(r[2])): int(r[3]) for r in
+                (l.split() for l in f if l.strip() and not l.startswith("#"))}
+    for name, nb, tied in (("gpt2-step", 12, 1), ("c4", 6, 1), ("c5", 12, 0)):
+        wl = gen.make_workload(name, B=1, T=4, full_params=True)
+        assert wl.n_coordinates() == rows[(nb, tied)], name
+
+
+def check_full_step_composition(o):
+    """Flat per-example norm over every parameter tensor of a tiny full-parameter
+    tied workload, from the materialised gradients, against the step's total;
+    huge C gives the plain sums."""
+    wl = gen.make_workload("c1-tied", B=3, T=6, full_params=True)
+    dec = lambda x: O.decode(x, wl.dtype)
+    h = wl.head
+    for i in range(wl.B):
+        parts = [O.linear_grad(dec(l.A[i]), dec(l.G[i])) for l in wl.linears]
+        parts.append(O.embedding_grad(h.ids[i], dec(h.dE[i]), h.V)
+                     + O.head_grad(dec(h.H[i]), dec(h.Gz[i]), h.V))
+        parts += [O.vector_grad(None if v.X is None else dec(v.X[i]), dec(v.G[i]))
+                  for v in wl.vectors]
+        parts.append(O.positional_grad(dec(h.dE[i]), wl.n_pos))
+        flat = np.concatenate([p.reshape(-1) for p in parts])
+        assert flat.size == wl.n_coordinates()
+        n = o.per_example_norms(wl, [i])["total"][0]
+        np.testing.assert_allclose(n, flat @ flat, rtol=1e-12)
+    wl.C = 1e30
+    r = o.step(wl, noise=False)
+    for v in wl.vectors:
+        X = 1.0 if v.X is None else dec(v.X)
+        np.testing.assert_allclose(r["sums"][v.name], (X * dec(v.G)).sum(axis=(0, 1)), rtol=1e-12)
+    np.testing.assert_allclose(r["sums"]["wpe"][: wl.T], dec(h.dE).sum(axis=0), rtol=1e-12)
+    assert not r["sums"]["wpe"][wl.T:].any()
+
+
+def test_full_step_composition():
+    check_full_step_composition(O)
+
+
+def test_full_step_noise_ids_follow_the_tensors():
+    wl = gen.make_workload("c1-tied", B=2, T=4, full_params=True)
+    r = O.step(wl, seed=5, step_id=3)
+    names = list(r["noisy"])
+    assert names[:2] == ["linear", "wte"] and names[-1] == "wpe"
+    assert names[2:-1] == [v.name for v in wl.vectors]
+    for tid, name in enumerate(names):
+        S = r["sums"][name]
+        z = O.gaussian(S.size, 5, tid, 3).reshape(S.shape)
+        np.testing.assert_allclose(r["noisy"][name], (S + wl.sigma * wl.C * z) / wl.B, rtol=1e-13)
+
+
+# ---------------------------------------------------------------------------
 # Mutation tests: plausible mistakes planted in a copy of the oracle
 # ---------------------------------------------------------------------------
 def _mutant(**overrides):
@@ -442,3 +563,27 @@ def test_pins_catch_philox_wrong_rounds():
         out = O.philox4x32_10(c, key)
         return [o ^ np.uint32(1) for o in out]
     assert _fails(check_philox_kat, _mutant(philox4x32_10=philox9))
+
+
+def test_pins_catch_gain_treated_as_bias():
+    m = _mutant(vector_grad=lambda X, G: G.sum(axis=0))
+    assert _fails(check_vector_and_position_grads_autograd, m)
+
+
+def test_pins_catch_shifted_positions():
+    def pos_bad(dE_i, n_pos):
+        g = np.zeros((n_pos, dE_i.shape[1]))
+        g[1: dE_i.shape[0] + 1] = dE_i
+        return g
+    assert _fails(check_vector_and_position_grads_autograd, _mutant(positional_grad=pos_bad))
+
+
+def test_pins_catch_dropped_vector_norms():
+    def norms_without_vectors(wl, examples=None):
+        saved = wl.vectors
+        wl.vectors = []
+        try:
+            return O.per_example_norms(wl, examples)
+        finally:
+            wl.vectors = saved
+    assert _fails(check_full_step_composition, _mutant(per_example_norms=norms_without_vectors))

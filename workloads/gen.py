@@ -21,7 +21,12 @@ workload is bf16):
   * logit grads of a causal LM: for t < T-1,
     Gz[t] = (softmax(z_t) - onehot(ids[t+1])) / T with z_t ~ N(0,1) over V
     (tag 1002); the last row has no next token and is zero;
-  * input-embedding output grads dE ~ N(0, e_std) [B,T,d] (tag 1003).
+  * input-embedding output grads dE ~ N(0, e_std) [B,T,d] (tag 1003);
+  * with ``full_params``: every linear layer's bias shares that layer's G; each
+    LayerNorm k (two per block, then the final one) gets normalised inputs
+    xhat ~ N(0,1) [B,T,d] (tag 3000+2k) and output grads gy ~ N(0, g_std)
+    (tag 3001+2k) for its gain and bias; the position table (1024 rows, or
+    2T in the tiny configs) shares the embedding-output grads dE.
 
 bf16 tensors are held as their uint16 bit patterns; fp32 tensors as float32.
 Nothing here computes any part of the DP-SGD method.
@@ -37,7 +42,7 @@ __all__ = [
     "GPT2_VOCAB", "GPT2_WIDTH", "GPT2_POSITIONS",
     "f32_to_bf16_bits", "bf16_bits_to_f32",
     "block_linears", "model_linears", "gpt2_param_count",
-    "LinearInputs", "HeadInputs", "Workload", "CONFIG_NAMES", "make_workload",
+    "LinearInputs", "HeadInputs", "VectorInputs", "Workload", "CONFIG_NAMES", "make_workload",
     "zipf_ids", "logit_grads", "draw", "draw_ids",
 ]
 
@@ -46,6 +51,7 @@ GPT2_WIDTH = 768
 GPT2_POSITIONS = 1024
 
 TAG_IDS, TAG_H, TAG_Z, TAG_DE = 1000, 1001, 1002, 1003
+TAG_LN = 3000
 
 
 # --------------------------------------------------------------------------
@@ -182,6 +188,17 @@ class HeadInputs:
 
 
 @dataclass
+class VectorInputs:
+    """A vector parameter applied to every token: its per-example gradient is
+    the sum over tokens of G (a bias; X is None) or of X * G (a LayerNorm gain,
+    X the normalised input)."""
+    name: str
+    d: int
+    X: Optional[np.ndarray]    # [B,T,d] or None
+    G: np.ndarray              # [B,T,d] (a slice of a linear layer's G for a bias)
+
+
+@dataclass
 class Workload:
     name: str
     dtype: str                 # "bf16" or "f32"
@@ -192,12 +209,17 @@ class Workload:
     linears: List[LinearInputs] = field(default_factory=list)
     head: Optional[HeadInputs] = None
     description: str = ""
+    vectors: List[VectorInputs] = field(default_factory=list)
+    n_pos: int = 0             # rows of the position table (0: no position embedding)
 
     def n_coordinates(self) -> int:
         n = sum(l.d_in * l.d_out for l in self.linears)
         if self.head is not None:
             h = self.head
             n += h.V * h.d * (1 if (h.tied or h.H is None) else 2)
+        n += sum(v.d for v in self.vectors)
+        if self.n_pos:
+            n += self.n_pos * self.head.d
         return n
 
 
@@ -227,12 +249,14 @@ def make_workload(name: str, seed: int = 0, *, B: Optional[int] = None,
                   layers: Optional[List[int]] = None, ldz: Optional[int] = None,
                   V: Optional[int] = None, d: Optional[int] = None,
                   with_head: bool = True, C: float = 1.0,
-                  sigma: float = 1.0) -> Workload:
+                  sigma: float = 1.0, full_params: bool = False) -> Workload:
     """Draw the inputs of one named workload (optionally at reduced size).
 
     ``layers`` selects a subset of the linear layers by index (each keeps the
     values it has in the full workload). ``ldz`` pads logit-grad rows to a
-    row stride >= V with zeros.
+    row stride >= V with zeros. ``full_params`` adds the remaining GPT-2
+    parameters: linear biases, LayerNorm gains and biases (two per block and a
+    final one) and the position table (needs the head's embedding inputs).
     """
     if name not in _DEFAULTS:
         raise KeyError(f"unknown workload {name!r}; choose from {CONFIG_NAMES}")
@@ -288,4 +312,24 @@ def make_workload(name: str, seed: int = 0, *, B: Optional[int] = None,
         del z, gz
     wl.head = HeadInputs(V=Vh, d=dd, ids=ids, dE=dE, H=H, Gz=Gz, ldz=ldz_eff,
                          tied=(head_kind == "tied"))
+    if full_params:
+        _add_full_params(wl, seed, enc, g_std, n_blocks=(1 if name.startswith("c1") else nb),
+                         n_pos=(2 * T if name.startswith("c1") else GPT2_POSITIONS))
     return wl
+
+
+def _add_full_params(wl: Workload, seed: int, enc, g_std: float, n_blocks: int,
+                     n_pos: int) -> None:
+    """Biases of the linear layers, LayerNorm gains and biases, position table."""
+    B, T, d = wl.B, wl.T, wl.head.d
+    if T > n_pos:
+        raise ValueError(f"T = {T} exceeds the position table ({n_pos} rows)")
+    for lin in wl.linears:
+        wl.vectors.append(VectorInputs(lin.name + ".bias", lin.d_out, None, lin.G))
+    names = [f"h.{b}.{ln}" for b in range(n_blocks) for ln in ("ln_1", "ln_2")] + ["ln_f"]
+    for k, name in enumerate(names):
+        xhat = enc(_normal(seed, TAG_LN + 2 * k, (B, T, d), 1.0))
+        gy = enc(_normal(seed, TAG_LN + 2 * k + 1, (B, T, d), g_std))
+        wl.vectors.append(VectorInputs(name + ".weight", d, xhat, gy))
+        wl.vectors.append(VectorInputs(name + ".bias", d, None, gy))
+    wl.n_pos = n_pos
