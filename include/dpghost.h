@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define DP_ABI_VERSION 1
+#define DP_ABI_VERSION 2
 
 typedef enum { DP_F32 = 0, DP_BF16 = 1 } dp_dtype_t;
 
@@ -246,6 +246,77 @@ dp_status_t dp_add_noise(float* grad, int64_t n, float sigma, float C, int B_nor
  * and limits as for dp_add_noise. */
 dp_status_t dp_noise_fill(float* out, int64_t n, float sigma, float C, int B_norm, uint64_t seed,
                           uint64_t tensor_id, uint64_t step, void* stream);
+
+/* ---------------------------------------------------------------------
+ * Vector parameters applied to every token: a linear layer's bias, a
+ * LayerNorm gain or bias. The paper's parameter counts include them, and the
+ * flat per-example norm (eq. 6) takes them in like every other parameter.
+ * By the chain rule the per-example gradient of parameter v is
+ *   g_v,i = sum_t X_v[i,t] * G_v[i,t]   (elementwise over the d_v features)
+ * with X the LayerNorm's normalised input for a gain, and the plain sum
+ * sum_t G_v[i,t] when X is NULL (a bias: y_t = ... + b; a LayerNorm bias).
+ * G is the gradient w.r.t. the parameter's output (for a linear layer's bias,
+ * the layer's own G). These gradients are d_v-vectors, so they are
+ * materialised rather than recovered from a Gram product.
+ * ------------------------------------------------------------------- */
+typedef struct {
+  const void* X;  /* [B*T rows, ldx] factor of a gain, or NULL (a bias) */
+  int64_t ldx;    /* row stride of X, >= d (ignored when X is NULL) */
+  const void* G;  /* [B*T rows, ldg] grads w.r.t. the parameter's output */
+  int64_t ldg;    /* row stride of G, >= d */
+  int32_t d;      /* features */
+} dp_vector_t;
+
+/* grads[v] (caller-owned fp32 [B, d_v], row stride d_v) receives g_v,i for
+ * every example i; when norm2 is not NULL, norm2[i] (+)= sum_v ||g_v,i||^2.
+ * Sums over tokens and features run in a fixed order (reproducible). The
+ * workspace is at least dp_vector_grads_workspace(...) bytes. */
+size_t dp_vector_grads_workspace(const dp_vector_t* params, int n, int B, int T, dp_dtype_t dt);
+dp_status_t dp_vector_grads_grouped(const dp_vector_t* params, int n, int B, int T,
+                                    dp_dtype_t dt, float* const* grads, float* norm2,
+                                    int accumulate, void* workspace, size_t workspace_bytes,
+                                    void* stream);
+
+/* Clipped sums of materialised per-example gradients with the Gaussian
+ * mechanism (eq. 3), for each parameter v:
+ *   outs[v][f] = (prior + sum_i c_i grads[v][i*d[v] + f] + sigma*C*z_f) / B_norm
+ * with prior = outs[v][f] if accumulate[v] != 0 (else 0), the sum over i in
+ * order, and z_f the draw dp_add_noise(outs[v], d[v], sigma, C, B_norm, seed,
+ * tensor_ids[v], step) would add to element f. sigma = 0 and B_norm = 0 give
+ * the plain clipped sum. grads, d, outs, tensor_ids and accumulate are host
+ * arrays of n entries (accumulate may be NULL: all 0). */
+dp_status_t dp_vector_clipped_sum_noised_grouped(const float* const* grads, const int32_t* d,
+                                                 int n, int B, const float* c,
+                                                 float* const* outs, const uint64_t* tensor_ids,
+                                                 const int32_t* accumulate, float sigma, float C,
+                                                 int B_norm, uint64_t seed, uint64_t step,
+                                                 void* stream);
+
+/* ---------------------------------------------------------------------
+ * Learned position table (n_pos rows of d features): token t of every
+ * example adds row t to its input embedding, so the per-example gradient has
+ * row t equal to that token's embedding-output grad dE[i,t] (t < T) and zero
+ * rows below; an example's positions are distinct, so its squared norm is
+ * sum_t ||dE[i,t]||^2 (contrast the token embedding, whose rows are keyed by
+ * token id). dE is the same [B, T, d] buffer dp_ghost_norm_embedding reads.
+ * norm2[i] (+)= sum_t ||dE[i,t]||^2; workspace >= the size returned.
+ * ------------------------------------------------------------------- */
+size_t dp_ghost_norm_positional_workspace(int B, int T, int d);
+dp_status_t dp_ghost_norm_positional(const void* dE, int64_t lde, int B, int T, int d,
+                                     dp_dtype_t dt, float* norm2, int accumulate,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* The position table's clipped sum with the Gaussian mechanism (eq. 3):
+ *   out[t, f] = (prior + [t < T] sum_i c_i dE[i,t,f] + sigma*C*z) / B_norm
+ * for every row t < n_pos (out has row stride ldo >= d; T <= n_pos), the sum
+ * over i in order, z the draw of element t*d + f of the table's stream
+ * (tensor_id), as dp_add_noise on a contiguous [n_pos, d] table would add. */
+dp_status_t dp_clipped_grad_sum_positional_noised(const void* dE, int64_t lde, const float* c,
+                                                  int B, int T, int d, dp_dtype_t dt, float* out,
+                                                  int n_pos, int64_t ldo, uint64_t tensor_id,
+                                                  int accumulate, float sigma, float C,
+                                                  int B_norm, uint64_t seed, uint64_t step,
+                                                  void* stream);
 
 #ifdef __cplusplus
 }

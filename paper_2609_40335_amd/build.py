@@ -20,7 +20,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdpghost.so")
-SOURCES = ["gram.hip", "gemm.hip", "embed.hip", "misc.hip", "api.cpp"]
+SOURCES = ["gram.hip", "gemm.hip", "embed.hip", "misc.hip", "vector.hip", "api.cpp"]
 HEADERS = ["common.hpp", "kernels.hpp"]
 
 ARCH = "gfx950"

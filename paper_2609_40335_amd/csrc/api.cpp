@@ -331,6 +331,87 @@ EsLayout es_layout(int64_t K, int d) {
   return l;
 }
 
+
+// ------------------------------------------------- vector parameters, positions
+struct VecEntry {
+  const void* X;
+  const void* G;
+  int64_t ldx, ldg;
+  int d, mode, chunks, slot_begin;
+  float* grad;
+  bool vec;
+};
+
+struct VecPlan {
+  std::vector<VecEntry> e;
+  int64_t slots = 0;
+};
+
+int vec_chunk_features(dp_dtype_t dt) { return 64 * elems_per_chunk(dt); }
+
+void plan_vec(VecPlan& p, const void* X, int64_t ldx, const void* G, int64_t ldg, int d, int mode,
+              float* grad, dp_dtype_t dt) {
+  VecEntry e{X, G, ldx, ldg, d, mode, (int)ceil_div(d, vec_chunk_features(dt)), (int)p.slots,
+             grad, vec_ok(G, ldg, dt) && (!X || vec_ok(X, ldx, dt))};
+  p.slots += e.chunks;
+  p.e.push_back(e);
+}
+
+dp_status_t check_vec(const dp_vector_t* params, int n, int B, int T, dp_dtype_t dt) {
+  if (!params) return fail(DP_EINVAL, "params is NULL");
+  if (n <= 0) return fail(DP_EINVAL, "n must be positive (got %d)", n);
+  if (B <= 0 || T <= 0) return fail(DP_EINVAL, "B and T must be positive (got %d, %d)", B, T);
+  if (!dtype_ok(dt)) return fail(DP_EINVAL, "unknown dtype %d", (int)dt);
+  for (int i = 0; i < n; ++i) {
+    const dp_vector_t& v = params[i];
+    if (!v.G) return fail(DP_EINVAL, "param %d: G is NULL", i);
+    if (v.d <= 0) return fail(DP_EINVAL, "param %d: d must be positive", i);
+    if (v.ldg < v.d || (v.X && v.ldx < v.d))
+      return fail(DP_EINVAL, "param %d: row stride smaller than d", i);
+    if (!span_ok((int64_t)B * T, v.ldg, dt) || (v.X && !span_ok((int64_t)B * T, v.ldx, dt)))
+      return fail(DP_EUNSUPPORTED, "param %d: an operand spans 4 GiB or more", i);
+  }
+  return DP_OK;
+}
+
+dp_status_t run_vec(const VecPlan& p, int B, int T, dp_dtype_t dt, float* ws, hipStream_t s) {
+  for (int pass = 0; pass < 2; ++pass) {
+    const bool vec = pass == 0;
+    std::vector<const VecEntry*> sel;
+    for (const auto& e : p.e)
+      if (e.vec == vec) sel.push_back(&e);
+    for (size_t i0 = 0; i0 < sel.size(); i0 += dpg::VR_MAX_PARAMS) {
+      dpg::VecArgs a{};
+      a.B = B; a.T = T; a.slots = (int32_t)p.slots; a.ws = ws;
+      uint64_t per_ex = 0;
+      const size_t n = std::min(sel.size() - i0, (size_t)dpg::VR_MAX_PARAMS);
+      for (size_t j = 0; j < n; ++j) {
+        const VecEntry& e = *sel[i0 + j];
+        dpg::VecParam& P = a.P[j];
+        P.X = e.X; P.G = e.G; P.ldx = e.ldx; P.ldg = e.ldg; P.d = e.d; P.mode = e.mode;
+        P.grad = e.grad; P.item_begin = (uint32_t)per_ex; P.slot_begin = e.slot_begin;
+        per_ex += (uint64_t)e.chunks;
+      }
+      const uint64_t items = per_ex * (uint64_t)B;
+      if (items > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many work items");
+      a.n_params = (int32_t)n;
+      a.per_ex = (uint32_t)per_ex;
+      a.n_items = (uint32_t)items;
+      dp_status_t st = hip_status(dpg::launch_vec_reduce(a, kdt(dt), vec, s), "vec_reduce launch");
+      if (st != DP_OK) return st;
+    }
+  }
+  return DP_OK;
+}
+
+dp_status_t check_noise_args(float sigma, float C, int B_norm, uint64_t step) {
+  if (!(sigma >= 0.f) || !std::isfinite(sigma)) return fail(DP_EINVAL, "sigma must be >= 0");
+  if (!(C > 0.f) || !std::isfinite(C)) return fail(DP_EINVAL, "C must be positive and finite");
+  if (B_norm < 0) return fail(DP_EINVAL, "B_norm must be >= 0");
+  if (step >> 32) return fail(DP_EINVAL, "step must be < 2^32");
+  return DP_OK;
+}
+
 }  // namespace
 
 // ======================================================================
@@ -613,6 +694,133 @@ dp_status_t dp_add_noise(float* grad, int64_t n, float sigma, float C, int B_nor
 dp_status_t dp_noise_fill(float* out, int64_t n, float sigma, float C, int B_norm, uint64_t seed,
                           uint64_t tensor_id, uint64_t step, void* stream) {
   return noise_call(out, n, sigma, C, B_norm, seed, tensor_id, step, false, stream);
+}
+
+
+size_t dp_vector_grads_workspace(const dp_vector_t* params, int n, int B, int T, dp_dtype_t dt) {
+  if (check_vec(params, n, B, T, dt) != DP_OK) return 0;
+  VecPlan p;
+  for (int i = 0; i < n; ++i)
+    plan_vec(p, params[i].X, params[i].ldx, params[i].G, params[i].ldg, params[i].d,
+             dpg::VEC_GRAD, nullptr, dt);
+  return align_up((size_t)B * p.slots * 4);
+}
+
+dp_status_t dp_vector_grads_grouped(const dp_vector_t* params, int n, int B, int T,
+                                    dp_dtype_t dt, float* const* grads, float* norm2,
+                                    int accumulate, void* workspace, size_t workspace_bytes,
+                                    void* stream) {
+  dp_status_t st = check_vec(params, n, B, T, dt);
+  if (st != DP_OK) return st;
+  if (!grads) return fail(DP_EINVAL, "grads is NULL");
+  VecPlan p;
+  for (int i = 0; i < n; ++i) {
+    if (!grads[i]) return fail(DP_EINVAL, "grads[%d] is NULL", i);
+    plan_vec(p, params[i].X, params[i].ldx, params[i].G, params[i].ldg, params[i].d,
+             dpg::VEC_GRAD, grads[i], dt);
+  }
+  const size_t need = align_up((size_t)B * p.slots * 4);
+  if (!workspace || workspace_bytes < need)
+    return fail(DP_EINVAL, "workspace of %zu bytes needed", need);
+  float* ws = static_cast<float*>(workspace);
+  hipStream_t s = as_stream(stream);
+  st = run_vec(p, B, T, dt, ws, s);
+  if (st != DP_OK || !norm2) return st;
+  return hip_status(dpg::launch_finish_rows(ws, B, (int)p.slots, norm2, accumulate, 1.f, s),
+                    "finish launch");
+}
+
+dp_status_t dp_vector_clipped_sum_noised_grouped(const float* const* grads, const int32_t* d,
+                                                 int n, int B, const float* c,
+                                                 float* const* outs, const uint64_t* tensor_ids,
+                                                 const int32_t* accumulate, float sigma, float C,
+                                                 int B_norm, uint64_t seed, uint64_t step,
+                                                 void* stream) {
+  if (!grads || !d || !outs || !c || !tensor_ids)
+    return fail(DP_EINVAL, "grads, d, outs, c or tensor_ids is NULL");
+  if (n <= 0 || B <= 0) return fail(DP_EINVAL, "n and B must be positive");
+  dp_status_t st = check_noise_args(sigma, C, B_norm, step);
+  if (st != DP_OK) return st;
+  for (int i = 0; i < n; ++i) {
+    if (!grads[i] || !outs[i]) return fail(DP_EINVAL, "grads[%d] or outs[%d] is NULL", i, i);
+    if (d[i] <= 0) return fail(DP_EINVAL, "d[%d] must be positive", i);
+    if (tensor_ids[i] >> 32) return fail(DP_EINVAL, "tensor_ids[%d] must be < 2^32", i);
+  }
+  hipStream_t s = as_stream(stream);
+  for (int i0 = 0; i0 < n; i0 += dpg::VS_MAX_PARAMS) {
+    dpg::VecSumArgs a{};
+    a.B = B; a.c = c; a.noise = 1;
+    a.sigma_c = (float)((double)sigma * (double)C);
+    a.inv_b = B_norm > 0 ? (float)(1.0 / (double)B_norm) : 1.f;
+    a.seed = seed; a.step = (uint32_t)step;
+    uint64_t quads = 0;
+    const int m = std::min(n - i0, dpg::VS_MAX_PARAMS);
+    for (int j = 0; j < m; ++j) {
+      dpg::VecSumParam& P = a.P[j];
+      P.grad = grads[i0 + j]; P.out = outs[i0 + j]; P.d = d[i0 + j];
+      P.quad_begin = (uint32_t)quads;
+      P.tensor_id = (uint32_t)tensor_ids[i0 + j];
+      P.accumulate = accumulate && accumulate[i0 + j] ? 1 : 0;
+      quads += (uint64_t)ceil_div(d[i0 + j], 4);
+    }
+    if (quads > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many features");
+    a.n_params = m;
+    a.n_quads = (uint32_t)quads;
+    st = hip_status(dpg::launch_vec_sum(a, s), "vec_sum launch");
+    if (st != DP_OK) return st;
+  }
+  return DP_OK;
+}
+
+size_t dp_ghost_norm_positional_workspace(int B, int T, int d) {
+  if (B <= 0 || T <= 0 || d <= 0) return 0;
+  // at most 256 features per chunk (fp32): an upper bound for both dtypes
+  return align_up((size_t)B * (size_t)ceil_div(d, 256) * 4);
+}
+
+dp_status_t dp_ghost_norm_positional(const void* dE, int64_t lde, int B, int T, int d,
+                                     dp_dtype_t dt, float* norm2, int accumulate,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  if (!dE || !norm2) return fail(DP_EINVAL, "dE or norm2 is NULL");
+  dp_vector_t v{nullptr, 0, dE, lde, d};
+  dp_status_t st = check_vec(&v, 1, B, T, dt);
+  if (st != DP_OK) return st;
+  VecPlan p;
+  plan_vec(p, nullptr, 0, dE, lde, d, dpg::VEC_SQ, nullptr, dt);
+  const size_t need = align_up((size_t)B * p.slots * 4);
+  if (!workspace || workspace_bytes < need)
+    return fail(DP_EINVAL, "workspace of %zu bytes needed", need);
+  float* ws = static_cast<float*>(workspace);
+  hipStream_t s = as_stream(stream);
+  st = run_vec(p, B, T, dt, ws, s);
+  if (st != DP_OK) return st;
+  return hip_status(dpg::launch_finish_rows(ws, B, (int)p.slots, norm2, accumulate, 1.f, s),
+                    "finish launch");
+}
+
+dp_status_t dp_clipped_grad_sum_positional_noised(const void* dE, int64_t lde, const float* c,
+                                                  int B, int T, int d, dp_dtype_t dt, float* out,
+                                                  int n_pos, int64_t ldo, uint64_t tensor_id,
+                                                  int accumulate, float sigma, float C,
+                                                  int B_norm, uint64_t seed, uint64_t step,
+                                                  void* stream) {
+  if (!dE || !c || !out) return fail(DP_EINVAL, "dE, c or out is NULL");
+  if (B <= 0 || T <= 0 || d <= 0 || n_pos <= 0)
+    return fail(DP_EINVAL, "B, T, d and n_pos must be positive");
+  if (T > n_pos) return fail(DP_EINVAL, "T = %d exceeds the table's %d rows", T, n_pos);
+  if (lde < d || ldo < d) return fail(DP_EINVAL, "row stride smaller than d");
+  if (!dtype_ok(dt)) return fail(DP_EINVAL, "unknown dtype %d", (int)dt);
+  if (tensor_id >> 32) return fail(DP_EINVAL, "tensor_id must be < 2^32");
+  dp_status_t st = check_noise_args(sigma, C, B_norm, step);
+  if (st != DP_OK) return st;
+  dpg::PosSumArgs a{};
+  a.E = dE; a.lde = lde; a.c = c; a.out = out; a.ldo = ldo;
+  a.B = B; a.T = T; a.d = d; a.n_pos = n_pos;
+  a.accumulate = accumulate ? 1 : 0; a.noise = 1;
+  a.sigma_c = (float)((double)sigma * (double)C);
+  a.inv_b = B_norm > 0 ? (float)(1.0 / (double)B_norm) : 1.f;
+  a.tensor_id = (uint32_t)tensor_id; a.step = (uint32_t)step; a.seed = seed;
+  return hip_status(dpg::launch_pos_sum(a, kdt(dt), as_stream(stream)), "pos_sum launch");
 }
 
 }  // extern "C"

@@ -152,6 +152,71 @@ struct EmbedSumArgs {
 hipError_t launch_embed_sum(const EmbedSumArgs& a, int dt, hipStream_t s);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 
+// ------------------------------------- vector parameters and position table
+enum { VEC_GRAD = 0, VEC_SQ = 1 };
+constexpr int VR_MAX_PARAMS = 52;   // entries per reduce launch (kernel arguments < 4 KiB)
+constexpr int VS_MAX_PARAMS = 64;   // entries per clipped-sum launch
+
+struct VecParam {
+  const void* X;        // [B*T rows, ldx] elementwise factor, or null (a plain sum)
+  const void* G;        // [B*T rows, ldg]
+  int64_t ldx, ldg;
+  int32_t d;            // features
+  int32_t mode;         // VEC_GRAD: per-example gradient; VEC_SQ: sum of squares only
+  float* grad;          // VEC_GRAD: [B, d] per-example gradients
+  uint32_t item_begin;  // first item of this entry among an example's items
+  int32_t slot_begin;   // first partial slot of this entry in an example's row
+};
+
+// Items example-major: example b owns [b * per_ex, (b + 1) * per_ex), one per
+// (entry, feature chunk of 64 lanes x 16 bytes).
+struct VecArgs {
+  VecParam P[VR_MAX_PARAMS];
+  int32_t n_params;
+  int32_t B, T;
+  int32_t slots;        // partial slots per example
+  uint32_t per_ex;
+  uint32_t n_items;
+  float* ws;            // [B, slots]
+};
+static_assert(sizeof(VecArgs) <= 4096, "kernel arguments must stay within 4 KiB");
+hipError_t launch_vec_reduce(const VecArgs& a, int dt, bool vec, hipStream_t s);
+
+struct VecSumParam {
+  const float* grad;    // [B, d]
+  float* out;           // [d]
+  int64_t d;
+  uint32_t quad_begin;  // first 4-feature group of this entry
+  uint32_t tensor_id;
+  int32_t accumulate;
+};
+struct VecSumArgs {
+  VecSumParam P[VS_MAX_PARAMS];
+  int32_t n_params, B;
+  uint32_t n_quads;
+  const float* c;       // [B]
+  int32_t noise;
+  float sigma_c, inv_b;
+  uint32_t step;
+  uint64_t seed;
+};
+static_assert(sizeof(VecSumArgs) <= 4096, "kernel arguments must stay within 4 KiB");
+hipError_t launch_vec_sum(const VecSumArgs& a, hipStream_t s);
+
+struct PosSumArgs {
+  const void* E;        // dE [B*T, lde]
+  int64_t lde;
+  const float* c;       // [B]
+  float* out;           // [n_pos, ldo]
+  int64_t ldo;
+  int32_t B, T, d, n_pos;
+  int32_t accumulate, noise;
+  float sigma_c, inv_b;
+  uint32_t tensor_id, step;
+  uint64_t seed;
+};
+hipError_t launch_pos_sum(const PosSumArgs& a, int dt, hipStream_t s);
+
 // ----------------------------------------------------------- clip and noise
 // c (nullable) = clip factors; cs (nullable) = scale * clip factors.
 hipError_t launch_clip_factors(const float* norm2, int B, float C, float scale, float* c,

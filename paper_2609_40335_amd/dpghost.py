@@ -21,8 +21,9 @@ __all__ = [
     "dp_ghost_norm_linear", "dp_ghost_norm_linear_grouped", "dp_ghost_norm_embedding",
     "dp_tied_cross_term", "dp_clip_factors", "dp_clip_factors_scaled", "dp_clipped_grad_sum",
     "dp_clipped_grad_sum_grouped", "dp_clipped_grad_sum_noised_grouped", "dp_add_noise",
-    "dp_noise_fill",
-    "LinearGroup",
+    "dp_noise_fill", "dp_vector_grads_grouped", "dp_vector_clipped_sum_noised_grouped",
+    "dp_ghost_norm_positional", "dp_clipped_grad_sum_positional_noised",
+    "LinearGroup", "VectorGroup",
 ]
 
 DP_F32, DP_BF16 = 0, 1
@@ -40,6 +41,11 @@ class dp_linear_t(ctypes.Structure):
     _fields_ = [("A", ctypes.c_void_p), ("lda", ctypes.c_int64), ("d_in", ctypes.c_int32),
                 ("G", ctypes.c_void_p), ("ldg", ctypes.c_int64), ("d_out", ctypes.c_int32),
                 ("algo", ctypes.c_int32)]
+
+
+class dp_vector_t(ctypes.Structure):
+    _fields_ = [("X", ctypes.c_void_p), ("ldx", ctypes.c_int64), ("G", ctypes.c_void_p),
+                ("ldg", ctypes.c_int64), ("d", ctypes.c_int32)]
 
 
 def library_path() -> str:
@@ -76,6 +82,17 @@ _SIGS = {
     "dp_add_noise": ([_VP, _I64, _F, _F, _I, _U64, _U64, _U64, _VP], _I),
     "dp_clip_factors_scaled": ([_VP, _I, _F, _F, _VP, _VP, _VP], _I),
     "dp_noise_fill": ([_VP, _I64, _F, _F, _I, _U64, _U64, _U64, _VP], _I),
+    "dp_vector_grads_workspace": ([ctypes.POINTER(dp_vector_t), _I, _I, _I, _I], _SZ),
+    "dp_vector_grads_grouped": ([ctypes.POINTER(dp_vector_t), _I, _I, _I, _I,
+                                 ctypes.POINTER(_VP), _VP, _I, _VP, _SZ, _VP], _I),
+    "dp_vector_clipped_sum_noised_grouped": ([ctypes.POINTER(_VP), ctypes.POINTER(ctypes.c_int32),
+                                              _I, _I, _VP, ctypes.POINTER(_VP),
+                                              ctypes.POINTER(_U64), ctypes.POINTER(ctypes.c_int32),
+                                              _F, _F, _I, _U64, _U64, _VP], _I),
+    "dp_ghost_norm_positional_workspace": ([_I, _I, _I], _SZ),
+    "dp_ghost_norm_positional": ([_VP, _I64, _I, _I, _I, _I, _VP, _I, _VP, _SZ, _VP], _I),
+    "dp_clipped_grad_sum_positional_noised": ([_VP, _I64, _VP, _I, _I, _I, _I, _VP, _I, _I64,
+                                               _U64, _I, _F, _F, _I, _U64, _U64, _VP], _I),
 }
 
 
@@ -331,6 +348,136 @@ def dp_noise_fill(out, sigma: float, C: float, B_norm: int, seed: int, tensor_id
                                int(seed), int(tensor_id), int(step), _stream(stream)),
            "dp_noise_fill")
     return out
+
+
+def _vector(X, G) -> dp_vector_t:
+    _dev(G, "G")
+    pg, B, T, d, ldg = _rows(G, "G")
+    if X is None:
+        return dp_vector_t(None, 0, pg, ldg, d)
+    _dev(X, "X")
+    px, B2, T2, d2, ldx = _rows(X, "X")
+    if (B, T, d) != (B2, T2, d2) or X.dtype != G.dtype:
+        raise DPError("X and G must share shape and dtype")
+    return dp_vector_t(px, ldx, pg, ldg, d)
+
+
+def dp_vector_grads_grouped(params: Sequence, grads: Sequence[torch.Tensor], norm2=None,
+                            accumulate: bool = False, stream=None) -> None:
+    """params: (X or None, G) per vector parameter, [B, T, d] each; grads:
+    fp32 [B, d] outputs (the per-example gradients); norm2 (optional) gets
+    their squared norms added (accumulate) or written."""
+    L = lib()
+    descs = (dp_vector_t * len(params))(*[_vector(*p) for p in params])
+    G0 = params[0][1]
+    B, T, dt = G0.shape[0], G0.shape[1], _dtype(G0)
+    for (X, G), g in zip(params, grads):
+        if tuple(G.shape[:2]) != (B, T) or _dtype(G) != dt:
+            raise DPError("all parameters of a group share B, T and dtype")
+        if g.dtype != torch.float32 or tuple(g.shape) != (B, G.shape[2]) or not g.is_contiguous():
+            raise DPError("grads must be contiguous fp32 [B, d]")
+    if len(grads) != len(params):
+        raise DPError("one gradient buffer per parameter")
+    gp = (ctypes.c_void_p * len(grads))(*[g.data_ptr() for g in grads])
+    ws = _ws(L.dp_vector_grads_workspace(descs, len(params), B, T, dt), G0.device)
+    _check(L.dp_vector_grads_grouped(descs, len(params), B, T, dt, gp,
+                                     None if norm2 is None else norm2.data_ptr(), int(accumulate),
+                                     ws.data_ptr(), ws.numel(), _stream(stream)),
+           "dp_vector_grads_grouped")
+
+
+def dp_vector_clipped_sum_noised_grouped(grads: Sequence[torch.Tensor], outs: Sequence[torch.Tensor],
+                                         c, tensor_ids: Sequence[int], sigma: float, C: float,
+                                         B_norm: int, seed: int, step: int, accumulate=None,
+                                         stream=None) -> None:
+    """outs[v] = (prior + sum_i c_i grads[v][i] + sigma C z) / B_norm."""
+    n = len(grads)
+    if len(outs) != n:
+        raise DPError("one output per parameter")
+    for g, o in zip(grads, outs):
+        if o.dtype != torch.float32 or o.numel() != g.shape[1] or not o.is_contiguous():
+            raise DPError("outs must be contiguous fp32 with d elements")
+    gp = (ctypes.c_void_p * n)(*[g.data_ptr() for g in grads])
+    op = (ctypes.c_void_p * n)(*[o.data_ptr() for o in outs])
+    dd = (ctypes.c_int32 * n)(*[int(g.shape[1]) for g in grads])
+    tids, acc = _noise_arrays(n, tensor_ids, accumulate)
+    _check(lib().dp_vector_clipped_sum_noised_grouped(gp, dd, n, int(grads[0].shape[0]),
+                                                      c.data_ptr(), op, tids, acc, float(sigma),
+                                                      float(C), int(B_norm), int(seed), int(step),
+                                                      _stream(stream)),
+           "dp_vector_clipped_sum_noised_grouped")
+
+
+def dp_ghost_norm_positional(dE, norm2, accumulate: bool = False, stream=None) -> torch.Tensor:
+    """norm2[i] (+)= sum_t ||dE[i, t]||^2 (the position table's per-example norm)."""
+    L = lib()
+    _dev(dE, "dE")
+    pe, B, T, d, lde = _rows(dE, "dE")
+    ws = _ws(L.dp_ghost_norm_positional_workspace(B, T, d), dE.device)
+    _check(L.dp_ghost_norm_positional(pe, lde, B, T, d, _dtype(dE), norm2.data_ptr(),
+                                      int(accumulate), ws.data_ptr(), ws.numel(), _stream(stream)),
+           "dp_ghost_norm_positional")
+    return norm2
+
+
+def dp_clipped_grad_sum_positional_noised(dE, c, out, tensor_id: int, sigma: float, C: float,
+                                          B_norm: int, seed: int, step: int,
+                                          accumulate: bool = False, stream=None) -> torch.Tensor:
+    """out [n_pos, d] fp32: rows t < T get sum_i c_i dE[i, t]; all rows the noise."""
+    _dev(dE, "dE")
+    pe, B, T, d, lde = _rows(dE, "dE")
+    if out.dtype != torch.float32 or out.dim() != 2 or out.shape[1] != d or out.stride(1) != 1:
+        raise DPError("out must be fp32 [n_pos, d] with unit column stride")
+    _check(lib().dp_clipped_grad_sum_positional_noised(pe, lde, c.data_ptr(), B, T, d, _dtype(dE),
+                                                       out.data_ptr(), out.shape[0], out.stride(0),
+                                                       int(tensor_id), int(accumulate),
+                                                       float(sigma), float(C), int(B_norm),
+                                                       int(seed), int(step), _stream(stream)),
+           "dp_clipped_grad_sum_positional_noised")
+    return out
+
+
+class VectorGroup:
+    """Descriptors, per-example gradient buffers and workspace of many vector
+    parameters of one batch, prepared once (see dp_vector_grads_grouped)."""
+
+    def __init__(self, params: Sequence):
+        L = lib()
+        self._tensors = [t for p in params for t in p if t is not None]
+        self.n = len(params)
+        self.descs = (dp_vector_t * self.n)(*[_vector(*p) for p in params])
+        G0 = params[0][1]
+        self.B, self.T, self.dt = G0.shape[0], G0.shape[1], _dtype(G0)
+        self.d = [int(p[1].shape[2]) for p in params]
+        self.grads = [torch.empty(self.B, d, device=G0.device) for d in self.d]
+        self._gp = (ctypes.c_void_p * self.n)(*[g.data_ptr() for g in self.grads])
+        self._dd = (ctypes.c_int32 * self.n)(*self.d)
+        self.ws = _ws(L.dp_vector_grads_workspace(self.descs, self.n, self.B, self.T, self.dt),
+                      G0.device)
+        self._noise_key = None
+
+    def grads_and_norm(self, norm2, accumulate: bool = False, stream=None) -> None:
+        _check(lib().dp_vector_grads_grouped(self.descs, self.n, self.B, self.T, self.dt, self._gp,
+                                             None if norm2 is None else norm2.data_ptr(),
+                                             int(accumulate), self.ws.data_ptr(), self.ws.numel(),
+                                             _stream(stream)), "dp_vector_grads_grouped")
+
+    def clipped_sum_noised(self, c, outs: Sequence[torch.Tensor], tensor_ids: Sequence[int],
+                           sigma: float, C: float, B_norm: int, seed: int, step: int,
+                           accumulate=None, stream=None) -> None:
+        key = (tuple(o.data_ptr() for o in outs), tuple(int(t) for t in tensor_ids),
+               accumulate if isinstance(accumulate, (bool, int, type(None)))
+               else tuple(bool(a) for a in accumulate))
+        if self._noise_key != key:
+            self._noise_key = key
+            self._op = (ctypes.c_void_p * self.n)(*[o.data_ptr() for o in outs])
+            self._na = _noise_arrays(self.n, tensor_ids, accumulate)
+        tids, acc = self._na
+        _check(lib().dp_vector_clipped_sum_noised_grouped(self._gp, self._dd, self.n, self.B,
+                                                          c.data_ptr(), self._op, tids, acc,
+                                                          float(sigma), float(C), int(B_norm),
+                                                          int(seed), int(step), _stream(stream)),
+               "dp_vector_clipped_sum_noised_grouped")
 
 
 class LinearGroup:

@@ -46,7 +46,7 @@ def test_binding_covers_every_entry_point():
 
 
 def test_version_and_strings(L):
-    assert L.dp_abi_version() == 1
+    assert L.dp_abi_version() == 2
     assert L.dp_status_string(0) == b"ok"
     assert L.dp_status_string(1) == b"invalid argument"
 
@@ -245,3 +245,54 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(D, "_HERE", str(tmp_path))
     with pytest.raises(D.DPError, match="not built"):
         D.lib()
+
+
+def test_vector_and_positional_validation(L):
+    vec = (D.dp_vector_t * 2)(D.dp_vector_t(None, 0, 1 << 21, 96, 96),
+                              D.dp_vector_t(1 << 22, 64, 1 << 23, 64, 64))
+    # workspace: one partial per 512-feature (bf16) or 256-feature (fp32) chunk per example
+    assert L.dp_vector_grads_workspace(vec, 2, 4, 16, D.DP_BF16) == 256
+    assert L.dp_vector_grads_workspace(vec, 2, 100, 16, D.DP_F32) == ((100 * 2 * 4 + 255) // 256) * 256
+    grads = (ctypes.c_void_p * 2)(1 << 24, 1 << 25)
+    ws, nws = 1 << 26, 1 << 20
+    ok = lambda *a: L.dp_vector_grads_grouped(vec, 2, 4, 16, D.DP_BF16, *a)
+    assert ok(None, None, 0, ws, nws, None) == EINVAL                    # grads NULL
+    assert ok(grads, None, 0, None, 0, None) == EINVAL                   # no workspace
+    assert L.dp_vector_grads_grouped(vec, 0, 4, 16, D.DP_BF16, grads, None, 0, ws, nws,
+                                     None) == EINVAL                     # n = 0
+    bad = (D.dp_vector_t * 1)(D.dp_vector_t(None, 0, 1 << 21, 90, 96))   # ldg < d
+    assert L.dp_vector_grads_grouped(bad, 1, 4, 16, D.DP_BF16, grads, None, 0, ws, nws,
+                                     None) == EINVAL
+    bad = (D.dp_vector_t * 1)(D.dp_vector_t(None, 0, None, 96, 96))      # G NULL
+    assert L.dp_vector_grads_grouped(bad, 1, 4, 16, D.DP_BF16, grads, None, 0, ws, nws,
+                                     None) == EINVAL
+    big = (D.dp_vector_t * 1)(D.dp_vector_t(None, 0, 1 << 21, 1 << 20, 64))
+    assert L.dp_vector_grads_grouped(big, 1, 4096, 1024, D.DP_BF16, grads, None, 0, ws, nws,
+                                     None) == EUNSUP                     # 8 TiB operand span
+    d = (ctypes.c_int32 * 2)(96, 64)
+    outs = (ctypes.c_void_p * 2)(1 << 27, 1 << 28)
+    tids = (ctypes.c_uint64 * 2)(1, 2)
+    vs = lambda *a: L.dp_vector_clipped_sum_noised_grouped(grads, d, 2, 4, 1 << 29, outs, tids,
+                                                           None, *a)
+    assert vs(-1.0, 1.0, 4, 0, 0, None) == EINVAL                        # sigma < 0
+    assert vs(1.0, 0.0, 4, 0, 0, None) == EINVAL                         # C = 0
+    assert vs(1.0, 1.0, -1, 0, 0, None) == EINVAL                        # B_norm < 0
+    assert vs(1.0, 1.0, 4, 0, 1 << 32, None) == EINVAL                   # step >= 2^32
+    tids_bad = (ctypes.c_uint64 * 2)(1, 1 << 33)
+    assert L.dp_vector_clipped_sum_noised_grouped(grads, d, 2, 4, 1 << 29, outs, tids_bad, None,
+                                                  1.0, 1.0, 4, 0, 0, None) == EINVAL
+    # position table
+    assert L.dp_ghost_norm_positional_workspace(4, 16, 768) == 256
+    assert L.dp_ghost_norm_positional_workspace(0, 16, 768) == 0
+    assert L.dp_ghost_norm_positional(None, 768, 4, 16, 768, D.DP_BF16, 1 << 20, 0, ws, nws,
+                                      None) == EINVAL
+    assert L.dp_ghost_norm_positional(1 << 21, 700, 4, 16, 768, D.DP_BF16, 1 << 20, 0, ws, nws,
+                                      None) == EINVAL                    # lde < d
+    ps = lambda T, n_pos, ldo: L.dp_clipped_grad_sum_positional_noised(
+        1 << 21, 768, 1 << 22, 4, T, 768, D.DP_BF16, 1 << 23, n_pos, ldo, 3, 0, 1.0, 1.0, 4, 0, 0,
+        None)
+    assert ps(2048, 1024, 768) == EINVAL                                  # T > n_pos
+    assert ps(16, 1024, 700) == EINVAL                                    # ldo < d
+    assert L.dp_clipped_grad_sum_positional_noised(1 << 21, 768, 1 << 22, 4, 16, 768, D.DP_BF16,
+                                                   1 << 23, 1024, 768, 1 << 32, 0, 1.0, 1.0, 4,
+                                                   0, 0, None) == EINVAL  # tensor_id >= 2^32

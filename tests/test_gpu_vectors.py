@@ -1,0 +1,238 @@
+"""GPU parity of the remaining GPT-2 parameters against the fp64 oracle:
+vector parameters (linear biases, LayerNorm gains and biases) and the
+learned position table, their per-example norms, clipped sums and noise.
+
+Inputs are seeded draws (workloads.gen); expected values come only from the
+oracle. Per-example gradients of these parameters are small, so full GPT-2
+sizes are checked in full.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+from workloads import gen
+from tests.helpers import TOL, dev, fro_rel, host, rel
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def dp():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_40335_amd.dpghost as d
+    d.lib()
+    return d
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _nan_pad(x, d):
+    """Fill the row-stride padding past column d with NaN (bf16 or fp32)."""
+    if x.shape[2] > d:
+        x[:, :, d:] = 0x7FC0 if x.dtype == np.uint16 else np.nan
+    return x
+
+
+VEC_CASES = [
+    # dtype, B, T, d, with X, row stride (None: d)
+    ("bf16", 3, 37, 520, True, None),      # ragged T (not a multiple of 16 rows), 2 chunks
+    ("bf16", 2, 130, 77, False, 80),       # width not a multiple of 8, aligned padded stride
+    ("bf16", 2, 5, 3000, True, None),      # 6 feature chunks, fewer rows than waves x unroll
+    ("bf16", 4, 1, 64, True, None),        # T = 1: x * g
+    ("bf16", 2, 16, 101, True, 103),       # unaligned stride: element-wise loads
+    ("f32", 4, 16, 64, True, None),
+    ("f32", 2, 33, 300, False, 303),       # unaligned fp32 stride
+    ("f32", 3, 70, 260, True, 264),        # 2 fp32 chunks, aligned padded stride
+]
+
+
+@pytest.mark.parametrize("case", VEC_CASES, ids=lambda c: "-".join(str(x) for x in c))
+def test_vector_grads_and_norms(dp, case):
+    dtype, B, T, d, with_x, ld = case
+    _say(f"vector grads {case}")
+    ld = ld or d
+    G = _nan_pad(gen.draw(71, 1, (B, T, ld), 1e-2, dtype), d)
+    X = _nan_pad(gen.draw(71, 2, (B, T, ld), 1.0, dtype), d) if with_x else None
+    Gd = O.decode(G[:, :, :d], dtype)
+    Xd = None if X is None else O.decode(X[:, :, :d], dtype)
+    ref_g = np.stack([O.vector_grad(None if Xd is None else Xd[i], Gd[i]) for i in range(B)])
+    ref_n = O.vector_norm2(Xd, Gd)
+    grads = [torch.full((B, d), 7.0, device="cuda")]
+    Xt = None if X is None else dev(X, dtype)[:, :, :d]
+    n2 = torch.full((B,), 2.0, device="cuda")
+    dp.dp_vector_grads_grouped([(Xt, dev(G, dtype)[:, :, :d])], grads, n2, accumulate=True)
+    got = host(grads[0])
+    assert np.isfinite(got).all()
+    for i in range(B):
+        assert fro_rel(got[i], ref_g[i]) <= TOL[dtype], i
+    assert rel(host(n2) - 2.0, ref_n).max() <= TOL[dtype]
+    # overwrite mode, no norm output
+    n3 = torch.full((B,), 5.0, device="cuda")
+    dp.dp_vector_grads_grouped([(Xt, dev(G, dtype)[:, :, :d])], grads, n3, accumulate=False)
+    assert rel(host(n3), ref_n).max() <= TOL[dtype]
+    dp.dp_vector_grads_grouped([(Xt, dev(G, dtype)[:, :, :d])], grads, None)
+
+
+def test_vector_grads_grouped_mixed(dp):
+    """Biases and gains of several widths, aligned and unaligned, one call."""
+    B, T = 3, 40
+    specs = [(96, False, None), (520, True, None), (77, True, 80), (33, False, 35), (1024, True, None)]
+    params, refs, norm_ref = [], [], np.zeros(B)
+    for k, (d, with_x, ld) in enumerate(specs):
+        ld = ld or d
+        G = gen.draw(80 + k, 1, (B, T, ld), 1e-2, "bf16")
+        X = gen.draw(80 + k, 2, (B, T, ld), 1.0, "bf16") if with_x else None
+        Gd = O.decode(G[:, :, :d], "bf16")
+        Xd = None if X is None else O.decode(X[:, :, :d], "bf16")
+        refs.append(np.stack([O.vector_grad(None if Xd is None else Xd[i], Gd[i])
+                              for i in range(B)]))
+        norm_ref += O.vector_norm2(Xd, Gd)
+        params.append((None if X is None else dev(X, "bf16")[:, :, :d], dev(G, "bf16")[:, :, :d]))
+    grads = [torch.empty(B, d, device="cuda") for d, _, _ in specs]
+    n2 = torch.zeros(B, device="cuda")
+    dp.dp_vector_grads_grouped(params, grads, n2)
+    for g, r in zip(grads, refs):
+        assert fro_rel(host(g), r) <= TOL["bf16"]
+    assert rel(host(n2), norm_ref).max() <= TOL["bf16"]
+
+
+def test_vector_clipped_sum_noised(dp):
+    """outs = (prior + sum_i c_i g_i + sigma C z) / B against the oracle's
+    add_noise with the same stream; widths not multiples of 4."""
+    B = 5
+    sigma, C, seed, step = 0.8, 1.3, 0xBEEF, 7
+    ds = [3, 64, 517, 2304]
+    tids = [4, 11, 12, 40]
+    acc = [False, True, False, True]
+    c = np.linspace(0.2, 1.0, B).astype(np.float32)
+    grads, outs, refs = [], [], []
+    for k, d in enumerate(ds):
+        g = gen.draw(90 + k, 1, (B, d), 1.0, "f32")
+        prior = gen.draw(90 + k, 2, (d,), 1e-1, "f32") if acc[k] else np.zeros(d, np.float32)
+        S = (c.astype(np.float64)[:, None] * g.astype(np.float64)).sum(axis=0)
+        refs.append(O.add_noise(prior.astype(np.float64) + S, sigma, C, B, seed, tids[k], step))
+        grads.append(dev(g))
+        outs.append(dev(prior.copy()))
+    dp.dp_vector_clipped_sum_noised_grouped(grads, outs, dev(c), tids, sigma, C, B, seed, step,
+                                            accumulate=acc)
+    for k in range(len(ds)):
+        err = fro_rel(host(outs[k]), refs[k])
+        _say(f"  d={ds[k]} rel err {err:.2e}")
+        assert err <= TOL["f32"]
+    # sigma = 0, B_norm = 0: the plain clipped sum
+    plain = [torch.zeros(d, device="cuda") for d in ds]
+    dp.dp_vector_clipped_sum_noised_grouped(grads, plain, dev(c), tids, 0.0, C, 0, seed, step)
+    for k, d in enumerate(ds):
+        S = (c.astype(np.float64)[:, None] * host(grads[k]).astype(np.float64)).sum(axis=0)
+        assert fro_rel(host(plain[k]), S) <= 1e-6
+
+
+@pytest.mark.parametrize("dtype,B,T,d,ld", [("bf16", 3, 37, 768, None), ("bf16", 2, 20, 77, 80),
+                                            ("f32", 4, 16, 64, None), ("f32", 2, 9, 101, 103)])
+def test_positional_norm(dp, dtype, B, T, d, ld):
+    ld = ld or d
+    dE = _nan_pad(gen.draw(101, 1, (B, T, ld), 1e-2, dtype), d)
+    ref = O.positional_norm2(O.decode(dE[:, :, :d], dtype), 2 * T)
+    n2 = torch.full((B,), 1.5, device="cuda")
+    dp.dp_ghost_norm_positional(dev(dE, dtype)[:, :, :d], n2, accumulate=True)
+    assert rel(host(n2) - 1.5, ref).max() <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype,B,T,d,n_pos,acc", [("bf16", 3, 37, 768, 64, False),
+                                                   ("bf16", 2, 16, 77, 16, True),
+                                                   ("f32", 4, 10, 101, 23, True)])
+def test_positional_clipped_sum_noised(dp, dtype, B, T, d, n_pos, acc):
+    """Rows t < T get the clipped sum, every row the noise of element t*d + f;
+    a width not a multiple of 4 draws per element."""
+    sigma, C, seed, step, tid = 0.6, 0.9, 12345, 3, 17
+    dE = gen.draw(111, 1, (B, T, d), 1e-2, dtype)
+    c = np.linspace(0.3, 1.0, B).astype(np.float32)
+    S = O.clipped_sum_positional(O.decode(dE, dtype), c.astype(np.float64), n_pos)
+    prior = gen.draw(111, 2, (n_pos, d), 1e-2, "f32") if acc else np.zeros((n_pos, d), np.float32)
+    ref = O.add_noise(prior.astype(np.float64) + S, sigma, C, B, seed, tid, step)
+    out = dev(prior.copy())
+    dp.dp_clipped_grad_sum_positional_noised(dev(dE, dtype), dev(c), out, tid, sigma, C, B, seed,
+                                             step, accumulate=acc)
+    got = host(out)
+    assert fro_rel(got[:T], ref[:T]) <= TOL[dtype]
+    assert fro_rel(got[T:], ref[T:]) <= 1e-4 if n_pos > T else True
+
+
+def test_full_param_tiny_step(dp):
+    """Every parameter of a tiny tied model (weights, biases, LayerNorms,
+    position table, tied embedding/head): norms, clip factors and noised sums
+    through the C ABI against the oracle's step."""
+    wl = gen.make_workload("c1-tied", full_params=True)
+    ref = O.step(wl, seed=9, step_id=4)
+    B, h = wl.B, wl.head
+    lin = wl.linears[0]
+    A, G = dev(lin.A), dev(lin.G)
+    ids, dE, H = dev(h.ids), dev(h.dE), dev(h.H)
+    Gz = dev(h.Gz)[:, :, :h.V]
+    n2 = torch.zeros(B, device="cuda")
+    dp.dp_ghost_norm_linear_grouped([(A, G), (H, Gz)], n2)
+    dp.dp_ghost_norm_embedding(ids, dE, h.V, n2, accumulate=True)
+    dp.dp_tied_cross_term(ids, dE, H, Gz, h.V, n2, scale=2.0, accumulate=True)
+    vg = dp.VectorGroup([(None if v.X is None else dev(v.X), dev(v.G)) for v in wl.vectors])
+    vg.grads_and_norm(n2, accumulate=True)
+    dp.dp_ghost_norm_positional(dE, n2, accumulate=True)
+    assert rel(host(n2), ref["norms"]["total"]).max() <= TOL["f32"]
+    c = torch.empty(B, device="cuda")
+    c_b = torch.empty(B, device="cuda")
+    dp.dp_clip_factors_scaled(n2, wl.C, 1.0 / B, c_b, c=c)
+    assert rel(host(c), ref["c"]).max() <= TOL["f32"]
+    names = list(ref["noisy"])
+    tid = {n: k for k, n in enumerate(names)}
+    S = torch.empty(lin.d_in, lin.d_out, device="cuda")
+    E = torch.empty(h.V, h.d, device="cuda")
+    dp.dp_clipped_grad_sum_noised_grouped([(A, G), (Gz, H)], [S, E], c,
+                                          [tid["linear"], tid["wte"]], wl.sigma, wl.C, B, 9, 4)
+    dp.dp_clipped_grad_sum(None, dE, c_b, E, ids=ids, V=h.V, accumulate=True)
+    outs = [torch.empty(v.d, device="cuda") for v in wl.vectors]
+    vg.clipped_sum_noised(c, outs, [tid[v.name] for v in wl.vectors], wl.sigma, wl.C, B, 9, 4)
+    P = torch.empty(wl.n_pos, h.d, device="cuda")
+    dp.dp_clipped_grad_sum_positional_noised(dE, c, P, tid["wpe"], wl.sigma, wl.C, B, 9, 4)
+    assert fro_rel(host(S), ref["noisy"]["linear"]) <= TOL["f32"]
+    assert fro_rel(host(E), ref["noisy"]["wte"]) <= TOL["f32"]
+    for v, o in zip(wl.vectors, outs):
+        assert fro_rel(host(o), ref["noisy"][v.name]) <= TOL["f32"], v.name
+    assert fro_rel(host(P), ref["noisy"]["wpe"]) <= TOL["f32"]
+
+
+def test_full_size_gpt2_vectors(dp):
+    """All 98 vector parameters and the position table of GPT-2-small at the
+    benchmark's B = 32, T = 128, checked in full against the oracle."""
+    wl = gen.make_workload("gpt2-step", full_params=True)
+    B, h = wl.B, wl.head
+    _say(f"full-size vectors: {len(wl.vectors)} parameters, B={B}, T={wl.T}")
+    vg = dp.VectorGroup([(None if v.X is None else dev(v.X), dev(v.G)) for v in wl.vectors])
+    n2 = torch.zeros(B, device="cuda")
+    vg.grads_and_norm(n2)
+    dE = dev(h.dE)
+    npos = torch.zeros(B, device="cuda")
+    dp.dp_ghost_norm_positional(dE, npos)
+    ref_n = np.zeros(B)
+    worst = 0.0
+    for v, g in zip(wl.vectors, vg.grads):
+        Xd = None if v.X is None else O.decode(v.X, "bf16")
+        Gd = O.decode(v.G, "bf16")
+        ref_g = np.stack([O.vector_grad(None if Xd is None else Xd[i], Gd[i]) for i in range(B)])
+        worst = max(worst, fro_rel(host(g), ref_g))
+        ref_n += (ref_g * ref_g).sum(axis=1)
+    _say(f"  worst per-parameter gradient rel err {worst:.2e}")
+    assert worst <= TOL["bf16"]
+    assert rel(host(n2), ref_n).max() <= TOL["bf16"]
+    assert rel(host(npos), O.positional_norm2(O.decode(h.dE, "bf16"), wl.n_pos)).max() <= TOL["bf16"]
+    c = (0.25 + 0.75 * np.arange(B) / B).astype(np.float32)
+    P = torch.empty(wl.n_pos, h.d, device="cuda")
+    dp.dp_clipped_grad_sum_positional_noised(dE, dev(c), P, 7, 0.0, 1.0, 0, 1, 0)
+    ref_p = O.clipped_sum_positional(O.decode(h.dE, "bf16"), c.astype(np.float64), wl.n_pos)
+    assert fro_rel(host(P), ref_p) <= TOL["bf16"]
