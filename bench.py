@@ -14,6 +14,9 @@ One step is the whole hot path on one batch, through the C ABI:
      the head accumulating onto the tied embedding gradient, with Gaussian
      noise and the division by B fused into the GEMM's store (eq. 3); one
      generator stream per parameter tensor
+With every parameter (--workload gpt2-full), the biases, LayerNorm gains and
+biases and the position table join: their per-example gradients and norms
+after the weight norms, their noised clipped sums after the GEMM.
 Inputs are resident in HBM before the timed region starts. Prints one JSON
 line; per-phase times go to stderr.
 """
@@ -50,7 +53,7 @@ def parse(argv=None):
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gpt2-step",
-                    choices=["gpt2-step", "c2", "c3", "c4", "c5"])
+                    choices=["gpt2-step", "gpt2-full", "c2", "c3", "c4", "c5"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--ldz-multiple", type=int, default=64,
                     help="pad logit-gradient rows to a multiple of this many columns")
@@ -91,7 +94,9 @@ class Step:
         n_lin = sum(l.d_in * l.d_out for l in wl.linears)
         n_head = 0 if h is None or h.H is None else h.V * h.d * (1 if h.tied else 1)
         n_emb = 0 if h is None else (h.V * h.d if (h.H is None or not h.tied) else 0)
-        self.n_coords = n_lin + n_head + n_emb
+        n_vec = sum(v.d for v in wl.vectors)
+        n_pos = wl.n_pos * h.d if wl.n_pos else 0
+        self.n_coords = n_lin + n_head + n_emb + n_vec + n_pos
         self.flat = torch.zeros(self.n_coords, device="cuda")
         off = 0
         self.outs = []
@@ -118,6 +123,25 @@ class Step:
                 self.E = self.W
             self.seg = torch.empty((B, T), dtype=torch.int32, device="cuda")
             self.nu = torch.empty(B, dtype=torch.int32, device="cuda")
+        # biases, LayerNorm gains/biases and the position table (full-parameter workloads)
+        self.vec_outs, self.vg, self.P = [], None, None
+        if wl.vectors:
+            # one device buffer per host array: a bias reads its linear layer's own
+            # G, and a LayerNorm's gain and bias share theirs (one pass over it)
+            same = {id(l.G): g for l, (_, g) in zip(wl.linears, self.lin)}
+
+            def shared(a):
+                if id(a) not in same:
+                    same[id(a)] = dev(a)
+                return same[id(a)]
+            self.vg = dp.VectorGroup([(None if v.X is None else dev(v.X), shared(v.G))
+                                      for v in wl.vectors])
+            for v in wl.vectors:
+                self.vec_outs.append(self.flat[off:off + v.d])
+                off += v.d
+        if wl.n_pos:
+            self.P = self.flat[off:off + wl.n_pos * h.d].view(wl.n_pos, h.d)
+            off += wl.n_pos * h.d
         assert off == self.n_coords
         self.norm_layers = norm_layers
         self.norm_group = dp.LinearGroup(norm_layers)
@@ -134,6 +158,10 @@ class Step:
         if h is not None and h.H is not None:
             self.sum_tids.append(L if h.tied else L + 1)
         self.e_tid = L
+        # after the weight matrices (and an untied head): the vectors, then the position table
+        t0 = L + (2 if (h is not None and h.H is not None and not h.tied) else 1)
+        self.vec_tids = list(range(t0, t0 + len(wl.vectors)))
+        self.pos_tid = t0 + len(wl.vectors)
         self.n2 = torch.zeros(B, device="cuda")
         self.c = torch.zeros(B, device="cuda")
         self.c_b = torch.zeros(B, device="cuda")   # c / B
@@ -158,6 +186,12 @@ class Step:
                 dp.dp_tied_cross_term(self.ids, self.dE, self.H, self.Gz, h.V, self.n2,
                                       scale=2.0, accumulate=True)
                 mark("cross_term")
+        if self.vg is not None:
+            self.vg.grads_and_norm(self.n2, accumulate=True)
+            mark("vector_norms")
+        if self.P is not None:
+            dp.dp_ghost_norm_positional(self.dE, self.n2, accumulate=True)
+            mark("position_norm")
         dp.dp_clip_factors_scaled(self.n2, wl.C, 1.0 / wl.B, self.c_b, c=self.c)
         mark("clip")
         # clipped sums of every GEMM-shaped tensor with the Gaussian mechanism
@@ -174,6 +208,15 @@ class Step:
             dp.dp_clipped_grad_sum(None, self.dE, self.c_b, self.E, ids=self.ids, V=h.V,
                                    accumulate=True)
             mark("embedding_sum")
+        if self.vg is not None:
+            self.vg.clipped_sum_noised(self.c, self.vec_outs, self.vec_tids, wl.sigma, wl.C, wl.B,
+                                       seed=1234, step=self.step_id)
+            mark("vector_sums")
+        if self.P is not None:
+            dp.dp_clipped_grad_sum_positional_noised(self.dE, self.c, self.P, self.pos_tid,
+                                                     wl.sigma, wl.C, wl.B, seed=1234,
+                                                     step=self.step_id)
+            mark("position_sum")
         self.step_id += 1
 
 

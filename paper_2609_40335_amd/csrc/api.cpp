@@ -340,6 +340,8 @@ struct VecEntry {
   int d, mode, chunks, slot_begin;
   float* grad;
   bool vec;
+  float* grad2 = nullptr;  // fused LayerNorm bias (same G, no X)
+  int tsplit = 1, trows = 0;
 };
 
 struct VecPlan {
@@ -349,12 +351,46 @@ struct VecPlan {
 
 int vec_chunk_features(dp_dtype_t dt) { return 64 * elems_per_chunk(dt); }
 
+// Rows per item of a sum-of-squares entry (its partials are scalars, so an
+// example's rows may be split into ranges for more parallel work).
+constexpr int VEC_SQ_ROWS = 32;
+
 void plan_vec(VecPlan& p, const void* X, int64_t ldx, const void* G, int64_t ldg, int d, int mode,
-              float* grad, dp_dtype_t dt) {
+              float* grad, dp_dtype_t dt, int T, float* grad2 = nullptr) {
   VecEntry e{X, G, ldx, ldg, d, mode, (int)ceil_div(d, vec_chunk_features(dt)), (int)p.slots,
              grad, vec_ok(G, ldg, dt) && (!X || vec_ok(X, ldx, dt))};
-  p.slots += e.chunks;
+  e.grad2 = grad2;
+  e.tsplit = mode == dpg::VEC_SQ ? (int)ceil_div(T, VEC_SQ_ROWS) : 1;
+  e.trows = mode == dpg::VEC_SQ ? VEC_SQ_ROWS : T;
+  p.slots += (int64_t)e.chunks * e.tsplit;
   p.e.push_back(e);
+}
+
+// The gradient entries of a grouped call. A LayerNorm's gain (X set) and bias
+// (no X, the same G, stride and width) are one entry: one pass over G.
+void plan_vec_grads(VecPlan& p, const dp_vector_t* params, int n, float* const* grads,
+                    dp_dtype_t dt, int T) {
+  std::vector<int> partner(n, -1);
+  std::vector<char> claimed(n, 0);
+  for (int i = 0; i < n; ++i) {
+    const dp_vector_t& v = params[i];
+    if (!v.X) continue;
+    for (int j = 0; j < n; ++j) {
+      const dp_vector_t& u = params[j];
+      if (!u.X && !claimed[j] && u.G == v.G && u.ldg == v.ldg && u.d == v.d) {
+        partner[i] = j;
+        claimed[j] = 1;
+        break;
+      }
+    }
+  }
+  for (int i = 0; i < n; ++i) {
+    if (claimed[i]) continue;
+    const dp_vector_t& v = params[i];
+    float* g2 = partner[i] >= 0 && grads ? grads[partner[i]] : nullptr;
+    float* g = grads ? grads[i] : nullptr;
+    plan_vec(p, v.X, v.ldx, v.G, v.ldg, v.d, dpg::VEC_GRAD, g, dt, T, partner[i] >= 0 ? g2 : nullptr);
+  }
 }
 
 dp_status_t check_vec(const dp_vector_t* params, int n, int B, int T, dp_dtype_t dt) {
@@ -389,8 +425,9 @@ dp_status_t run_vec(const VecPlan& p, int B, int T, dp_dtype_t dt, float* ws, hi
         const VecEntry& e = *sel[i0 + j];
         dpg::VecParam& P = a.P[j];
         P.X = e.X; P.G = e.G; P.ldx = e.ldx; P.ldg = e.ldg; P.d = e.d; P.mode = e.mode;
-        P.grad = e.grad; P.item_begin = (uint32_t)per_ex; P.slot_begin = e.slot_begin;
-        per_ex += (uint64_t)e.chunks;
+        P.grad = e.grad; P.grad2 = e.grad2; P.tsplit = e.tsplit; P.trows = e.trows;
+        P.item_begin = (uint32_t)per_ex; P.slot_begin = e.slot_begin;
+        per_ex += (uint64_t)e.chunks * e.tsplit;
       }
       const uint64_t items = per_ex * (uint64_t)B;
       if (items > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many work items");
@@ -700,9 +737,7 @@ dp_status_t dp_noise_fill(float* out, int64_t n, float sigma, float C, int B_nor
 size_t dp_vector_grads_workspace(const dp_vector_t* params, int n, int B, int T, dp_dtype_t dt) {
   if (check_vec(params, n, B, T, dt) != DP_OK) return 0;
   VecPlan p;
-  for (int i = 0; i < n; ++i)
-    plan_vec(p, params[i].X, params[i].ldx, params[i].G, params[i].ldg, params[i].d,
-             dpg::VEC_GRAD, nullptr, dt);
+  plan_vec_grads(p, params, n, nullptr, dt, T);
   return align_up((size_t)B * p.slots * 4);
 }
 
@@ -713,12 +748,10 @@ dp_status_t dp_vector_grads_grouped(const dp_vector_t* params, int n, int B, int
   dp_status_t st = check_vec(params, n, B, T, dt);
   if (st != DP_OK) return st;
   if (!grads) return fail(DP_EINVAL, "grads is NULL");
-  VecPlan p;
-  for (int i = 0; i < n; ++i) {
+  for (int i = 0; i < n; ++i)
     if (!grads[i]) return fail(DP_EINVAL, "grads[%d] is NULL", i);
-    plan_vec(p, params[i].X, params[i].ldx, params[i].G, params[i].ldg, params[i].d,
-             dpg::VEC_GRAD, grads[i], dt);
-  }
+  VecPlan p;
+  plan_vec_grads(p, params, n, grads, dt, T);
   const size_t need = align_up((size_t)B * p.slots * 4);
   if (!workspace || workspace_bytes < need)
     return fail(DP_EINVAL, "workspace of %zu bytes needed", need);
@@ -775,7 +808,7 @@ dp_status_t dp_vector_clipped_sum_noised_grouped(const float* const* grads, cons
 size_t dp_ghost_norm_positional_workspace(int B, int T, int d) {
   if (B <= 0 || T <= 0 || d <= 0) return 0;
   // at most 256 features per chunk (fp32): an upper bound for both dtypes
-  return align_up((size_t)B * (size_t)ceil_div(d, 256) * 4);
+  return align_up((size_t)B * (size_t)ceil_div(d, 256) * (size_t)ceil_div(T, VEC_SQ_ROWS) * 4);
 }
 
 dp_status_t dp_ghost_norm_positional(const void* dE, int64_t lde, int B, int T, int d,
@@ -786,7 +819,7 @@ dp_status_t dp_ghost_norm_positional(const void* dE, int64_t lde, int B, int T, 
   dp_status_t st = check_vec(&v, 1, B, T, dt);
   if (st != DP_OK) return st;
   VecPlan p;
-  plan_vec(p, nullptr, 0, dE, lde, d, dpg::VEC_SQ, nullptr, dt);
+  plan_vec(p, nullptr, 0, dE, lde, d, dpg::VEC_SQ, nullptr, dt, T);
   const size_t need = align_up((size_t)B * p.slots * 4);
   if (!workspace || workspace_bytes < need)
     return fail(DP_EINVAL, "workspace of %zu bytes needed", need);

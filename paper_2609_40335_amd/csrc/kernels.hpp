@@ -154,7 +154,7 @@ hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 
 // ------------------------------------- vector parameters and position table
 enum { VEC_GRAD = 0, VEC_SQ = 1 };
-constexpr int VR_MAX_PARAMS = 52;   // entries per reduce launch (kernel arguments < 4 KiB)
+constexpr int VR_MAX_PARAMS = 44;   // entries per reduce launch (kernel arguments < 4 KiB)
 constexpr int VS_MAX_PARAMS = 64;   // entries per clipped-sum launch
 
 struct VecParam {
@@ -163,13 +163,16 @@ struct VecParam {
   int64_t ldx, ldg;
   int32_t d;            // features
   int32_t mode;         // VEC_GRAD: per-example gradient; VEC_SQ: sum of squares only
-  float* grad;          // VEC_GRAD: [B, d] per-example gradients
+  float* grad;          // VEC_GRAD: [B, d] per-example gradients (of X * G, or of G)
+  float* grad2;         // VEC_GRAD with X: [B, d] sums of G as well (a LayerNorm bias), or null
+  int32_t tsplit;       // row ranges per feature chunk (VEC_SQ; 1 for VEC_GRAD)
+  int32_t trows;        // rows per range
   uint32_t item_begin;  // first item of this entry among an example's items
   int32_t slot_begin;   // first partial slot of this entry in an example's row
 };
 
 // Items example-major: example b owns [b * per_ex, (b + 1) * per_ex), one per
-// (entry, feature chunk of 64 lanes x 16 bytes).
+// (entry, feature chunk of 64 lanes x 16 bytes, row range).
 struct VecArgs {
   VecParam P[VR_MAX_PARAMS];
   int32_t n_params;

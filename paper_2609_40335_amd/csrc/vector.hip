@@ -12,10 +12,12 @@
 //
 // vec_reduce_kernel streams the token rows once: work item = (parameter,
 // example, chunk of 64 lanes x 16 bytes of features); four waves take every
-// fourth row each, with four rows' loads in flight per wave; the per-lane
+// fourth row each, with two rows' loads in flight per wave; the per-lane
 // partial sums meet in LDS. VEC_GRAD writes the example's gradient chunk
-// and the chunk's squared norm; VEC_SQ (the position table) only the sum
-// of the squared elements. Items are numbered example-major, as in the Gram
+// and the chunk's squared norm; a LayerNorm's gain and bias, which share G,
+// take one pass (the bias's plain sum rides along as a second output).
+// VEC_SQ (the position table) only sums the squared elements, so its items
+// also split the example's rows (a scalar partial per row range). Items are numbered example-major, as in the Gram
 // kernel, so each XCD's contiguous item range holds whole examples.
 //
 // vec_sum_kernel and pos_sum_kernel form the clipped sums sum_i c_i g_i of
@@ -28,7 +30,9 @@ namespace dpg {
 
 constexpr int VR_THREADS = 256;
 constexpr int VR_WAVES = VR_THREADS / WAVE;
-constexpr int VR_UNROLL = 4;  // rows in flight per wave
+// Rows in flight per wave: two measured faster than four or eight (fewer
+// requests pending at once per CU), with four or eight waves per workgroup.
+constexpr int VR_UNROLL = 2;
 
 template <int DT, bool VEC>
 __device__ __forceinline__ void widen(const u32x4& v, float (&x)[DT == DT_BF16 ? 8 : 4]) {
@@ -58,7 +62,9 @@ __global__ __launch_bounds__(VR_THREADS) void vec_reduce_kernel(VecArgs args) {
   int p = 0;
   while (p + 1 < a.n_params && rel >= a.P[p + 1].item_begin) ++p;
   const VecParam& P = a.P[p];
-  const int fc = (int)(rel - P.item_begin);
+  const int fc = (int)((rel - P.item_begin) / (uint32_t)P.tsplit);
+  const int tc = (int)((rel - P.item_begin) - (uint32_t)fc * P.tsplit);
+  const int t_end = min(a.T, (tc + 1) * P.trows);
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t col = (int64_t)fc * WAVE * EPC + lane * EPC;
@@ -72,18 +78,21 @@ __global__ __launch_bounds__(VR_THREADS) void vec_reduce_kernel(VecArgs args) {
   const uint32_t g0 = (uint32_t)(((int64_t)b * a.T * P.ldg + col) * ES);
   const uint32_t x0 = (uint32_t)(((int64_t)b * a.T * (has_x ? P.ldx : 0) + col) * ES);
 
-  float acc[EPC];
+  // acc: sum of x * g (or of g, or of g * g); acc2: the plain sum of g when a
+  // LayerNorm's bias shares this entry's G (grad2 set).
+  const bool two = P.grad2 != nullptr;
+  float acc[EPC], acc2[EPC];
 #pragma unroll
-  for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
+  for (int e = 0; e < EPC; ++e) acc[e] = acc2[e] = 0.f;
   const bool live = col < P.d;  // a chunk wholly past d loads nothing
   if (live) {
-    for (int t0 = w; t0 < a.T; t0 += VR_WAVES * VR_UNROLL) {
+    for (int t0 = tc * P.trows + w; t0 < t_end; t0 += VR_WAVES * VR_UNROLL) {
       u32x4 gv[VR_UNROLL], xv[VR_UNROLL];
 #pragma unroll
       for (int u = 0; u < VR_UNROLL; ++u) {
         const int t = t0 + u * VR_WAVES;
-        // Rows past the example (t >= T) and elements past d read as zero.
-        const bool in = t < a.T;
+        // Rows past this item's rows and elements past d read as zero.
+        const bool in = t < t_end;
         const uint32_t so = in ? (uint32_t)t * ldg_b : 0u;
         gv[u] = in ? buf_chunk<DT, VEC, true>(rg, g0, so, col, P.d) : u32x4{0u, 0u, 0u, 0u};
         if (has_x && P.mode == VEC_GRAD) {
@@ -103,6 +112,10 @@ __global__ __launch_bounds__(VR_THREADS) void vec_reduce_kernel(VecArgs args) {
           widen<DT, VEC>(xv[u], x);
 #pragma unroll
           for (int e = 0; e < EPC; ++e) acc[e] += x[e] * g[e];
+          if (two) {
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) acc2[e] += g[e];
+          }
         } else {
 #pragma unroll
           for (int e = 0; e < EPC; ++e) acc[e] += g[e];
@@ -111,11 +124,11 @@ __global__ __launch_bounds__(VR_THREADS) void vec_reduce_kernel(VecArgs args) {
     }
   }
   // The four waves' partial sums, added in wave order by wave 0.
+  float sq = 0.f;
 #pragma unroll
   for (int e = 0; e < EPC; ++e) part[w][lane * EPC + e] = acc[e];
   __syncthreads();
   if (w == 0) {
-    float sq = 0.f;
 #pragma unroll
     for (int e = 0; e < EPC; ++e) {
       float v = part[0][lane * EPC + e];
@@ -128,8 +141,26 @@ __global__ __launch_bounds__(VR_THREADS) void vec_reduce_kernel(VecArgs args) {
         if (col + e < P.d) P.grad[(int64_t)b * P.d + col + e] = v;
       }
     }
+  }
+  if (two) {
+    __syncthreads();  // wave 0 is done reading the first sums
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) part[w][lane * EPC + e] = acc2[e];
+    __syncthreads();
+    if (w == 0) {
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) {
+        float v = part[0][lane * EPC + e];
+#pragma unroll
+        for (int q = 1; q < VR_WAVES; ++q) v += part[q][lane * EPC + e];
+        sq += v * v;
+        if (col + e < P.d) P.grad2[(int64_t)b * P.d + col + e] = v;
+      }
+    }
+  }
+  if (w == 0) {
     sq = wave_sum(sq);
-    if (lane == 0) a.ws[(int64_t)b * a.slots + P.slot_begin + fc] = sq;
+    if (lane == 0) a.ws[(int64_t)b * a.slots + P.slot_begin + fc * P.tsplit + tc] = sq;
   }
 }
 
@@ -147,13 +178,32 @@ __global__ __launch_bounds__(256) void vec_sum_kernel(VecSumArgs a) {
   }
   const VecSumParam& P = a.P[lo];
   const int64_t f = 4 * (int64_t)(q - P.quad_begin);
+  // Examples in order; eight examples' loads are issued before their
+  // products are added, so the loop is not one memory round trip per example.
   float s[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int i = 0; i < a.B; ++i) {
-    const float ci = a.c[i];
-    const float* g = P.grad + (int64_t)i * P.d + f;
+  const bool vec4 = (P.d & 3) == 0 && (((uintptr_t)P.grad) & 15) == 0;
+  constexpr int U = 8;
+  for (int i0 = 0; i0 < a.B; i0 += U) {
+    f32x4 g[U];
+    float ci[U];
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
-      if (f + k < P.d) s[k] += ci * g[k];
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + u;
+      ci[u] = i < a.B ? a.c[i] : 0.f;
+      const float* gp = P.grad + (int64_t)i * P.d + f;
+      if (i >= a.B) {
+        g[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      } else if (vec4) {
+        g[u] = *(const f32x4*)gp;
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) g[u][k] = f + k < P.d ? gp[k] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) s[k] += ci[u] * g[u][k];
   }
   float z[4] = {0.f, 0.f, 0.f, 0.f};
   if (a.noise) gauss4((uint64_t)f >> 2, a.seed, P.tensor_id, a.step, z);
@@ -179,20 +229,48 @@ __global__ __launch_bounds__(256) void pos_sum_kernel(PosSumArgs a) {
   const int t = (int)(q / qpr);
   const int64_t f = 4 * (q - (int64_t)t * qpr);
   float s[4] = {0.f, 0.f, 0.f, 0.f};
+  constexpr int ES = DT == DT_BF16 ? 2 : 4;
+  const bool vec4 = f + 4 <= a.d && (a.lde & 3) == 0 && (((uintptr_t)a.E) & (4 * ES - 1)) == 0;
   if (t < a.T) {
-    for (int i = 0; i < a.B; ++i) {
-      const float ci = a.c[i];
-      const int64_t row = (int64_t)i * a.T + t;
+    constexpr int U = 8;  // examples whose loads are in flight together
+    for (int i0 = 0; i0 < a.B; i0 += U) {
+      float e[U][4], ci[U];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        if (f + k >= a.d) break;
-        float e;
-        if constexpr (DT == DT_BF16)
-          e = bf16_to_f32(((const uint16_t*)a.E)[row * a.lde + f + k]);
-        else
-          e = ((const float*)a.E)[row * a.lde + f + k];
-        s[k] += ci * e;
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u;
+        ci[u] = i < a.B ? a.c[i] : 0.f;
+        const int64_t at = ((int64_t)i * a.T + t) * a.lde + f;  // element (i, t, f)
+        if (i >= a.B) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) e[u][k] = 0.f;
+        } else if (vec4) {  // the 4 elements in one 8- (bf16) or 16-byte (fp32) load
+          if constexpr (DT == DT_BF16) {
+            const uint2 w = *(const uint2*)((const uint16_t*)a.E + at);
+            e[u][0] = __uint_as_float(w.x << 16); e[u][1] = __uint_as_float(w.x & 0xFFFF0000u);
+            e[u][2] = __uint_as_float(w.y << 16); e[u][3] = __uint_as_float(w.y & 0xFFFF0000u);
+          } else {
+            const f32x4 w = *(const f32x4*)((const float*)a.E + at);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) e[u][k] = w[k];
+          }
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            if (f + k < a.d) {
+              if constexpr (DT == DT_BF16)
+                e[u][k] = bf16_to_f32(((const uint16_t*)a.E)[at + k]);
+              else
+                e[u][k] = ((const float*)a.E)[at + k];
+            } else {
+              e[u][k] = 0.f;
+            }
+          }
+        }
       }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) s[k] += ci[u] * e[u][k];
     }
   }
   float* o = a.out + (int64_t)t * a.ldo + f;

@@ -104,6 +104,31 @@ def test_vector_grads_grouped_mixed(dp):
     assert rel(host(n2), norm_ref).max() <= TOL["bf16"]
 
 
+def test_vector_grads_layernorm_pairs(dp):
+    """A gain and a bias on one G buffer take one fused pass; listed in either
+    order, next to a bias on another buffer and a gain whose bias differs in
+    width (not fused)."""
+    B, T = 3, 45
+    G1 = gen.draw(120, 1, (B, T, 768), 1e-2, "bf16")
+    X1 = gen.draw(120, 2, (B, T, 768), 1.0, "bf16")
+    G2 = gen.draw(121, 1, (B, T, 136), 1e-2, "bf16")
+    X2 = gen.draw(121, 2, (B, T, 136), 1.0, "bf16")
+    g1, x1, g2, x2 = dev(G1, "bf16"), dev(X1, "bf16"), dev(G2, "bf16"), dev(X2, "bf16")
+    params = [(None, g1), (x2, g2), (x1, g1), (None, g2[:, :, :100])]
+    grads = [torch.empty(B, p[1].shape[2], device="cuda") for p in params]
+    n2 = torch.zeros(B, device="cuda")
+    dp.dp_vector_grads_grouped(params, grads, n2)
+    norm = np.zeros(B)
+    for (X, G), g, Xh, Gh in zip(params, grads, [None, X2, X1, None],
+                                 [G1, G2, G1, G2[:, :, :100]]):
+        Gd = O.decode(Gh, "bf16")
+        Xd = None if Xh is None else O.decode(Xh, "bf16")
+        ref = np.stack([O.vector_grad(None if Xd is None else Xd[i], Gd[i]) for i in range(B)])
+        assert fro_rel(host(g), ref) <= TOL["bf16"]
+        norm += (ref * ref).sum(axis=1)
+    assert rel(host(n2), norm).max() <= TOL["bf16"]
+
+
 def test_vector_clipped_sum_noised(dp):
     """outs = (prior + sum_i c_i g_i + sigma C z) / B against the oracle's
     add_noise with the same stream; widths not multiples of 4."""
@@ -213,7 +238,13 @@ def test_full_size_gpt2_vectors(dp):
     wl = gen.make_workload("gpt2-step", full_params=True)
     B, h = wl.B, wl.head
     _say(f"full-size vectors: {len(wl.vectors)} parameters, B={B}, T={wl.T}")
-    vg = dp.VectorGroup([(None if v.X is None else dev(v.X), dev(v.G)) for v in wl.vectors])
+    bufs = {}
+
+    def once(a):  # one device buffer per host array: LayerNorm gain/bias pairs fuse
+        if id(a) not in bufs:
+            bufs[id(a)] = dev(a)
+        return bufs[id(a)]
+    vg = dp.VectorGroup([(None if v.X is None else dev(v.X), once(v.G)) for v in wl.vectors])
     n2 = torch.zeros(B, device="cuda")
     vg.grads_and_norm(n2)
     dE = dev(h.dE)

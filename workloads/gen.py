@@ -223,7 +223,7 @@ class Workload:
         return n
 
 
-CONFIG_NAMES = ("c1", "c1-tied", "c2", "c3", "c4", "c5", "gpt2-step")
+CONFIG_NAMES = ("c1", "c1-tied", "c2", "c3", "c4", "c5", "gpt2-step", "gpt2-full")
 
 _DEFAULTS = {
     # name: (dtype, B, T, n_blocks, head kind, description)
@@ -241,6 +241,9 @@ _DEFAULTS = {
            "long-sequence GPT-2-small untied step: 12 blocks + head + E_in, B=16 T=1024, bf16"),
     "gpt2-step": ("bf16", 32, 128, 12, "tied",
                   "GPT-2-small tied step: 12 blocks + tied V=50257 head, B=32 T=128, bf16"),
+    "gpt2-full": ("bf16", 32, 128, 12, "tied",
+                  "GPT-2-small tied step, every parameter (weights, biases, LayerNorms, "
+                  "position table, tied embedding): 124,439,808 coordinates, B=32 T=128, bf16"),
 }
 
 
@@ -261,6 +264,7 @@ def make_workload(name: str, seed: int = 0, *, B: Optional[int] = None,
     if name not in _DEFAULTS:
         raise KeyError(f"unknown workload {name!r}; choose from {CONFIG_NAMES}")
     dtype, B0, T0, nb0, head_kind, desc = _DEFAULTS[name]
+    full_params = full_params or name == "gpt2-full"
     B = B0 if B is None else int(B)
     T = T0 if T is None else int(T)
     if B <= 0 or T <= 0:
