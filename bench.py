@@ -9,11 +9,13 @@ One step is the whole hot path on one batch, through the C ABI:
   2. input-embedding norm and token buckets
   3. tied cross term folded in as + 2 <g_in, g_out> (eq. 11, eq. 13)
   4. clip factors (eq. 2, eq. 7)
-  5. the input-embedding part of the tied gradient (sorted segment sums)
-  6. clipped sums of all linears and of the head (one grouped GEMM, K = B*T),
-     the head accumulating onto the tied embedding gradient, with Gaussian
-     noise and the division by B fused into the GEMM's store (eq. 3); one
-     generator stream per parameter tensor
+  5. clipped sums of all linears and of the head (one grouped GEMM, K = B*T),
+     with Gaussian noise and the division by B fused into the GEMM's store
+     (eq. 3); one generator stream per parameter tensor
+  6. the input-embedding part of the tied gradient (sorted segment sums)
+     added onto the matrix the head's tiles wrote; sums that do not read the
+     GEMM's outputs (an untied embedding's, the vectors', the position
+     table's) run on a second stream beside the GEMM
 With every parameter (--workload gpt2-full), the biases, LayerNorm gains and
 biases and the position table join: their per-example gradients and norms
 after the weight norms, their noised clipped sums after the GEMM.
@@ -86,7 +88,10 @@ class Step:
     def __init__(self, wl, dp, torch):
         self.wl, self.dp, self.torch = wl, dp, torch
         B, T = wl.B, wl.T
-        dev = lambda a: torch.from_numpy(a.view("int16")).view(torch.bfloat16).cuda()
+        def dev(a):  # bf16 bit patterns or fp32 values
+            if a.dtype.kind == "u":
+                return torch.from_numpy(a.view("int16")).view(torch.bfloat16).cuda()
+            return torch.from_numpy(a).cuda()
         self.lin = [(dev(l.A), dev(l.G)) for l in wl.linears]
         h = wl.head
         self.h = h
@@ -145,7 +150,6 @@ class Step:
         assert off == self.n_coords
         self.norm_layers = norm_layers
         self.norm_group = dp.LinearGroup(norm_layers)
-        self.sum_group = dp.LinearGroup(sum_layers, sum_outs) if sum_layers else None
         # Noise generator ids per parameter tensor, as in the oracle's step:
         # linear l -> l, the input embedding (or tied matrix) -> L, an untied
         # head -> L + 1. Every GEMM-shaped output is written once with its
@@ -158,6 +162,19 @@ class Step:
         if h is not None and h.H is not None:
             self.sum_tids.append(L if h.tied else L + 1)
         self.e_tid = L
+        # One grouped launch for every GEMM-shaped clipped sum (split in two, the
+        # second launch waits for the first to drain and costs more than any
+        # work it lets overlap). The sums that do not read the GEMM's outputs
+        # (an untied embedding's noise and sum, the vector and position sums)
+        # run on a second stream (default priority) beside it; a tied
+        # embedding sum adds onto the matrix the head's tiles write, so it
+        # follows the GEMM on the main stream.
+        self.sum_groups = [(dp.LinearGroup(sum_layers, sum_outs), list(self.sum_tids))] \
+            if sum_layers else []
+        side_work = (h is not None and not self.tied) or bool(wl.vectors) or bool(wl.n_pos)
+        self.side = torch.cuda.Stream() if side_work else None
+        self.ev_clip = torch.cuda.Event()
+        self.ev_side = torch.cuda.Event()
         # after the weight matrices (and an untied head): the vectors, then the position table
         t0 = L + (2 if (h is not None and h.H is not None and not h.tied) else 1)
         self.vec_tids = list(range(t0, t0 + len(wl.vectors)))
@@ -194,29 +211,36 @@ class Step:
             mark("position_norm")
         dp.dp_clip_factors_scaled(self.n2, wl.C, 1.0 / wl.B, self.c_b, c=self.c)
         mark("clip")
-        # clipped sums of every GEMM-shaped tensor with the Gaussian mechanism
-        # fused into their store (eq. 3): (S + sigma C z) / B
-        if self.sum_group is not None:
-            self.sum_group.clipped_sum_noised(self.c, self.sum_tids, wl.sigma, wl.C, wl.B,
-                                              seed=1234, step=self.step_id)
+        # clipped sums with the Gaussian mechanism fused into their store
+        # (eq. 3): (S + sigma C z) / B
+        main = self.torch.cuda.current_stream()
+        kw = dict(seed=1234, step=self.step_id)
+        if self.side is not None:
+            self.ev_clip.record(main)
+            self.side.wait_event(self.ev_clip)
+            with self.torch.cuda.stream(self.side):
+                if h is not None and not self.tied:
+                    dp.dp_noise_fill(self.E, wl.sigma, wl.C, wl.B, tensor_id=self.e_tid, **kw)
+                    dp.dp_clipped_grad_sum(None, self.dE, self.c_b, self.E, ids=self.ids, V=h.V,
+                                           accumulate=True)
+                if self.vg is not None:
+                    self.vg.clipped_sum_noised(self.c, self.vec_outs, self.vec_tids, wl.sigma,
+                                               wl.C, wl.B, **kw)
+                if self.P is not None:
+                    dp.dp_clipped_grad_sum_positional_noised(self.dE, self.c, self.P,
+                                                             self.pos_tid, wl.sigma, wl.C, wl.B,
+                                                             **kw)
+            self.ev_side.record(self.side)
+        for grp, tids in self.sum_groups:
+            grp.clipped_sum_noised(self.c, tids, wl.sigma, wl.C, wl.B, **kw)
             mark("clipped_sum_noise")
-        if h is not None:
-            if not self.tied:
-                dp.dp_noise_fill(self.E, wl.sigma, wl.C, wl.B, seed=1234, tensor_id=self.e_tid,
-                                 step=self.step_id)
-                mark("embedding_noise")
+        if h is not None and self.tied:
             dp.dp_clipped_grad_sum(None, self.dE, self.c_b, self.E, ids=self.ids, V=h.V,
                                    accumulate=True)
             mark("embedding_sum")
-        if self.vg is not None:
-            self.vg.clipped_sum_noised(self.c, self.vec_outs, self.vec_tids, wl.sigma, wl.C, wl.B,
-                                       seed=1234, step=self.step_id)
-            mark("vector_sums")
-        if self.P is not None:
-            dp.dp_clipped_grad_sum_positional_noised(self.dE, self.c, self.P, self.pos_tid,
-                                                     wl.sigma, wl.C, wl.B, seed=1234,
-                                                     step=self.step_id)
-            mark("position_sum")
+        if self.side is not None:
+            main.wait_event(self.ev_side)
+            mark("side_sums_join")
         self.step_id += 1
 
 
