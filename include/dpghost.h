@@ -221,6 +221,27 @@ dp_status_t dp_clipped_grad_sum_noised_grouped(const dp_linear_t* layers, float*
                                                int B_norm, uint64_t seed, uint64_t step,
                                                void* stream);
 
+/* The same with a caller-owned workspace of at least
+ * dp_clipped_grad_sum_noised_grouped_workspace(...) bytes (a NULL workspace
+ * of 0 bytes gives the call above). Where a launch's last round of 256 x 256
+ * output tiles would keep at most half of the compute units busy (bf16,
+ * 16-byte rows, T a multiple of 32), each of its tiles is computed as 2-8
+ * consecutive K ranges on separate compute units; the fp32 partial tiles go
+ * to the workspace and are added in order before the prior and the noise, so
+ * results differ from the call above by fp32 rounding only. The workspace
+ * is dead after the call's kernels finish. */
+size_t dp_clipped_grad_sum_noised_grouped_workspace(const dp_linear_t* layers, int n_layers,
+                                                    int B, int T, dp_dtype_t dt,
+                                                    int transpose_out);
+dp_status_t dp_clipped_grad_sum_noised_grouped_ws(const dp_linear_t* layers, float* const* outs,
+                                                  const uint64_t* tensor_ids,
+                                                  const int32_t* accumulate, int n_layers,
+                                                  const float* c, int B, int T, dp_dtype_t dt,
+                                                  int transpose_out, float sigma, float C,
+                                                  int B_norm, uint64_t seed, uint64_t step,
+                                                  void* workspace, size_t workspace_bytes,
+                                                  void* stream);
+
 /* ---------------------------------------------------------------------
  * Gaussian mechanism (eq. 3): grad[j] = (grad[j] + sigma*C*z_j) / B_norm
  * (no division when B_norm = 0), in place, for j < n; the division is a

@@ -272,44 +272,72 @@ dp_status_t run_gram(const NormPlan& p, int B, int T, dp_dtype_t dt, float* ws, 
   return DP_OK;
 }
 
-// mode 0: clipped sum (c, out); mode 1: direct norm (ws, slots)
-dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int T, dp_dtype_t dt,
-                     const float* c, float* ws, int64_t slots, int transpose, const NoiseCfg& nz,
-                     hipStream_t s) {
+// The launches of a GEMM plan: entries with 16-byte rows first, then the
+// others, at most GM_MAX_LAYERS per launch.
+std::vector<std::pair<bool, std::vector<const GemmEntry*>>> gemm_launches(
+    const std::vector<GemmEntry>& entries) {
+  std::vector<std::pair<bool, std::vector<const GemmEntry*>>> out;
   for (int pass = 0; pass < 2; ++pass) {
     const bool vec = pass == 0;
     std::vector<const GemmEntry*> sel;
     for (const auto& e : entries)
       if (e.vec == vec) sel.push_back(&e);
     for (size_t i0 = 0; i0 < sel.size(); i0 += dpg::GM_MAX_LAYERS) {
-      dpg::GemmArgs a{};
-      a.B = B; a.T = T; a.c = c; a.ws = ws; a.slots = (int32_t)slots;
-      a.transpose = transpose;
-      a.noise = nz.on ? 1 : 0;
-      a.sigma_c = nz.sigma_c; a.inv_b = nz.inv_b; a.step = nz.step; a.seed = nz.seed;
-      uint64_t items = 0;
       const size_t n = std::min(sel.size() - i0, (size_t)dpg::GM_MAX_LAYERS);
-      for (size_t j = 0; j < n; ++j) {
-        const GemmEntry& e = *sel[i0 + j];
-        dpg::GemmLayer& L = a.L[j];
-        L.X = e.X; L.Y = e.Y; L.ldx = e.ldx; L.ldy = e.ldy;
-        L.M = e.M; L.N = e.N;
-        L.tm = (uint16_t)e.tm; L.tn = (uint16_t)e.tn;
-        L.tile_begin = (uint32_t)items;
-        if (mode == 0) L.tensor_id = e.tensor_id;
-        else L.slot_begin = e.slot_begin;
-        L.accumulate = e.acc;
-        L.out = e.out; L.ldo = e.ldo;
-        items += (uint64_t)e.tm * e.tn * (mode == 1 ? (uint64_t)B : 1ull);
-      }
-      if (items > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many work items");
-      a.n_layers = (int32_t)n;
-      a.n_items = (uint32_t)items;
-      hipError_t e = mode == 0 ? dpg::launch_clipped_sum(a, kdt(dt), vec, s)
-                               : dpg::launch_direct_norm(a, kdt(dt), vec, s);
-      dp_status_t st = hip_status(e, mode == 0 ? "clipped_sum launch" : "direct_norm launch");
-      if (st != DP_OK) return st;
+      out.emplace_back(vec, std::vector<const GemmEntry*>(sel.begin() + i0, sel.begin() + i0 + n));
     }
+  }
+  return out;
+}
+
+// Bytes of partial tiles the split tail of a clipped-sum plan needs (the
+// largest over its launches, which run one after another).
+size_t sum_split_bytes(const std::vector<GemmEntry>& entries, int B, int T, dp_dtype_t dt) {
+  size_t need = 0;
+  for (const auto& [vec, sel] : gemm_launches(entries)) {
+    if (!dpg::dl_sum_applies(kdt(dt), vec, T, B)) continue;
+    uint64_t tiles = 0;
+    for (const GemmEntry* e : sel) tiles += (uint64_t)e->tm * e->tn;
+    const dpg::TailSplit t = dpg::tail_split(tiles, (int)((int64_t)B * T / dpg::DL_SUM_BK),
+                                             device_cus());
+    need = std::max(need, (size_t)t.n_split * t.ks * dpg::SPLIT_TILE_BYTES);
+  }
+  return need;
+}
+
+// mode 0: clipped sum (c, out); mode 1: direct norm (ws, slots). A clipped sum
+// given `part` (part_bytes) splits the tail of its direct-load launches.
+dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int T, dp_dtype_t dt,
+                     const float* c, float* ws, int64_t slots, int transpose, const NoiseCfg& nz,
+                     hipStream_t s, float* part = nullptr, size_t part_bytes = 0) {
+  for (const auto& [vec, sel] : gemm_launches(entries)) {
+    dpg::GemmArgs a{};
+    a.B = B; a.T = T; a.c = c; a.ws = ws; a.slots = (int32_t)slots;
+    a.transpose = transpose;
+    a.noise = nz.on ? 1 : 0;
+    a.sigma_c = nz.sigma_c; a.inv_b = nz.inv_b; a.step = nz.step; a.seed = nz.seed;
+    a.part = part;
+    uint64_t items = 0;
+    for (size_t j = 0; j < sel.size(); ++j) {
+      const GemmEntry& e = *sel[j];
+      dpg::GemmLayer& L = a.L[j];
+      L.X = e.X; L.Y = e.Y; L.ldx = e.ldx; L.ldy = e.ldy;
+      L.M = e.M; L.N = e.N;
+      L.tm = (uint16_t)e.tm; L.tn = (uint16_t)e.tn;
+      L.tile_begin = (uint32_t)items;
+      if (mode == 0) L.tensor_id = e.tensor_id;
+      else L.slot_begin = e.slot_begin;
+      L.accumulate = e.acc;
+      L.out = e.out; L.ldo = e.ldo;
+      items += (uint64_t)e.tm * e.tn * (mode == 1 ? (uint64_t)B : 1ull);
+    }
+    if (items > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many work items");
+    a.n_layers = (int32_t)sel.size();
+    a.n_items = (uint32_t)items;
+    hipError_t e = mode == 0 ? dpg::launch_clipped_sum(a, kdt(dt), vec, device_cus(), part_bytes, s)
+                             : dpg::launch_direct_norm(a, kdt(dt), vec, s);
+    dp_status_t st = hip_status(e, mode == 0 ? "clipped_sum launch" : "direct_norm launch");
+    if (st != DP_OK) return st;
   }
   return DP_OK;
 }
@@ -630,6 +658,60 @@ dp_status_t dp_clipped_grad_sum_grouped(const dp_linear_t* layers, float* const*
   return run_gemm(entries, 0, B, T, dt, c, nullptr, 0, 0, NoiseCfg{}, as_stream(stream));
 }
 
+static dp_status_t noised_sum_plan(const dp_linear_t* layers, float* const* outs,
+                                   const uint64_t* tensor_ids, const int32_t* accumulate,
+                                   int n_layers, int B, int T, dp_dtype_t dt, int transpose_out,
+                                   std::vector<GemmEntry>& entries) {
+  dp_status_t st = check_layers(layers, n_layers, B, T, dt);
+  if (st != DP_OK) return st;
+  if ((int64_t)B * T > (int64_t(1) << 40)) return fail(DP_EUNSUPPORTED, "B*T too large");
+  for (int i = 0; i < n_layers; ++i) {
+    if (outs && !outs[i]) return fail(DP_EINVAL, "outs[%d] is NULL", i);
+    if (tensor_ids && tensor_ids[i] >> 32)
+      return fail(DP_EINVAL, "tensor_ids[%d] must be < 2^32", i);
+    plan_sum(layers[i], transpose_out, dt, outs ? outs[i] : nullptr, entries);
+    entries.back().acc = accumulate && accumulate[i] ? 1 : 0;
+    entries.back().tensor_id = tensor_ids ? (uint32_t)tensor_ids[i] : 0u;
+  }
+  return DP_OK;
+}
+
+size_t dp_clipped_grad_sum_noised_grouped_workspace(const dp_linear_t* layers, int n_layers,
+                                                    int B, int T, dp_dtype_t dt,
+                                                    int transpose_out) {
+  std::vector<GemmEntry> entries;
+  if (noised_sum_plan(layers, nullptr, nullptr, nullptr, n_layers, B, T, dt, transpose_out,
+                      entries) != DP_OK)
+    return 0;
+  return align_up(sum_split_bytes(entries, B, T, dt));
+}
+
+dp_status_t dp_clipped_grad_sum_noised_grouped_ws(const dp_linear_t* layers, float* const* outs,
+                                                  const uint64_t* tensor_ids,
+                                                  const int32_t* accumulate, int n_layers,
+                                                  const float* c, int B, int T, dp_dtype_t dt,
+                                                  int transpose_out, float sigma, float C,
+                                                  int B_norm, uint64_t seed, uint64_t step,
+                                                  void* workspace, size_t workspace_bytes,
+                                                  void* stream) {
+  if (!outs || !c || !tensor_ids) return fail(DP_EINVAL, "outs, c or tensor_ids is NULL");
+  std::vector<GemmEntry> entries;
+  dp_status_t st = noised_sum_plan(layers, outs, tensor_ids, accumulate, n_layers, B, T, dt,
+                                   transpose_out, entries);
+  if (st != DP_OK) return st;
+  st = check_noise_args(sigma, C, B_norm, step);
+  if (st != DP_OK) return st;
+  if (workspace_bytes && !workspace) return fail(DP_EINVAL, "workspace is NULL");
+  NoiseCfg nz;
+  nz.on = true;
+  nz.sigma_c = (float)((double)sigma * (double)C);
+  nz.inv_b = B_norm > 0 ? (float)(1.0 / (double)B_norm) : 1.f;
+  nz.seed = seed;
+  nz.step = (uint32_t)step;
+  return run_gemm(entries, 0, B, T, dt, c, nullptr, 0, 0, nz, as_stream(stream),
+                  static_cast<float*>(workspace), workspace ? workspace_bytes : 0);
+}
+
 dp_status_t dp_clipped_grad_sum_noised_grouped(const dp_linear_t* layers, float* const* outs,
                                                const uint64_t* tensor_ids,
                                                const int32_t* accumulate, int n_layers,
@@ -637,29 +719,9 @@ dp_status_t dp_clipped_grad_sum_noised_grouped(const dp_linear_t* layers, float*
                                                int transpose_out, float sigma, float C,
                                                int B_norm, uint64_t seed, uint64_t step,
                                                void* stream) {
-  dp_status_t st = check_layers(layers, n_layers, B, T, dt);
-  if (st != DP_OK) return st;
-  if (!outs || !c || !tensor_ids) return fail(DP_EINVAL, "outs, c or tensor_ids is NULL");
-  if ((int64_t)B * T > (int64_t(1) << 40)) return fail(DP_EUNSUPPORTED, "B*T too large");
-  if (!(sigma >= 0.f) || !std::isfinite(sigma)) return fail(DP_EINVAL, "sigma must be >= 0");
-  if (!(C > 0.f) || !std::isfinite(C)) return fail(DP_EINVAL, "C must be positive and finite");
-  if (B_norm < 0) return fail(DP_EINVAL, "B_norm must be >= 0");
-  if (step >> 32) return fail(DP_EINVAL, "step must be < 2^32");
-  std::vector<GemmEntry> entries;
-  for (int i = 0; i < n_layers; ++i) {
-    if (!outs[i]) return fail(DP_EINVAL, "outs[%d] is NULL", i);
-    if (tensor_ids[i] >> 32) return fail(DP_EINVAL, "tensor_ids[%d] must be < 2^32", i);
-    plan_sum(layers[i], transpose_out, dt, outs[i], entries);
-    entries.back().acc = accumulate && accumulate[i] ? 1 : 0;
-    entries.back().tensor_id = (uint32_t)tensor_ids[i];
-  }
-  NoiseCfg nz;
-  nz.on = true;
-  nz.sigma_c = (float)((double)sigma * (double)C);
-  nz.inv_b = B_norm > 0 ? (float)(1.0 / (double)B_norm) : 1.f;
-  nz.seed = seed;
-  nz.step = (uint32_t)step;
-  return run_gemm(entries, 0, B, T, dt, c, nullptr, 0, 0, nz, as_stream(stream));
+  return dp_clipped_grad_sum_noised_grouped_ws(layers, outs, tensor_ids, accumulate, n_layers, c,
+                                               B, T, dt, transpose_out, sigma, C, B_norm, seed,
+                                               step, nullptr, 0, stream);
 }
 
 dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64_t ldg,

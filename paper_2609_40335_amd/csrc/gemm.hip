@@ -337,6 +337,75 @@ __device__ __forceinline__ void store_tile_rows(const GemmArgs& a, const GemmLay
     }
 }
 
+// A raw 256 x 256 partial tile, row-major, staged through LDS like
+// store_tile_rows (8 lanes write 128 contiguous bytes of a row).
+__device__ __forceinline__ void store_partial(float* dst, int wm, int wn, int lane,
+                                              f32x16 (&acc)[4][2], float* slice) {
+  const int rw = (lane >> 5) * 4, cw = lane & 31, c4 = 4 * (lane & 7);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) slice[(rw + (e >> 2) * 8 + (e & 3)) * EP_LD + cw] = acc[i][j][e];
+      const int mb = wm * 128 + i * 32, nb = wn * 64 + j * 32;
+#pragma unroll
+      for (int it = 0; it < 4; ++it) {
+        const int r = (lane >> 3) + 8 * it;
+        const f32x4 v = *(const f32x4*)(slice + r * EP_LD + c4);
+        __builtin_nontemporal_store(v, (f32x4*)(dst + (mb + r) * GM_BN + nb + c4));
+      }
+    }
+}
+
+// The split tail tiles: one thread per 4 consecutive elements of a row of
+// one tile; the ksplit partials are added in order, then the prior, the
+// noise and the division as in store_tile_rows.
+__global__ __launch_bounds__(256) void split_fixup_kernel(GemmArgs args) {
+  const GemmArgs& a = *(const GemmArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  (void)args;
+  constexpr int QPT = GM_BM * GM_BN / 4;            // float4s per tile
+  const uint32_t t = blockIdx.x / (QPT / 256);      // split tile
+  const int q = (int)(blockIdx.x - t * (QPT / 256)) * 256 + (int)threadIdx.x;
+  const uint32_t tile = a.n_full + t;
+  int l = 0;
+  while (l + 1 < a.n_layers && tile >= a.L[l + 1].tile_begin) ++l;
+  const GemmLayer& L = a.L[l];
+  int mt, nt;
+  tile_of(L, tile - L.tile_begin, mt, nt);
+  const int r = q / (GM_BN / 4), c4 = (q - r * (GM_BN / 4)) * 4;
+  const int64_t m = (int64_t)mt * GM_BM + r, n = (int64_t)nt * GM_BN + c4;
+  if (m >= L.M || n >= L.N) return;
+  f32x4 v = {0.f, 0.f, 0.f, 0.f};
+  const float* src = a.part + (size_t)t * a.ksplit * (GM_BM * GM_BN) + r * GM_BN + c4;
+  for (int k = 0; k < a.ksplit; ++k) v += *(const f32x4*)(src + (size_t)k * (GM_BM * GM_BN));
+  float* p = L.out + m * L.ldo + n;
+  const bool accum = L.accumulate != 0, noise = a.noise != 0;
+  const bool vec = n + 4 <= L.N && (L.N & 3) == 0 && (L.ldo & 3) == 0 &&
+                   (((uintptr_t)L.out) & 15) == 0;
+  if (vec) {
+    if (noise) {
+      float z[4];
+      gauss4(((uint64_t)m * (uint64_t)L.N + (uint64_t)n) >> 2, a.seed, L.tensor_id, a.step, z);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) v[k] += a.sigma_c * z[k];
+    }
+    if (accum) v += *(const f32x4*)p;
+    if (noise) v *= a.inv_b;
+    *(f32x4*)p = v;
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (n + k < L.N) {
+        float x = (accum ? p[k] : 0.f) + v[k];
+        if (noise)
+          x = (x + a.sigma_c * noise_at(a, L.tensor_id, (uint64_t)m * (uint64_t)L.N + n + k)) *
+              a.inv_b;
+        p[k] = x;
+      }
+  }
+}
+
 // Scaling of the clipped sum: SC_NONE (direct norm), SC_STAGE (rows scaled
 // while staged, any T), SC_ACC (every stage lies inside one example, so the
 // fp32 accumulators are rescaled by c_prev / c_next at example boundaries and
@@ -563,12 +632,12 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
 // memory instruction; each is read one example ahead, so that a rescale never
 // waits behind the fragment reads. Scaling is on the fp32 accumulators as in
 // SC_ACC.
-constexpr int DL_BK = 32;                   // k rows per stage
+constexpr int DL_BK = DL_SUM_BK;            // k rows per stage
 constexpr int DL_NS = 4;                    // stages in the ring
 constexpr int DL_ROWB = GM_BM * 2;          // bytes per LDS row (256 bf16)
 constexpr int DL_OPB = DL_BK * DL_ROWB;     // one operand's stage: 16 KB
 constexpr int DL_STB = 2 * DL_OPB;          // one stage: X then Y
-constexpr int DL_MAXB = 4096;               // clip factors held in LDS
+constexpr int DL_MAXB = DL_SUM_MAXB;        // clip factors held in LDS
 constexpr int DL_LOADS = 4;                 // loads per wave per stage
 static_assert(GM_BM == GM_BN, "square tiles");
 static_assert(DL_STB == (GM_THREADS / WAVE) * DL_LOADS * 1024, "one KB per load");
@@ -618,7 +687,17 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
   __shared__ float cs[DL_MAXB];
   lds_char_t* ring = (lds_char_t*)(lds_void_t*)ring_raw;
 
-  const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
+  // Whole tiles come first (spread over the XCDs); the K ranges of the split
+  // tail tiles are dispatched last, in round-robin over the XCDs.
+  uint32_t item;
+  int kc = -1;  // K range of a split tile, or -1
+  if (MODE == MODE_NORM || blockIdx.x < a.n_full) {
+    item = xcd_remap(blockIdx.x, MODE == MODE_NORM ? gridDim.x : a.n_full);
+  } else {
+    const uint32_t j = blockIdx.x - a.n_full;
+    item = a.n_full + j / (uint32_t)a.ksplit;
+    kc = (int)(j - (j / (uint32_t)a.ksplit) * (uint32_t)a.ksplit);
+  }
   int l = 0;
   while (l + 1 < a.n_layers && item >= a.L[l + 1].tile_begin) ++l;
   const GemmLayer& L = a.L[l];
@@ -626,6 +705,11 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
   const int64_t K = (int64_t)a.B * a.T;
   int b = 0;
   int64_t k_begin = 0, k_end = K;
+  if (MODE == MODE_SUM && kc >= 0) {
+    const int64_t per = (K / DL_BK + a.ksplit - 1) / a.ksplit * DL_BK;  // rows per range
+    k_begin = kc * per;
+    k_end = k_begin + per < K ? k_begin + per : K;
+  }
   if constexpr (MODE == MODE_NORM) {
     const uint32_t ntile = (uint32_t)L.tm * (uint32_t)L.tn;
     b = (int)(rel / ntile);
@@ -708,10 +792,16 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
   if constexpr (MODE == MODE_SUM)
     for (int i = tid; i < a.B; i += GM_THREADS) cs[i] = a.c[i];
   const int spe = a.T / DL_BK;  // stages per example
+  // Stage indices below are local to this item's K range, which starts at
+  // global stage gs0, inside example e0 (at its start unless this is a split
+  // range): the first stage is treated as a boundary, where nothing is yet
+  // accumulated.
+  const int gs0 = (int)(k_begin / DL_BK);
+  const int e0 = gs0 / spe;
   float c_acc = 0.f;            // factor of what is accumulated; 0: nothing yet
   float c_nx = 0.f;             // factor of the example that starts at stage s_nx
   bool skip = false;
-  int s_nx = 0, e_nx = 0;       // next example boundary (a stage) and its example
+  int s_nx = 0, e_nx = e0;      // next example boundary (a local stage) and its example
   // Called once per stage, in increasing order, in the memory phase before
   // that stage's MFMAs: at an example boundary, rescales the accumulators by
   // c_prev / c_next and fetches the factor of the example after.
@@ -719,7 +809,7 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
     if (MODE == MODE_SUM && s == s_nx) {
       const float ce = c_nx;
       ++e_nx;
-      s_nx += spe;
+      s_nx = e_nx * spe - gs0;
       if (e_nx < a.B) c_nx = cs[e_nx];
       skip = !(ce != 0.f);
       if (!skip) {
@@ -789,7 +879,7 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
       for (int t = 0; t < DL_LOADS; ++t) issue(p, t);
     wait_vmcnt<DL_LOADS * (DL_NS - 1)>();
     bar();  // stage 0 has landed, the factor table is filled
-    if constexpr (MODE == MODE_SUM) c_nx = cs[0];
+    if constexpr (MODE == MODE_SUM) c_nx = cs[e0];
     rd(0, fr);
     enter(0);
     for (int s = 0; s < nS; ++s) {
@@ -807,7 +897,7 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
       for (int t = 0; t < DL_LOADS; ++t) issue(p, t);
     wait_vmcnt<DL_LOADS * (DL_NS - 2)>();
     bar();
-    if constexpr (MODE == MODE_SUM) c_nx = cs[0];
+    if constexpr (MODE == MODE_SUM) c_nx = cs[e0];
     for (int s = 0; s < nS; ++s) {
       rd_issue(s, s + DL_NS - 1, fr);
       enter(s);
@@ -824,7 +914,13 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[i][j] *= c_acc;
-    if (a.transpose) {
+    if (kc >= 0) {
+      // A split range: its raw partial tile, for the fixup kernel.
+      __syncthreads();
+      float* slice = (float*)ring_raw + w * 32 * EP_LD;
+      store_partial(a.part + ((size_t)(item - a.n_full) * a.ksplit + kc) * (GM_BM * GM_BN),
+                    wm, wn, lane, acc, slice);
+    } else if (a.transpose) {
       store_tile(a, L, m0, n0, wm, wn, lane, acc);
     } else {
       // The ring is free once every wave is past its last read of it.
@@ -877,13 +973,32 @@ static void launch_sc(const GemmArgs& a, int sc, hipStream_t s) {
 }
 
 template <int MODE>
-static hipError_t launch_kt(const GemmArgs& a, int dt, bool vec, hipStream_t s) {
-  if (a.n_items == 0) return hipSuccess;
+static hipError_t launch_kt(const GemmArgs& a0, int dt, bool vec, int cus, size_t part_bytes,
+                            hipStream_t s) {
+  if (a0.n_items == 0) return hipSuccess;
+  GemmArgs a = a0;
+  a.n_full = a.n_items;
+  a.n_split = 0;
+  a.ksplit = 1;
   // The accumulator form needs every K-stage inside one example.
   const int ks = dt == DT_BF16 ? KT<DT_BF16>::KS : KT<DT_F32>::KS;
   const int sc = MODE == MODE_NORM ? SC_NONE : (a.T % ks == 0 ? SC_ACC : SC_STAGE);
   if (dt == DT_BF16 && vec && a.T % DL_BK == 0 && (MODE == MODE_NORM || a.B <= DL_MAXB)) {
-    hipLaunchKernelGGL(dl_gemm_kernel<MODE>, dim3(a.n_items), dim3(GM_THREADS), 0, s, a);
+    uint32_t grid = a.n_items;
+    if (MODE == MODE_SUM && a.part != nullptr) {
+      const TailSplit t = tail_split(a.n_items, (int)((int64_t)a.B * a.T / DL_BK), cus);
+      if (t.n_split > 0 && (size_t)t.n_split * t.ks * SPLIT_TILE_BYTES <= part_bytes) {
+        a.n_full = t.n_full;
+        a.n_split = t.n_split;
+        a.ksplit = t.ks;
+        grid = t.n_full + t.n_split * (uint32_t)t.ks;
+      }
+    }
+    hipLaunchKernelGGL(dl_gemm_kernel<MODE>, dim3(grid), dim3(GM_THREADS), 0, s, a);
+    if (a.n_split > 0) {
+      hipLaunchKernelGGL(split_fixup_kernel, dim3(a.n_split * (GM_BM * GM_BN / 4 / 256)),
+                         dim3(256), 0, s, a);
+    }
     return hipGetLastError();
   }
   if (dt == DT_BF16) {
@@ -896,12 +1011,13 @@ static hipError_t launch_kt(const GemmArgs& a, int dt, bool vec, hipStream_t s) 
   return hipGetLastError();
 }
 
-hipError_t launch_clipped_sum(const GemmArgs& a, int dt, bool vec, hipStream_t s) {
-  return launch_kt<MODE_SUM>(a, dt, vec, s);
+hipError_t launch_clipped_sum(const GemmArgs& a, int dt, bool vec, int cus, size_t part_bytes,
+                              hipStream_t s) {
+  return launch_kt<MODE_SUM>(a, dt, vec, cus, part_bytes, s);
 }
 
 hipError_t launch_direct_norm(const GemmArgs& a, int dt, bool vec, hipStream_t s) {
-  return launch_kt<MODE_NORM>(a, dt, vec, s);
+  return launch_kt<MODE_NORM>(a, dt, vec, 0, 0, s);
 }
 
 }  // namespace dpg

@@ -108,12 +108,56 @@ struct GemmArgs {
   float sigma_c, inv_b;
   uint32_t step;
   uint64_t seed;
+  // Tail split of the clipped sum (direct-load kernel): tiles [0, n_full) are
+  // whole work items; each of the n_split tiles after them is ksplit items
+  // over consecutive K ranges, whose fp32 partial tiles (256 x 256, row-major)
+  // go to part and are added by the fixup kernel. n_full = n_items, ksplit = 1
+  // when nothing is split.
+  uint32_t n_full, n_split;
+  int32_t ksplit;
+  float* part;
 };
 
 static_assert(sizeof(GemmArgs) <= 4096, "kernel arguments must stay within 4 KiB");
 
+// The bf16 direct-load clipped-sum kernel's conditions (16-byte rows, whole
+// 32-row stages per example, the factor table in LDS).
+constexpr int DL_SUM_BK = 32;
+constexpr int DL_SUM_MAXB = 4096;
+inline bool dl_sum_applies(int dt, bool vec, int T, int B) {
+  return dt == DT_BF16 && vec && T % DL_SUM_BK == 0 && B <= DL_SUM_MAXB;
+}
+
+// The last round of a launch of n_tiles equal tiles on `cus` CUs holds
+// r = n_tiles mod cus of them (all of them if n_tiles < cus). When r is at most
+// half the CUs, each of those tiles is split into ks consecutive K ranges of at
+// least 4 stages (ks <= 8, r * ks <= cus), so the round takes about 1/ks of a
+// tile's time.
+struct TailSplit {
+  uint32_t n_full, n_split;
+  int32_t ks;
+};
+inline TailSplit tail_split(uint64_t n_tiles, int k_stages, int cus) {
+  TailSplit t{(uint32_t)n_tiles, 0u, 1};
+  if (cus <= 0 || n_tiles == 0) return t;
+  const uint64_t r = n_tiles % (uint64_t)cus;
+  if (r == 0 || 2 * r > (uint64_t)cus) return t;
+  int ks = (int)((uint64_t)cus / r);
+  ks = ks < 8 ? ks : 8;
+  ks = ks < k_stages / 4 ? ks : k_stages / 4;
+  if (ks < 2) return t;
+  t.n_full = (uint32_t)(n_tiles - r);
+  t.n_split = (uint32_t)r;
+  t.ks = ks;
+  return t;
+}
+constexpr size_t SPLIT_TILE_BYTES = (size_t)GM_BM * GM_BN * 4;  // one fp32 partial tile
+
 // Clipped sum: out (+)= sum_i c_i X_i^T Y_i over all B*T rows (K = B*T).
-hipError_t launch_clipped_sum(const GemmArgs& a, int dt, bool vec, hipStream_t s);
+// With a.part set (and room for the split that tail_split gives on `cus` CUs),
+// the direct-load kernel splits its last round and a fixup kernel follows.
+hipError_t launch_clipped_sum(const GemmArgs& a, int dt, bool vec, int cus, size_t part_bytes,
+                              hipStream_t s);
 // Direct norm: ws[b, slot] = ||tile of X_b^T Y_b||_F^2 for every output tile.
 hipError_t launch_direct_norm(const GemmArgs& a, int dt, bool vec, hipStream_t s);
 

@@ -80,6 +80,12 @@ _SIGS = {
                                             _I, _VP, _I, _I, _I, _I, _F, _F, _I, _U64, _U64, _VP],
                                            _I),
     "dp_add_noise": ([_VP, _I64, _F, _F, _I, _U64, _U64, _U64, _VP], _I),
+    "dp_clipped_grad_sum_noised_grouped_workspace": ([ctypes.POINTER(dp_linear_t), _I, _I, _I, _I,
+                                                      _I], _SZ),
+    "dp_clipped_grad_sum_noised_grouped_ws": ([ctypes.POINTER(dp_linear_t), ctypes.POINTER(_VP),
+                                               ctypes.POINTER(_U64), ctypes.POINTER(ctypes.c_int32),
+                                               _I, _VP, _I, _I, _I, _I, _F, _F, _I, _U64, _U64,
+                                               _VP, _SZ, _VP], _I),
     "dp_clip_factors_scaled": ([_VP, _I, _F, _F, _VP, _VP, _VP], _I),
     "dp_noise_fill": ([_VP, _I64, _F, _F, _I, _U64, _U64, _U64, _VP], _I),
     "dp_vector_grads_workspace": ([ctypes.POINTER(dp_vector_t), _I, _I, _I, _I], _SZ),
@@ -314,7 +320,8 @@ def dp_clipped_grad_sum_noised_grouped(layers: Sequence, outs: Sequence[torch.Te
                                        transpose_out: bool = False, stream=None) -> None:
     """Clipped sums with the Gaussian mechanism fused into their store; the
     noise each output gets is the one dp_add_noise(outs[l], ..., tensor_ids[l],
-    step) would add. ``accumulate`` is a bool or one bool per layer."""
+    step) would add. ``accumulate`` is a bool or one bool per layer. (No
+    workspace: the last round of tiles is not split; LinearGroup passes one.)"""
     L = lib()
     descs = [_layer(l[0], l[1]) for l in layers]
     arr = (dp_linear_t * len(descs))(*descs)
@@ -541,9 +548,19 @@ class LinearGroup:
             self._noise_key = key
             self._noise_arr = _noise_arrays(self.n, tensor_ids, accumulate)
         tids, acc = self._noise_arr
-        _check(lib().dp_clipped_grad_sum_noised_grouped(self.descs, self.outs, tids, acc, self.n,
-                                                        c.data_ptr(), self.B, self.T, self.dt,
-                                                        int(transpose_out), float(sigma),
-                                                        float(C), int(B_norm), int(seed),
-                                                        int(step), _stream(stream)),
-               "dp_clipped_grad_sum_noised_grouped")
+        L = lib()
+        if getattr(self, "_split_ws_key", None) != bool(transpose_out):
+            self._split_ws_key = bool(transpose_out)
+            nbytes = L.dp_clipped_grad_sum_noised_grouped_workspace(self.descs, self.n, self.B,
+                                                                    self.T, self.dt,
+                                                                    int(transpose_out))
+            self._split_ws = _ws(nbytes, self.ws.device) if nbytes else None
+        ws = self._split_ws
+        _check(L.dp_clipped_grad_sum_noised_grouped_ws(self.descs, self.outs, tids, acc, self.n,
+                                                       c.data_ptr(), self.B, self.T, self.dt,
+                                                       int(transpose_out), float(sigma), float(C),
+                                                       int(B_norm), int(seed), int(step),
+                                                       None if ws is None else ws.data_ptr(),
+                                                       0 if ws is None else ws.numel(),
+                                                       _stream(stream)),
+               "dp_clipped_grad_sum_noised_grouped_ws")

@@ -296,3 +296,27 @@ def test_vector_and_positional_validation(L):
     assert L.dp_clipped_grad_sum_positional_noised(1 << 21, 768, 1 << 22, 4, 16, 768, D.DP_BF16,
                                                    1 << 23, 1024, 768, 1 << 32, 0, 1.0, 1.0, 4,
                                                    0, 0, None) == EINVAL  # tensor_id >= 2^32
+
+
+def test_split_tail_workspace(L):
+    """The clipped sum's split tail: 95 of GPT-2's 1887 tiles (256 CUs) split
+    in 2 K ranges; a launch of whole rounds, or fp32, needs nothing."""
+    body = [(768, 2304), (768, 768), (768, 3072), (3072, 768)] * 12
+    ptr = [1 << 30]
+
+    def lin(di, do):
+        ptr[0] += 1 << 26
+        return D.dp_linear_t(ptr[0], di, di, ptr[0] + (1 << 25), do, do, 0)
+    # the head as the benchmark passes it: Gz rows padded to 50304 (16-byte aligned)
+    descs = [lin(di, do) for di, do in body] + [D.dp_linear_t(1 << 40, 50304, 50257,
+                                                              (1 << 40) + (1 << 35), 768, 768, 0)]
+    arr = (D.dp_linear_t * len(descs))(*descs)
+    ws = L.dp_clipped_grad_sum_noised_grouped_workspace(arr, len(descs), 32, 128, D.DP_BF16, 0)
+    assert ws == 95 * 2 * 256 * 256 * 4
+    # 48 body layers: 1296 tiles, 16 in the last round -> 8 K ranges each
+    ws = L.dp_clipped_grad_sum_noised_grouped_workspace(arr, 48, 32, 128, D.DP_BF16, 0)
+    assert ws == 16 * 8 * 256 * 256 * 4
+    assert L.dp_clipped_grad_sum_noised_grouped_workspace(arr, 49, 32, 128, D.DP_F32, 0) == 0
+    assert L.dp_clipped_grad_sum_noised_grouped_workspace(arr, 49, 32, 100, D.DP_BF16, 0) == 0
+    # K = 64 rows = 2 stages: too short to split
+    assert L.dp_clipped_grad_sum_noised_grouped_workspace(arr, 1, 2, 32, D.DP_BF16, 0) == 0

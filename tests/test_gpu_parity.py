@@ -376,6 +376,48 @@ def test_clipped_sum_noised(dp, case, transpose):
         assert fro_rel(got, host(plain[l])) <= (1e-5 if exact else 2e-3)
 
 
+SPLIT_CASES = [
+    # B, T, [(d_in, d_out), ...], c (None: linspace); widths multiples of 8 (16-byte rows)
+    (4, 64, [(520, 304)], None),                           # 6 ragged tiles, all split
+    (4, 64, [(2304, 3072)] * 3, None),                     # 324 tiles: 256 whole + 68 split
+    (5, 96, [(768, 768), (296, 1000)], [0.5, 0.0, 1.0, 0.25, 0.7]),  # ranges start mid-example
+]
+
+
+@pytest.mark.parametrize("case", SPLIT_CASES, ids=lambda c: f"B{c[0]}-T{c[1]}-{len(c[2])}")
+def test_clipped_sum_split_tail(dp, case):
+    """The workspace form splits the last round's tiles along K; its result
+    equals the unsplit call's up to fp32 rounding, and the oracle's."""
+    B, T, shapes, cl = case
+    sigma, C, seed, step = 0.5, 1.1, 77, 4
+    c = np.asarray(cl if cl is not None else np.linspace(0.3, 1.0, B), np.float32)
+    layers, refs, priors = [], [], []
+    for l, (di, do) in enumerate(shapes):
+        A, G = _layer_inputs("bf16", B, T, di, do, seed=130 + l)
+        layers.append((dev(A, "bf16"), dev(G, "bf16")))
+        S = O.clipped_sum_linear(O.decode(A, "bf16"), O.decode(G, "bf16"), c.astype(np.float64))
+        prior = gen.draw(131 + l, 3, S.shape, 1e-2, "f32") if l % 2 else np.zeros(S.shape, np.float32)
+        priors.append(prior)
+        refs.append(O.add_noise(prior.astype(np.float64) + S, sigma, C, B, seed, 10 + l, step))
+    tids = [10 + l for l in range(len(shapes))]
+    acc = [bool(l % 2) for l in range(len(shapes))]
+    split = [dev(p.copy()) for p in priors]
+    grp = dp.LinearGroup(layers, split)
+    assert grp  # the group passes its workspace
+    grp.clipped_sum_noised(dev(c), tids, sigma, C, B, seed, step, accumulate=acc)
+    plain = [dev(p.copy()) for p in priors]
+    dp.dp_clipped_grad_sum_noised_grouped(layers, plain, dev(c), tids, sigma, C, B, seed, step,
+                                          accumulate=acc)
+    assert grp._split_ws is not None   # these launches do split their tail
+    for l in range(len(shapes)):
+        got, ref = host(split[l]), refs[l]
+        assert np.isfinite(got).all()
+        assert fro_rel(got, host(plain[l])) <= 1e-5
+        err = fro_rel(got, ref)
+        _say(f"  split tail layer {l}: vs oracle {err:.2e}")
+        assert err <= TOL["bf16"]
+
+
 def test_clipped_sum_many_examples(dp):
     """B above the direct-load kernel's factor table (4096): general kernel."""
     B, T, d_in, d_out = 4100, 32, 64, 72
