@@ -6,9 +6,10 @@
 One step is the whole hot path on one batch, through the C ABI:
   1. squared per-example norms of every linear layer and of the output head
      (grouped T x T Gram kernel; eq. 4-6)
-  2. input-embedding norm and token buckets
-  3. tied cross term folded in as + 2 <g_in, g_out> (eq. 11, eq. 13)
-  4. clip factors (eq. 2, eq. 7)
+  2. input-embedding norm and token buckets, and the tied cross term
+     + 2 <g_in, g_out> (eq. 11, eq. 13), on a second stream beside step 1
+     into a second norm array
+  4. clip factors from both norm arrays (eq. 2, eq. 7)
   5. clipped sums of all linears and of the head (one grouped GEMM, K = B*T),
      with Gaussian noise and the division by B fused into the GEMM's store
      (eq. 3); one generator stream per parameter tensor
@@ -172,14 +173,22 @@ class Step:
         self.sum_groups = [(dp.LinearGroup(sum_layers, sum_outs), list(self.sum_tids))] \
             if sum_layers else []
         side_work = (h is not None and not self.tied) or bool(wl.vectors) or bool(wl.n_pos)
-        self.side = torch.cuda.Stream() if side_work else None
+        # The norm terms other than the weight matrices' (embedding, cross
+        # term, vectors, position table) go to the side stream into a second
+        # array, beside the HBM-bound Gram launch; the clip adds both parts.
+        self.side_norms = h is not None or bool(wl.vectors) or bool(wl.n_pos)
+        self.side = torch.cuda.Stream() if (side_work or self.side_norms) else None
+        self.ev_start = torch.cuda.Event()
+        self.ev_norms = torch.cuda.Event()
         self.ev_clip = torch.cuda.Event()
         self.ev_side = torch.cuda.Event()
+        self.side_sums = side_work
         # after the weight matrices (and an untied head): the vectors, then the position table
         t0 = L + (2 if (h is not None and h.H is not None and not h.tied) else 1)
         self.vec_tids = list(range(t0, t0 + len(wl.vectors)))
         self.pos_tid = t0 + len(wl.vectors)
         self.n2 = torch.zeros(B, device="cuda")
+        self.n2b = torch.zeros(B, device="cuda")   # the side stream's norm terms
         self.c = torch.zeros(B, device="cuda")
         self.c_b = torch.zeros(B, device="cuda")   # c / B
         # algorithmic work of the grouped clipped-sum GEMM (the dominant kernel)
@@ -189,33 +198,45 @@ class Step:
         self.norm_bytes = 2.0 * K * sum(a.shape[2] + g.shape[2] for a, g in norm_layers)
         self.step_id = 0
 
+    def total_norm2(self):
+        """Per-example squared norms of the last step (both parts summed)."""
+        return self.n2 + self.n2b if self.side_norms else self.n2.clone()
+
     def run(self, marks=None):
         """One step; marks(name) records an event after each phase if given."""
         dp, wl, h = self.dp, self.wl, self.h
         mark = marks or (lambda name: None)
+        main = self.torch.cuda.current_stream()
+        if self.side_norms:
+            # after everything enqueued so far (the previous step's clip read n2b)
+            self.ev_start.record(main)
+            self.side.wait_event(self.ev_start)
+            with self.torch.cuda.stream(self.side):
+                self.n2b.zero_()
+                if h is not None:
+                    dp.dp_ghost_norm_embedding(self.ids, self.dE, h.V, self.n2b, accumulate=True,
+                                               seg_id=self.seg, n_unique=self.nu)
+                    if h.H is not None and h.tied:
+                        dp.dp_tied_cross_term(self.ids, self.dE, self.H, self.Gz, h.V, self.n2b,
+                                              scale=2.0, accumulate=True)
+                if self.vg is not None:
+                    self.vg.grads_and_norm(self.n2b, accumulate=True)
+                if self.P is not None:
+                    dp.dp_ghost_norm_positional(self.dE, self.n2b, accumulate=True)
+            self.ev_norms.record(self.side)
         self.norm_group.ghost_norm(self.n2, accumulate=False)
         mark("norms")
-        if h is not None:
-            dp.dp_ghost_norm_embedding(self.ids, self.dE, h.V, self.n2, accumulate=True,
-                                       seg_id=self.seg, n_unique=self.nu)
-            mark("embedding_norm")
-            if h.H is not None and h.tied:
-                dp.dp_tied_cross_term(self.ids, self.dE, self.H, self.Gz, h.V, self.n2,
-                                      scale=2.0, accumulate=True)
-                mark("cross_term")
-        if self.vg is not None:
-            self.vg.grads_and_norm(self.n2, accumulate=True)
-            mark("vector_norms")
-        if self.P is not None:
-            dp.dp_ghost_norm_positional(self.dE, self.n2, accumulate=True)
-            mark("position_norm")
-        dp.dp_clip_factors_scaled(self.n2, wl.C, 1.0 / wl.B, self.c_b, c=self.c)
+        if self.side_norms:
+            main.wait_event(self.ev_norms)
+            mark("side_norms_join")
+            dp.dp_clip_factors_scaled2(self.n2, self.n2b, wl.C, 1.0 / wl.B, self.c_b, c=self.c)
+        else:
+            dp.dp_clip_factors_scaled(self.n2, wl.C, 1.0 / wl.B, self.c_b, c=self.c)
         mark("clip")
         # clipped sums with the Gaussian mechanism fused into their store
         # (eq. 3): (S + sigma C z) / B
-        main = self.torch.cuda.current_stream()
         kw = dict(seed=1234, step=self.step_id)
-        if self.side is not None:
+        if self.side_sums:
             self.ev_clip.record(main)
             self.side.wait_event(self.ev_clip)
             with self.torch.cuda.stream(self.side):
@@ -238,7 +259,7 @@ class Step:
             dp.dp_clipped_grad_sum(None, self.dE, self.c_b, self.E, ids=self.ids, V=h.V,
                                    accumulate=True)
             mark("embedding_sum")
-        if self.side is not None:
+        if self.side_sums:
             main.wait_event(self.ev_side)
             mark("side_sums_join")
         self.step_id += 1

@@ -169,6 +169,12 @@ dp_status_t dp_clip_factors(const float* norm2, int B, float C, float* c, void* 
 dp_status_t dp_clip_factors_scaled(const float* norm2, int B, float C, float scale, float* c,
                                    float* c_scaled, void* stream);
 
+/* The same from a squared norm held in two parts (terms computed on two
+ * streams, say): norm2[b] = norm2_a[b] + norm2_b[b], added in fp32 as an
+ * accumulating norm call would. Both are device arrays of B floats. */
+dp_status_t dp_clip_factors_scaled2(const float* norm2_a, const float* norm2_b, int B, float C,
+                                    float scale, float* c, float* c_scaled, void* stream);
+
 /* ---------------------------------------------------------------------
  * Clipped gradient sum (the bracket of eq. 3 without noise): the gradient
  * of the loss reweighted by the clip factors, as one GEMM over the B*T

@@ -622,7 +622,8 @@ dp_status_t dp_clip_factors(const float* norm2, int B, float C, float* c, void* 
   if (!norm2 || !c) return fail(DP_EINVAL, "norm2 or c is NULL");
   if (B <= 0) return fail(DP_EINVAL, "B must be positive");
   if (!(C > 0.f) || !std::isfinite(C)) return fail(DP_EINVAL, "C must be positive and finite");
-  return hip_status(dpg::launch_clip_factors(norm2, B, C, 1.f, c, nullptr, as_stream(stream)),
+  return hip_status(dpg::launch_clip_factors(norm2, nullptr, B, C, 1.f, c, nullptr,
+                                            as_stream(stream)),
                     "clip launch");
 }
 
@@ -632,7 +633,20 @@ dp_status_t dp_clip_factors_scaled(const float* norm2, int B, float C, float sca
   if (B <= 0) return fail(DP_EINVAL, "B must be positive");
   if (!(C > 0.f) || !std::isfinite(C)) return fail(DP_EINVAL, "C must be positive and finite");
   if (!std::isfinite(scale)) return fail(DP_EINVAL, "scale must be finite");
-  return hip_status(dpg::launch_clip_factors(norm2, B, C, scale, c, c_scaled, as_stream(stream)),
+  return hip_status(dpg::launch_clip_factors(norm2, nullptr, B, C, scale, c, c_scaled,
+                                            as_stream(stream)),
+                    "clip launch");
+}
+
+dp_status_t dp_clip_factors_scaled2(const float* norm2_a, const float* norm2_b, int B, float C,
+                                    float scale, float* c, float* c_scaled, void* stream) {
+  if (!norm2_a || !norm2_b || !c_scaled)
+    return fail(DP_EINVAL, "norm2_a, norm2_b or c_scaled is NULL");
+  if (B <= 0) return fail(DP_EINVAL, "B must be positive");
+  if (!(C > 0.f) || !std::isfinite(C)) return fail(DP_EINVAL, "C must be positive and finite");
+  if (!std::isfinite(scale)) return fail(DP_EINVAL, "scale must be finite");
+  return hip_status(dpg::launch_clip_factors(norm2_a, norm2_b, B, C, scale, c, c_scaled,
+                                            as_stream(stream)),
                     "clip launch");
 }
 

@@ -265,9 +265,10 @@ struct PosSumArgs {
 hipError_t launch_pos_sum(const PosSumArgs& a, int dt, hipStream_t s);
 
 // ----------------------------------------------------------- clip and noise
-// c (nullable) = clip factors; cs (nullable) = scale * clip factors.
-hipError_t launch_clip_factors(const float* norm2, int B, float C, float scale, float* c,
-                               float* cs, hipStream_t s);
+// c (nullable) = clip factors; cs (nullable) = scale * clip factors; the
+// squared norm is norm2 (+ norm2_b when not null).
+hipError_t launch_clip_factors(const float* norm2, const float* norm2_b, int B, float C,
+                               float scale, float* c, float* cs, hipStream_t s);
 // accumulate: g = (g + sigma_c z) inv_b; else g = sigma_c z inv_b (g not read).
 hipError_t launch_add_noise(float* g, int64_t n, float sigma_c, float inv_b, uint64_t seed,
                             uint32_t tensor_id, uint32_t step, bool accumulate, hipStream_t s);

@@ -7,12 +7,14 @@ namespace dpg {
 // c_i = min(1, C / ||g_i||), and 1 when the norm is 0 (the limit of the
 // expression); computed in double and rounded once. cs (optional) receives
 // scale * c_i, also rounded once from double; c may be null when only cs is
-// wanted.
-__global__ void clip_factors_kernel(const float* __restrict__ norm2, int B, float C, float scale,
+// wanted. The squared norm is norm2[i], plus norm2_b[i] (in fp32, as an
+// accumulating norm call would add it) when a second part is given.
+__global__ void clip_factors_kernel(const float* __restrict__ norm2,
+                                    const float* __restrict__ norm2_b, int B, float C, float scale,
                                     float* c, float* cs) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= B) return;
-  const double n2 = (double)norm2[i];
+  const double n2 = (double)(norm2_b ? norm2[i] + norm2_b[i] : norm2[i]);
   double r = 1.0;
   if (n2 > 0.0) {
     r = (double)C / sqrt(n2);
@@ -49,10 +51,11 @@ __global__ void add_noise_kernel(float* g, int64_t n, float sigma_c, float inv_b
   }
 }
 
-hipError_t launch_clip_factors(const float* norm2, int B, float C, float scale, float* c,
-                               float* cs, hipStream_t s) {
+hipError_t launch_clip_factors(const float* norm2, const float* norm2_b, int B, float C,
+                               float scale, float* c, float* cs, hipStream_t s) {
   if (B == 0) return hipSuccess;
-  hipLaunchKernelGGL(clip_factors_kernel, dim3((B + 255) / 256), dim3(256), 0, s, norm2, B, C,
+  hipLaunchKernelGGL(clip_factors_kernel, dim3((B + 255) / 256), dim3(256), 0, s, norm2, norm2_b,
+                     B, C,
                      scale, c, cs);
   return hipGetLastError();
 }

@@ -87,6 +87,7 @@ _SIGS = {
                                                _I, _VP, _I, _I, _I, _I, _F, _F, _I, _U64, _U64,
                                                _VP, _SZ, _VP], _I),
     "dp_clip_factors_scaled": ([_VP, _I, _F, _F, _VP, _VP, _VP], _I),
+    "dp_clip_factors_scaled2": ([_VP, _VP, _I, _F, _F, _VP, _VP, _VP], _I),
     "dp_noise_fill": ([_VP, _I64, _F, _F, _I, _U64, _U64, _U64, _VP], _I),
     "dp_vector_grads_workspace": ([ctypes.POINTER(dp_vector_t), _I, _I, _I, _I], _SZ),
     "dp_vector_grads_grouped": ([ctypes.POINTER(dp_vector_t), _I, _I, _I, _I,
@@ -257,6 +258,16 @@ def dp_clip_factors_scaled(norm2, C: float, scale: float, c_scaled, c=None,
                                         None if c is None else c.data_ptr(),
                                         c_scaled.data_ptr(), _stream(stream)),
            "dp_clip_factors_scaled")
+    return c_scaled
+
+
+def dp_clip_factors_scaled2(norm2_a, norm2_b, C: float, scale: float, c_scaled, c=None,
+                            stream=None) -> torch.Tensor:
+    """dp_clip_factors_scaled of norm2_a + norm2_b."""
+    _check(lib().dp_clip_factors_scaled2(norm2_a.data_ptr(), norm2_b.data_ptr(), norm2_a.numel(),
+                                         float(C), float(scale), None if c is None else c.data_ptr(),
+                                         c_scaled.data_ptr(), _stream(stream)),
+           "dp_clip_factors_scaled2")
     return c_scaled
 
 

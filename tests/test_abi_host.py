@@ -173,6 +173,13 @@ def test_cross_and_clip_reject_bad_arguments(L):
     assert g(1 << 20, 0, 1.0, 0.5, None, 1 << 21, None) == EINVAL
     assert g(1 << 20, 4, -1.0, 0.5, None, 1 << 21, None) == EINVAL
     assert g(1 << 20, 4, 1.0, float("inf"), None, 1 << 21, None) == EINVAL
+    g2 = L.dp_clip_factors_scaled2
+    assert g2(1 << 20, None, 4, 1.0, 0.5, None, 1 << 21, None) == EINVAL  # no second array
+    assert g2(None, 1 << 22, 4, 1.0, 0.5, None, 1 << 21, None) == EINVAL  # no first array
+    assert g2(1 << 20, 1 << 22, 4, 1.0, 0.5, None, None, None) == EINVAL  # no c_scaled
+    assert g2(1 << 20, 1 << 22, 0, 1.0, 0.5, None, 1 << 21, None) == EINVAL
+    assert g2(1 << 20, 1 << 22, 4, 0.0, 0.5, None, 1 << 21, None) == EINVAL
+    assert g2(1 << 20, 1 << 22, 4, 1.0, float("nan"), None, 1 << 21, None) == EINVAL
 
 
 def test_clipped_sum_rejects_bad_arguments(L):

@@ -44,7 +44,7 @@ def test_bench_step_matches_oracle(parts, name, kw):
     torch.cuda.synchronize()
     ref = O.step(wl, seed=1234, step_id=0)
     tol = TOL[wl.dtype]
-    assert rel(st.n2.cpu().numpy(), ref["norms"]["total"]).max() <= tol
+    assert rel(st.total_norm2().cpu().numpy(), ref["norms"]["total"]).max() <= tol
     assert rel(st.c.cpu().numpy(), ref["c"]).max() <= tol
     got = {l.name: o for l, o in zip(wl.linears, st.outs)}
     got["wte"] = st.E

@@ -251,6 +251,25 @@ def test_clip_factors_scaled(dp):
         assert torch.equal(cs, cs2)
 
 
+def test_clip_factors_of_two_norm_parts(dp):
+    """The squared norm given as two arrays whose sum is the total (eq. 6 is
+    a sum over parameter tensors): the factors are those of the sum."""
+    rng = np.random.default_rng(11)
+    a = np.array([0.0, 0.0, 0.2, 1.0, 0.5, 3e5, 1e-3, 9.0, 0.7], np.float32)
+    b = np.array([0.0, 1e-12, 0.05, 0.0, 0.5000001, 7e5, 2.3e-3, 8.0, 0.3], np.float32)
+    a = np.concatenate([a, rng.gamma(2.0, 1.0, 300).astype(np.float32)])
+    b = np.concatenate([b, rng.gamma(2.0, 1.0, 300).astype(np.float32)])
+    total = a.astype(np.float64) + b.astype(np.float64)
+    for C, scale in ((1.0, 1 / 32), (0.5, 1 / 7)):
+        ref = O.clip_factors(total, C)
+        c = torch.full((len(a),), -1.0, device="cuda")
+        cs = torch.empty(len(a), device="cuda")
+        dp.dp_clip_factors_scaled2(dev(a), dev(b), C, scale, cs, c=c)
+        assert rel(host(c), ref).max() <= 1e-6
+        assert rel(host(cs), np.float32(scale) * ref).max() <= 1e-6
+        assert host(c)[0] == 1.0
+
+
 # ---------------------------------------------------------------------------
 # a7 / a8: clipped sums
 # ---------------------------------------------------------------------------
