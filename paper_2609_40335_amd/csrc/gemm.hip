@@ -792,6 +792,9 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
   if constexpr (MODE == MODE_SUM)
     for (int i = tid; i < a.B; i += GM_THREADS) cs[i] = a.c[i];
   const int spe = a.T / DL_BK;  // stages per example
+  // Held in a register: a kernel-argument read inside the loop would be a
+  // scalar load whose wait (lgkmcnt) also waits for every LDS read in flight.
+  const int nB = __builtin_amdgcn_readfirstlane(a.B);
   // Stage indices below are local to this item's K range, which starts at
   // global stage gs0, inside example e0 (at its start unless this is a split
   // range): the first stage is treated as a boundary, where nothing is yet
@@ -810,7 +813,7 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
       const float ce = c_nx;
       ++e_nx;
       s_nx = e_nx * spe - gs0;
-      if (e_nx < a.B) c_nx = cs[e_nx];
+      if (e_nx < nB) c_nx = cs[e_nx];
       skip = !(ce != 0.f);
       if (!skip) {
         if (c_acc != 0.f) {
