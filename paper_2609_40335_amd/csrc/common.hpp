@@ -53,6 +53,18 @@ __device__ __forceinline__ double wave_sum_d(double v) {
   return v;
 }
 
+// Entry of a launch's table that work index x falls in: the last of the n
+// entries (n <= 64, begins increasing from begin 0) whose begin is <= x. Lane
+// j passes entry j's begin; a ballot counts the entries after the first that
+// start at or before x. One load per lane instead of a chain of dependent
+// scalar loads (one per entry, each a round trip when the scalar cache is
+// cold). x must be the same on every lane, and the whole wave active.
+__device__ __forceinline__ int wave_find(uint32_t x, uint32_t lane_begin, int n) {
+  const int lane = (int)(threadIdx.x & (WAVE - 1));
+  const uint64_t m = __ballot(lane >= 1 && lane < n && x >= lane_begin);
+  return __builtin_amdgcn_readfirstlane(__popcll(m));
+}
+
 // 32x32 output block MFMA step; K per call is 16 (bf16) or 2 (fp32).
 __device__ __forceinline__ f32x16 mfma32_bf16(const u32x4& a, const u32x4& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),

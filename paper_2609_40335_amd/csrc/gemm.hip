@@ -368,8 +368,8 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(GemmArgs args) {
   const uint32_t t = blockIdx.x / (QPT / 256);      // split tile
   const int q = (int)(blockIdx.x - t * (QPT / 256)) * 256 + (int)threadIdx.x;
   const uint32_t tile = a.n_full + t;
-  int l = 0;
-  while (l + 1 < a.n_layers && tile >= a.L[l + 1].tile_begin) ++l;
+  const int ln = (int)(threadIdx.x & (WAVE - 1));
+  const int l = wave_find(tile, ln < a.n_layers ? a.L[ln].tile_begin : 0u, a.n_layers);
   const GemmLayer& L = a.L[l];
   int mt, nt;
   tile_of(L, tile - L.tile_begin, mt, nt);
@@ -423,8 +423,8 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
   __shared__ float red[GM_THREADS / WAVE];
 
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
-  int l = 0;
-  while (l + 1 < a.n_layers && item >= a.L[l + 1].tile_begin) ++l;
+  const int ln = (int)(threadIdx.x & (WAVE - 1));
+  const int l = wave_find(item, ln < a.n_layers ? a.L[ln].tile_begin : 0u, a.n_layers);
   const GemmLayer& L = a.L[l];
   uint32_t rel = item - L.tile_begin;
   const uint32_t ntile = (uint32_t)L.tm * (uint32_t)L.tn;
@@ -698,8 +698,8 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
     item = a.n_full + j / (uint32_t)a.ksplit;
     kc = (int)(j - (j / (uint32_t)a.ksplit) * (uint32_t)a.ksplit);
   }
-  int l = 0;
-  while (l + 1 < a.n_layers && item >= a.L[l + 1].tile_begin) ++l;
+  const int ln = (int)(threadIdx.x & (WAVE - 1));
+  const int l = wave_find(item, ln < a.n_layers ? a.L[ln].tile_begin : 0u, a.n_layers);
   const GemmLayer& L = a.L[l];
   uint32_t rel = item - L.tile_begin;
   const int64_t K = (int64_t)a.B * a.T;

@@ -37,8 +37,8 @@ __device__ __forceinline__ GramItem gram_item(const GramArgs& a, uint32_t item) 
   GramItem g;
   g.b = (int)(item / a.per_ex);
   uint32_t rel = item - (uint32_t)g.b * a.per_ex;
-  int l = 0;
-  while (l + 1 < a.n_layers && rel >= a.L[l + 1].item_begin) ++l;
+  const int ln = (int)(threadIdx.x & (WAVE - 1));
+  const int l = wave_find(rel, ln < a.n_layers ? a.L[ln].item_begin : 0u, a.n_layers);
   g.l = l;
   g.rel = rel - a.L[l].item_begin;
   return g;

@@ -200,6 +200,8 @@ hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 enum { VEC_GRAD = 0, VEC_SQ = 1 };
 constexpr int VR_MAX_PARAMS = 44;   // entries per reduce launch (kernel arguments < 4 KiB)
 constexpr int VS_MAX_PARAMS = 64;   // entries per clipped-sum launch
+static_assert(GR_MAX_LAYERS <= 64 && GM_MAX_LAYERS <= 64 && VR_MAX_PARAMS <= 64,
+              "a wave finds a work item's table entry with one lane per entry");
 
 struct VecParam {
   const void* X;        // [B*T rows, ldx] elementwise factor, or null (a plain sum)

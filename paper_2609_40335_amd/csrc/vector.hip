@@ -59,8 +59,8 @@ __global__ __launch_bounds__(VR_THREADS) void vec_reduce_kernel(VecArgs args) {
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
   const int b = (int)(item / a.per_ex);
   uint32_t rel = item - (uint32_t)b * a.per_ex;
-  int p = 0;
-  while (p + 1 < a.n_params && rel >= a.P[p + 1].item_begin) ++p;
+  const int pl = (int)(threadIdx.x & (WAVE - 1));
+  const int p = wave_find(rel, pl < a.n_params ? a.P[pl].item_begin : 0u, a.n_params);
   const VecParam& P = a.P[p];
   const int fc = (int)((rel - P.item_begin) / (uint32_t)P.tsplit);
   const int tc = (int)((rel - P.item_begin) - (uint32_t)fc * P.tsplit);
