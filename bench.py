@@ -9,14 +9,15 @@ One step is the whole hot path on one batch, through the C ABI:
   2. input-embedding norm and token buckets, and the tied cross term
      + 2 <g_in, g_out> (eq. 11, eq. 13), on a second stream beside step 1
      into a second norm array
-  4. clip factors from both norm arrays (eq. 2, eq. 7)
-  5. clipped sums of all linears and of the head (one grouped GEMM, K = B*T),
+  3. clip factors from both norm arrays (eq. 2, eq. 7)
+  4. clipped sums of all linears and of the head (one grouped GEMM, K = B*T),
      with Gaussian noise and the division by B fused into the GEMM's store
      (eq. 3); one generator stream per parameter tensor
-  6. the input-embedding part of the tied gradient (sorted segment sums)
-     added onto the matrix the head's tiles wrote; sums that do not read the
-     GEMM's outputs (an untied embedding's, the vectors', the position
-     table's) run on a second stream beside the GEMM
+  5. the input-embedding part of the tied gradient: its rows (sorted
+     segment sums) are formed on the second stream beside the GEMM and
+     added onto the matrix the head's tiles wrote once the GEMM is done;
+     the other sums that do not read the GEMM's outputs (an untied
+     embedding's, the vectors', the position table's) also run there
 With every parameter (--workload gpt2-full), the biases, LayerNorm gains and
 biases and the position table join: their per-example gradients and norms
 after the weight norms, their noised clipped sums after the GEMM.
@@ -168,11 +169,12 @@ class Step:
         # work it lets overlap). The sums that do not read the GEMM's outputs
         # (an untied embedding's noise and sum, the vector and position sums)
         # run on a second stream (default priority) beside it; a tied
-        # embedding sum adds onto the matrix the head's tiles write, so it
-        # follows the GEMM on the main stream.
+        # embedding sum adds onto the matrix the head's tiles write, so only
+        # its rows are formed there and their addition follows the GEMM.
         self.sum_groups = [(dp.LinearGroup(sum_layers, sum_outs), list(self.sum_tids))] \
             if sum_layers else []
-        side_work = (h is not None and not self.tied) or bool(wl.vectors) or bool(wl.n_pos)
+        side_work = h is not None or bool(wl.vectors) or bool(wl.n_pos)
+        self.emb_rows = dp.EmbeddingRows(B, T, h.V, h.d) if self.tied else None
         # The norm terms other than the weight matrices' (embedding, cross
         # term, vectors, position table) go to the side stream into a second
         # array, beside the HBM-bound Gram launch; the clip adds both parts.
@@ -251,17 +253,20 @@ class Step:
                     dp.dp_clipped_grad_sum_positional_noised(self.dE, self.c, self.P,
                                                              self.pos_tid, wl.sigma, wl.C, wl.B,
                                                              **kw)
+                # last, so that one wait covers the whole second stream: every
+                # wait across streams costs ~10 us, even on a finished event
+                if self.emb_rows is not None:
+                    self.emb_rows.compute(self.dE, self.ids, self.c_b)
             self.ev_side.record(self.side)
         for grp, tids in self.sum_groups:
             grp.clipped_sum_noised(self.c, tids, wl.sigma, wl.C, wl.B, **kw)
             mark("clipped_sum_noise")
-        if h is not None and self.tied:
-            dp.dp_clipped_grad_sum(None, self.dE, self.c_b, self.E, ids=self.ids, V=h.V,
-                                   accumulate=True)
-            mark("embedding_sum")
         if self.side_sums:
             main.wait_event(self.ev_side)
             mark("side_sums_join")
+        if self.emb_rows is not None:
+            self.emb_rows.add_to(self.E)
+            mark("embedding_sum")
         self.step_id += 1
 
 

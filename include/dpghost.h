@@ -196,6 +196,32 @@ dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64
                                 int d_out, dp_dtype_t dt, int transpose_out, float* out,
                                 int accumulate, void* workspace, size_t workspace_bytes,
                                 void* stream);
+/* The embedding form in two calls, so that the part that does not touch
+ * `out` can run while something else (the head's clipped-sum GEMM, say)
+ * writes it. The embedding reads row ids[b,t] of E (Sec. "Weight Tying in
+ * Decoder-Only LLMs"), so its share of the bracket of eq. 3 has one row per
+ * id: row v of sum_b c[b] onehot(ids_b)^T G_b is the sum of c[b] G[b,t,:]
+ * over the tokens with ids[b,t] = v.
+ * dp_embedding_rows sorts the B*T tokens by id and writes one fp32 row per
+ * distinct id (a run of equal ids) into the workspace, with the run list;
+ * it reads G [B*T, ldg] (dt), ids [B,T] and c [B] (device) and touches
+ * nothing else. Ids at or past V form one run that the add skips.
+ * dp_embedding_rows_add then adds every run's row onto out[v,:] (out is
+ * [V, d], or [d, V] with transpose_out; contiguous; always accumulated),
+ * and must follow dp_embedding_rows on the same workspace with the same
+ * B, T, V, d (same stream, or ordered by an event). Each row is added with
+ * one fp32 addition, so the pair gives the same result, bit for bit, as the
+ * embedding form of dp_clipped_grad_sum with accumulate = 1.
+ * Workspace: dp_embedding_rows_workspace(B, T, d) bytes (B*T rows of d
+ * floats plus the sort's buffers), owned by the caller and live from the
+ * first call to the end of the second. Limits as for the embedding form. */
+size_t dp_embedding_rows_workspace(int B, int T, int d);
+dp_status_t dp_embedding_rows(const void* G, int64_t ldg, const int32_t* ids, const float* c,
+                              int B, int T, int V, int d, dp_dtype_t dt, void* workspace,
+                              size_t workspace_bytes, void* stream);
+dp_status_t dp_embedding_rows_add(const void* workspace, size_t workspace_bytes, int B, int T,
+                                  int V, int d, int transpose_out, float* out, void* stream);
+
 /* Many linear layers in one launch; outs[l] is layer l's output. */
 dp_status_t dp_clipped_grad_sum_grouped(const dp_linear_t* layers, float* const* outs,
                                         int n_layers, const float* c, int B, int T,

@@ -346,15 +346,22 @@ size_t norm_ws_bytes(const NormPlan& p, int B) { return align_up((size_t)B * p.s
 
 // Embedding-sum workspace layout (bytes): sorted keys, block head/tail partials.
 struct EsLayout {
-  size_t keys, head, tail, total;
+  size_t keys, head, tail, rank, seg, n_runs, rows, total;
 };
-EsLayout es_layout(int64_t K, int d) {
+// compact: also the ranks, run starts, run count and [K, d] run rows.
+EsLayout es_layout(int64_t K, int d, bool compact = false) {
   EsLayout l{};
   const int64_t nb = ceil_div(K, dpg::ES_BLOCK);
   size_t off = 0;
   l.keys = off; off = align_up(off + (size_t)K * 4);
   l.head = off; off = align_up(off + (size_t)nb * d * 4);
   l.tail = off; off = align_up(off + (size_t)nb * d * 4);
+  if (compact) {
+    l.rank = off; off = align_up(off + (size_t)K * 4);
+    l.seg = off; off = align_up(off + (size_t)(K + 1) * 4);
+    l.n_runs = off; off = align_up(off + 4);
+    l.rows = off; off = align_up(off + (size_t)K * d * 4);
+  }
   l.total = off;
   return l;
 }
@@ -738,6 +745,69 @@ dp_status_t dp_clipped_grad_sum_noised_grouped(const dp_linear_t* layers, float*
                                                step, nullptr, 0, stream);
 }
 
+// Shared checks and argument set-up of the embedding-form sums.
+static dp_status_t embed_sum_args(const int32_t* ids, const void* G, int64_t ldg, const float* c,
+                                  int B, int T, int V, int d, bool compact, void* workspace,
+                                  size_t workspace_bytes, dpg::EmbedSumArgs& a) {
+  if (B <= 0 || T <= 0 || V <= 0 || d <= 0)
+    return fail(DP_EINVAL, "B, T, V and d must be positive");
+  const int64_t K = (int64_t)B * T;
+  if (K > dpg::ES_MAX_K)
+    return fail(DP_EUNSUPPORTED, "B*T = %lld exceeds %d", (long long)K, dpg::ES_MAX_K);
+  const int pbits = std::max(1, bits_for(K));
+  if (bits_for((int64_t)V + 1) + pbits > 32)  // ids are clamped to V, so V + 1 values
+    return fail(DP_EUNSUPPORTED, "V and B*T do not fit a 32-bit sort key");
+  const EsLayout l = es_layout(K, d, compact);
+  if (!workspace || workspace_bytes < l.total)
+    return fail(DP_EINVAL, "workspace of %zu bytes needed", l.total);
+  char* w = static_cast<char*>(workspace);
+  a = dpg::EmbedSumArgs{};
+  a.ids = ids; a.E = G; a.lde = ldg; a.c = c;
+  a.B = B; a.K = (int32_t)K; a.T = T; a.V = V; a.d = d;
+  a.pbits = pbits;
+  a.keys = reinterpret_cast<uint32_t*>(w + l.keys);
+  a.head = reinterpret_cast<float*>(w + l.head);
+  a.tail = reinterpret_cast<float*>(w + l.tail);
+  if (compact) {
+    a.rank = reinterpret_cast<int32_t*>(w + l.rank);
+    a.seg = reinterpret_cast<int32_t*>(w + l.seg);
+    a.n_runs = reinterpret_cast<int32_t*>(w + l.n_runs);
+    a.rows = reinterpret_cast<float*>(w + l.rows);
+  }
+  return DP_OK;
+}
+
+size_t dp_embedding_rows_workspace(int B, int T, int d) {
+  if (B <= 0 || T <= 0 || d <= 0) return 0;
+  return es_layout((int64_t)B * T, d, true).total;
+}
+
+dp_status_t dp_embedding_rows(const void* G, int64_t ldg, const int32_t* ids, const float* c,
+                              int B, int T, int V, int d, dp_dtype_t dt, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  if (!G || !ids || !c) return fail(DP_EINVAL, "G, ids or c is NULL");
+  if (!dtype_ok(dt)) return fail(DP_EINVAL, "unknown dtype %d", (int)dt);
+  if (ldg < d) return fail(DP_EINVAL, "ldg < d");
+  dpg::EmbedSumArgs a;
+  dp_status_t st = embed_sum_args(ids, G, ldg, c, B, T, V, d, true, workspace, workspace_bytes,
+                                  a);
+  if (st != DP_OK) return st;
+  return hip_status(dpg::launch_embed_rows(a, kdt(dt), as_stream(stream)), "embed_rows launch");
+}
+
+dp_status_t dp_embedding_rows_add(const void* workspace, size_t workspace_bytes, int B, int T,
+                                  int V, int d, int transpose_out, float* out, void* stream) {
+  if (!out) return fail(DP_EINVAL, "out is NULL");
+  dpg::EmbedSumArgs a;
+  dp_status_t st = embed_sum_args(nullptr, nullptr, d, nullptr, B, T, V, d, true,
+                                  const_cast<void*>(workspace), workspace_bytes, a);
+  if (st != DP_OK) return st;
+  a.out = out;
+  a.ldo = transpose_out ? V : d;
+  a.transpose = transpose_out ? 1 : 0;
+  return hip_status(dpg::launch_embed_scatter(a, as_stream(stream)), "embed_scatter launch");
+}
+
 dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64_t ldg,
                                 const int32_t* ids, const float* c, int B, int T, int d_in,
                                 int d_out, dp_dtype_t dt, int transpose_out, float* out,
@@ -751,32 +821,17 @@ dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64
   // Embedding form: A = onehot(ids), d_in = V.
   if (A) return fail(DP_EINVAL, "pass either A or ids, not both");
   if (!G || !c || !out) return fail(DP_EINVAL, "G, c or out is NULL");
-  if (B <= 0 || T <= 0 || d_in <= 0 || d_out <= 0)
-    return fail(DP_EINVAL, "B, T, d_in (= V) and d_out must be positive");
   if (ldg < d_out) return fail(DP_EINVAL, "ldg < d_out");
   if (!dtype_ok(dt)) return fail(DP_EINVAL, "unknown dtype %d", (int)dt);
-  const int64_t K = (int64_t)B * T;
-  if (K > dpg::ES_MAX_K)
-    return fail(DP_EUNSUPPORTED, "B*T = %lld exceeds %d", (long long)K, dpg::ES_MAX_K);
-  const int pbits = std::max(1, bits_for(K));
-  if (bits_for((int64_t)d_in + 1) + pbits > 32)  // ids are clamped to V, so V + 1 values
-    return fail(DP_EUNSUPPORTED, "V and B*T do not fit a 32-bit sort key");
-  const EsLayout l = es_layout(K, d_out);
-  if (!workspace || workspace_bytes < l.total)
-    return fail(DP_EINVAL, "workspace of %zu bytes needed", l.total);
+  dpg::EmbedSumArgs a;
+  dp_status_t st = embed_sum_args(ids, G, ldg, c, B, T, d_in, d_out, false, workspace,
+                                  workspace_bytes, a);
+  if (st != DP_OK) return st;
   hipStream_t s = as_stream(stream);
   if (!accumulate) {
-    dp_status_t st = hip_status(dpg::launch_fill_zero(out, (int64_t)d_in * d_out, s), "fill");
+    st = hip_status(dpg::launch_fill_zero(out, (int64_t)d_in * d_out, s), "fill");
     if (st != DP_OK) return st;
   }
-  char* w = static_cast<char*>(workspace);
-  dpg::EmbedSumArgs a{};
-  a.ids = ids; a.E = G; a.lde = ldg; a.c = c;
-  a.B = B; a.K = (int32_t)K; a.T = T; a.V = d_in; a.d = d_out;
-  a.pbits = pbits;
-  a.keys = reinterpret_cast<uint32_t*>(w + l.keys);
-  a.head = reinterpret_cast<float*>(w + l.head);
-  a.tail = reinterpret_cast<float*>(w + l.tail);
   a.out = out;
   a.ldo = transpose_out ? d_in : d_out;
   a.transpose = transpose_out ? 1 : 0;

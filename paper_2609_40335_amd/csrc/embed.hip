@@ -262,6 +262,11 @@ __global__ __launch_bounds__(ES_THREADS) void embed_sort_kernel(EmbedSumArgs a) 
   __syncthreads();
   const int r = lds_radix_sort<RS_WAVES>(kbuf[0], kbuf[1], K, pb, V, cnt, wave_tot);
   for (int p = tid; p < K; p += ES_THREADS) a.keys[p] = kbuf[r][p];
+  if (a.rows) {
+    // Compact form: ranks and run starts straight to the workspace.
+    const int n = rank_sorted(kbuf[r], K, pb, a.rank, a.seg, wave_tot, tid, ES_THREADS);
+    if (tid == 0) *a.n_runs = n;
+  }
 }
 
 __device__ __forceinline__ void out_add(const EmbedSumArgs& a, uint32_t v, int f, float val) {
@@ -270,13 +275,24 @@ __device__ __forceinline__ void out_add(const EmbedSumArgs& a, uint32_t v, int f
   *o += val;
 }
 
+// A closed run's sum: added onto out[v], or (compact form) written to the
+// run's row.
+template <bool COMPACT>
+__device__ __forceinline__ void run_out(const EmbedSumArgs& a, int rank, uint32_t v, int f,
+                                        float val) {
+  if constexpr (COMPACT)
+    a.rows[(int64_t)rank * a.d + f] = val;
+  else
+    out_add(a, v, f, val);
+}
+
 // One wave per (block of ES_BLOCK sorted tokens, 64-feature chunk). Lanes
 // 0..ES_BLOCK-1 first fetch the block's keys and the tokens' clip factors;
 // then every lane (one feature) issues the loads of all ES_BLOCK rows back to
 // back, and the runs of equal ids are closed in order with the keys broadcast
 // from the lanes that hold them.
 static_assert(ES_BLOCK <= WAVE, "one key per lane");
-template <int DT>
+template <int DT, bool COMPACT>
 __global__ __launch_bounds__(ES_WAVES * WAVE) void embed_block_kernel(EmbedSumArgs a) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n_fc = (a.d + WAVE - 1) / WAVE;
@@ -292,6 +308,7 @@ __global__ __launch_bounds__(ES_WAVES * WAVE) void embed_block_kernel(EmbedSumAr
   // Keys of this block (lane j < n holds key p0 + j) and their factors.
   const uint32_t mykey = lane < n ? a.keys[p0 + lane] : 0xFFFFFFFFu;
   const float myc = lane < n ? a.c[(int)((mykey & pmask) / (uint32_t)a.T)] : 0.f;
+  const int myrank = (COMPACT && lane < n) ? a.rank[p0 + lane] : 0;
   const uint32_t id_before = p0 > 0 ? (a.keys[p0 - 1] >> pb) : 0xFFFFFFFFu;
   const uint32_t id_after = p0 + n < K ? (a.keys[p0 + n] >> pb) : 0xFFFFFFFFu;
   // Every load has a valid address (the last key repeats past the block, the
@@ -325,7 +342,7 @@ __global__ __launch_bounds__(ES_WAVES * WAVE) void embed_block_kernel(EmbedSumAr
         else if (open_tail)
           a.tail[(int64_t)q * a.d + f] = acc;
         else
-          out_add(a, id, f, acc);
+          run_out<COMPACT>(a, __builtin_amdgcn_readlane(myrank, j), id, f, acc);
       }
       acc = 0.f;
       run_start = j + 1;
@@ -335,6 +352,7 @@ __global__ __launch_bounds__(ES_WAVES * WAVE) void embed_block_kernel(EmbedSumAr
 
 // One wave per (block, feature chunk): closes the run that starts in block q
 // and continues past it, adding the partials of the blocks it spans in order.
+template <bool COMPACT>
 __global__ __launch_bounds__(ES_WAVES * WAVE) void embed_fixup_kernel(EmbedSumArgs a) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int n_fc = (a.d + WAVE - 1) / WAVE;
@@ -356,7 +374,26 @@ __global__ __launch_bounds__(ES_WAVES * WAVE) void embed_fixup_kernel(EmbedSumAr
     const int e = min(qq * ES_BLOCK + ES_BLOCK, K);
     if (e >= K || (a.keys[e] >> pb) != id) break;   // the run ends in block qq
   }
-  out_add(a, id, f, acc);
+  run_out<COMPACT>(a, COMPACT ? a.rank[p1 - 1] : 0, id, f, acc);
+}
+
+// One thread per 4 consecutive features of one run's row: out[v] (+)= row.
+__global__ __launch_bounds__(256) void embed_scatter_kernel(EmbedSumArgs a) {
+  const int nq = (a.d + 3) / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int r = (int)(i / nq);
+  if (r >= a.K || r >= *a.n_runs) return;
+  const uint32_t v = a.keys[a.seg[r]] >> a.pbits;
+  if (v >= (uint32_t)a.V) return;  // invalid ids: contribute nothing
+  const int f0 = (int)(i - (int64_t)r * nq) * 4;
+  const float* src = a.rows + (int64_t)r * a.d + f0;
+  if (!a.transpose && f0 + 4 <= a.d && (a.d & 3) == 0 && (a.ldo & 3) == 0 &&
+      (((uintptr_t)a.out) & 15) == 0) {
+    f32x4* o = (f32x4*)(a.out + (int64_t)v * a.ldo + f0);
+    *o += *(const f32x4*)src;
+  } else {
+    for (int k = 0; k < 4 && f0 + k < a.d; ++k) out_add(a, v, f0 + k, src[k]);
+  }
 }
 
 __global__ void fill_zero_kernel(float* p, int64_t n) {
@@ -385,12 +422,38 @@ hipError_t launch_embed_sum(const EmbedSumArgs& a, int dt, hipStream_t s) {
   const int units = n_blocks * n_fc;
   const dim3 g((units + ES_WAVES - 1) / ES_WAVES), blk(ES_WAVES * WAVE);
   if (dt == DT_BF16)
-    hipLaunchKernelGGL(embed_block_kernel<DT_BF16>, g, blk, 0, s, a);
+    hipLaunchKernelGGL((embed_block_kernel<DT_BF16, false>), g, blk, 0, s, a);
   else
-    hipLaunchKernelGGL(embed_block_kernel<DT_F32>, g, blk, 0, s, a);
+    hipLaunchKernelGGL((embed_block_kernel<DT_F32, false>), g, blk, 0, s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(embed_fixup_kernel, g, blk, 0, s, a);
+  hipLaunchKernelGGL(embed_fixup_kernel<false>, g, blk, 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_rows(const EmbedSumArgs& a, int dt, hipStream_t s) {
+  if (a.K == 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_sort_kernel, dim3(1), dim3(ES_THREADS), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int n_fc = (a.d + WAVE - 1) / WAVE;
+  const int n_blocks = (a.K + ES_BLOCK - 1) / ES_BLOCK;
+  const int units = n_blocks * n_fc;
+  const dim3 g((units + ES_WAVES - 1) / ES_WAVES), blk(ES_WAVES * WAVE);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL((embed_block_kernel<DT_BF16, true>), g, blk, 0, s, a);
+  else
+    hipLaunchKernelGGL((embed_block_kernel<DT_F32, true>), g, blk, 0, s, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(embed_fixup_kernel<true>, g, blk, 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_scatter(const EmbedSumArgs& a, hipStream_t s) {
+  if (a.K == 0) return hipSuccess;
+  const int64_t n = (int64_t)a.K * ((a.d + 3) / 4);
+  hipLaunchKernelGGL(embed_scatter_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -192,8 +192,19 @@ struct EmbedSumArgs {
   float* out;           // [V, ldo] or transposed [d, ldo]; accumulated into
   int64_t ldo;
   int32_t transpose;
+  // Compact form: each run of equal ids gets one row of `rows` (its index is
+  // the run's rank among the batch's runs), written once, instead of being
+  // added onto out[id]; a later scatter adds the rows onto out.
+  int32_t* rank;        // workspace [K] run index of every sorted position
+  int32_t* seg;         // workspace [K + 1] first sorted position of every run
+  int32_t* n_runs;      // workspace [1] number of runs
+  float* rows;          // workspace [K, d] run sums
 };
 hipError_t launch_embed_sum(const EmbedSumArgs& a, int dt, hipStream_t s);
+// The compact form: sort, ranks, run sums into a.rows.
+hipError_t launch_embed_rows(const EmbedSumArgs& a, int dt, hipStream_t s);
+// out[id of run r] (+)= rows[r] for every run (reads a.keys, a.seg, a.n_runs).
+hipError_t launch_embed_scatter(const EmbedSumArgs& a, hipStream_t s);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 
 // ------------------------------------- vector parameters and position table

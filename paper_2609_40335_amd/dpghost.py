@@ -20,6 +20,7 @@ __all__ = [
     "lib", "library_path", "dp_abi_version",
     "dp_ghost_norm_linear", "dp_ghost_norm_linear_grouped", "dp_ghost_norm_embedding",
     "dp_tied_cross_term", "dp_clip_factors", "dp_clip_factors_scaled", "dp_clipped_grad_sum",
+    "dp_embedding_rows", "dp_embedding_rows_add", "EmbeddingRows",
     "dp_clipped_grad_sum_grouped", "dp_clipped_grad_sum_noised_grouped", "dp_add_noise",
     "dp_noise_fill", "dp_vector_grads_grouped", "dp_vector_clipped_sum_noised_grouped",
     "dp_ghost_norm_positional", "dp_clipped_grad_sum_positional_noised",
@@ -71,6 +72,9 @@ _SIGS = {
                             _I, _VP, _SZ, _VP], _I),
     "dp_clip_factors": ([_VP, _I, _F, _VP, _VP], _I),
     "dp_clipped_grad_sum_workspace": ([_I, _I, _I, _I], _SZ),
+    "dp_embedding_rows_workspace": ([_I, _I, _I], _SZ),
+    "dp_embedding_rows": ([_VP, _I64, _VP, _VP, _I, _I, _I, _I, _I, _VP, _SZ, _VP], _I),
+    "dp_embedding_rows_add": ([_VP, _SZ, _I, _I, _I, _I, _I, _VP, _VP], _I),
     "dp_clipped_grad_sum": ([_VP, _I64, _VP, _I64, _VP, _VP, _I, _I, _I, _I, _I, _I, _VP, _I,
                              _VP, _SZ, _VP], _I),
     "dp_clipped_grad_sum_grouped": ([ctypes.POINTER(dp_linear_t), ctypes.POINTER(_VP), _I, _VP,
@@ -296,6 +300,52 @@ def dp_clipped_grad_sum(A, G, c, out, ids=None, V: Optional[int] = None,
                                  ws.data_ptr(), ws.numel(), _stream(stream)),
            "dp_clipped_grad_sum")
     return out
+
+
+class EmbeddingRows:
+    """The embedding form of the clipped sum in two calls on one workspace:
+    compute() writes one row per distinct id (c-weighted sums of G's rows)
+    and touches nothing else; add_to() adds those rows onto the [V, d] (or
+    transposed) output, bit for bit as dp_clipped_grad_sum(..., ids=ids,
+    accumulate=True) would. add_to() must be ordered after compute()."""
+
+    def __init__(self, B: int, T: int, V: int, d: int, device=None):
+        self.B, self.T, self.V, self.d = B, T, V, d
+        L = lib()
+        n = L.dp_embedding_rows_workspace(B, T, d)
+        if n == 0:
+            raise DPError("B, T and d must be positive")
+        self.ws = _ws(n, device if device is not None else torch.device("cuda"))
+
+    def compute(self, G, ids, c, stream=None) -> None:
+        dp_embedding_rows(G, ids, c, self.V, self.ws, stream=stream)
+
+    def add_to(self, out, transpose_out: bool = False, stream=None) -> None:
+        dp_embedding_rows_add(self.ws, self.B, self.T, self.V, self.d, out,
+                              transpose_out=transpose_out, stream=stream)
+
+
+def dp_embedding_rows(G, ids, c, V: int, ws, stream=None) -> None:
+    L = lib()
+    _dev(G, "G")
+    pg, B, T, d, ldg = _rows(G, "G")
+    if ids.dtype != torch.int32 or tuple(ids.shape) != (B, T) or not ids.is_contiguous():
+        raise DPError("ids must be contiguous int32 [B, T]")
+    _check(L.dp_embedding_rows(pg, ldg, ids.data_ptr(), c.data_ptr(), B, T, V, d, _dtype(G),
+                               ws.data_ptr(), ws.numel() * ws.element_size(), _stream(stream)),
+           "dp_embedding_rows")
+
+
+def dp_embedding_rows_add(ws, B: int, T: int, V: int, d: int, out, transpose_out: bool = False,
+                          stream=None) -> None:
+    L = lib()
+    if out.dtype != torch.float32 or not out.is_contiguous():
+        raise DPError("out must be contiguous float32")
+    if tuple(out.shape) != ((d, V) if transpose_out else (V, d)):
+        raise DPError("out must be [V, d] ([d, V] with transpose_out)")
+    _check(L.dp_embedding_rows_add(ws.data_ptr(), ws.numel() * ws.element_size(), B, T, V, d,
+                                   int(transpose_out), out.data_ptr(), _stream(stream)),
+           "dp_embedding_rows_add")
 
 
 def dp_clipped_grad_sum_grouped(layers: Sequence, outs: Sequence[torch.Tensor], c,

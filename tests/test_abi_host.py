@@ -200,6 +200,41 @@ def test_clipped_sum_rejects_bad_arguments(L):
     assert L.dp_clipped_grad_sum_grouped(arr, outs, 1, 1 << 20, 4, 16, 0, 0, 0, None) == EINVAL
 
 
+def _up(x):
+    return (x + 255) // 256 * 256
+
+
+def test_embedding_rows_workspace_and_validation(L):
+    """Two-call embedding form: workspace = the one-call form's (sorted keys,
+    block partials) plus ranks, run starts, the run count and B*T rows of d
+    floats, each 256-byte aligned; every bad argument fails before a launch."""
+    for B, T, d in ((32, 128, 768), (3, 50, 70), (1, 1, 8)):
+        K = B * T
+        nb = -(-K // 32)
+        want = (_up(K * 4) + 2 * _up(nb * d * 4) + _up(K * 4) + _up((K + 1) * 4) + _up(4)
+                + _up(K * d * 4))
+        assert L.dp_embedding_rows_workspace(B, T, d) == want
+        assert L.dp_clipped_grad_sum_workspace(B, T, d, 1) == _up(K * 4) + 2 * _up(nb * d * 4)
+    assert L.dp_embedding_rows_workspace(0, 16, 64) == 0
+    ws = L.dp_embedding_rows_workspace(4, 16, 64)
+    f = L.dp_embedding_rows
+    args = [1 << 21, 64, 1 << 22, 1 << 23, 4, 16, 512, 64, D.DP_BF16, 1 << 25, ws, None]
+    for i, bad in ((0, None), (2, None), (3, None), (1, 32), (4, 0), (6, 0), (8, 9), (9, None),
+                   (10, ws - 1)):
+        a = list(args)
+        a[i] = bad
+        assert f(*a) == EINVAL, (i, bad)
+    big = list(args)
+    big[4], big[5] = 64, 512                  # B*T past the in-LDS sort
+    big[10] = 1 << 40
+    assert f(*big) == EUNSUP
+    g = L.dp_embedding_rows_add
+    assert g(1 << 25, ws, 4, 16, 512, 64, 0, None, None) == EINVAL        # no out
+    assert g(None, ws, 4, 16, 512, 64, 0, 1 << 24, None) == EINVAL        # no workspace
+    assert g(1 << 25, ws - 1, 4, 16, 512, 64, 0, 1 << 24, None) == EINVAL
+    assert g(1 << 25, ws, 4, 16, 0, 64, 0, 1 << 24, None) == EINVAL       # V = 0
+
+
 def test_noised_sum_rejects_bad_arguments(L):
     """The fused clipped sum + noise validates everything on the host (no launch)."""
     f = L.dp_clipped_grad_sum_noised_grouped
