@@ -19,8 +19,10 @@ One step is the whole hot path on one batch, through the C ABI:
      the other sums that do not read the GEMM's outputs (an untied
      embedding's, the vectors', the position table's) also run there
 With every parameter (--workload gpt2-full), the biases, LayerNorm gains and
-biases and the position table join: their per-example gradients and norms
-after the weight norms, their noised clipped sums after the GEMM.
+biases and the position table join: a linear layer's bias gradient is summed
+inside that layer's Gram launch (which streams its G anyway), the LayerNorm
+and position terms on the second stream; their noised clipped sums run on
+the second stream beside the GEMM.
 Inputs are resident in HBM before the timed region starts. Prints one JSON
 line; per-phase times go to stderr.
 """
@@ -132,17 +134,35 @@ class Step:
             self.nu = torch.empty(B, dtype=torch.int32, device="cuda")
         # biases, LayerNorm gains/biases and the position table (full-parameter workloads)
         self.vec_outs, self.vg, self.P = [], None, None
+        self.vec_grads = []
+        bias_grads = [None] * len(norm_layers)
         if wl.vectors:
-            # one device buffer per host array: a bias reads its linear layer's own
-            # G, and a LayerNorm's gain and bias share theirs (one pass over it)
+            # One device buffer per host array: a LayerNorm's gain and bias share
+            # theirs (one pass over it). A linear layer's bias (no X, the layer's
+            # own G) is fused into that layer's norm launch, which streams G
+            # anyway; the LayerNorm parameters go to the vector kernel.
             same = {id(l.G): g for l, (_, g) in zip(wl.linears, self.lin)}
+            lin_of = {id(l.G): k for k, l in enumerate(wl.linears)}
 
             def shared(a):
                 if id(a) not in same:
                     same[id(a)] = dev(a)
                 return same[id(a)]
-            self.vg = dp.VectorGroup([(None if v.X is None else dev(v.X), shared(v.G))
-                                      for v in wl.vectors])
+            self.vec_grads = [None] * len(wl.vectors)
+            rest = []
+            for j, v in enumerate(wl.vectors):
+                k = lin_of.get(id(v.G)) if v.X is None else None
+                if k is not None and bias_grads[k] is None:
+                    bias_grads[k] = torch.empty(B, v.d, device="cuda")
+                    self.vec_grads[j] = bias_grads[k]
+                else:
+                    rest.append(j)
+            if rest:
+                self.vg = dp.VectorGroup([(None if wl.vectors[j].X is None
+                                           else dev(wl.vectors[j].X), shared(wl.vectors[j].G))
+                                          for j in rest])
+                for j, g in zip(rest, self.vg.grads):
+                    self.vec_grads[j] = g
             for v in wl.vectors:
                 self.vec_outs.append(self.flat[off:off + v.d])
                 off += v.d
@@ -151,7 +171,9 @@ class Step:
             off += wl.n_pos * h.d
         assert off == self.n_coords
         self.norm_layers = norm_layers
-        self.norm_group = dp.LinearGroup(norm_layers)
+        self.n_fused_biases = sum(g is not None for g in bias_grads)
+        self.norm_group = dp.LinearGroup(norm_layers,
+                                         bias_grads=bias_grads if self.n_fused_biases else None)
         # Noise generator ids per parameter tensor, as in the oracle's step:
         # linear l -> l, the input embedding (or tied matrix) -> L, an untied
         # head -> L + 1. Every GEMM-shaped output is written once with its
@@ -189,6 +211,8 @@ class Step:
         t0 = L + (2 if (h is not None and h.H is not None and not h.tied) else 1)
         self.vec_tids = list(range(t0, t0 + len(wl.vectors)))
         self.pos_tid = t0 + len(wl.vectors)
+        self.vsum = dp.VectorSums(self.vec_grads, self.vec_outs, self.vec_tids) \
+            if wl.vectors else None
         self.n2 = torch.zeros(B, device="cuda")
         self.n2b = torch.zeros(B, device="cuda")   # the side stream's norm terms
         self.c = torch.zeros(B, device="cuda")
@@ -246,9 +270,8 @@ class Step:
                     dp.dp_noise_fill(self.E, wl.sigma, wl.C, wl.B, tensor_id=self.e_tid, **kw)
                     dp.dp_clipped_grad_sum(None, self.dE, self.c_b, self.E, ids=self.ids, V=h.V,
                                            accumulate=True)
-                if self.vg is not None:
-                    self.vg.clipped_sum_noised(self.c, self.vec_outs, self.vec_tids, wl.sigma,
-                                               wl.C, wl.B, **kw)
+                if self.vsum is not None:
+                    self.vsum.noised(self.c, wl.sigma, wl.C, wl.B, **kw)
                 if self.P is not None:
                     dp.dp_clipped_grad_sum_positional_noised(self.dE, self.c, self.P,
                                                              self.pos_tid, wl.sigma, wl.C, wl.B,

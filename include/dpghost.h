@@ -115,6 +115,28 @@ dp_status_t dp_ghost_norm_linear(const void* A, int64_t lda, const void* G, int6
                                  float* norm2, int accumulate, void* workspace,
                                  size_t workspace_bytes, void* stream);
 
+/* The grouped norm with the layers' bias vectors. A bias b_l adds
+ * y_t = ... + b_l to layer l, so its per-example gradient is the sum over
+ * the example's tokens of the layer's own output gradient,
+ *   bias_grads[l][i, :] = sum_t G_l[i,t,:]      (fp32 [B, d_out], caller-owned)
+ * and the flat norm (eq. 6) takes its square in like every other parameter:
+ * norm2[i] (+)= sum_l ||A_l,i^T G_l,i||^2 + sum_l ||bias_grads[l][i,:]||^2.
+ * bias_grads (host array of n_layers device pointers, or NULL for no biases)
+ * holds NULL for a layer without bias. Where the layer's Gram launch already
+ * streams G with every token row of an example in LDS (bf16, 16-byte rows,
+ * T <= 256) the bias sums ride along in the same pass; other layers get them
+ * from the vector kernel (a second pass over their G). Either way the result
+ * equals dp_ghost_norm_linear_grouped plus dp_vector_grads_grouped over the
+ * biases (X = NULL), up to fp32 summation order. The workspace is
+ * dp_ghost_norm_linear_bias_workspace(...) bytes (only bias_grads[l] != NULL
+ * matters to it). */
+size_t dp_ghost_norm_linear_bias_workspace(const dp_linear_t* layers, float* const* bias_grads,
+                                           int n_layers, int B, int T, dp_dtype_t dt);
+dp_status_t dp_ghost_norm_linear_bias_grouped(const dp_linear_t* layers, float* const* bias_grads,
+                                              int n_layers, int B, int T, dp_dtype_t dt,
+                                              float* norm2, int accumulate, void* workspace,
+                                              size_t workspace_bytes, void* stream);
+
 /* ---------------------------------------------------------------------
  * Input-embedding ghost norm and token buckets (Sec. "Weight Tying in
  * Decoder-Only LLMs"; the embedding reads row ids[b,t] of E in R^{V x d}).

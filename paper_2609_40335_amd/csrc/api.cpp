@@ -80,6 +80,7 @@ struct GramEntry {
   int d_in, g0, g1, kg, nc;
   int slot_begin;
   bool vec;
+  float* bias = nullptr;  // fused bias gradient [B, g1], or null
 };
 
 struct GemmEntry {
@@ -103,9 +104,19 @@ struct NoiseCfg {
   uint64_t seed = 0;
 };
 
+// A layer bias whose gradient the layer's norm launch cannot fuse: reduced
+// by the vector kernel instead.
+struct BiasEntry {
+  const void* G;
+  int64_t ldg;
+  int d;
+  float* grad;
+};
+
 struct NormPlan {
   std::vector<GramEntry> gram;
   std::vector<GemmEntry> direct;
+  std::vector<BiasEntry> bias_vec;
   int n_t = 0, P = 0;
   int64_t slots = 0;
 };
@@ -172,7 +183,8 @@ int pick_chunks(int64_t width, int ks, int64_t items_per_chunk, int64_t other, i
   return (int)best;
 }
 
-NormPlan plan_norm(const dp_linear_t* layers, int n, int B, int T, dp_dtype_t dt) {
+NormPlan plan_norm(const dp_linear_t* layers, int n, int B, int T, dp_dtype_t dt,
+                   float* const* bias = nullptr) {
   NormPlan p;
   p.n_t = (int)ceil_div(T, dpg::GR_TM);
   p.P = p.n_t * (p.n_t + 1) / 2;
@@ -187,8 +199,10 @@ NormPlan plan_norm(const dp_linear_t* layers, int n, int B, int T, dp_dtype_t dt
   }
   for (int i = 0; i < n; ++i) {
     const dp_linear_t& L = layers[i];
+    float* const bg = bias ? bias[i] : nullptr;
     if (use_direct(L, T)) {
       plan_gemm(L.A, L.lda, L.d_in, L.G, L.ldg, L.d_out, dt, nullptr, 0, p.direct, &p.slots, 1);
+      if (bg) p.bias_vec.push_back({L.G, L.ldg, L.d_out, bg});
       continue;
     }
     const bool vec = vec_ok(L.A, L.lda, dt) && vec_ok(L.G, L.ldg, dt);
@@ -202,6 +216,12 @@ NormPlan plan_norm(const dp_linear_t* layers, int n, int B, int T, dp_dtype_t dt
     }
     GramEntry e{L.A, L.G, L.lda, L.ldg, L.d_in, 0, L.d_out, kg, (int)ceil_div(L.d_out, kg),
                 (int)p.slots, vec};
+    if (bg) {
+      if (dpg::gram_fuses_bias(kdt(dt), vec, T))
+        e.bias = bg;
+      else
+        p.bias_vec.push_back({L.G, L.ldg, L.d_out, bg});
+    }
     p.slots += (int64_t)gram_pairs(p, dt, e.vec, T) * e.nc;
     p.gram.push_back(e);
   }
@@ -257,6 +277,7 @@ dp_status_t run_gram(const NormPlan& p, int B, int T, dp_dtype_t dt, float* ws, 
         L.d_in = e.d_in; L.g0 = e.g0; L.g1 = e.g1; L.kg = e.kg; L.nc = e.nc;
         L.item_begin = (uint32_t)per_ex;
         L.slot_begin = e.slot_begin;
+        L.bias = e.bias;
         per_ex += (uint64_t)a.P * e.nc;
       }
       const uint64_t items = per_ex * (uint64_t)B;
@@ -503,21 +524,35 @@ const char* dp_status_string(dp_status_t s) {
 
 const char* dp_last_error(void) { return g_last_error.c_str(); }
 
-size_t dp_ghost_norm_linear_workspace(const dp_linear_t* layers, int n_layers, int B, int T,
-                                      dp_dtype_t dt) {
+size_t dp_ghost_norm_linear_bias_workspace(const dp_linear_t* layers, float* const* bias_grads,
+                                           int n_layers, int B, int T, dp_dtype_t dt) {
   if (check_layers(layers, n_layers, B, T, dt) != DP_OK) return 0;
-  return norm_ws_bytes(plan_norm(layers, n_layers, B, T, dt), B);
+  const NormPlan p = plan_norm(layers, n_layers, B, T, dt, bias_grads);
+  VecPlan vp;
+  for (const BiasEntry& e : p.bias_vec)
+    plan_vec(vp, nullptr, 0, e.G, e.ldg, e.d, dpg::VEC_GRAD, e.grad, dt, T);
+  return norm_ws_bytes(p, B) + align_up((size_t)B * vp.slots * 4);
 }
 
-dp_status_t dp_ghost_norm_linear_grouped(const dp_linear_t* layers, int n_layers, int B, int T,
-                                         dp_dtype_t dt, float* norm2, int accumulate,
-                                         void* workspace, size_t workspace_bytes, void* stream) {
+size_t dp_ghost_norm_linear_workspace(const dp_linear_t* layers, int n_layers, int B, int T,
+                                      dp_dtype_t dt) {
+  return dp_ghost_norm_linear_bias_workspace(layers, nullptr, n_layers, B, T, dt);
+}
+
+dp_status_t dp_ghost_norm_linear_bias_grouped(const dp_linear_t* layers, float* const* bias_grads,
+                                              int n_layers, int B, int T, dp_dtype_t dt,
+                                              float* norm2, int accumulate, void* workspace,
+                                              size_t workspace_bytes, void* stream) {
   dp_status_t st = check_layers(layers, n_layers, B, T, dt);
   if (st != DP_OK) return st;
   if (!norm2) return fail(DP_EINVAL, "norm2 is NULL");
-  const NormPlan p = plan_norm(layers, n_layers, B, T, dt);
+  const NormPlan p = plan_norm(layers, n_layers, B, T, dt, bias_grads);
   if ((uint64_t)B * p.slots > 0x7FFFFFFFull) return fail(DP_EUNSUPPORTED, "too many partials");
-  const size_t need = norm_ws_bytes(p, B);
+  VecPlan vp;
+  for (const BiasEntry& e : p.bias_vec)
+    plan_vec(vp, nullptr, 0, e.G, e.ldg, e.d, dpg::VEC_GRAD, e.grad, dt, T);
+  const size_t norm_bytes = norm_ws_bytes(p, B);
+  const size_t need = norm_bytes + align_up((size_t)B * vp.slots * 4);
   if (!workspace || workspace_bytes < need)
     return fail(DP_EINVAL, "workspace of %zu bytes needed, %zu given", need,
                 workspace ? workspace_bytes : (size_t)0);
@@ -527,8 +562,23 @@ dp_status_t dp_ghost_norm_linear_grouped(const dp_linear_t* layers, int n_layers
   if (st != DP_OK) return st;
   st = run_gemm(p.direct, 1, B, T, dt, nullptr, ws, p.slots, 0, NoiseCfg{}, s);
   if (st != DP_OK) return st;
-  return hip_status(dpg::launch_finish_rows(ws, B, (int)p.slots, norm2, accumulate, 1.f, s),
+  float* vws = reinterpret_cast<float*>(static_cast<char*>(workspace) + norm_bytes);
+  if (!vp.e.empty()) {
+    st = run_vec(vp, B, T, dt, vws, s);
+    if (st != DP_OK) return st;
+  }
+  st = hip_status(dpg::launch_finish_rows(ws, B, (int)p.slots, norm2, accumulate, 1.f, s),
+                  "finish launch");
+  if (st != DP_OK || vp.e.empty()) return st;
+  return hip_status(dpg::launch_finish_rows(vws, B, (int)vp.slots, norm2, 1, 1.f, s),
                     "finish launch");
+}
+
+dp_status_t dp_ghost_norm_linear_grouped(const dp_linear_t* layers, int n_layers, int B, int T,
+                                         dp_dtype_t dt, float* norm2, int accumulate,
+                                         void* workspace, size_t workspace_bytes, void* stream) {
+  return dp_ghost_norm_linear_bias_grouped(layers, nullptr, n_layers, B, T, dt, norm2, accumulate,
+                                           workspace, workspace_bytes, stream);
 }
 
 dp_status_t dp_ghost_norm_linear(const void* A, int64_t lda, const void* G, int64_t ldg, int B,

@@ -319,9 +319,55 @@ __device__ __forceinline__ void dg_wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// Fused bias gradient. While a G stage (64 features of every example row)
+// sits in LDS, NT threads sum its columns: thread t adds chunk t%8 (8
+// features) of rows t/8, t/8 + NT/8, ...; the 8 row groups of a wave meet
+// by shuffles and each wave leaves 64 partials in bred. After the next
+// barrier wave 0 adds the waves' partials, writes the example's bias row for
+// those features and keeps its square.
+template <int ROWS, int NT>
+__device__ __forceinline__ void bias_stage(const u32x4* st, float* bred, int tid) {
+  const int c = tid & 7;
+  float sm[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) sm[e] = 0.f;
+#pragma unroll
+  for (int i = 0; i < ROWS / (NT / 8); ++i) {
+    const int r = (tid >> 3) + i * (NT / 8);
+    const u32x4 v = st[r * 8 + swz(r, c)];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      sm[2 * q] += __builtin_bit_cast(float, v[q] << 16);
+      sm[2 * q + 1] += __builtin_bit_cast(float, v[q] & 0xFFFF0000u);
+    }
+  }
+#pragma unroll
+  for (int off = 8; off < WAVE; off <<= 1)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sm[e] += __shfl_xor(sm[e], off, WAVE);
+  const int lane = tid & 63;
+  if (lane < 8)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bred[(tid >> 6) * 64 + lane * 8 + e] = sm[e];
+}
+
+// Wave 0: features c0 .. c0+63 of the bias row `out` (up to c1); returns the
+// square of this lane's feature.
+template <int NT>
+__device__ __forceinline__ float bias_finish(const float* bred, float* out, int64_t c0, int64_t c1,
+                                             int tid) {
+  if (tid >= 64) return 0.f;
+  float v = 0.f;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) v += bred[w * 64 + tid];
+  if (c0 + tid >= c1) return 0.f;
+  out[c0 + tid] = v;
+  return v * v;
+}
+
 template <int PAT>
 __device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int ti, int tj,
-                                         int chunk, u32x4* ring) {
+                                         int chunk, u32x4* ring, float* bred) {
   constexpr int NB = PatNB<PAT>::NB;
   constexpr int ROWS = PatRows<PAT>::ROWS;        // 128 or 256
   constexpr int STB = ROWS * DG_ROWB;             // bytes per stage
@@ -406,24 +452,41 @@ __device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int t
 #pragma unroll
     for (int e = 0; e < 16; ++e) { accP[j][e] = 0.f; accQ[j][e] = 0.f; }
 
+  // The bias applies to single-tile items (T <= 128), whose stages hold all
+  // of the example's rows.
+  float* const bout =
+      (ROWS == GR_TM && T <= GR_TM && L.bias) ? L.bias + (int64_t)b * L.g1 : nullptr;
+  float bsq = 0.f;
+  auto g_c0 = [&](int s) { return y0 + (int64_t)(s - nX) * 64; };
+
   // Every iteration issues one stage's loads (past the end they read zeros into
   // a slot nobody reads), so the wait count is a constant.
 #pragma unroll
   for (int p = 0; p < DG_NS - 1; ++p) issue(p);
-  auto phase = [&](int s_begin, int s_end, f32x16 (&acc)[NB]) {
+  auto phase = [&](int s_begin, int s_end, f32x16 (&acc)[NB], bool with_bias) {
     for (int s = s_begin; s < s_end; ++s) {
       dg_wait_vmcnt<LOADS * (DG_NS - 2)>();
       __syncthreads();
       fix(s);
+      if (with_bias && s > s_begin)
+        bsq += bias_finish<GR_THREADS>(bred + ((s - 1) & 1) * GR_THREADS, bout, g_c0(s - 1), y1,
+                                       tid);
       issue(s + DG_NS - 1);
       stage_mfma<DT_BF16, NB>(ring + (s % DG_NS) * (STB / 16), ra, rb, acc, lane);
+      if (with_bias)
+        bias_stage<ROWS, GR_THREADS>(ring + (s % DG_NS) * (STB / 16),
+                                     bred + (s & 1) * GR_THREADS, tid);
     }
   };
-  phase(0, nX, accP);
-  phase(nX, n, accQ);
+  phase(0, nX, accP, false);
+  phase(nX, n, accQ, bout != nullptr);
+  if (bout) {
+    __syncthreads();
+    bsq += bias_finish<GR_THREADS>(bred + ((n - 1) & 1) * GR_THREADS, bout, g_c0(n - 1), y1, tid);
+  }
   // No load may still be writing LDS when the workgroup moves on.
   dg_wait_vmcnt<0>();
-  float part = 0.f;
+  float part = bsq;
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     float s = 0.f;
@@ -440,6 +503,7 @@ __global__ __launch_bounds__(GR_THREADS, SINGLE ? 2 : 1) void dl_gram_kernel(Gra
   (void)args;
   __shared__ __attribute__((aligned(1024))) u32x4 ring[DG_NS * (SINGLE ? GR_TM : GR_ROWS) * 8];
   __shared__ float red[GR_THREADS / WAVE];
+  __shared__ float bred[SINGLE ? 2 * GR_THREADS : 1];
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
   const GramItem gi = gram_item(a, item);
   const GramLayer& L = a.L[gi.l];
@@ -452,11 +516,11 @@ __global__ __launch_bounds__(GR_THREADS, SINGLE ? 2 : 1) void dl_gram_kernel(Gra
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   float part;
   if (!SINGLE && ti != tj)
-    part = dg_item<PAT_OFF>(L, b, a.T, ti, tj, chunk, ring);
+    part = dg_item<PAT_OFF>(L, b, a.T, ti, tj, chunk, ring, bred);
   else if (w < 2)
-    part = dg_item<PAT_D1>(L, b, a.T, ti, tj, chunk, ring);
+    part = dg_item<PAT_D1>(L, b, a.T, ti, tj, chunk, ring, bred);
   else
-    part = dg_item<PAT_D2>(L, b, a.T, ti, tj, chunk, ring);
+    part = dg_item<PAT_D2>(L, b, a.T, ti, tj, chunk, ring, bred);
   part = wave_sum(part);
   if ((threadIdx.x & 63) == 0) red[w] = part;
   __syncthreads();
@@ -479,7 +543,8 @@ constexpr int DW_LOADS = DW_STB / 1024 / (DW_THREADS / WAVE);
 static_assert(DW_LOADS * 8 * (DW_THREADS / WAVE) == DW_ROWS, "rows per load");
 
 template <int NB>
-__device__ __forceinline__ float dw_item(const GramLayer& L, int b, int T, int chunk, u32x4* ring) {
+__device__ __forceinline__ float dw_item(const GramLayer& L, int b, int T, int chunk, u32x4* ring,
+                                         float* bred) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const uint64_t ex_rows = (uint64_t)b * T;
@@ -564,21 +629,34 @@ __device__ __forceinline__ float dw_item(const GramLayer& L, int b, int T, int c
 #pragma unroll
     for (int e = 0; e < 16; ++e) { accP[j][e] = 0.f; accQ[j][e] = 0.f; }
 
+  float* const bout = L.bias ? L.bias + (int64_t)b * L.g1 : nullptr;
+  float bsq = 0.f;
+  auto g_c0 = [&](int s) { return y0 + (int64_t)(s - nX) * 64; };
 #pragma unroll
   for (int p = 0; p < DW_NS - 1; ++p) issue(p);
-  auto phase = [&](int s_begin, int s_end, f32x16 (&acc)[NB]) {
+  auto phase = [&](int s_begin, int s_end, f32x16 (&acc)[NB], bool with_bias) {
     for (int s = s_begin; s < s_end; ++s) {
       dg_wait_vmcnt<DW_LOADS * (DW_NS - 2)>();
       __syncthreads();
       fix(s);
+      if (with_bias && s > s_begin)
+        bsq += bias_finish<DW_THREADS>(bred + ((s - 1) & 1) * DW_THREADS, bout, g_c0(s - 1), y1,
+                                       tid);
       issue(s + DW_NS - 1);
       stage_mfma<DT_BF16, NB>(ring + (s % DW_NS) * (DW_STB / 16), ra, rb, acc, lane);
+      if (with_bias)
+        bias_stage<DW_ROWS, DW_THREADS>(ring + (s % DW_NS) * (DW_STB / 16),
+                                        bred + (s & 1) * DW_THREADS, tid);
     }
   };
-  phase(0, nX, accP);
-  phase(nX, n, accQ);
+  phase(0, nX, accP, false);
+  phase(nX, n, accQ, bout != nullptr);
+  if (bout) {
+    __syncthreads();
+    bsq += bias_finish<DW_THREADS>(bred + ((n - 1) & 1) * DW_THREADS, bout, g_c0(n - 1), y1, tid);
+  }
   dg_wait_vmcnt<0>();
-  float part = 0.f;
+  float part = bsq;
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     float s = 0.f;
@@ -593,6 +671,7 @@ __global__ __launch_bounds__(DW_THREADS) void dl_gram_whole_kernel(GramArgs args
   const GramArgs& a = *(const GramArgs*)__builtin_amdgcn_kernarg_segment_ptr();
   (void)args;
   __shared__ __attribute__((aligned(1024))) u32x4 ring[DW_NS * DW_STB / 16];
+  __shared__ float bred[2 * DW_THREADS];
   // The partial sums reuse the ring: every load has landed by then.
   float* red = (float*)ring;
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
@@ -601,7 +680,8 @@ __global__ __launch_bounds__(DW_THREADS) void dl_gram_whole_kernel(GramArgs args
   const int b = gi.b;
   const int chunk = (int)gi.rel;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  float part = w < 4 ? dw_item<5>(L, b, a.T, chunk, ring) : dw_item<4>(L, b, a.T, chunk, ring);
+  float part = w < 4 ? dw_item<5>(L, b, a.T, chunk, ring, bred)
+                     : dw_item<4>(L, b, a.T, chunk, ring, bred);
   part = wave_sum(part);
   __syncthreads();  // every wave is done reading the ring
   if ((threadIdx.x & 63) == 0) red[w] = part;

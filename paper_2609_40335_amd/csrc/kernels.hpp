@@ -21,6 +21,11 @@ inline bool gram_whole(int dt, bool vec, int T) {
 inline int gram_groups_per_cu(int dt, bool vec, int T) {
   return dt == DT_BF16 && vec && T <= GR_TM ? 2 : 1;
 }
+// Gram launches that can fuse a layer's bias gradient (every example row of
+// a stage is in LDS at once).
+inline bool gram_fuses_bias(int dt, bool vec, int T) {
+  return dt == DT_BF16 && vec && T <= 2 * GR_TM;
+}
 
 struct GramLayer {
   const void* A;        // [B*T rows, lda] activations
@@ -32,6 +37,10 @@ struct GramLayer {
   int32_t nc;           // number of G chunks
   uint32_t item_begin;  // first work item of this layer among an example's items
   int32_t slot_begin;   // first partial slot of this layer in an example's row
+  // The layer's bias gradient, fused (bf16, 16-byte rows, T <= 256 only):
+  // row b of [B, g1] gets sum_t G[b,t,:], and its squared norm joins the
+  // example's partial sums. Null: no bias.
+  float* bias;
 };
 
 // Work items are numbered example-major: example b owns items

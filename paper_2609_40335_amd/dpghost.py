@@ -23,6 +23,7 @@ __all__ = [
     "dp_embedding_rows", "dp_embedding_rows_add", "EmbeddingRows",
     "dp_clipped_grad_sum_grouped", "dp_clipped_grad_sum_noised_grouped", "dp_add_noise",
     "dp_noise_fill", "dp_vector_grads_grouped", "dp_vector_clipped_sum_noised_grouped",
+    "dp_ghost_norm_linear_bias_grouped", "VectorSums",
     "dp_ghost_norm_positional", "dp_clipped_grad_sum_positional_noised",
     "LinearGroup", "VectorGroup",
 ]
@@ -60,6 +61,10 @@ _SIGS = {
     "dp_status_string": ([_I], ctypes.c_char_p),
     "dp_last_error": ([], ctypes.c_char_p),
     "dp_ghost_norm_linear_workspace": ([ctypes.POINTER(dp_linear_t), _I, _I, _I, _I], _SZ),
+    "dp_ghost_norm_linear_bias_workspace": ([ctypes.POINTER(dp_linear_t), ctypes.POINTER(_VP), _I,
+                                             _I, _I, _I], _SZ),
+    "dp_ghost_norm_linear_bias_grouped": ([ctypes.POINTER(dp_linear_t), ctypes.POINTER(_VP), _I,
+                                           _I, _I, _I, _VP, _I, _VP, _SZ, _VP], _I),
     "dp_ghost_norm_linear_grouped": ([ctypes.POINTER(dp_linear_t), _I, _I, _I, _I, _VP, _I,
                                       _VP, _SZ, _VP], _I),
     "dp_ghost_norm_linear": ([_VP, _I64, _VP, _I64, _I, _I, _I, _I, _I, _I, _VP, _I, _VP, _SZ,
@@ -175,6 +180,13 @@ def _layer(A, G, algo=DP_NORM_AUTO) -> dp_linear_t:
     if A.dtype != G.dtype:
         raise DPError("A and G must share a dtype")
     return dp_linear_t(pa, lda, d_in, pg, ldg, d_out, algo)
+
+
+def dp_ghost_norm_linear_bias_grouped(layers: Sequence, bias_grads: Sequence, norm2: torch.Tensor,
+                                      accumulate: bool = False, stream=None) -> torch.Tensor:
+    """The grouped norm that also writes bias_grads[l] (fp32 [B, d_out], or
+    None for a layer without bias) = sum over tokens of G_l, norms included."""
+    return LinearGroup(layers, bias_grads=bias_grads).ghost_norm(norm2, accumulate, stream)
 
 
 def dp_ghost_norm_linear_grouped(layers: Sequence, norm2: torch.Tensor, accumulate: bool = False,
@@ -476,6 +488,39 @@ def dp_vector_clipped_sum_noised_grouped(grads: Sequence[torch.Tensor], outs: Se
            "dp_vector_clipped_sum_noised_grouped")
 
 
+class VectorSums:
+    """Noised clipped sums of many vector parameters from per-example
+    gradients already in memory (fp32 [B, d] each: from dp_vector_grads_grouped
+    or from a fused bias), pointer arrays prepared once."""
+
+    def __init__(self, grads: Sequence[torch.Tensor], outs: Sequence[torch.Tensor],
+                 tensor_ids: Sequence[int], accumulate=None):
+        n = len(grads)
+        if n == 0 or len(outs) != n:
+            raise DPError("one output per gradient, at least one")
+        B = grads[0].shape[0]
+        for g, o in zip(grads, outs):
+            if g.dtype != torch.float32 or g.dim() != 2 or g.shape[0] != B or not g.is_contiguous():
+                raise DPError("grads must be contiguous fp32 [B, d] with one B")
+            if o.dtype != torch.float32 or o.numel() != g.shape[1] or not o.is_contiguous():
+                raise DPError("outs must be contiguous fp32 with d elements")
+        self._keep = (list(grads), list(outs))
+        self.n, self.B = n, int(B)
+        self._gp = (ctypes.c_void_p * n)(*[g.data_ptr() for g in grads])
+        self._op = (ctypes.c_void_p * n)(*[o.data_ptr() for o in outs])
+        self._dd = (ctypes.c_int32 * n)(*[int(g.shape[1]) for g in grads])
+        self._tids, self._acc = _noise_arrays(n, tensor_ids, accumulate)
+
+    def noised(self, c, sigma: float, C: float, B_norm: int, seed: int, step: int,
+               stream=None) -> None:
+        _check(lib().dp_vector_clipped_sum_noised_grouped(self._gp, self._dd, self.n, self.B,
+                                                          c.data_ptr(), self._op, self._tids,
+                                                          self._acc, float(sigma), float(C),
+                                                          int(B_norm), int(seed), int(step),
+                                                          _stream(stream)),
+               "dp_vector_clipped_sum_noised_grouped")
+
+
 def dp_ghost_norm_positional(dE, norm2, accumulate: bool = False, stream=None) -> torch.Tensor:
     """norm2[i] (+)= sum_t ||dE[i, t]||^2 (the position table's per-example norm)."""
     L = lib()
@@ -554,9 +599,13 @@ class LinearGroup:
     Holds the ctypes descriptor array, the output-pointer array and the norm
     workspace so that repeated steps only pass pointers. ``layers`` is a
     sequence of (A, G) or (A, G, algo) with a common B, T and dtype.
+    ``bias_grads`` (one fp32 [B, d_out] tensor or None per layer) makes
+    ghost_norm also write the layers' per-example bias gradients and count
+    their norms (dp_ghost_norm_linear_bias_grouped).
     """
 
-    def __init__(self, layers: Sequence, outs: Optional[Sequence[torch.Tensor]] = None):
+    def __init__(self, layers: Sequence, outs: Optional[Sequence[torch.Tensor]] = None,
+                 bias_grads: Optional[Sequence[Optional[torch.Tensor]]] = None):
         L = lib()
         self._tensors = [t for l in layers for t in l[:2]]
         self.n = len(layers)
@@ -566,7 +615,19 @@ class LinearGroup:
         for l in layers:
             if tuple(l[0].shape[:2]) != (self.B, self.T) or _dtype(l[0]) != self.dt:
                 raise DPError("all layers of a group share B, T and dtype")
-        nbytes = L.dp_ghost_norm_linear_workspace(self.descs, self.n, self.B, self.T, self.dt)
+        self._bias = None
+        if bias_grads is not None:
+            if len(bias_grads) != self.n:
+                raise DPError("one bias gradient (or None) per layer")
+            for l, g in zip(layers, bias_grads):
+                if g is not None and (g.dtype != torch.float32 or not g.is_contiguous()
+                                      or tuple(g.shape) != (self.B, l[1].shape[2])):
+                    raise DPError("bias gradients must be contiguous fp32 [B, d_out]")
+            self._bias_t = list(bias_grads)
+            self._bias = (ctypes.c_void_p * self.n)(*[None if g is None else g.data_ptr()
+                                                      for g in bias_grads])
+        nbytes = L.dp_ghost_norm_linear_bias_workspace(self.descs, self._bias, self.n, self.B,
+                                                       self.T, self.dt)
         self.ws = _ws(nbytes, A0.device)
         self.outs = None
         if outs is not None:
@@ -579,11 +640,11 @@ class LinearGroup:
         self.outs = (ctypes.c_void_p * self.n)(*[o.data_ptr() for o in outs])
 
     def ghost_norm(self, norm2: torch.Tensor, accumulate: bool = False, stream=None):
-        _check(lib().dp_ghost_norm_linear_grouped(self.descs, self.n, self.B, self.T, self.dt,
-                                                  norm2.data_ptr(), int(accumulate),
-                                                  self.ws.data_ptr(), self.ws.numel(),
-                                                  _stream(stream)),
-               "dp_ghost_norm_linear_grouped")
+        _check(lib().dp_ghost_norm_linear_bias_grouped(self.descs, self._bias, self.n, self.B,
+                                                       self.T, self.dt, norm2.data_ptr(),
+                                                       int(accumulate), self.ws.data_ptr(),
+                                                       self.ws.numel(), _stream(stream)),
+               "dp_ghost_norm_linear_bias_grouped")
         return norm2
 
     def clipped_sum(self, c: torch.Tensor, transpose_out: bool = False,

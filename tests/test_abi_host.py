@@ -204,6 +204,29 @@ def _up(x):
     return (x + 255) // 256 * 256
 
 
+def test_bias_norm_workspace_and_validation(L):
+    """Fused biases (bf16, 16-byte rows, T <= 256) add nothing to the norm
+    workspace; a bias the Gram launch cannot fuse (fp32 here, or T > 256)
+    adds the vector kernel's partials: B x ceil(d / features per chunk)."""
+    lay = (D.dp_linear_t * 2)(D.dp_linear_t(1 << 20, 768, 768, 1 << 21, 3072, 3072, 0),
+                              D.dp_linear_t(1 << 22, 768, 768, 1 << 23, 768, 768, 0))
+    bias = (ctypes.c_void_p * 2)(1 << 24, None)
+    for T in (128, 256):
+        plain = L.dp_ghost_norm_linear_workspace(lay, 2, 32, T, D.DP_BF16)
+        assert L.dp_ghost_norm_linear_bias_workspace(lay, bias, 2, 32, T, D.DP_BF16) == plain
+        assert L.dp_ghost_norm_linear_bias_workspace(lay, None, 2, 32, T, D.DP_BF16) == plain
+    plain = L.dp_ghost_norm_linear_workspace(lay, 2, 32, 300, D.DP_BF16)
+    assert L.dp_ghost_norm_linear_bias_workspace(lay, bias, 2, 32, 300, D.DP_BF16) == \
+        plain + _up(32 * 6 * 4)                       # 3072 / 512 bf16 features per chunk
+    plain = L.dp_ghost_norm_linear_workspace(lay, 2, 32, 64, D.DP_F32)
+    assert L.dp_ghost_norm_linear_bias_workspace(lay, bias, 2, 32, 64, D.DP_F32) == \
+        plain + _up(32 * 12 * 4)                      # 3072 / 256 fp32 features per chunk
+    f = L.dp_ghost_norm_linear_bias_grouped
+    assert f(lay, bias, 2, 32, 64, D.DP_BF16, None, 0, 1 << 25, 1 << 30, None) == EINVAL
+    assert f(lay, bias, 2, 32, 64, D.DP_BF16, 1 << 26, 0, None, 0, None) == EINVAL
+    assert f(lay, bias, 0, 32, 64, D.DP_BF16, 1 << 26, 0, 1 << 25, 1 << 30, None) == EINVAL
+
+
 def test_embedding_rows_workspace_and_validation(L):
     """Two-call embedding form: workspace = the one-call form's (sorted keys,
     block partials) plus ranks, run starts, the run count and B*T rows of d

@@ -181,3 +181,44 @@ def test_library_on_captured_gpt2_widths_bf16(dp):
         worst = max(worst, err)
         assert err <= TOL["bf16"], (name, err)
     _say(f"  worst clipped-sum rel err {worst:.2e}")
+
+
+@pytest.mark.gpu
+def test_dp_adam_steps_on_captured_gpt2(dp):
+    """Two DP-Adam steps (the paper trains with Adam, lr 2e-4 for GPT-2) on a
+    tiny GPT-2: one copy takes the library's noised clipped sums as p.grad
+    (operands captured afresh after each update), the other the mean of the
+    true per-example gradients clipped with the true norms plus the oracle's
+    noise. The parameter updates agree to the fp32 tolerance."""
+    import copy
+    V, n_pos, d, T, B = 97, 24, 32, 12, 3
+    C, sigma, seed, lr = 0.05, 0.5, 5, 2e-4
+    m_lib = cap.tiny_gpt2(3, V, n_pos, d, 2, 2)
+    m_ref = copy.deepcopy(m_lib)
+    p0 = {n: p.detach().clone() for n, p in m_ref.named_parameters()}
+    opt_lib = torch.optim.Adam(m_lib.parameters(), lr=lr)
+    opt_ref = torch.optim.Adam(m_ref.parameters(), lr=lr)
+    lib_params, ref_params = dict(m_lib.named_parameters()), dict(m_ref.named_parameters())
+    for step in range(2):
+        ids = torch.randint(0, V, (B, T), generator=torch.Generator().manual_seed(10 + step))
+        wl = _workload(cap.capture(m_lib, ids), ids, V, d, n_pos, "f32", C=C, sigma=sigma)
+        _, _, outs = _library_step(dp, wl, seed=seed, step=step)
+        names = _names(wl)
+        for name in names:
+            p = lib_params[cap.hf_name(name)]
+            p.grad = torch.from_numpy(outs[name].astype(np.float64)).reshape(p.shape)
+        opt_lib.step()
+        true = cap.per_example_grads(m_ref, ids)
+        c_ref = O.clip_factors(_true_norm2(true), C)
+        for tid, name in enumerate(names):
+            p = ref_params[cap.hf_name(name)]
+            S = np.tensordot(c_ref, true[cap.hf_name(name)], axes=(0, 0))
+            p.grad = torch.from_numpy(O.add_noise(S, sigma, C, B, seed, tid, step)).reshape(p.shape)
+        opt_ref.step()
+    worst = 0.0
+    for n, p in ref_params.items():
+        du_ref = (p.detach() - p0[n]).numpy()
+        du_lib = (lib_params[n].detach() - p0[n]).numpy()
+        worst = max(worst, fro_rel(du_lib, du_ref))
+    _say(f"  worst parameter-update rel err after 2 DP-Adam steps {worst:.2e}")
+    assert worst <= TOL["f32"]

@@ -267,3 +267,65 @@ def test_full_size_gpt2_vectors(dp):
     dp.dp_clipped_grad_sum_positional_noised(dE, dev(c), P, 7, 0.0, 1.0, 0, 1, 0)
     ref_p = O.clipped_sum_positional(O.decode(h.dE, "bf16"), c.astype(np.float64), wl.n_pos)
     assert fro_rel(host(P), ref_p) <= TOL["bf16"]
+
+
+# ---------------------------------------------------------------------------
+# Linear-layer biases fused into the grouped norm
+# ---------------------------------------------------------------------------
+BIAS_CASES = [
+    # dtype, B, T, layers: (d_in, d_out, bias?, G row stride or None, algo)
+    ("bf16", 4, 64, [(96, 200, True, None, "gram"), (64, 72, False, None, "gram"),
+                     (128, 520, True, None, "gram")]),            # single-tile Gram: fused
+    ("bf16", 3, 200, [(96, 136, True, None, "gram"), (72, 64, True, None, "gram")]),  # whole
+    ("bf16", 2, 300, [(64, 96, True, None, "gram")]),             # tile pairs: vector pass
+    ("bf16", 2, 64, [(64, 4200, True, None, "gram")]),            # G in 2 chunks: fused
+    ("bf16", 3, 40, [(80, 101, True, 103, "gram"),                # unaligned rows: vector pass
+                     (64, 64, True, None, "direct")]),            # direct norm: vector pass
+    ("f32", 3, 50, [(48, 70, True, None, "gram"), (32, 40, False, None, "gram")]),
+]
+
+
+@pytest.mark.parametrize("case", BIAS_CASES, ids=lambda c: f"{c[0]}-B{c[1]}-T{c[2]}-{len(c[3])}")
+def test_linear_norm_with_biases(dp, case):
+    dtype, B, T, spec = case
+    _say(f"linear norm with biases {dtype} B={B} T={T} {spec}")
+    algos = {"gram": dp.DP_NORM_GRAM, "direct": dp.DP_NORM_DIRECT}
+    layers, biases, ref_n2, refs = [], [], np.zeros(B), []
+    for k, (di, do, has_b, ldg, algo) in enumerate(spec):
+        ldg = ldg or do
+        A = gen.draw(81 + k, 1, (B, T, di), 1.0, dtype)
+        G = _nan_pad(gen.draw(81 + k, 2, (B, T, ldg), 1e-2, dtype), do)
+        Ad, Gd = O.decode(A, dtype), O.decode(G[:, :, :do], dtype)
+        ref_n2 = ref_n2 + O.linear_norm2(Ad, Gd)
+        layers.append((dev(A, dtype), dev(G, dtype)[:, :, :do], algos[algo]))
+        if has_b:
+            refs.append(np.stack([O.vector_grad(None, Gd[i]) for i in range(B)]))
+            ref_n2 = ref_n2 + O.vector_norm2(None, Gd)
+            biases.append(torch.full((B, do), 7.0, device="cuda"))
+        else:
+            refs.append(None)
+            biases.append(None)
+    n2 = torch.full((B,), 3.0, device="cuda")
+    grp = dp.LinearGroup(layers, bias_grads=biases)
+    grp.ghost_norm(n2, accumulate=True)
+    got_n2 = host(n2) - 3.0
+    _say(f"  norm rel err {rel(got_n2, ref_n2).max():.2e}")
+    assert rel(got_n2, ref_n2).max() <= TOL[dtype]
+    for k, (g, r) in enumerate(zip(biases, refs)):
+        if g is None:
+            continue
+        got = host(g)
+        assert np.isfinite(got).all(), k
+        for i in range(B):
+            assert fro_rel(got[i], r[i]) <= TOL[dtype], (k, i)
+    # overwrite mode gives the same norms; a group without biases gives the
+    # weight-only part
+    n3 = torch.full((B,), 9.0, device="cuda")
+    grp.ghost_norm(n3, accumulate=False)
+    assert rel(host(n3), ref_n2).max() <= TOL[dtype]
+    n4 = torch.zeros(B, device="cuda")
+    dp.LinearGroup(layers).ghost_norm(n4)
+    bias_n2 = sum(O.vector_norm2(None, O.decode(
+        gen.draw(81 + k, 2, (B, T, s[3] or s[1]), 1e-2, dtype)[:, :, :s[1]], dtype))
+        for k, s in enumerate(spec) if s[2])
+    assert rel(host(n4), ref_n2 - bias_n2).max() <= TOL[dtype]
