@@ -45,8 +45,8 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 # HBM bytes per launch of the clipped-sum kernel: rocprofv3 FETCH_SIZE x 2 +
 # WRITE_SIZE x 1 (factors from a plain 1 GiB copy), recorded for the kernel
 # source with this SHA-256; any other source reports null.
-GEMM_TRAFFIC = {"gemm.hip sha256": "de5636d665dc4d9eb4f2c319818ad240a8d5d83706ce0c650dbf89374eb2248d",
-                "bytes": 2697363133}
+GEMM_TRAFFIC = {"gemm.hip sha256": "3e00d9520e7154f6929b0f7380dd40036d1b16581e76f3fdf464a567753eae6d",
+                "bytes": 2697902056}
 
 
 def log(*a):
