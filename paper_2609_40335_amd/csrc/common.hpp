@@ -83,36 +83,45 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t nbytes) {
   const uint32_t n = nbytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)nbytes;
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, RSRC_WORD3);
 }
+// Cache policy of a load: 0, or CPOL_STREAM (sc1 nt: device scope,
+// non-temporal) for data read once, which keeps the streamed lines from
+// crowding the caches (measured faster on the kernels that stream every byte
+// once; slower where tiles share operands through L2).
+constexpr int CPOL_STREAM = 18;
+
 // voff: per-lane byte offset; soff: wave-uniform byte offset (an SGPR).
+template <int CPOL = 0>
 __device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t voff, uint32_t soff = 0) {
-  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, CPOL));
 }
+template <int CPOL = 0>
 __device__ __forceinline__ uint32_t buf_load4(rsrc_t r, uint32_t voff, uint32_t soff = 0) {
-  return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+  return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, CPOL);
 }
+template <int CPOL = 0>
 __device__ __forceinline__ uint32_t buf_load2(rsrc_t r, uint32_t voff, uint32_t soff = 0) {
-  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, CPOL);
 }
 
 // 16-byte chunk of elements [col, col+EPC) of a row, through a buffer
 // resource; the chunk starts at byte voff + soff. VEC: one 16-byte load (the
 // row is 16-byte aligned); otherwise one load per element. Elements at or past
 // `ncol` are zeroed when MASK is set.
-template <int DT, bool VEC, bool MASK>
+template <int DT, bool VEC, bool MASK, int CPOL = 0>
 __device__ __forceinline__ u32x4 buf_chunk(rsrc_t r, uint32_t voff, uint32_t soff, int64_t col,
                                            int64_t ncol) {
   constexpr int ES = (DT == DT_BF16) ? 2 : 4;
   u32x4 v;
   if constexpr (VEC) {
-    v = buf_load16(r, voff, soff);
+    v = buf_load16<CPOL>(r, voff, soff);
   } else if constexpr (DT == DT_BF16) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      v[q] = buf_load2(r, voff + (2 * q) * ES, soff) |
-             (buf_load2(r, voff + (2 * q + 1) * ES, soff) << 16);
+      v[q] = buf_load2<CPOL>(r, voff + (2 * q) * ES, soff) |
+             (buf_load2<CPOL>(r, voff + (2 * q + 1) * ES, soff) << 16);
   } else {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = buf_load4(r, voff + q * ES, soff);
+    for (int q = 0; q < 4; ++q) v[q] = buf_load4<CPOL>(r, voff + q * ES, soff);
   }
   if constexpr (MASK) {
     const int64_t nv = ncol - col;  // valid elements in the chunk (may be <= 0)

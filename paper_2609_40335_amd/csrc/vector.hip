@@ -94,10 +94,12 @@ __global__ __launch_bounds__(VR_THREADS) void vec_reduce_kernel(VecArgs args) {
         // Rows past this item's rows and elements past d read as zero.
         const bool in = t < t_end;
         const uint32_t so = in ? (uint32_t)t * ldg_b : 0u;
-        gv[u] = in ? buf_chunk<DT, VEC, true>(rg, g0, so, col, P.d) : u32x4{0u, 0u, 0u, 0u};
+        gv[u] = in ? buf_chunk<DT, VEC, true, CPOL_STREAM>(rg, g0, so, col, P.d)
+                    : u32x4{0u, 0u, 0u, 0u};
         if (has_x && P.mode == VEC_GRAD) {
           const uint32_t sx = in ? (uint32_t)t * ldx_b : 0u;
-          xv[u] = in ? buf_chunk<DT, VEC, true>(rx, x0, sx, col, P.d) : u32x4{0u, 0u, 0u, 0u};
+          xv[u] = in ? buf_chunk<DT, VEC, true, CPOL_STREAM>(rx, x0, sx, col, P.d)
+                      : u32x4{0u, 0u, 0u, 0u};
         }
       }
 #pragma unroll
