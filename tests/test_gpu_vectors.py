@@ -282,6 +282,9 @@ BIAS_CASES = [
     ("bf16", 3, 40, [(80, 101, True, 103, "gram"),                # unaligned rows: vector pass
                      (64, 64, True, None, "direct")]),            # direct norm: vector pass
     ("f32", 3, 50, [(48, 70, True, None, "gram"), (32, 40, False, None, "gram")]),
+    ("bf16", 1, 1, [(64, 72, True, None, "gram")]),               # one example, one token
+    ("bf16", 2, 129, [(64, 200, True, None, "gram")]),            # whole kernel, ragged T
+    ("bf16", 2, 256, [(128, 64, True, None, "gram")]),            # whole kernel, full T
 ]
 
 
