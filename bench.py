@@ -45,8 +45,8 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 # HBM bytes per launch of the clipped-sum kernel: rocprofv3 FETCH_SIZE x 2 +
 # WRITE_SIZE x 1 (factors from a plain 1 GiB copy), recorded for the kernel
 # source with this SHA-256; any other source reports null.
-GEMM_TRAFFIC = {"gemm.hip sha256": "3e00d9520e7154f6929b0f7380dd40036d1b16581e76f3fdf464a567753eae6d",
-                "bytes": 2697902056}
+GEMM_TRAFFIC = {"gemm.hip sha256": "052ae33183eea6e1cb318d15784a30ec1e567337c7b8998f5f4ab13a94a110e3",
+                "bytes": 2697537801}
 
 
 def log(*a):

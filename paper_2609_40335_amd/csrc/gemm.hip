@@ -757,8 +757,11 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
       const uint32_t m0v = (uint32_t)__builtin_amdgcn_readfirstlane((int)(dst + t * 1024));
       const uint32_t so = (uint32_t)__builtin_amdgcn_readfirstlane((int)(sbase + 2 * t * ld_bytes));
       // M0 (the LDS destination) is a reserved register that the compiler
-      // sets right before each of its own users; this kernel has none.
-      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+      // sets right before each of its own users; this kernel has none. The
+      // loads are device-scope (sc1), which measured 0-3 % faster; unlike the
+      // Gram's streams they keep the temporal hint, as neighbouring tiles
+      // share operand panels through L2 (nt measured slower).
+      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 lds"
                    :: "s"(m0v), "v"(lvo[t & 1]), "s"(desc), "s"(so));
     }
   };
