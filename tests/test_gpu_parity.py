@@ -704,3 +704,36 @@ def test_full_size_gpt2_head_sampled(dp):
         assert rel(host(n_out)[i], O.sqnorm(gW)) <= TOL["bf16"]
         cr = float(np.sum(gE * gW))
         assert abs(host(cross)[i] - cr) <= TOL["bf16"] * np.sqrt(O.sqnorm(gE) * O.sqnorm(gW))
+
+
+@pytest.mark.parametrize("n_layers", [52, 53])
+def test_layer_table_extremes(dp, n_layers):
+    """As many layers as one launch's table holds (52: every lane of the
+    work-item decode used) and one more (two launches): grouped Gram norms
+    with fused biases, direct norms and the grouped clipped sum against the
+    oracle, all layers of distinct widths."""
+    B, T = 3, 64
+    _say(f"layer table: {n_layers} layers")
+    layers, biases, sums, ref_n2, refs = [], [], [], np.zeros(B), []
+    c = np.array([0.3, 1.0, 0.55], np.float32)
+    for l in range(n_layers):
+        di, do = 32 + 8 * (l % 7), 40 + 16 * (l % 11)
+        A, G = _layer_inputs("bf16", B, T, di, do, seed=300 + l)
+        Ad, Gd = O.decode(A, "bf16"), O.decode(G, "bf16")
+        ref_n2 = ref_n2 + O.linear_norm2(Ad, Gd)
+        algo = dp.DP_NORM_DIRECT if l % 5 == 4 else dp.DP_NORM_GRAM
+        layers.append((dev(A, "bf16"), dev(G, "bf16"), algo))
+        if l % 3 == 0:
+            ref_n2 = ref_n2 + O.vector_norm2(None, Gd)
+            biases.append(torch.zeros(B, do, device="cuda"))
+        else:
+            biases.append(None)
+        refs.append(O.clipped_sum_linear(Ad, Gd, c.astype(np.float64)))
+        sums.append(torch.empty(di, do, device="cuda"))
+    n2 = torch.zeros(B, device="cuda")
+    dp.LinearGroup(layers, bias_grads=biases).ghost_norm(n2)
+    assert rel(host(n2), ref_n2).max() <= TOL["bf16"]
+    dp.dp_clipped_grad_sum_grouped([(a, g) for a, g, _ in layers], sums, dev(c))
+    worst = max(fro_rel(host(o), r) for o, r in zip(sums, refs))
+    _say(f"  norm rel err {rel(host(n2), ref_n2).max():.2e}, worst clipped sum {worst:.2e}")
+    assert worst <= TOL["bf16"]
