@@ -231,7 +231,9 @@ dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64
  * dp_embedding_rows_add then adds every run's row onto out[v,:] (out is
  * [V, d], or [d, V] with transpose_out; contiguous; always accumulated),
  * and must follow dp_embedding_rows on the same workspace with the same
- * B, T, V, d (same stream, or ordered by an event). Each row is added with
+ * B, T, V, d (same stream, or ordered by an event); on a workspace that call
+ * has not filled, its result is undefined but its reads and writes stay
+ * inside the workspace and out. Each row is added with
  * one fp32 addition, so the pair gives the same result, bit for bit, as the
  * embedding form of dp_clipped_grad_sum with accumulate = 1.
  * Workspace: dp_embedding_rows_workspace(B, T, d) bytes (B*T rows of d

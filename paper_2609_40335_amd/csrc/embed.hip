@@ -383,7 +383,11 @@ __global__ __launch_bounds__(256) void embed_scatter_kernel(EmbedSumArgs a) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int r = (int)(i / nq);
   if (r >= a.K || r >= *a.n_runs) return;
-  const uint32_t v = a.keys[a.seg[r]] >> a.pbits;
+  // The run list comes from the workspace; a position outside it (a
+  // workspace dp_embedding_rows has not filled) adds nothing.
+  const int p = a.seg[r];
+  if (p < 0 || p >= a.K) return;
+  const uint32_t v = a.keys[p] >> a.pbits;
   if (v >= (uint32_t)a.V) return;  // invalid ids: contribute nothing
   const int f0 = (int)(i - (int64_t)r * nq) * 4;
   const float* src = a.rows + (int64_t)r * a.d + f0;
