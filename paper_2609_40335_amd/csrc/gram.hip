@@ -23,6 +23,8 @@
 // so <g_in, g_out> = sum_{t,s} Gz[s, x_t] <dE_t, h_s>: one T x T product of
 // dE and H on MFMA, multiplied element-wise by logit gradients gathered at the
 // token ids. No V x d gradient is formed.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -106,6 +108,102 @@ __device__ __forceinline__ void stage_mfma(const u32x4* __restrict__ lds, const 
           acc[j] = mfma32_f32(__uint_as_float(fa[m]), __uint_as_float(fb[m]), acc[j]);
       }
     }
+  }
+}
+
+// A wave's blocks as products of distinct fragments (direct-load kernels,
+// bf16): block j multiplies fragment ia(j) (its rows) by fragment ib(j) (its
+// columns); the nf fragments are 32-row slices of the stage at row offsets
+// rows[0..nf). A fragment that several blocks use (both operands of a
+// diagonal block, the blocks of one block row) is read from LDS once per
+// k-step, half the reads of one pair per block.
+struct FpD1 {   // waves 0, 1 of a diagonal tile: (x,x) (x,y) (y,y); rows {x, y}
+  static constexpr int NB = 3, NF = 2;
+  static constexpr int ia(int j) { return j < 2 ? 0 : 1; }
+  static constexpr int ib(int j) { return j < 1 ? 0 : 1; }
+};
+struct FpD2 {   // waves 2, 3 of a diagonal tile: (x,64) (x,96); rows {x, 64, 96}
+  static constexpr int NB = 2, NF = 3;
+  static constexpr int ia(int) { return 0; }
+  static constexpr int ib(int j) { return 1 + j; }
+};
+struct FpOff {  // a 64x64 quadrant of an off-diagonal pair; rows {x, x+32, y, y+32}
+  static constexpr int NB = 4, NF = 4;
+  static constexpr int ia(int j) { return j >> 1; }
+  static constexpr int ib(int j) { return 2 + (j & 1); }
+};
+// Whole-example Gram (8 waves, block rows 0..7): wave g < 4 takes (g,g)..(g,g+4)
+// (rows g..g+4); waves 4..7 the rest of row pairs {g, 7-g}.
+struct FpW0 {
+  static constexpr int NB = 5, NF = 5;
+  static constexpr int ia(int) { return 0; }
+  static constexpr int ib(int j) { return j; }
+  static constexpr int row(int g, int q) { return 32 * (g + q); }
+};
+struct FpW4 {   // (0,5) (0,6) (0,7) (7,7)
+  static constexpr int NB = 4, NF = 4;
+  static constexpr int ia(int j) { return j < 3 ? 0 : 3; }
+  static constexpr int ib(int j) { return j < 3 ? 1 + j : 3; }
+  static constexpr int row(int, int q) { return q == 0 ? 0 : 32 * (4 + q); }
+};
+struct FpW5 {   // (1,6) (1,7) (6,6) (6,7)
+  static constexpr int NB = 4, NF = 3;
+  static constexpr int ia(int j) { return j < 2 ? 0 : 1; }
+  static constexpr int ib(int j) { return 1 + (j & 1); }
+  static constexpr int row(int, int q) { return q == 0 ? 32 : 32 * (5 + q); }
+};
+struct FpW6 {   // (2,7) (5,5) (5,6) (5,7)
+  static constexpr int NB = 4, NF = 4;
+  static constexpr int ia(int j) { return j == 0 ? 0 : 2; }
+  static constexpr int ib(int j) { return j == 0 || j == 3 ? 1 : j + 1; }
+  static constexpr int row(int, int q) { return q == 0 ? 64 : (q == 1 ? 224 : 32 * (3 + q)); }
+};
+struct FpW7 {   // (4,4) (4,5) (4,6) (4,7)
+  static constexpr int NB = 4, NF = 4;
+  static constexpr int ia(int) { return 0; }
+  static constexpr int ib(int j) { return j; }
+  static constexpr int row(int, int q) { return 32 * (4 + q); }
+};
+
+// The whole-example patterns reproduce the block list (entry k of row pair g
+// is (g, g+k) for k < 8-g, else (7-g, 7-g + k-(8-g)); wave g takes entries
+// 0..4, wave g+4 entries 5..8), checked at compile time.
+template <class P>
+constexpr bool fp_whole_matches(int w) {
+  const int g = w & 3, k0 = (w >> 2) * 5;
+  for (int j = 0; j < P::NB; ++j) {
+    const int k = k0 + j;
+    const int bi = k < 8 - g ? g : 7 - g;
+    const int bj = k < 8 - g ? g + k : 7 - g + (k - (8 - g));
+    if (P::row(g, P::ia(j)) != 32 * bi || P::row(g, P::ib(j)) != 32 * bj) return false;
+  }
+  for (int q = 0; q < P::NF; ++q)
+    for (int r = 0; r < q; ++r)
+      if (P::row(g, q) == P::row(g, r)) return false;
+  return true;
+}
+static_assert(fp_whole_matches<FpW0>(0) && fp_whole_matches<FpW0>(1) &&
+                  fp_whole_matches<FpW0>(2) && fp_whole_matches<FpW0>(3) &&
+                  fp_whole_matches<FpW4>(4) && fp_whole_matches<FpW5>(5) &&
+                  fp_whole_matches<FpW6>(6) && fp_whole_matches<FpW7>(7),
+              "fragment patterns of the whole-example Gram");
+
+template <class P>
+__device__ __forceinline__ void stage_mfma_fp(const u32x4* __restrict__ lds,
+                                              const int (&rows)[P::NF], f32x16 (&acc)[P::NB],
+                                              int lane) {
+  const int r32 = lane & 31, half = lane >> 5;
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int c = 2 * ks + half;
+    u32x4 f[P::NF];
+#pragma unroll
+    for (int q = 0; q < P::NF; ++q) {
+      const int row = rows[q] + r32;
+      f[q] = lds[row * 8 + swz(row, c)];
+    }
+#pragma unroll
+    for (int j = 0; j < P::NB; ++j) acc[j] = mfma32_bf16(f[P::ia(j)], f[P::ib(j)], acc[j]);
   }
 }
 
@@ -451,6 +549,17 @@ __device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int t
   int ra[4], rb[4];
   float wt[4];
   block_rows<PAT>(w, ra, rb, wt);
+  using FP = std::conditional_t<PAT == PAT_OFF, FpOff,
+                                std::conditional_t<PAT == PAT_D1, FpD1, FpD2>>;
+  static_assert(FP::NB == NB, "block list");
+  int rows[FP::NF];
+  if constexpr (PAT == PAT_D1) {
+    rows[0] = ra[0]; rows[1] = ra[2];
+  } else if constexpr (PAT == PAT_D2) {
+    rows[0] = ra[0]; rows[1] = rb[0]; rows[2] = rb[1];
+  } else {
+    rows[0] = ra[0]; rows[1] = ra[2]; rows[2] = rb[0]; rows[3] = rb[1];
+  }
   f32x16 accP[NB], accQ[NB];
 #pragma unroll
   for (int j = 0; j < NB; ++j)
@@ -477,7 +586,7 @@ __device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int t
         bsq += bias_finish<GR_THREADS>(bred + ((s - 1) & 1) * GR_THREADS, bout, g_c0(s - 1), y1,
                                        tid);
       issue(s + DG_NS - 1);
-      stage_mfma<DT_BF16, NB>(ring + (s % DG_NS) * (STB / 16), ra, rb, acc, lane);
+      stage_mfma_fp<FP>(ring + (s % DG_NS) * (STB / 16), rows, acc, lane);
       if (with_bias)
         bias_stage<ROWS, GR_THREADS>(ring + (s % DG_NS) * (STB / 16),
                                      bred + (s & 1) * GR_THREADS, tid);
@@ -547,9 +656,10 @@ constexpr int DW_STB = DW_ROWS * DG_ROWB;
 constexpr int DW_LOADS = DW_STB / 1024 / (DW_THREADS / WAVE);
 static_assert(DW_LOADS * 8 * (DW_THREADS / WAVE) == DW_ROWS, "rows per load");
 
-template <int NB>
+template <class P>
 __device__ __forceinline__ float dw_item(const GramLayer& L, int b, int T, int chunk, u32x4* ring,
                                          float* bred) {
+  constexpr int NB = P::NB;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const uint64_t ex_rows = (uint64_t)b * T;
@@ -617,17 +727,15 @@ __device__ __forceinline__ float dw_item(const GramLayer& L, int b, int T, int c
   };
 
   // Block list: entry k of row pair g is (g, g+k) for k < 8-g, else
-  // (7-g, 7-g + k-(8-g)); wave g takes entries 0..4, wave g+4 entries 5..8.
-  const int g = w & 3, k0 = (w >> 2) * 5;
-  int ra[NB], rb[NB];
+  // (7-g, 7-g + k-(8-g)); wave g takes entries 0..4, wave g+4 entries 5..8
+  // (the patterns FpW0 .. FpW7 list them by fragment).
+  const int g = w & 3;
+  int rows[P::NF];
+#pragma unroll
+  for (int q = 0; q < P::NF; ++q) rows[q] = P::row(g, q);
   float wt[NB];
 #pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    const int k = k0 + j;
-    const int bi = k < 8 - g ? g : 7 - g;
-    const int bj = k < 8 - g ? g + k : 7 - g + (k - (8 - g));
-    ra[j] = 32 * bi; rb[j] = 32 * bj; wt[j] = bi == bj ? 1.f : 2.f;
-  }
+  for (int j = 0; j < NB; ++j) wt[j] = P::ia(j) == P::ib(j) ? 1.f : 2.f;
   f32x16 accP[NB], accQ[NB];
 #pragma unroll
   for (int j = 0; j < NB; ++j)
@@ -648,7 +756,7 @@ __device__ __forceinline__ float dw_item(const GramLayer& L, int b, int T, int c
         bsq += bias_finish<DW_THREADS>(bred + ((s - 1) & 1) * DW_THREADS, bout, g_c0(s - 1), y1,
                                        tid);
       issue(s + DW_NS - 1);
-      stage_mfma<DT_BF16, NB>(ring + (s % DW_NS) * (DW_STB / 16), ra, rb, acc, lane);
+      stage_mfma_fp<P>(ring + (s % DW_NS) * (DW_STB / 16), rows, acc, lane);
       if (with_bias)
         bias_stage<DW_ROWS, DW_THREADS>(ring + (s % DW_NS) * (DW_STB / 16),
                                         bred + (s & 1) * DW_THREADS, tid);
@@ -685,8 +793,14 @@ __global__ __launch_bounds__(DW_THREADS) void dl_gram_whole_kernel(GramArgs args
   const int b = gi.b;
   const int chunk = (int)gi.rel;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  float part = w < 4 ? dw_item<5>(L, b, a.T, chunk, ring, bred)
-                     : dw_item<4>(L, b, a.T, chunk, ring, bred);
+  float part;
+  switch (w) {
+    case 4: part = dw_item<FpW4>(L, b, a.T, chunk, ring, bred); break;
+    case 5: part = dw_item<FpW5>(L, b, a.T, chunk, ring, bred); break;
+    case 6: part = dw_item<FpW6>(L, b, a.T, chunk, ring, bred); break;
+    case 7: part = dw_item<FpW7>(L, b, a.T, chunk, ring, bred); break;
+    default: part = dw_item<FpW0>(L, b, a.T, chunk, ring, bred); break;
+  }
   part = wave_sum(part);
   __syncthreads();  // every wave is done reading the ring
   if ((threadIdx.x & 63) == 0) red[w] = part;
