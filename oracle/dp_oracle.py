@@ -22,7 +22,7 @@ gradient is materialised in fp64 and its norm taken directly.
     sum of the input-embedding and output-projection contributions, whose
     squared norm carries the cross term 2<g_in, g_out> (eq. 11, eq. 13).
 
-Readings taken where the paper is silent (each is also listed in the design doc):
+Readings taken where the paper is silent:
   * ||g_i|| = 0 gives R_i = 1 (the limit of min(1, C/x) as x -> 0).
   * The batch divisor of eq. 3 is the actual batch size B.
   * "N(0, s^2 C^2 I)" is drawn with standard deviation s*C per coordinate; a
