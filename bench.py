@@ -338,10 +338,13 @@ def cpu_baseline(wl, n_coords, budget):
     noise on a slice of coordinates, extrapolated to one full step."""
     import numpy as np
     import oracle
+    blas = "unknown"
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()
-                       if p.get("user_api") == "blas"] or [os.cpu_count() or 1])
+        libs = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        threads = max([p.get("num_threads", 1) for p in libs] or [os.cpu_count() or 1])
+        if libs:
+            blas = " ".join(str(libs[0].get(k, "")) for k in ("internal_api", "version")).strip()
     except Exception:
         threads = os.cpu_count() or 1
     t0 = time.perf_counter()
@@ -365,7 +368,25 @@ def cpu_baseline(wl, n_coords, budget):
                    f"{n_slice} coordinates; extrapolated to B={wl.B} examples and "
                    f"{n_coords} coordinates per step"),
         "seconds_per_example": per_ex, "seconds_noise_per_step": n_coords * per_coord,
+        "host": host_cpu(), "blas": blas,
     }
+
+
+def host_cpu():
+    """CPU model name and socket count from /proc/cpuinfo (Linux)."""
+    model, sockets = "unknown", set()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                key, _, val = line.partition(":")
+                key = key.strip()
+                if key == "model name" and model == "unknown":
+                    model = val.strip()
+                elif key == "physical id":
+                    sockets.add(val.strip())
+    except OSError:
+        pass
+    return {"model": model, "sockets": max(1, len(sockets))}
 
 
 def main(argv=None) -> int:
