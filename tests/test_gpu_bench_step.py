@@ -58,3 +58,65 @@ def test_bench_step_matches_oracle(parts, name, kw):
     for k, t in got.items():
         err = fro_rel(t.cpu().numpy(), ref["noisy"][k])
         assert err <= tol, (k, err)
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def test_full_size_step_sampled(parts):
+    """The benchmark's step at its full size (GPT-2-small, tied head V = 50257,
+    B = 32, T = 128: every GEMM-shaped tensor in one noised launch with its
+    split tail, the embedding rows on the second stream) against the oracle
+    on what it can compute one piece at a time: every example's norm (for
+    the clip factors), and sampled rows of the noisy sums of five linear
+    layers and of the tied matrix, noise included."""
+    bench, dp = parts
+    wl = gen.make_workload("gpt2-step", ldz=50304)
+    B, T, L, h = wl.B, wl.T, len(wl.linears), wl.head
+    _say(f"full-size step: {L} linears + tied head V={h.V}, B={B}, T={T}")
+    st = bench.Step(wl, dp, torch)
+    st.run()
+    torch.cuda.synchronize()
+    seed, step_id = 1234, 0                     # the step's noise key (first step)
+    norms = O.per_example_norms(wl)
+    _say("  oracle norms done")
+    c = O.clip_factors(norms["total"], wl.C)
+    tol = TOL["bf16"]
+    assert rel(st.total_norm2().cpu().numpy(), norms["total"]).max() <= tol
+    assert rel(st.c.cpu().numpy(), c).max() <= tol
+    sc = wl.sigma * wl.C
+    for l in (0, 1, 2, 3, L - 1):
+        lay = wl.linears[l]
+        rows = [0, lay.d_in // 2 + 3, lay.d_in - 1]
+        S = sum(c[i] * O.linear_grad(O.decode(lay.A[i][:, rows], "bf16"),
+                                     O.decode(lay.G[i], "bf16")) for i in range(B))
+        z = np.stack([O.gaussian(lay.d_out, seed, l, step_id, start=r * lay.d_out) for r in rows])
+        got = st.outs[l].cpu().numpy()[rows]
+        err = fro_rel(got, (S + sc * z) / B)
+        # the noise (~sigma C) dwarfs the clipped sum (~1e-3 here): the sum
+        # is also checked alone, with the oracle's noise taken out
+        err_s = fro_rel(got * B - sc * z, S)
+        _say(f"  linear {l} ({lay.d_in}x{lay.d_out}) rows {rows}: fro rel err {err:.2e}, "
+             f"clipped sum alone {err_s:.2e}")
+        assert err <= tol and err_s <= tol, (l, err, err_s)
+    # tied matrix rows: the most frequent id, an id no token carries, the last
+    # rows (the head's last output tiles)
+    ids = h.ids
+    counts = np.bincount(ids.ravel(), minlength=h.V)
+    absent = int(np.flatnonzero(counts == 0)[0])
+    rows = [int(counts.argmax()), absent, h.V - 300, h.V - 1]
+    n = len(rows)
+    where = {v: k for k, v in enumerate(rows)}
+    S = np.zeros((n, h.d))
+    for i in range(B):
+        ids_map = np.array([where.get(int(v), n) for v in ids[i]])
+        gE = O.embedding_grad(ids_map, O.decode(h.dE[i], "bf16"), n + 1)[:n]
+        gW = O.head_grad(O.decode(h.H[i], "bf16"), O.decode(h.Gz[i][:, rows], "bf16"), n)
+        S += c[i] * (gE + gW)
+    z = np.stack([O.gaussian(h.d, seed, L, step_id, start=r * h.d) for r in rows])
+    got = st.E.cpu().numpy()[rows]
+    err = fro_rel(got, (S + sc * z) / B)
+    err_s = fro_rel(got * B - sc * z, S)
+    _say(f"  tied matrix rows {rows}: fro rel err {err:.2e}, clipped sum alone {err_s:.2e}")
+    assert err <= tol and err_s <= tol
