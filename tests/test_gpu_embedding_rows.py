@@ -60,6 +60,7 @@ CASES = [
     ("bf16", 4, 64, 50, 64, "same", 0, False),      # one run through every block
     ("f32", 1, 1, 10, 8, "uniform", 0, False),      # a single token
     ("bf16", 32, 128, 50257, 768, "zipf", 0, False),  # GPT-2 step
+    ("bf16", 64, 256, 50257, 768, "zipf", 0, False),  # B*T = 16384, the most the sort takes
 ]
 
 

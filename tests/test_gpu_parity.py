@@ -141,7 +141,8 @@ def test_head_norm(dp, dtype, V, ldz):
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("kind,T,V", [("zipf", 130, 50257), ("uniform", 16, 512),
                                       ("same", 64, 1000), ("distinct", 100, 300),
-                                      ("zipf", 1, 50257), ("zipf", 1024, 50257)])
+                                      ("zipf", 1, 50257), ("zipf", 1024, 50257),
+                                      ("zipf", 4096, 50257)])  # the most tokens bucketed in LDS
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_embedding_norm_and_buckets(dp, kind, T, V, dtype):
     B, d = 3, 200
