@@ -52,9 +52,19 @@ extern "C" {
 
 #define DP_ABI_VERSION 2
 
-typedef enum { DP_F32 = 0, DP_BF16 = 1 } dp_dtype_t;
+/* Enumerations are int-sized in both languages. Compiled as C++ they have
+ * int as their fixed underlying type, so that every int a C caller passes
+ * (an unknown dtype, say, which the entry points reject) is a value of the
+ * type: C++ leaves values outside an unfixed enumeration's range undefined. */
+#ifdef __cplusplus
+#define DP_INT_ENUM(tag) enum tag : int
+#else
+#define DP_INT_ENUM(tag) enum tag
+#endif
 
-typedef enum {
+typedef DP_INT_ENUM(dp_dtype_e) { DP_F32 = 0, DP_BF16 = 1 } dp_dtype_t;
+
+typedef DP_INT_ENUM(dp_status_e) {
   DP_OK = 0,
   DP_EINVAL = 1,
   DP_EUNSUPPORTED = 2,
@@ -73,7 +83,7 @@ typedef enum {
  *         to the direct kernel's on MI355X (bf16, T = 1024: ~560 vs ~980
  *         TFLOP/s). With it AUTO picked the faster kernel for every GPT-2
  *         layer shape at T = 128, 256 and 1024. */
-typedef enum { DP_NORM_AUTO = 0, DP_NORM_GRAM = 1, DP_NORM_DIRECT = 2 } dp_norm_algo_t;
+typedef DP_INT_ENUM(dp_norm_algo_e) { DP_NORM_AUTO = 0, DP_NORM_GRAM = 1, DP_NORM_DIRECT = 2 } dp_norm_algo_t;
 
 /* One linear layer y = x W with W [d_in, d_out]: activations A [B,T,d_in]
  * (row stride lda) entering it and output gradients G [B,T,d_out] (row

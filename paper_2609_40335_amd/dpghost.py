@@ -51,7 +51,9 @@ class dp_vector_t(ctypes.Structure):
 
 
 def library_path() -> str:
-    return os.path.join(_HERE, "libdpghost.so")
+    """libdpghost.so beside this file, or the library that DPGHOST_LIBRARY
+    names (a build of the host code with sanitizers, say)."""
+    return os.environ.get("DPGHOST_LIBRARY") or os.path.join(_HERE, "libdpghost.so")
 
 
 _VP, _I, _I64, _U64, _F, _SZ = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_uint64,

@@ -306,6 +306,7 @@ def test_noise_rejects_bad_arguments(L):
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.delenv("DPGHOST_LIBRARY", raising=False)
     monkeypatch.setattr(D, "_LIB", None)
     monkeypatch.setattr(D, "_HERE", str(tmp_path))
     with pytest.raises(D.DPError, match="not built"):
