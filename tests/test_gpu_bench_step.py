@@ -120,3 +120,34 @@ def test_full_size_step_sampled(parts):
     err_s = fro_rel(got * B - sc * z, S)
     _say(f"  tied matrix rows {rows}: fro rel err {err:.2e}, clipped sum alone {err_s:.2e}")
     assert err <= tol and err_s <= tol
+
+
+def _snapshot(st):
+    outs = [st.total_norm2(), st.c, st.c_b, *st.outs, st.E]
+    for name in ("W", "P"):
+        t = getattr(st, name, None)
+        if t is not None:
+            outs.append(t)
+    outs += list(getattr(st, "vec_outs", None) or [])
+    return [t.detach().clone() for t in outs]
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("gpt2-full", dict(B=4, T=32, n_blocks=1, V=4000, ldz=4032)),
+    ("gpt2-step", dict(ldz=50304)),
+], ids=["gpt2-full-small", "gpt2-step"])
+def test_bench_step_is_deterministic(parts, name, kw):
+    """Two runs of the benchmark's step with the same noise key give the same
+    bits in every output: its reductions have a fixed order (no float
+    atomics), across both streams and the split tail."""
+    bench, dp = parts
+    wl = gen.make_workload(name, **kw)
+    st = bench.Step(wl, dp, torch)
+    runs = []
+    for _ in range(2):
+        st.step_id = 0
+        st.run()
+        torch.cuda.synchronize()
+        runs.append(_snapshot(st))
+    for k, (a, b) in enumerate(zip(*runs)):
+        assert torch.equal(a, b), k
