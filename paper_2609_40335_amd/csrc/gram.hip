@@ -406,11 +406,13 @@ __global__ __launch_bounds__(GR_THREADS) void gram_norm_kernel(GramArgs args) {
 // past the range; a chunk that straddles it is masked in LDS after it lands.
 // SINGLE (T <= 128): 16 KB stages, two workgroups per CU; otherwise 32 KB
 // stages and one workgroup per CU.
-// The loads carry the non-temporal hint at device scope (sc1 nt): each byte
-// is read once (a head's activation rows, re-read per logit chunk, still hit
-// L2), and the hint keeps the streamed lines from crowding the caches. The
-// T = 128 Gram of a GPT-2 step went from 5.7 to 6.4 TB/s with it, the
-// T = 256 one from 4.5 to 4.8 TB/s.
+// In single-tile launches the loads carry the non-temporal hint at device
+// scope (sc1 nt): each byte is read once (a head's activation rows, re-read
+// per logit chunk, still hit L2), and the hint keeps the streamed lines from
+// crowding the caches. The T = 128 Gram of a GPT-2 step went from 5.7 to
+// 6.4 TB/s with it, the T = 256 one from 4.5 to 4.8 TB/s. Tile-pair launches
+// (T > 256) read every T-tile once per pair it belongs to, so their loads keep
+// the temporal hint (sc1 only): with nt the T = 1024 Gram took 8-14 % longer.
 constexpr int DG_NS = 4;
 constexpr int DG_ROWB = 128;                  // 64 bf16 per LDS row
 
@@ -468,7 +470,7 @@ __device__ __forceinline__ float bias_finish(const float* bred, float* out, int6
   return v * v;
 }
 
-template <int PAT>
+template <int PAT, bool STREAM>
 __device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int ti, int tj,
                                          int chunk, u32x4* ring, float* bred) {
   constexpr int NB = PatNB<PAT>::NB;
@@ -521,8 +523,12 @@ __device__ __forceinline__ float dg_item(const GramLayer& L, int b, int T, int t
           (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)(ex_row0 + 8 * t) * ld));
       // Issued from asm so that the compiler does not drain all of them before
       // every LDS read; M0 has no other user in this kernel.
-      asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 nt lds"
-                   :: "s"(m0v), "v"(voff), "s"(d), "s"(so));
+      if constexpr (STREAM)
+        asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 nt lds"
+                     :: "s"(m0v), "v"(voff), "s"(d), "s"(so));
+      else
+        asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 lds"
+                     :: "s"(m0v), "v"(voff), "s"(d), "s"(so));
     }
   };
   // Zero the features at or past c1 inside the chunk that straddles c1.
@@ -630,11 +636,11 @@ __global__ __launch_bounds__(GR_THREADS, SINGLE ? 2 : 1) void dl_gram_kernel(Gra
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   float part;
   if (!SINGLE && ti != tj)
-    part = dg_item<PAT_OFF>(L, b, a.T, ti, tj, chunk, ring, bred);
+    part = dg_item<PAT_OFF, false>(L, b, a.T, ti, tj, chunk, ring, bred);
   else if (w < 2)
-    part = dg_item<PAT_D1>(L, b, a.T, ti, tj, chunk, ring, bred);
+    part = dg_item<PAT_D1, SINGLE>(L, b, a.T, ti, tj, chunk, ring, bred);
   else
-    part = dg_item<PAT_D2>(L, b, a.T, ti, tj, chunk, ring, bred);
+    part = dg_item<PAT_D2, SINGLE>(L, b, a.T, ti, tj, chunk, ring, bred);
   part = wave_sum(part);
   if ((threadIdx.x & 63) == 0) red[w] = part;
   __syncthreads();
