@@ -183,13 +183,19 @@ dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, 
 
 /* ---------------------------------------------------------------------
  * Clip factors (eq. 2, eq. 7): c[b] = min(1, C / sqrt(norm2[b])), and 1
- * when norm2[b] <= 0. C must be positive and finite.
+ * when norm2[b] <= 0. A squared norm that is not finite (inf from an
+ * overflow, or NaN) gives c[b] = 0: min(1, C/inf) is 0, and NaN is read the
+ * same way, so that no such example enters a sum unclipped (eq. 2). Every
+ * clipped-sum entry point below leaves an example with c[b] = 0 out (it is
+ * skipped, not multiplied by zero), so inf or NaN in its operands cannot
+ * reach the outputs. C must be positive and finite.
  * ------------------------------------------------------------------- */
 dp_status_t dp_clip_factors(const float* norm2, int B, float C, float* c, void* stream);
 
 /* ---------------------------------------------------------------------
  * Scaled clip factors (eq. 2, eq. 7 and the 1/B of eq. 3):
- *   c_scaled[b] = scale * min(1, C / sqrt(norm2[b]))   (1 when norm2 <= 0)
+ *   c_scaled[b] = scale * min(1, C / sqrt(norm2[b]))   (1 when norm2 <= 0,
+ *                                                         0 when not finite)
  * evaluated in double and rounded once to fp32; c (may be NULL) receives
  * the unscaled factors of dp_clip_factors in the same launch. With scale =
  * 1/B these factors let an embedding-form clipped sum add its part of eq. 3
@@ -212,6 +218,7 @@ dp_status_t dp_clip_factors_scaled2(const float* norm2_a, const float* norm2_b, 
  * of the loss reweighted by the clip factors, as one GEMM over the B*T
  * tokens (K = B*T) with token k of example b scaled by c[b]:
  *   out (+)= sum_b c[b] A_b^T G_b            [d_in, d_out]
+ * (examples with c[b] = 0 are left out, whatever their rows hold)
  * or its transpose [d_out, d_in] when transpose_out = 1 (out is contiguous).
  * Embedding form: pass A = NULL and ids [B,T]; A_b is then onehot(ids_b)
  * with d_in = V, i.e. out[v,:] (+)= sum over tokens with id v of

@@ -24,6 +24,9 @@ gradient is materialised in fp64 and its norm taken directly.
 
 Readings taken where the paper is silent:
   * ||g_i|| = 0 gives R_i = 1 (the limit of min(1, C/x) as x -> 0).
+  * A squared norm that is not finite gives R_i = 0 (min(1, C/inf) = 0; NaN
+    is read the same way), and such an example is left out of every clipped
+    sum rather than multiplied by 0, so the bound of eq. 2 holds for it.
   * The batch divisor of eq. 3 is the actual batch size B.
   * "N(0, s^2 C^2 I)" is drawn with standard deviation s*C per coordinate; a
     tied matrix is one tensor and is noised once.
@@ -189,47 +192,62 @@ def buckets(ids: np.ndarray):
 # Clipping and the clipped sum
 # --------------------------------------------------------------------------
 def clip_factors(norm2: np.ndarray, C: float) -> np.ndarray:
-    """R_i = min(1, C / ||g_i||) (eq. 2, eq. 7), with R_i = 1 when ||g_i|| = 0."""
-    n = np.sqrt(np.asarray(norm2, dtype=np.float64))
-    c = np.ones_like(n)
-    nz = n > 0
-    c[nz] = np.minimum(1.0, C / n[nz])
+    """R_i = min(1, C / ||g_i||) (eq. 2, eq. 7), with R_i = 1 when ||g_i|| = 0
+    and R_i = 0 when ||g_i||^2 is not finite (inf, where min(1, C/inf) = 0,
+    and NaN, read the same way so that such an example can never enter the
+    sum unclipped)."""
+    n2 = np.asarray(norm2, dtype=np.float64)
+    c = np.zeros(n2.shape)
+    fin = np.isfinite(n2)
+    n = np.sqrt(np.where(fin & (n2 > 0), n2, 1.0))
+    c[fin] = np.where(n2[fin] > 0, np.minimum(1.0, C / n[fin]), 1.0)
     return c
+
+
+def _kept(c, i) -> bool:
+    """An example with R_i = 0 contributes nothing to a clipped sum: it is
+    left out rather than multiplied by 0 (0 * inf would be NaN)."""
+    return c[i] != 0.0
 
 
 def clipped_sum_linear(A, G, c) -> np.ndarray:
     """sum_i c_i g_i for one linear layer (the bracket of eq. 3 without noise)."""
     S = np.zeros((A.shape[2], G.shape[2]))
     for i in range(A.shape[0]):
-        S += c[i] * linear_grad(A[i], G[i])
+        if _kept(c, i):
+            S += c[i] * linear_grad(A[i], G[i])
     return S
 
 
 def clipped_sum_embedding(ids, dE, c, V) -> np.ndarray:
     S = np.zeros((V, dE.shape[2]))
     for i in range(ids.shape[0]):
-        S += c[i] * embedding_grad(ids[i], dE[i], V)
+        if _kept(c, i):
+            S += c[i] * embedding_grad(ids[i], dE[i], V)
     return S
 
 
 def clipped_sum_head(H, Gz, c, V) -> np.ndarray:
     S = np.zeros((V, H.shape[2]))
     for i in range(H.shape[0]):
-        S += c[i] * head_grad(H[i], Gz[i], V)
+        if _kept(c, i):
+            S += c[i] * head_grad(H[i], Gz[i], V)
     return S
 
 
 def clipped_sum_vector(X: Optional[np.ndarray], G: np.ndarray, c) -> np.ndarray:
     S = np.zeros(G.shape[2])
     for i in range(G.shape[0]):
-        S += c[i] * vector_grad(None if X is None else X[i], G[i])
+        if _kept(c, i):
+            S += c[i] * vector_grad(None if X is None else X[i], G[i])
     return S
 
 
 def clipped_sum_positional(dE: np.ndarray, c, n_pos: int) -> np.ndarray:
     S = np.zeros((n_pos, dE.shape[2]))
     for i in range(dE.shape[0]):
-        S += c[i] * positional_grad(dE[i], n_pos)
+        if _kept(c, i):
+            S += c[i] * positional_grad(dE[i], n_pos)
     return S
 
 
@@ -371,16 +389,22 @@ def step(wl, seed: int = 0, step_id: int = 0, examples: Optional[List[int]] = No
     for l, lay in enumerate(wl.linears):
         S = np.zeros((lay.d_in, lay.d_out))
         for k, i in enumerate(ex):
+            if not _kept(c, k):
+                continue
             S += c[k] * linear_grad(decode(lay.A[i], dt), decode(lay.G[i], dt))
         sums[lay.name] = S
     h = wl.head
     if h is not None:
         SE = np.zeros((h.V, h.d))
         for k, i in enumerate(ex):
+            if not _kept(c, k):
+                continue
             SE += c[k] * embedding_grad(h.ids[i], decode(h.dE[i], dt), h.V)
         if h.H is not None:
             SW = np.zeros((h.V, h.d))
             for k, i in enumerate(ex):
+                if not _kept(c, k):
+                    continue
                 SW += c[k] * head_grad(decode(h.H[i], dt), decode(h.Gz[i], dt), h.V)
             if h.tied:
                 sums["wte"] = SE + SW
@@ -391,12 +415,16 @@ def step(wl, seed: int = 0, step_id: int = 0, examples: Optional[List[int]] = No
     for vec in getattr(wl, "vectors", []):
         S = np.zeros(vec.d)
         for k, i in enumerate(ex):
+            if not _kept(c, k):
+                continue
             X = None if vec.X is None else decode(vec.X[i], dt)
             S += c[k] * vector_grad(X, decode(vec.G[i], dt))
         sums[vec.name] = S
     if getattr(wl, "n_pos", 0):
         SP = np.zeros((wl.n_pos, h.d))
         for k, i in enumerate(ex):
+            if not _kept(c, k):
+                continue
             SP += c[k] * positional_grad(decode(h.dE[i], dt), wl.n_pos)
         sums["wpe"] = SP
     noisy: Dict[str, np.ndarray] = {}

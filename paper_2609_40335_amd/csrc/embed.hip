@@ -321,7 +321,8 @@ __global__ __launch_bounds__(ES_WAVES * WAVE) void embed_block_kernel(EmbedSumAr
     const uint32_t kj = j < n ? (uint32_t)__builtin_amdgcn_readlane((int)mykey, j) : lastkey;
     const float cj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, myc), j));
     const float v = load_elem<DT>(a.E, (int64_t)(kj & pmask) * a.lde + fs);
-    ev[j] = (j < n && fok) ? cj * v : 0.f;
+    // A token of an example with c = 0 (a non-finite norm) is left out.
+    ev[j] = (j < n && fok && cj != 0.f) ? cj * v : 0.f;
   }
   float acc = 0.f;
   int run_start = 0;

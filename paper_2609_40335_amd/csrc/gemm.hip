@@ -407,9 +407,11 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(GemmArgs args) {
 }
 
 // Scaling of the clipped sum: SC_NONE (direct norm), SC_STAGE (rows scaled
-// while staged, any T), SC_ACC (every stage lies inside one example, so the
-// fp32 accumulators are rescaled by c_prev / c_next at example boundaries and
-// by the last factor at the end; examples with c = 0 are skipped).
+// while staged, any T; rows of examples with c = 0 zeroed in both operands),
+// SC_ACC (every stage lies inside one example, so the fp32 accumulators are
+// rescaled by c_prev / c_next at example boundaries and by the last factor at
+// the end; examples with c = 0 are skipped). Either way an example with
+// c = 0 contributes nothing, even where its rows hold inf or NaN.
 enum { SC_NONE = 0, SC_STAGE = 1, SC_ACC = 2 };
 
 template <int DT, bool VEC, int MODE, int SC>
@@ -478,12 +480,18 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
     // direct norm, whose tile sum must not see them (nor the next example).
     load_block<DT, VEC, MODE == MODE_NORM, MODE == MODE_NORM>(
         rsrc, voff, (uint32_t)(ks0 * ld_bytes), ld_bytes, r0, k_end - ks0, col, ncol, r);
-    if (SC == SC_STAGE && stage_x) {
+    if (SC == SC_STAGE) {
 #pragma unroll
       for (int j = 0; j < P::RPT; ++j) {
         int64_t e = (int64_t)(((double)(ks0 + r0 + j) + 0.5) * invT);
         e = e < a.B ? e : a.B - 1;
         sc[j] = a.c[e];
+        // An example with c = 0 (a non-finite norm) is left out of the sum:
+        // its rows are zeroed in both operands (0 * inf would be NaN).
+        if (sc[j] == 0.f) {
+#pragma unroll
+          for (int h = 0; h < P::CPR; ++h) r[j * P::CPR + h] = u32x4{0u, 0u, 0u, 0u};
+        }
       }
     }
   };

@@ -5,10 +5,14 @@
 namespace dpg {
 
 // c_i = min(1, C / ||g_i||), and 1 when the norm is 0 (the limit of the
-// expression); computed in double and rounded once. cs (optional) receives
-// scale * c_i, also rounded once from double; c may be null when only cs is
-// wanted. The squared norm is norm2[i], plus norm2_b[i] (in fp32, as an
-// accumulating norm call would add it) when a second part is given.
+// expression); computed in double and rounded once. A squared norm that is
+// not finite (inf, or NaN from an overflowed or corrupt gradient) gives
+// c_i = 0: min(1, C/inf) is 0, and a NaN norm is read the same way, so that
+// no such example can enter the sum unclipped (the bound of eq. 2). cs
+// (optional) receives scale * c_i, also rounded once from double; c may be
+// null when only cs is wanted. The squared norm is norm2[i], plus norm2_b[i]
+// (in fp32, as an accumulating norm call would add it) when a second part is
+// given.
 __global__ void clip_factors_kernel(const float* __restrict__ norm2,
                                     const float* __restrict__ norm2_b, int B, float C, float scale,
                                     float* c, float* cs) {
@@ -16,7 +20,9 @@ __global__ void clip_factors_kernel(const float* __restrict__ norm2,
   if (i >= B) return;
   const double n2 = (double)(norm2_b ? norm2[i] + norm2_b[i] : norm2[i]);
   double r = 1.0;
-  if (n2 > 0.0) {
+  if (!__builtin_isfinite(n2)) {
+    r = 0.0;
+  } else if (n2 > 0.0) {
     r = (double)C / sqrt(n2);
     if (r > 1.0) r = 1.0;
   }

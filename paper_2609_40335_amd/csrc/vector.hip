@@ -202,10 +202,12 @@ __global__ __launch_bounds__(256) void vec_sum_kernel(VecSumArgs a) {
         for (int k = 0; k < 4; ++k) g[u][k] = f + k < P.d ? gp[k] : 0.f;
       }
     }
+    // An example with c = 0 (a non-finite norm) is left out, not multiplied
+    // by zero: its gradient may hold inf or NaN.
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int k = 0; k < 4; ++k) s[k] += ci[u] * g[u][k];
+      for (int k = 0; k < 4; ++k) s[k] += ci[u] != 0.f ? ci[u] * g[u][k] : 0.f;
   }
   float z[4] = {0.f, 0.f, 0.f, 0.f};
   if (a.noise) gauss4((uint64_t)f >> 2, a.seed, P.tensor_id, a.step, z);
@@ -272,7 +274,7 @@ __global__ __launch_bounds__(256) void pos_sum_kernel(PosSumArgs a) {
 #pragma unroll
       for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int k = 0; k < 4; ++k) s[k] += ci[u] * e[u][k];
+        for (int k = 0; k < 4; ++k) s[k] += ci[u] != 0.f ? ci[u] * e[u][k] : 0.f;  // c = 0: left out
     }
   }
   float* o = a.out + (int64_t)t * a.ldo + f;

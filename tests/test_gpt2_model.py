@@ -20,7 +20,7 @@ pytest.importorskip("transformers")
 import oracle as O  # noqa: E402
 from workloads import gen  # noqa: E402
 from tests import gpt2_capture as cap  # noqa: E402
-from tests.helpers import TOL, dev, fro_rel, host, rel  # noqa: E402
+from tests.helpers import TOL, assert_close, dev, fro_rel, host, rel  # noqa: E402
 
 
 def _say(*a):
@@ -81,7 +81,7 @@ def test_oracle_on_captured_gpt2():
     assert (r["c"] < 1).all()  # C small enough that every example is clipped
     for name in _names(wl):
         ref = np.tensordot(r["c"], true[cap.hf_name(name)], axes=(0, 0))
-        assert fro_rel(r["sums"][name], ref) <= 1e-5, name
+        assert_close(r["sums"][name], ref, 1e-5, name)
 
 
 def _library_step(dp, wl, seed=5, step=2, sigma=None):
@@ -153,7 +153,7 @@ def test_library_on_captured_gpt2_fp32(dp):
     for tid, name in enumerate(_names(wl)):
         S = np.tensordot(c_ref, true[cap.hf_name(name)], axes=(0, 0))
         ref = O.add_noise(S, wl.sigma, wl.C, B, 5, tid, 2)
-        assert fro_rel(outs[name], ref) <= TOL["f32"], name
+        assert_close(outs[name], ref, TOL["f32"], name)
 
 
 @pytest.mark.gpu
@@ -177,6 +177,10 @@ def test_library_on_captured_gpt2_widths_bf16(dp):
     worst = 0.0
     for name in _names(wl):
         S = np.tensordot(c_ref, true[cap.hf_name(name)], axes=(0, 0)) / B
+        # Against the model's true fp32 per-example gradients, from operands
+        # the library received rounded to bf16: a whole-tensor bar (the
+        # element-wise parity with the oracle on identical operands is in
+        # the parity tests).
         err = fro_rel(outs[name], S)
         worst = max(worst, err)
         assert err <= TOL["bf16"], (name, err)

@@ -11,7 +11,7 @@ import pytest
 
 import oracle as O
 from workloads import gen
-from tests.helpers import TOL, dev, fro_rel, host
+from tests.helpers import TOL, assert_close, dev, host
 
 pytestmark = pytest.mark.gpu
 
@@ -81,9 +81,8 @@ def test_rows_then_add_equals_one_call(dp, dtype, B, T, V, d, kind, bad_every, t
     assert torch.equal(one, two)
     ref = _oracle(ids, dE, c, bad, V, dtype)
     got = host(two - prior)
-    err = fro_rel(got.T if tr else got, ref)
-    _say(f"  fro rel err vs oracle {err:.3e}")
-    assert err <= TOL[dtype]
+    err = assert_close(got.T if tr else got, ref, TOL[dtype])
+    _say(f"  fro / element rel err vs oracle {err[0]:.3e} / {err[1]:.3e}")
 
 
 def test_workspace_reused_with_new_ids(dp):
@@ -97,7 +96,7 @@ def test_workspace_reused_with_new_ids(dp):
         rows.compute(dev(dE, "bf16"), dev(ids), dev(c))
         rows.add_to(out)
         ref = _oracle(ids, dE, c, bad, V, "bf16")
-        assert fro_rel(host(out), ref) <= TOL["bf16"], kind
+        assert_close(host(out), ref, TOL["bf16"], kind)
 
 
 def test_rows_beside_a_writer_of_out(dp):

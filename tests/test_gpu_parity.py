@@ -11,7 +11,7 @@ import pytest
 
 import oracle as O
 from workloads import gen
-from tests.helpers import TOL, dev, fro_rel, host, rel
+from tests.helpers import TOL, assert_close, dev, fro_rel, host, rel
 
 pytestmark = pytest.mark.gpu
 
@@ -298,14 +298,13 @@ def test_clipped_sum_linear(dp, case, transpose):
                            transpose_out=transpose)
     got = host(out)
     got = got.T if transpose else got
-    err = fro_rel(got, ref)
-    _say(f"  fro rel err {err:.3e}")
-    assert err <= TOL[dtype]
+    err = assert_close(got, ref, TOL[dtype])
+    _say(f"  fro / element rel err {err[0]:.3e} / {err[1]:.3e}")
     dp.dp_clipped_grad_sum(dev(A, dtype)[:, :, :d_in], dev(G, dtype)[:, :, :d_out], dev(c), out,
                            transpose_out=transpose, accumulate=True)
     got2 = host(out)
     got2 = got2.T if transpose else got2
-    assert fro_rel(got2, 2 * ref) <= TOL[dtype]
+    assert_close(got2, 2 * ref, TOL[dtype])
 
 
 # bf16 sums on 16-byte aligned rows with T % 32 == 0 take the direct-load
@@ -342,9 +341,8 @@ def test_clipped_sum_direct_load(dp, case, transpose):
     got = host(out)
     got = got.T if transpose else got
     assert np.isfinite(got).all()
-    err = fro_rel(got, ref)
-    _say(f"  fro rel err {err:.3e}")
-    assert err <= TOL["bf16"]
+    err = assert_close(got, ref, TOL["bf16"])
+    _say(f"  fro / element rel err {err[0]:.3e} / {err[1]:.3e}")
 
 
 NOISED_CASES = [
@@ -382,7 +380,7 @@ def test_clipped_sum_noised(dp, case, transpose):
     dp.dp_clipped_grad_sum_grouped(layers, plain, dev(c), transpose_out=transpose)
     for l in range(len(shapes)):
         got = host(outs[l])
-        assert fro_rel(got, refs[l]) <= TOL[dtype]
+        assert_close(got, refs[l], TOL[dtype])
         if acc[l]:
             plain[l] += dev(priors[l])
         dp.dp_add_noise(plain[l], sigma, C, B, seed, tids[l], step)
@@ -393,7 +391,7 @@ def test_clipped_sum_noised(dp, case, transpose):
         # multiple of the stage depth) the rounding then falls on the other
         # operand; elsewhere the two paths agree to fp32 accumulation.
         exact = dtype == "f32" or T % 64 == 0
-        assert fro_rel(got, host(plain[l])) <= (1e-5 if exact else 2e-3)
+        assert_close(got, host(plain[l]), 1e-5 if exact else 2e-3)
 
 
 SPLIT_CASES = [
@@ -432,10 +430,9 @@ def test_clipped_sum_split_tail(dp, case):
     for l in range(len(shapes)):
         got, ref = host(split[l]), refs[l]
         assert np.isfinite(got).all()
-        assert fro_rel(got, host(plain[l])) <= 1e-5
-        err = fro_rel(got, ref)
-        _say(f"  split tail layer {l}: vs oracle {err:.2e}")
-        assert err <= TOL["bf16"]
+        assert_close(got, host(plain[l]), 1e-5)
+        err = assert_close(got, ref, TOL["bf16"])
+        _say(f"  split tail layer {l}: vs oracle {err[0]:.2e} / {err[1]:.2e}")
 
 
 def test_clipped_sum_many_examples(dp):
@@ -447,7 +444,7 @@ def test_clipped_sum_many_examples(dp):
     ref = O.clipped_sum_linear(O.decode(A, "bf16"), O.decode(G, "bf16"), c.astype(np.float64))
     out = torch.zeros((d_in, d_out), device="cuda")
     dp.dp_clipped_grad_sum(dev(A, "bf16"), dev(G, "bf16"), dev(c), out)
-    assert fro_rel(host(out), ref) <= TOL["bf16"]
+    assert_close(host(out), ref, TOL["bf16"])
 
 
 def test_clipped_sum_grouped(dp):
@@ -463,7 +460,7 @@ def test_clipped_sum_grouped(dp):
                                          c.astype(np.float64)))
     dp.dp_clipped_grad_sum_grouped(layers, outs, dev(c))
     for o, r in zip(outs, refs):
-        assert fro_rel(host(o), r) <= TOL["bf16"]
+        assert_close(host(o), r, TOL["bf16"])
 
 
 @pytest.mark.parametrize("dtype,B,T,V,d,kind", [("f32", 4, 16, 512, 64, "uniform"),
@@ -478,13 +475,12 @@ def test_clipped_sum_embedding(dp, dtype, B, T, V, d, kind):
     ref = O.clipped_sum_embedding(ids, O.decode(dE, dtype), c.astype(np.float64), V)
     out = torch.full((V, d), 5.0, device="cuda")
     dp.dp_clipped_grad_sum(None, dev(dE, dtype), dev(c), out, ids=dev(ids), V=V)
-    err = fro_rel(host(out), ref)
-    _say(f"  fro rel err {err:.3e}")
-    assert err <= TOL[dtype]
+    err = assert_close(host(out), ref, TOL[dtype])
+    _say(f"  fro / element rel err {err[0]:.3e} / {err[1]:.3e}")
     outT = torch.zeros((d, V), device="cuda")
     dp.dp_clipped_grad_sum(None, dev(dE, dtype), dev(c), outT, ids=dev(ids), V=V,
                            transpose_out=True)
-    assert fro_rel(host(outT).T, ref) <= TOL[dtype]
+    assert_close(host(outT).T, ref, TOL[dtype])
 
 
 def test_clipped_sum_embedding_invalid_ids(dp):
@@ -504,7 +500,7 @@ def test_clipped_sum_embedding_invalid_ids(dp):
     ref = O.clipped_sum_embedding(ids_ref, dE_ref, c.astype(np.float64), V)
     out = torch.full((V, d), 2.0, device="cuda")
     dp.dp_clipped_grad_sum(None, dev(dE, "bf16"), dev(c), out, ids=dev(ids), V=V)
-    assert fro_rel(host(out), ref) <= TOL["bf16"]
+    assert_close(host(out), ref, TOL["bf16"])
 
 
 @pytest.mark.parametrize("T,ldz", [(100, 1001), (64, 1008)])   # general / direct-load head
@@ -519,7 +515,7 @@ def test_tied_clipped_sum_one_buffer(dp, T, ldz):
     out = torch.empty((V, d), device="cuda")
     dp.dp_clipped_grad_sum(dev(Gz, dtype)[:, :, :V], dev(H, dtype), dev(c), out)   # Gz^T H -> [V, d]
     dp.dp_clipped_grad_sum(None, dev(dE, dtype), dev(c), out, ids=dev(ids), V=V, accumulate=True)
-    assert fro_rel(host(out), ref) <= TOL[dtype]
+    assert_close(host(out), ref, TOL[dtype])
 
 
 # ---------------------------------------------------------------------------
@@ -534,9 +530,8 @@ def test_noise_matches_oracle_stream(dp):
     g = dev(S)
     dp.dp_add_noise(g, sigma, C, B, seed=0x1234_5678_9ABC, tensor_id=7, step=42)
     got = host(g)
-    err = fro_rel(got, ref)
-    _say(f"  noise fro rel err {err:.3e}")
-    assert err <= TOL["f32"]
+    err = assert_close(got, ref, TOL["f32"])
+    _say(f"  noise fro / element rel err {err[0]:.3e} / {err[1]:.3e}")
     z = (got.astype(np.float64) * B - S) / (sigma * C)
     zref = O.gaussian(n, seed=0x1234_5678_9ABC, tensor_id=7, step=42)
     zerr = np.abs(z - zref)
@@ -552,12 +547,12 @@ def test_noise_sigma_zero_and_unaligned(dp):
     S = gen.draw(9, 2, (1001,), 1.0, "f32")
     g = dev(S)
     dp.dp_add_noise(g, 0.0, 1.0, 4, 1, 2, 3)
-    assert fro_rel(host(g), S / 4) <= 1e-7
+    assert_close(host(g), S / 4, 1e-7)
     g2 = dev(S)
     sub = g2[1:]  # 4-byte but not 16-byte aligned
     dp.dp_add_noise(sub, 1.0, 1.0, 0, 1, 2, 3)
     ref = O.add_noise(S[1:].astype(np.float64), 1.0, 1.0, 0, 1, 2, 3)
-    assert fro_rel(host(sub), ref) <= TOL["f32"]
+    assert_close(host(sub), ref, TOL["f32"])
 
 
 @pytest.mark.parametrize("n,offset", [(1_000_003, 0), (1001, 1), (4, 0), (3, 2)])
@@ -572,7 +567,7 @@ def test_noise_fill(dp, n, offset):
     dp.dp_add_noise(zeros, sigma, C, B, seed=99, tensor_id=4, step=11)
     assert torch.equal(out, zeros)
     ref = O.add_noise(np.zeros(n), sigma, C, B, seed=99, tensor_id=4, step=11)
-    assert fro_rel(host(out), ref) <= TOL["f32"]
+    assert_close(host(out), ref, TOL["f32"])
 
 
 # ---------------------------------------------------------------------------
@@ -606,12 +601,12 @@ def test_tiny_step(dp, name):
         dp.dp_clipped_grad_sum(None, dE, c, E, ids=ids, V=h.V, accumulate=True)
     else:
         dp.dp_clipped_grad_sum(None, dE, c, E, ids=ids, V=h.V)
-    assert fro_rel(host(S), ref["sums"]["linear"]) <= TOL[dt]
-    assert fro_rel(host(E), ref["sums"]["wte"]) <= TOL[dt]
+    assert_close(host(S), ref["sums"]["linear"], TOL[dt])
+    assert_close(host(E), ref["sums"]["wte"], TOL[dt])
     dp.dp_add_noise(S, wl.sigma, wl.C, B, 3, 0, 5)
     dp.dp_add_noise(E, wl.sigma, wl.C, B, 3, 1, 5)
-    assert fro_rel(host(S), ref["noisy"]["linear"]) <= TOL[dt]
-    assert fro_rel(host(E), ref["noisy"]["wte"]) <= TOL[dt]
+    assert_close(host(S), ref["noisy"]["linear"], TOL[dt])
+    assert_close(host(E), ref["noisy"]["wte"], TOL[dt])
     # The same step in the benchmark's order: the noise fused into the GEMM
     # store (the tied head written first), then the embedding part added with
     # the factors c/B; an embedding without a tied head starts from noise alone.
@@ -627,8 +622,8 @@ def test_tiny_step(dp, name):
         dp.dp_clipped_grad_sum_noised_grouped([(A, G)], [S2], c, [0], wl.sigma, wl.C, B, 3, 5)
         dp.dp_noise_fill(E2, wl.sigma, wl.C, B, 3, 1, 5)
     dp.dp_clipped_grad_sum(None, dE, c_b, E2, ids=ids, V=h.V, accumulate=True)
-    assert fro_rel(host(S2), ref["noisy"]["linear"]) <= TOL[dt]
-    assert fro_rel(host(E2), ref["noisy"]["wte"]) <= TOL[dt]
+    assert_close(host(S2), ref["noisy"]["linear"], TOL[dt])
+    assert_close(host(E2), ref["noisy"]["wte"], TOL[dt])
 
 
 # ---------------------------------------------------------------------------
@@ -656,7 +651,7 @@ def test_full_size_gpt2_body_sampled(dp):
         Ad = O.decode(l.A[:, :, rows], "bf16")         # [B, T, 3]
         Gd = O.decode(l.G, "bf16")
         ref = sum(c[i] * Ad[i].T @ Gd[i] for i in range(B))
-        assert fro_rel(host(o)[rows], ref) <= TOL["bf16"]
+        assert_close(host(o)[rows], ref, TOL["bf16"])
 
 
 @pytest.mark.parametrize("algo", ["gram", "direct"])
@@ -735,6 +730,6 @@ def test_layer_table_extremes(dp, n_layers):
     dp.LinearGroup(layers, bias_grads=biases).ghost_norm(n2)
     assert rel(host(n2), ref_n2).max() <= TOL["bf16"]
     dp.dp_clipped_grad_sum_grouped([(a, g) for a, g, _ in layers], sums, dev(c))
-    worst = max(fro_rel(host(o), r) for o, r in zip(sums, refs))
+    worst = max(assert_close(host(o), r, TOL["bf16"])[1] for o, r in zip(sums, refs))
     _say(f"  norm rel err {rel(host(n2), ref_n2).max():.2e}, worst clipped sum {worst:.2e}")
     assert worst <= TOL["bf16"]

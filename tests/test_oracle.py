@@ -213,6 +213,54 @@ def test_clip_bounds():
     check_clip(O)
 
 
+def check_nonfinite_norms(o):
+    """A squared norm that is not finite (inf from an overflow, NaN) gives a
+    clip factor of 0 (min(1, C/inf) = 0; NaN read the same way), and the
+    example is left out of the clipped sum, which stays finite: the bound
+    ||c_i g_i|| <= C of eq. 2 holds for every example."""
+    c = o.clip_factors(np.array([np.inf, np.nan, -np.inf, 4.0, 0.0, -1e-20]), 1.0)
+    np.testing.assert_array_equal(c, [0.0, 0.0, 0.0, 0.5, 1.0, 1.0])
+    A = _rand(5, 4, 3)
+    G = _rand(5, 4, 2)
+    A[1, 2, 0] = np.nan
+    G[3, 0, 1] = np.inf
+    C = 0.8
+    n2 = o.linear_norm2(A, G)
+    assert not np.isfinite(n2[1]) and not np.isfinite(n2[3])
+    c = o.clip_factors(n2, C)
+    assert c[1] == 0.0 and c[3] == 0.0 and np.all(c[[0, 2, 4]] > 0)
+    S = o.clipped_sum_linear(A, G, c)
+    assert np.isfinite(S).all()
+    keep = [0, 2, 4]
+    ref = np.einsum("i,itm,itn->mn", c[keep], A[keep], G[keep])
+    np.testing.assert_allclose(S, ref, rtol=1e-12, atol=1e-12)
+    for i in keep:
+        assert np.sqrt(o.sqnorm(c[i] * o.linear_grad(A[i], G[i]))) <= C * (1 + 1e-12)
+
+
+def test_nonfinite_norms_are_clipped_to_zero():
+    check_nonfinite_norms(O)
+
+
+def test_nonfinite_example_left_out_of_every_sum():
+    """The whole step on a tied full-parameter workload with one NaN
+    activation in example 1 and one inf embedding gradient in example 2:
+    both get c = 0, every clipped sum is finite, and equals the step over the
+    other examples with the same factors."""
+    wl = gen.make_workload("c1-tied", full_params=True)
+    wl.linears[0].A = wl.linears[0].A.copy()
+    wl.linears[0].A[1, 3, 5] = np.nan
+    wl.head.dE = wl.head.dE.copy()
+    wl.head.dE[2, 0, 7] = np.inf
+    r = O.step(wl, noise=False)
+    assert r["c"][1] == 0.0 and r["c"][2] == 0.0 and np.all(r["c"][[0, 3]] > 0)
+    r_ok = O.step(wl, examples=[0, 3], noise=False)
+    np.testing.assert_array_equal(r_ok["c"], r["c"][[0, 3]])
+    for k, S in r["sums"].items():
+        assert np.isfinite(S).all(), k
+        np.testing.assert_allclose(S, r_ok["sums"][k], rtol=1e-12, atol=1e-15, err_msg=k)
+
+
 def check_huge_C_is_plain_gradient(o):
     """C -> infinity: the clipped sum is the non-private gradient, one GEMM over B*T rows."""
     A = _rand(4, 6, 5)
@@ -555,6 +603,22 @@ def test_pins_catch_clip_max_instead_of_min():
         c[nz] = np.maximum(1.0, C / n[nz])
         return c
     assert _fails(check_clip, _mutant(clip_factors=clip_bad))
+
+
+def test_pins_catch_nan_norm_summed_unclipped():
+    def clip_nan_is_one(norm2, C):     # NaN fails n > 0, so it keeps c = 1
+        n = np.sqrt(np.asarray(norm2, np.float64))
+        c = np.ones_like(n)
+        nz = n > 0
+        c[nz] = np.minimum(1.0, C / n[nz])
+        return c
+    assert _fails(check_nonfinite_norms, _mutant(clip_factors=clip_nan_is_one))
+
+
+def test_pins_catch_zero_factor_multiplied_not_skipped():
+    def sum_multiplies(A, G, c):       # 0 * inf = NaN
+        return np.einsum("i,itm,itn->mn", c, A, G)
+    assert _fails(check_nonfinite_norms, _mutant(clipped_sum_linear=sum_multiplies))
 
 
 def test_pins_catch_philox_wrong_rounds():
