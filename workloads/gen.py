@@ -9,9 +9,11 @@ distributions of those workloads.
 
 Recipe (all draws fp32, then rounded to bf16 by round-to-nearest-even when the
 workload is bf16):
-  * one independent stream per tensor: ``np.random.default_rng([seed, tag])``
-    with a fixed integer tag per tensor, so any subset of tensors can be
-    regenerated alone and always gets the same values;
+  * one independent stream per tensor and example: the [B, T, w] draws of
+    example b come from ``np.random.default_rng([seed, tag, b])`` with a fixed
+    integer tag per tensor (other shapes: one stream ``default_rng([seed,
+    tag])``), so any subset of tensors or examples can be regenerated alone
+    and always gets the same values, and examples are drawn in parallel;
   * linear layer l: activations A ~ N(0, a_std) [B,T,d_in] (tag 2l),
     output grads G ~ N(0, g_std) [B,T,d_out] (tag 2l+1); "N(0,s)" means
     standard deviation s;
@@ -33,6 +35,8 @@ Nothing here computes any part of the DP-SGD method.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 from typing import List, Optional
 
@@ -102,15 +106,48 @@ def gpt2_param_count(n_blocks: int, tied: bool, V: int = GPT2_VOCAB,
 # --------------------------------------------------------------------------
 # Draws
 # --------------------------------------------------------------------------
-def _rng(seed: int, tag: int) -> np.random.Generator:
-    return np.random.default_rng([int(seed), int(tag)])
+def _rng(seed: int, tag: int, example: Optional[int] = None) -> np.random.Generator:
+    key = [int(seed), int(tag)] if example is None else [int(seed), int(tag), int(example)]
+    return np.random.default_rng(key)
 
 
-def _normal(seed, tag, shape, std) -> np.ndarray:
-    x = _rng(seed, tag).standard_normal(size=shape, dtype=np.float32)
-    if std != 1.0:
-        x *= np.float32(std)
-    return x
+_POOL: Optional[ThreadPoolExecutor] = None
+
+
+def _per_example(fn, B: int) -> None:
+    """fn(b) for every example b, on a thread pool (numpy's generators and
+    ufuncs release the GIL on large arrays)."""
+    global _POOL
+    if B == 1:
+        fn(0)
+        return
+    if _POOL is None:
+        _POOL = ThreadPoolExecutor(max_workers=max(1, min(16, os.cpu_count() or 1)))
+    for f in [_POOL.submit(fn, b) for b in range(B)]:
+        f.result()
+
+
+def _normal(seed, tag, shape, std, enc=None) -> np.ndarray:
+    """N(0, std) draws of one tensor; a [B, T, w] tensor takes one stream per
+    example. enc (optional) encodes each example's draws (fp32 -> bf16 bits)."""
+    shape = tuple(int(x) for x in shape)
+    if len(shape) != 3:
+        x = _rng(seed, tag).standard_normal(size=shape, dtype=np.float32)
+        if std != 1.0:
+            x *= np.float32(std)
+        return x if enc is None else enc(x)
+    out = None
+
+    def one(b):
+        nonlocal out
+        x = _rng(seed, tag, b).standard_normal(size=shape[1:], dtype=np.float32)
+        if std != 1.0:
+            x *= np.float32(std)
+        out[b] = x if enc is None else enc(x)
+    probe = np.zeros((1, 1), np.float32) if enc is None else enc(np.zeros((1, 1), np.float32))
+    out = np.empty(shape, dtype=probe.dtype)
+    _per_example(one, shape[0])
+    return out
 
 
 def zipf_ids(rng: np.random.Generator, shape, V: int, s: float = 1.1) -> np.ndarray:
@@ -143,8 +180,7 @@ def logit_grads(z: np.ndarray, ids: np.ndarray) -> np.ndarray:
 
 def draw(seed: int, tag: int, shape, std: float = 1.0, dtype: str = "bf16") -> np.ndarray:
     """One seeded N(0, std) tensor, encoded as bf16 bits or fp32."""
-    x = _normal(seed, tag, shape, std)
-    return f32_to_bf16_bits(x) if dtype == "bf16" else x
+    return _normal(seed, tag, shape, std, f32_to_bf16_bits if dtype == "bf16" else None)
 
 
 def draw_ids(seed: int, tag: int, shape, V: int, kind: str = "zipf") -> np.ndarray:
@@ -287,8 +323,8 @@ def make_workload(name: str, seed: int = 0, *, B: Optional[int] = None,
     idx = range(len(shapes)) if layers is None else layers
     for l in idx:
         lname, di, do = shapes[l]
-        A = enc(_normal(seed, 2 * l, (B, T, di), a_std))
-        G = enc(_normal(seed, 2 * l + 1, (B, T, do), g_std))
+        A = _normal(seed, 2 * l, (B, T, di), a_std, enc)
+        G = _normal(seed, 2 * l + 1, (B, T, do), g_std, enc)
         wl.linears.append(LinearInputs(lname, di, do, A, G))
 
     if head_kind is None or not with_head:
@@ -299,21 +335,27 @@ def make_workload(name: str, seed: int = 0, *, B: Optional[int] = None,
         ids = rng_ids.integers(0, Vh, size=(B, T), dtype=np.int64).astype(np.int32)
     else:
         ids = zipf_ids(rng_ids, (B, T), Vh, 1.1)
-    dE = enc(_normal(seed, TAG_DE, (B, T, dd), e_std))
+    dE = _normal(seed, TAG_DE, (B, T, dd), e_std, enc)
     H = Gz = None
     ldz_eff = Vh if ldz is None else int(ldz)
     if ldz_eff < Vh:
         raise ValueError("ldz must be >= V")
     if head_kind in ("tied", "untied"):
-        H = enc(_normal(seed, TAG_H, (B, T, dd), 1.0))
-        z = _normal(seed, TAG_Z, (B, T, Vh), 1.0)
-        gz = logit_grads(z, ids)
-        if ldz_eff > Vh:
-            pad = np.zeros((B, T, ldz_eff), dtype=np.float32)
-            pad[:, :, :Vh] = gz
-            gz = pad
-        Gz = enc(gz)
-        del z, gz
+        H = _normal(seed, TAG_H, (B, T, dd), 1.0, enc)
+        Gz = None
+
+        def one(b):
+            # example b's logits, its logit gradients, padded to ldz, encoded
+            z = _rng(seed, TAG_Z, b).standard_normal(size=(1, T, Vh), dtype=np.float32)
+            gz = logit_grads(z, ids[b:b + 1])[0]
+            if ldz_eff > Vh:
+                pad = np.zeros((T, ldz_eff), dtype=np.float32)
+                pad[:, :Vh] = gz
+                gz = pad
+            Gz[b] = enc(gz)
+        probe = enc(np.zeros((1, 1), np.float32))
+        Gz = np.empty((B, T, ldz_eff), dtype=probe.dtype)
+        _per_example(one, B)
     wl.head = HeadInputs(V=Vh, d=dd, ids=ids, dE=dE, H=H, Gz=Gz, ldz=ldz_eff,
                          tied=(head_kind == "tied"))
     if full_params:
@@ -332,8 +374,8 @@ def _add_full_params(wl: Workload, seed: int, enc, g_std: float, n_blocks: int,
         wl.vectors.append(VectorInputs(lin.name + ".bias", lin.d_out, None, lin.G))
     names = [f"h.{b}.{ln}" for b in range(n_blocks) for ln in ("ln_1", "ln_2")] + ["ln_f"]
     for k, name in enumerate(names):
-        xhat = enc(_normal(seed, TAG_LN + 2 * k, (B, T, d), 1.0))
-        gy = enc(_normal(seed, TAG_LN + 2 * k + 1, (B, T, d), g_std))
+        xhat = _normal(seed, TAG_LN + 2 * k, (B, T, d), 1.0, enc)
+        gy = _normal(seed, TAG_LN + 2 * k + 1, (B, T, d), g_std, enc)
         wl.vectors.append(VectorInputs(name + ".weight", d, xhat, gy))
         wl.vectors.append(VectorInputs(name + ".bias", d, None, gy))
     wl.n_pos = n_pos
