@@ -147,6 +147,26 @@ dp_status_t dp_ghost_norm_linear_bias_grouped(const dp_linear_t* layers, float* 
                                               float* norm2, int accumulate, void* workspace,
                                               size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * operation as dp_ghost_norm_linear_bias_grouped, bit for bit, with the
+ * partial sums in a static device scratch of DP_NOALLOC_SCRATCH_BYTES that
+ * the library holds on each device from its load to the end of the process,
+ * instead of a caller's workspace. It calls no allocating routine; the first
+ * call on a device looks up that device's scratch address
+ * (hipGetSymbolAddress) once. A call whose partials need more than the
+ * scratch holds (dp_ghost_norm_linear_bias_workspace(...) bytes, so
+ * B * (partials per example) * 4 rounded up) returns DP_EUNSUPPORTED before
+ * any launch. Every call on one device shares that device's scratch: calls
+ * that overlap on one device (other streams, other threads) race and must be
+ * ordered by the caller; nothing in the scratch needs to start at zero (every
+ * partial is written before it is read). */
+#define DP_NOALLOC_SCRATCH_BYTES (8u << 20)
+dp_status_t dp_ghost_norm_linear_bias_grouped_noalloc(const dp_linear_t* layers,
+                                                      float* const* bias_grads, int n_layers,
+                                                      int B, int T, dp_dtype_t dt, float* norm2,
+                                                      int accumulate, void* stream);
+
 /* ---------------------------------------------------------------------
  * Input-embedding ghost norm and token buckets (Sec. "Weight Tying in
  * Decoder-Only LLMs"; the embedding reads row ids[b,t] of E in R^{V x d}).

@@ -8,10 +8,18 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 #include <vector>
 
 #include "kernels.hpp"
+
+// Device scratch of dp_ghost_norm_linear_bias_grouped_noalloc (for callers
+// that cannot allocate): every device the library runs on holds its own copy
+// from the library's load until the process ends. In host code `scratch`
+// names a host-side stand-in, never the device memory: host code uses only
+// the per-device address hipGetSymbolAddress returns (static_scratch below).
+static __device__ __align__(256) unsigned char scratch[DP_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -365,6 +373,31 @@ dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int
 
 size_t norm_ws_bytes(const NormPlan& p, int B) { return align_up((size_t)B * p.slots * 4); }
 
+// The device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+dp_status_t static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(DP_EUNSUPPORTED, "device %d: the static scratch serves devices 0..%d", dev,
+                kMaxDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(DP_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DP_OK;
+}
+
 // Embedding-sum workspace layout (bytes): sorted keys, block head/tail partials.
 struct EsLayout {
   size_t keys, head, tail, rank, seg, n_runs, rows, total;
@@ -539,10 +572,15 @@ size_t dp_ghost_norm_linear_workspace(const dp_linear_t* layers, int n_layers, i
   return dp_ghost_norm_linear_bias_workspace(layers, nullptr, n_layers, B, T, dt);
 }
 
-dp_status_t dp_ghost_norm_linear_bias_grouped(const dp_linear_t* layers, float* const* bias_grads,
-                                              int n_layers, int B, int T, dp_dtype_t dt,
-                                              float* norm2, int accumulate, void* workspace,
-                                              size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+// The grouped norm with biases. workspace == NULL with use_static: the
+// partials go to this device's static scratch (nothing is allocated).
+dp_status_t norm_bias_grouped(const dp_linear_t* layers, float* const* bias_grads, int n_layers,
+                              int B, int T, dp_dtype_t dt, float* norm2, int accumulate,
+                              void* workspace, size_t workspace_bytes, void* stream,
+                              bool use_static) {
   dp_status_t st = check_layers(layers, n_layers, B, T, dt);
   if (st != DP_OK) return st;
   if (!norm2) return fail(DP_EINVAL, "norm2 is NULL");
@@ -553,6 +591,16 @@ dp_status_t dp_ghost_norm_linear_bias_grouped(const dp_linear_t* layers, float* 
     plan_vec(vp, nullptr, 0, e.G, e.ldg, e.d, dpg::VEC_GRAD, e.grad, dt, T);
   const size_t norm_bytes = norm_ws_bytes(p, B);
   const size_t need = norm_bytes + align_up((size_t)B * vp.slots * 4);
+  if (use_static) {
+    if (need > (size_t)DP_NOALLOC_SCRATCH_BYTES)
+      return fail(DP_EUNSUPPORTED,
+                  "this call needs %zu bytes of scratch; the static scratch holds %zu "
+                  "(use dp_ghost_norm_linear_bias_grouped with a workspace)",
+                  need, (size_t)DP_NOALLOC_SCRATCH_BYTES);
+    st = static_scratch(&workspace);
+    if (st != DP_OK) return st;
+    workspace_bytes = DP_NOALLOC_SCRATCH_BYTES;
+  }
   if (!workspace || workspace_bytes < need)
     return fail(DP_EINVAL, "workspace of %zu bytes needed, %zu given", need,
                 workspace ? workspace_bytes : (size_t)0);
@@ -572,6 +620,25 @@ dp_status_t dp_ghost_norm_linear_bias_grouped(const dp_linear_t* layers, float* 
   if (st != DP_OK || vp.e.empty()) return st;
   return hip_status(dpg::launch_finish_rows(vws, B, (int)vp.slots, norm2, 1, 1.f, s),
                     "finish launch");
+}
+}  // namespace
+
+extern "C" {
+
+dp_status_t dp_ghost_norm_linear_bias_grouped(const dp_linear_t* layers, float* const* bias_grads,
+                                              int n_layers, int B, int T, dp_dtype_t dt,
+                                              float* norm2, int accumulate, void* workspace,
+                                              size_t workspace_bytes, void* stream) {
+  return norm_bias_grouped(layers, bias_grads, n_layers, B, T, dt, norm2, accumulate, workspace,
+                           workspace_bytes, stream, false);
+}
+
+dp_status_t dp_ghost_norm_linear_bias_grouped_noalloc(const dp_linear_t* layers,
+                                                      float* const* bias_grads, int n_layers,
+                                                      int B, int T, dp_dtype_t dt, float* norm2,
+                                                      int accumulate, void* stream) {
+  return norm_bias_grouped(layers, bias_grads, n_layers, B, T, dt, norm2, accumulate, nullptr, 0,
+                           stream, true);
 }
 
 dp_status_t dp_ghost_norm_linear_grouped(const dp_linear_t* layers, int n_layers, int B, int T,

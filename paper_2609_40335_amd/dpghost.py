@@ -67,6 +67,9 @@ _SIGS = {
                                              _I, _I, _I], _SZ),
     "dp_ghost_norm_linear_bias_grouped": ([ctypes.POINTER(dp_linear_t), ctypes.POINTER(_VP), _I,
                                            _I, _I, _I, _VP, _I, _VP, _SZ, _VP], _I),
+    "dp_ghost_norm_linear_bias_grouped_noalloc": ([ctypes.POINTER(dp_linear_t),
+                                                   ctypes.POINTER(_VP), _I, _I, _I, _I, _VP, _I,
+                                                   _VP], _I),
     "dp_ghost_norm_linear_grouped": ([ctypes.POINTER(dp_linear_t), _I, _I, _I, _I, _VP, _I,
                                       _VP, _SZ, _VP], _I),
     "dp_ghost_norm_linear": ([_VP, _I64, _VP, _I64, _I, _I, _I, _I, _I, _I, _VP, _I, _VP, _SZ,
@@ -189,6 +192,35 @@ def dp_ghost_norm_linear_bias_grouped(layers: Sequence, bias_grads: Sequence, no
     """The grouped norm that also writes bias_grads[l] (fp32 [B, d_out], or
     None for a layer without bias) = sum over tokens of G_l, norms included."""
     return LinearGroup(layers, bias_grads=bias_grads).ghost_norm(norm2, accumulate, stream)
+
+
+def dp_ghost_norm_linear_bias_grouped_noalloc(layers: Sequence, bias_grads: Optional[Sequence],
+                                              norm2: torch.Tensor, accumulate: bool = False,
+                                              stream=None) -> torch.Tensor:
+    """The grouped norm (with optional bias gradients) in the library's static
+    device scratch: no workspace is allocated here or in the library."""
+    descs = [_layer(*l) for l in layers]
+    A0 = layers[0][0]
+    B, T = A0.shape[0], A0.shape[1]
+    for l in layers:
+        if tuple(l[0].shape[:2]) != (B, T) or l[0].dtype != A0.dtype:
+            raise DPError("all layers of a group share B, T and dtype")
+    arr = (dp_linear_t * len(descs))(*descs)
+    bias = None
+    if bias_grads is not None:
+        if len(bias_grads) != len(descs):
+            raise DPError("one bias gradient (or None) per layer")
+        for l, g in zip(layers, bias_grads):
+            if g is not None and (g.dtype != torch.float32 or not g.is_contiguous()
+                                  or tuple(g.shape) != (B, l[1].shape[2])):
+                raise DPError("bias gradients must be contiguous fp32 [B, d_out]")
+        bias = (ctypes.c_void_p * len(descs))(*[None if g is None else g.data_ptr()
+                                                for g in bias_grads])
+    _check(lib().dp_ghost_norm_linear_bias_grouped_noalloc(arr, bias, len(descs), B, T,
+                                                          _dtype(A0), norm2.data_ptr(),
+                                                          int(accumulate), _stream(stream)),
+           "dp_ghost_norm_linear_bias_grouped_noalloc")
+    return norm2
 
 
 def dp_ghost_norm_linear_grouped(layers: Sequence, norm2: torch.Tensor, accumulate: bool = False,

@@ -134,6 +134,28 @@ def test_grouped_rejects_bad_layers(L):
                                           None) == EINVAL
 
 
+def test_noalloc_norm_rejects_bad_and_oversized_calls(L):
+    """The no-allocation grouped norm validates like the workspace form, and
+    rejects a call whose partials exceed its static scratch before any HIP
+    call (so this runs without a GPU)."""
+    f = L.dp_ghost_norm_linear_bias_grouped_noalloc
+    arr = (D.dp_linear_t * 2)(_lin(), _lin(G=0))
+    assert f(arr, None, 2, 4, 16, 0, 1 << 22, 0, None) == EINVAL
+    assert b"layer 1" in L.dp_last_error()
+    one = (D.dp_linear_t * 1)(_lin())
+    assert f(one, None, 1, 4, 16, 0, None, 0, None) == EINVAL           # no norm2
+    assert f(None, None, 1, 4, 16, 0, 1 << 22, 0, None) == EINVAL
+    # direct norm of a 4352 x 4352 layer: 17 x 17 tiles per example, so at
+    # B = 8192 the partials take 8192 * 289 * 4 bytes > 8 MiB
+    big = (D.dp_linear_t * 1)(_lin(d_in=4352, lda=4352, d_out=4352, ldg=4352,
+                                   algo=D.DP_NORM_DIRECT))
+    need = L.dp_ghost_norm_linear_bias_workspace(big, None, 1, 8192, 1, D.DP_BF16)
+    assert need == 8192 * 289 * 4
+    assert need > (8 << 20)
+    assert f(big, None, 1, 8192, 1, D.DP_BF16, 1 << 22, 0, None) == EUNSUP
+    assert b"static scratch" in L.dp_last_error()
+
+
 def test_embedding_rejects_bad_arguments(L):
     f = L.dp_ghost_norm_embedding
     args = dict(ids=1 << 20, dE=1 << 21, lde=64, B=4, T=16, V=512, d=64, dt=0, norm2=1 << 22,
