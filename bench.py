@@ -42,6 +42,7 @@ if ROOT not in sys.path:
 METRIC = "examples/sec for ghost-norm + clipped grad sum (GPT-2-small shapes); % MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
 # HBM bytes per launch of the clipped-sum kernel: rocprofv3 FETCH_SIZE x 2 +
 # WRITE_SIZE x 1 (factors from a plain 1 GiB copy), recorded for the kernel
 # source with this SHA-256; any other source reports null.
@@ -68,6 +69,9 @@ def parse(argv=None):
     ap.add_argument("--cpu-budget", type=float, default=25.0,
                     help="seconds of oracle work for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--configs", default="c2,c3,c4,c5",
+                    help="further workloads measured after the headline one, each with the "
+                         "same warm-up and steps, reported under \"configs\" ('none': skip)")
     ap.add_argument("--crossover", action="store_true",
                     help="instead of the step: time each distinct layer shape's grouped norm "
                          "with the Gram kernel and with the direct kernel (one JSON line)")
@@ -221,9 +225,22 @@ class Step:
         self.c_b = torch.zeros(B, device="cuda")   # c / B
         # algorithmic work of the grouped clipped-sum GEMM (the dominant kernel)
         K = B * T
+        es = 2 if wl.dtype == "bf16" else 4
         self.gemm_flops = 2.0 * K * sum(a.shape[2] * g.shape[2] for a, g in sum_layers)
-        # algorithmic bytes of the grouped norm kernel: every A and G element once
-        self.norm_bytes = 2.0 * K * sum(a.shape[2] + g.shape[2] for a, g in norm_layers)
+        self.gemm_bytes = K * es * sum(a.shape[2] + g.shape[2] for a, g in sum_layers) + \
+            4.0 * sum(a.shape[2] * g.shape[2] for a, g in sum_layers)
+        # algorithmic work of the grouped norm launch: every A and G element read
+        # once; flops of the form the library's AUTO rule picks per layer (the
+        # symmetric T x T Gram counted once, or the direct per-example GEMM)
+        self.norm_bytes = float(K * es * sum(a.shape[2] + g.shape[2] for a, g in norm_layers))
+        self.norm_flops, self.norm_direct = 0.0, 0
+        for a, g in norm_layers:
+            di, do = a.shape[2], g.shape[2]
+            if T + 1 > 0.57 * 2.0 * di * do / (di + do):
+                self.norm_flops += 2.0 * K * di * do
+                self.norm_direct += 1
+            else:
+                self.norm_flops += float(B) * T * (T + 1) * (di + do)
         self.step_id = 0
 
     def total_norm2(self):
@@ -389,6 +406,87 @@ def host_cpu():
     return {"model": model, "sockets": max(1, len(sockets))}
 
 
+def timed_run(st, torch, steps, warmup):
+    """warmup untimed steps, then `steps` steps bracketed by HIP events on the
+    main stream (the one every main-stream kernel is launched on), recording
+    only the two events around the clipped-sum launch inside them; then up to
+    10 more steps with every phase marked. Returns (ms per step, clipped-sum
+    launch us, {phase: us})."""
+    for _ in range(warmup):
+        st.run()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = []
+
+    def marks(name):
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        ev[-1].append((name, e))
+
+    # every timing event costs the stream a few microseconds (all the phase
+    # marks together add ~20 us to a GPT-2 step), so the timed steps record
+    # only the two around the clipped-sum launch
+    def gemm_marks(name):
+        if name in ("clip", "clipped_sum_noise"):
+            marks(name)
+
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        ev.append([])
+        st.run(gemm_marks)
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    gemm_us = sum(step[0][1].elapsed_time(step[-1][1]) for step in ev) / len(ev) * 1e3
+    ev.clear()
+    for _ in range(min(steps, 10)):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        ev.append([("start", e0)])
+        st.run(marks)
+    torch.cuda.synchronize()
+    phases = {}
+    for step_ev in ev:
+        for (_, a), (n1, b) in zip(step_ev[:-1], step_ev[1:]):
+            phases.setdefault(n1, []).append(a.elapsed_time(b) * 1e3)
+    return ms, gemm_us, {k: sum(v) / len(v) for k, v in phases.items()}
+
+
+def rooflines(st, gemm_us, phase_us):
+    """The clipped-sum GEMM against the MFMA peak of its dtype, and the grouped
+    norm launch (the norms phase of the main stream) against HBM when it is
+    the Gram form and against the MFMA peak when every layer takes the direct
+    form."""
+    peak = PEAK_BF16_TFLOPS if st.wl.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS
+    achieved = st.gemm_flops / (gemm_us * 1e-6) / 1e12
+    gemm = {"bound": "mfma", "kernel": "dl_gemm_kernel (clipped sum with fused noise)",
+            "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+            "timed": "HIP events on the main stream around the grouped clipped-sum call, "
+                     "inside the timed steps: the GEMM launch and the split-tail fix-up "
+                     "kernel that follows it (~16 us at the GPT-2 step), beside the second "
+                     "stream's embedding rows",
+            "algorithmic_flop_per_launch": st.gemm_flops,
+            "algorithmic_bytes_per_launch": st.gemm_bytes}
+    norm_us = phase_us["norms"]
+    n_layers = len(st.norm_layers)
+    if st.norm_direct == n_layers:
+        ach = st.norm_flops / (norm_us * 1e-6) / 1e12
+        norm = {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+                "frac": ach / peak}
+    else:
+        ach = st.norm_bytes / (norm_us * 1e-6) / 1e9
+        norm = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": ach / PEAK_HBM_GBS}
+    norm.update({"kernel": f"grouped norm launch ({n_layers - st.norm_direct} Gram, "
+                           f"{st.norm_direct} direct layers)",
+                 "timed": "the norms phase of the phase-marked steps",
+                 "algorithmic_bytes_per_launch": st.norm_bytes,
+                 "algorithmic_flop_per_launch": st.norm_flops})
+    return gemm, norm
+
+
 def main(argv=None) -> int:
     args = parse(argv)
     if args.gpus != 1:
@@ -414,11 +512,16 @@ def main(argv=None) -> int:
         print(json.dumps({"copy_calibration_bytes": src.numel() * 4, "copies": 3}), flush=True)
         return 0
     dp.lib()
-    t0 = time.perf_counter()
     V = gen.GPT2_VOCAB
-    wl = gen.make_workload(args.workload, seed=args.seed, ldz=round_up(V, args.ldz_multiple))
-    log(f"[bench] generated {args.workload}: {wl.description} in {time.perf_counter() - t0:.1f}s")
-    st = Step(wl, dp, torch)
+    ldz = round_up(V, args.ldz_multiple)
+
+    def load(name):
+        t0 = time.perf_counter()
+        wl = gen.make_workload(name, seed=args.seed, ldz=ldz)
+        log(f"[bench] generated {name}: {wl.description} in {time.perf_counter() - t0:.1f}s")
+        return wl, Step(wl, dp, torch)
+
+    wl, st = load(args.workload)
     log(f"[bench] {len(wl.linears)} linear layers, head={'none' if wl.head is None else ('tied' if wl.head.tied else 'untied')}, "
         f"{st.n_coords} gradient coordinates")
 
@@ -428,60 +531,19 @@ def main(argv=None) -> int:
               flush=True)
         return 0
 
-    for _ in range(args.warmup):
-        st.run()
-    torch.cuda.synchronize()
-
-    stream = torch.cuda.current_stream()
-    ev = []
-
-    def marks(name):
-        e = torch.cuda.Event(enable_timing=True)
-        e.record(stream)
-        ev[-1].append((name, e))
-
-    # The timed steps record only the two events around the clipped-sum
-    # launch (every timing event costs the stream a few microseconds; all the
-    # phase marks together add ~20 us to a GPT-2 step).
-    def gemm_marks(name):
-        if name in ("clip", "clipped_sum_noise"):
-            marks(name)
-
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(args.steps):
-        ev.append([])
-        st.run(gemm_marks)
-    end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(end)
-    ms = total_ms / args.steps
-    gemm_ms = [step[0][1].elapsed_time(step[-1][1]) for step in ev]
-    gemm_s = sum(gemm_ms) / len(gemm_ms) / 1e3
-
-    # Per-phase times (stderr and config.phase_us) from a few more steps with
-    # every phase marked, after the timed region.
-    ev.clear()
-    for _ in range(min(args.steps, 10)):
-        e0 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        ev.append([("start", e0)])
-        st.run(marks)
-    torch.cuda.synchronize()
-    phases = {}
-    for step_ev in ev:
-        for (n0, a), (n1, b) in zip(step_ev[:-1], step_ev[1:]):
-            phases.setdefault(n1, []).append(a.elapsed_time(b))
-    phase_ms = {k: sum(v) / len(v) for k, v in phases.items()}
-    for k, v in phase_ms.items():
-        log(f"[bench]   {k:16s} {v * 1e3:9.1f} us")
-    norm_s = phase_ms["norms"] / 1e3
-    achieved = st.gemm_flops / gemm_s / 1e12
-    log(f"[bench] clipped-sum GEMM {st.gemm_flops / 1e9:.1f} GFLOP in {gemm_s * 1e6:.1f} us = "
-        f"{achieved:.1f} TFLOP/s; grouped norm {st.norm_bytes / 1e9:.3f} GB in "
-        f"{norm_s * 1e6:.1f} us = {st.norm_bytes / norm_s / 1e9:.0f} GB/s")
+    ms, gemm_us, phase_us = timed_run(st, torch, args.steps, args.warmup)
+    for k, v in phase_us.items():
+        log(f"[bench]   {k:16s} {v:9.1f} us")
+    gemm_rf, norm_rf = rooflines(st, gemm_us, phase_us)
+    gemm_rf["traffic"] = gemm_traffic()
+    gemm_rf["traffic_source"] = (
+        "rocprofv3 FETCH_SIZE and WRITE_SIZE of this kernel source at this workload, scaled "
+        "by a 1 GiB copy (profiles/hbm_traffic_gpt2_step_B32_T128.md); null when the source "
+        "differs from the one measured")
+    log(f"[bench] clipped-sum GEMM {st.gemm_flops / 1e9:.1f} GFLOP in {gemm_us:.1f} us = "
+        f"{gemm_rf['achieved']:.1f} TFLOP/s ({gemm_rf['frac']:.3f}); grouped norm "
+        f"{st.norm_bytes / 1e9:.3f} GB in {phase_us['norms']:.1f} us: {norm_rf['frac']:.3f} of "
+        f"its {norm_rf['bound']} peak")
 
     h = wl.head
     config = {"workload": f"{args.workload}: {wl.description}", "B": wl.B, "T": wl.T,
@@ -490,21 +552,44 @@ def main(argv=None) -> int:
                                                                    else "embedding-only")),
               "V": None if h is None else h.V, "ldz": None if h is None else h.ldz,
               "gradient_coordinates": st.n_coords, "C": wl.C, "sigma": wl.sigma,
-              "phase_us": {k: round(v * 1e3, 1) for k, v in phase_ms.items()}}
+              "phase_us": {k: round(v, 1) for k, v in phase_us.items()}}
     out = {
         "metric": METRIC, "value": wl.B / (ms / 1e3), "unit": "examples/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-        "data": "synthetic", "config": config,
-        "roofline": {"bound": "mfma",
-                     "kernel": "dl_gemm_kernel (clipped sum with fused noise, bf16)",
-                     "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": gemm_traffic(),
-                     "algorithmic_flop_per_launch": st.gemm_flops},
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic", "config": config, "roofline": gemm_rf, "norm_roofline": norm_rf,
     }
+    del st
+    torch.cuda.empty_cache()
+
+    # The other workloads of the metric (GPT-2 body alone, tied head alone,
+    # DistilGPT2 tied at T = 256, GPT-2 untied at T = 1024): the same step,
+    # warm-up and timing, one after another.
+    extra = [c for c in args.configs.split(",") if c and c != "none" and c != args.workload]
+    if extra:
+        out["configs"] = {}
+    for name in extra:
+        wl_c, st_c = load(name)
+        ms_c, gemm_c, ph_c = timed_run(st_c, torch, args.steps, args.warmup)
+        g_c, n_c = rooflines(st_c, gemm_c, ph_c)
+        hc = wl_c.head
+        out["configs"][name] = {
+            "workload": wl_c.description, "B": wl_c.B, "T": wl_c.T, "dtype": wl_c.dtype,
+            "head": None if hc is None else ("tied" if hc.tied else "untied"),
+            "ms_per_step": ms_c, "examples_per_s": wl_c.B / (ms_c / 1e3),
+            "clipped_sum_us": gemm_c, "clipped_sum_mfma_frac": g_c["frac"],
+            "norms_us": ph_c["norms"], "norms_bound": n_c["bound"], "norms_frac": n_c["frac"],
+            "phase_us": {k: round(v, 1) for k, v in ph_c.items()}}
+        log(f"[bench] {name}: {ms_c:.3f} ms/step, {wl_c.B / (ms_c / 1e3):.0f} ex/s, clipped sum "
+            f"{gemm_c:.1f} us ({g_c['frac']:.3f} of MFMA), norms {ph_c['norms']:.1f} us "
+            f"({n_c['frac']:.3f} of {n_c['bound']})")
+        del st_c, wl_c
+        torch.cuda.empty_cache()
+
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
-        out["cpu_baseline"] = cpu_baseline(wl, st.n_coords, args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(wl, out["config"]["gradient_coordinates"],
+                                           args.cpu_budget)
         log(f"[bench] cpu baseline took {time.perf_counter() - t0:.1f}s")
     print(json.dumps(out), flush=True)
     return 0
