@@ -75,6 +75,10 @@ def parse(argv=None):
     ap.add_argument("--crossover", action="store_true",
                     help="instead of the step: time each distinct layer shape's grouped norm "
                          "with the Gram kernel and with the direct kernel (one JSON line)")
+    ap.add_argument("--token-kernels", action="store_true",
+                    help="instead of the step: time the token-keyed norm calls (embedding norm "
+                         "with buckets, tied cross term) alone on the workload's inputs, "
+                         "one after another on an idle GPU (one JSON line)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="instead of the step: three plain 1 GiB device copies, the reference "
                          "for scaling the FETCH_SIZE / WRITE_SIZE counters to bytes")
@@ -350,6 +354,37 @@ def crossover(st, dp, torch, reps=10):
     return rows
 
 
+def token_kernels(st, dp, torch, reps=30):
+    """The embedding norm (with bucket ids) and the tied cross term alone, each
+    call timed by HIP events around it on the main stream (kernel plus the
+    partials' reduction launch), medians over `reps` calls after 5 warm-ups."""
+    import numpy as np
+    h = st.h
+    if h is None:
+        return {}
+    calls = {"embedding_norm": lambda n2: dp.dp_ghost_norm_embedding(
+        st.ids, st.dE, h.V, n2, seg_id=st.seg, n_unique=st.nu)}
+    if h.H is not None and h.tied:
+        calls["tied_cross"] = lambda n2: dp.dp_tied_cross_term(st.ids, st.dE, st.H, st.Gz, h.V, n2)
+    n2 = torch.zeros(st.wl.B, device="cuda")
+    out = {}
+    for name, fn in calls.items():
+        for _ in range(5):
+            fn(n2)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn(n2)
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3)
+        out[name] = {"median_us": round(float(np.median(ts)), 1), "min_us": round(min(ts), 1)}
+        log(f"[bench] {name}: median {out[name]['median_us']} us, min {out[name]['min_us']} us")
+    return out
+
+
 def cpu_baseline(wl, n_coords, budget):
     """The fp64 oracle on the host: per-example work on a sample of examples,
     noise on a slice of coordinates, extrapolated to one full step."""
@@ -529,6 +564,11 @@ def main(argv=None) -> int:
         rows = crossover(st, dp, torch)
         print(json.dumps({"crossover": rows, "workload": args.workload, "B": wl.B, "T": wl.T}),
               flush=True)
+        return 0
+
+    if args.token_kernels:
+        print(json.dumps({"token_kernels": token_kernels(st, dp, torch),
+                          "workload": args.workload, "B": wl.B, "T": wl.T}), flush=True)
         return 0
 
     ms, gemm_us, phase_us = timed_run(st, torch, args.steps, args.warmup)

@@ -657,9 +657,12 @@ dp_status_t dp_ghost_norm_linear(const void* A, int64_t lda, const void* G, int6
                                       workspace_bytes, stream);
 }
 
+// Partials per example: one per 64-feature chunk (embed_norm_kernel) or per
+// EN_P sorted positions (embed_norm_runs_kernel); the size query cannot know
+// which kernel a call takes, so it covers both.
 size_t dp_ghost_norm_embedding_workspace(int B, int T, int d) {
   if (B <= 0 || T <= 0 || d <= 0) return 0;
-  return align_up((size_t)B * ceil_div(d, 64) * 4);
+  return align_up((size_t)B * std::max(ceil_div(d, 64), ceil_div(T, dpg::EN_P)) * 4);
 }
 
 dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t lde, int B, int T,
@@ -682,7 +685,12 @@ dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t 
   a.ids = ids; a.E = dE; a.lde = lde;
   a.B = B; a.T = T; a.V = V; a.d = d;
   a.pbits = pbits;
-  a.n_chunks = (int)ceil_div(d, 64);
+  // Rows read 8 bytes per lane when they allow it (and an example's rows
+  // span less than 4 GiB, for the buffer offsets).
+  const int64_t es = esize(dt);
+  a.runs = ((uintptr_t)dE % dpg::EN_VB == 0 && (lde * es) % dpg::EN_VB == 0 &&
+            (d * es) % dpg::EN_VB == 0 && span_ok(T, lde, dt)) ? 1 : 0;
+  a.n_chunks = (int)(a.runs ? ceil_div(T, dpg::EN_P) : ceil_div(d, 64));
   a.seg_id = seg_id; a.n_unique = n_unique;
   a.ws = static_cast<float*>(workspace);
   hipStream_t s = as_stream(stream);
@@ -693,20 +701,25 @@ dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t 
 }
 
 // Partials per example: (128-row tile pair, 128-feature chunk) for the
-// register-staged kernel, (64-row block pair) for the direct-load one. The
-// size query cannot know which kernel a call takes, so it covers both.
-int64_t cross_slots(int T, int d, bool direct) {
-  if (direct) {
-    const int64_t nq = ceil_div(T, dpg::CR_DL_ROWS);
-    return nq * nq;
-  }
-  const int64_t nt = ceil_div(T, dpg::GR_TM);
-  return nt * nt * ceil_div(d, dpg::CR_FCHUNK);
+// register-staged kernel, (64-row block pair) for the direct-load one,
+// (32-token block, 32-row block) for the register-direct one (T <= CX_ROWS_T
+// only). The size query cannot know the dtype or alignment of a call, so it
+// covers every kernel the call's T allows.
+int64_t cross_blocks(int T, int kind) {
+  return ceil_div(T, kind == dpg::CROSS_ROWS ? dpg::CR_RX_ROWS
+                     : kind == dpg::CROSS_DL ? dpg::CR_DL_ROWS : dpg::GR_TM);
+}
+int64_t cross_slots(int T, int d, int kind) {
+  const int64_t nq = cross_blocks(T, kind);
+  return nq * nq * (kind == dpg::CROSS_STAGED ? ceil_div(d, dpg::CR_FCHUNK) : 1);
 }
 
 size_t dp_tied_cross_term_workspace(int B, int T, int d) {
   if (B <= 0 || T <= 0 || d <= 0) return 0;
-  return align_up((size_t)B * std::max(cross_slots(T, d, true), cross_slots(T, d, false)) * 4);
+  int64_t m = 0;
+  for (int kind : {dpg::CROSS_STAGED, dpg::CROSS_DL, dpg::CROSS_ROWS})
+    if (kind != dpg::CROSS_ROWS || T <= dpg::CX_ROWS_T) m = std::max(m, cross_slots(T, d, kind));
+  return align_up((size_t)B * m * 4);
 }
 
 dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, const void* H,
@@ -730,10 +743,15 @@ dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, 
   a.lde = lde; a.ldh = ldh; a.ldz = ldz;
   a.B = B; a.T = T; a.V = V; a.d = d;
   const bool vec = vec_ok(dE, lde, dt) && vec_ok(H, ldh, dt);
-  const bool direct = dpg::cross_direct(kdt(dt), vec);
-  a.n_t = (int)ceil_div(T, direct ? dpg::CR_DL_ROWS : dpg::GR_TM);
-  a.n_fc = direct ? 1 : (int)ceil_div(d, dpg::CR_FCHUNK);
-  a.slots = (int32_t)cross_slots(T, d, direct);
+  a.kind = dpg::cross_kind(kdt(dt), vec, T);
+  a.n_t = (int)cross_blocks(T, a.kind);
+  a.n_fc = a.kind == dpg::CROSS_STAGED ? (int)ceil_div(d, dpg::CR_FCHUNK) : 1;
+  a.slots = (int32_t)cross_slots(T, d, a.kind);
+  a.pbits = std::max(1, bits_for(T));
+  // Sorting only orders the gathers; where a key would not fit 32 bits the
+  // tokens stay in position order.
+  a.sort = (a.kind == dpg::CROSS_ROWS && T <= dpg::CX_SORT_T &&
+            bits_for((int64_t)V + 1) + a.pbits <= 32) ? 1 : 0;
   a.ws = static_cast<float*>(workspace);
   hipStream_t s = as_stream(stream);
   dp_status_t st = hip_status(dpg::launch_tied_cross(a, kdt(dt), vec, s), "tied_cross launch");

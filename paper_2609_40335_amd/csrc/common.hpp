@@ -65,6 +65,20 @@ __device__ __forceinline__ int wave_find(uint32_t x, uint32_t lane_begin, int n)
   return __builtin_amdgcn_readfirstlane(__popcll(m));
 }
 
+// Number of the n keys (n a multiple of 8, 16-byte aligned LDS) below k:
+// 16-byte reads, eight keys per step, two steps' reads in flight.
+__device__ __forceinline__ int count_below(const uint32_t* keys, int n, uint32_t k) {
+  const u32x4* k4 = (const u32x4*)keys;
+  int r0 = 0, r1 = 0;
+#pragma unroll 4
+  for (int j = 0; j < n / 4; j += 2) {
+    const u32x4 x = k4[j], y = k4[j + 1];
+    r0 += (x[0] < k) + (x[1] < k) + (x[2] < k) + (x[3] < k);
+    r1 += (y[0] < k) + (y[1] < k) + (y[2] < k) + (y[3] < k);
+  }
+  return r0 + r1;
+}
+
 // 32x32 output block MFMA step; K per call is 16 (bf16) or 2 (fp32).
 __device__ __forceinline__ f32x16 mfma32_bf16(const u32x4& a, const u32x4& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),

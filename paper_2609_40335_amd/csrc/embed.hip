@@ -22,6 +22,7 @@
 namespace dpg {
 
 constexpr int EN_THREADS = 256;
+static_assert(EN_CT_T <= EN_THREADS, "counting rank: one key per thread");
 constexpr int ES_THREADS = 1024;
 constexpr int ES_WAVES = 4;  // waves per workgroup of the block and fix-up passes
 
@@ -241,6 +242,142 @@ __global__ __launch_bounds__(EN_THREADS) void embed_norm_kernel(EmbedNormArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// Per-example bucketing and input-embedding norm on rows read 8 bytes per
+// lane (EN_VB bytes: 4 bf16 or 2 fp32). Grid (B, S): workgroup s of example b
+// owns the runs of equal ids that START at sorted positions
+// [s*EN_P, (s+1)*EN_P) and walks each of them to its end, so no run is split
+// between workgroups and each bucket's squared norm is formed whole. Every
+// workgroup sorts the example's keys itself (T <= EN_CT_T: each key's rank is
+// counted against all others; longer: the LDS radix sort), which costs less
+// than a second launch. Lane q of the workgroup owns features
+// [q*VEC, q*VEC + VEC) of every row (nq = d/VEC lanes per row, several
+// passes when nq exceeds the workgroup); its loads of up to EN_BATCH
+// positions are issued together.
+// ---------------------------------------------------------------------------
+template <int DT, int MAXT>
+__global__ __launch_bounds__(EN_THREADS) void embed_norm_runs_kernel(EmbedNormArgs a) {
+  constexpr int VEC = EN_VB / ((DT == DT_BF16) ? 2 : 4);  // elements per lane load
+  constexpr int NW = EN_THREADS / WAVE;
+  __shared__ __attribute__((aligned(16))) uint32_t kbuf[(MAXT > EN_CT_T) ? 2 : 1][MAXT];
+  __shared__ int32_t rank[MAXT];
+  __shared__ int32_t seg[MAXT + 1];
+  __shared__ int cnt[(MAXT > EN_CT_T) ? NW * 256 : 1];
+  __shared__ int wave_tot[NW];
+  __shared__ float red[NW];
+  const int b = blockIdx.x, s = blockIdx.y, tid = threadIdx.x;
+  const int T = a.T, pb = a.pbits;
+  const uint32_t pmask = (1u << pb) - 1u;
+  const uint32_t V = (uint32_t)a.V;
+  const int32_t* ids = a.ids + (int64_t)b * T;
+  const uint32_t* keys;
+  if constexpr (MAXT <= EN_CT_T) {
+    // Keys are distinct (the position is in the low bits), so a key's rank
+    // is the number of smaller keys: T <= EN_THREADS, one key per thread.
+    uint32_t k = 0xFFFFFFFFu;
+    if (tid < T) {
+      const uint32_t id = (uint32_t)ids[tid];
+      k = ((id < V ? id : V) << pb) | (uint32_t)tid;
+    }
+    kbuf[0][tid] = k;  // past T: the largest key, counted by no real key
+    __syncthreads();
+    const int r = count_below(kbuf[0], (T + 7) & ~7, k);
+    __syncthreads();
+    if (tid < T) kbuf[0][r] = k;
+    __syncthreads();
+    keys = kbuf[0];
+  } else {
+    for (int p = tid; p < T; p += EN_THREADS) {
+      const uint32_t id = (uint32_t)ids[p];
+      kbuf[0][p] = ((id < V ? id : V) << pb) | (uint32_t)p;
+    }
+    __syncthreads();
+    keys = kbuf[lds_radix_sort<NW>(kbuf[0], kbuf[1], T, pb, V, cnt, wave_tot)];
+  }
+  const int nseg = rank_sorted(keys, T, pb, rank, seg, wave_tot, tid, EN_THREADS);
+  // Sorted positions [p_lo, p_hi) of this workgroup: bucket ids for them, and
+  // the runs that start there.
+  const int p_lo = min(s * EN_P, T), p_hi = min(p_lo + EN_P, T);
+  if (a.seg_id)
+    for (int p = p_lo + tid; p < p_hi; p += EN_THREADS)
+      a.seg_id[(int64_t)b * T + (keys[p] & pmask)] = rank[p];
+  if (a.n_unique && s == 0 && tid == 0) a.n_unique[b] = nseg;
+  // First run start at or after position p (T if none).
+  auto run_from = [&](int p) {
+    if (p >= T) return T;
+    const int r = rank[p];
+    return seg[r] == p ? p : seg[r + 1];
+  };
+  const int q0 = run_from(p_lo), q1 = run_from(p_hi);
+  const int nq = a.d / VEC;
+  const int64_t row0 = (int64_t)b * T;
+  const int esz = (DT == DT_BF16) ? 2 : 4;
+  const uint32_t ldb = (uint32_t)(a.lde * esz);
+  const rsrc_t rE = make_rsrc((const char*)a.E + row0 * ldb, (uint64_t)T * ldb);
+  float sq = 0.f;
+  const int lane = tid & 63;
+  // Each wave walks the same sorted positions over its own feature lanes (no
+  // barrier below). Per batch of EN_BATCH positions, lane j reads position
+  // base + j's key and whether a run ends there; the row offsets then go to
+  // the loads as wave-uniform offsets (readlane) and the run ends as a ballot
+  // mask, so no load or step of the walk waits on an LDS read.
+  static_assert(EN_BATCH <= WAVE, "one position per lane");
+  for (int q0l = tid - lane; q0l < nq; q0l += EN_THREADS) {
+    const int q = q0l + lane;
+    const uint32_t coff = (uint32_t)(min(q, nq - 1) * EN_VB);  // lanes past the row repeat its last chunk
+    float acc[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+    for (int base = q0; base < q1; base += EN_BATCH) {
+      const int nb = min(EN_BATCH, q1 - base);
+      const int pj = base + min(lane, nb - 1);
+      const uint32_t myrow = keys[pj] & pmask;
+      const bool end_here = lane < nb && (pj + 1 == q1 || rank[pj + 1] != rank[pj]);
+      const uint64_t ends = __ballot(end_here);
+      uint32_t raw[EN_BATCH][2];
+#pragma unroll
+      for (int j = 0; j < EN_BATCH; ++j) {
+        const uint32_t row = (uint32_t)__builtin_amdgcn_readlane((int)myrow, j);
+        const auto v = __builtin_amdgcn_raw_buffer_load_b64(rE, coff, row * ldb, CPOL_STREAM);
+        raw[j][0] = v[0];
+        raw[j][1] = v[1];
+      }
+      // predicated, not exited early, so that raw[] stays in registers; the
+      // repeated last position past nb is never added
+#pragma unroll
+      for (int j = 0; j < EN_BATCH; ++j) {
+        if (j >= nb) continue;
+        if constexpr (DT == DT_BF16) {
+          acc[0] += __uint_as_float(raw[j][0] << 16);
+          acc[1] += __uint_as_float(raw[j][0] & 0xFFFF0000u);
+          acc[2] += __uint_as_float(raw[j][1] << 16);
+          acc[3] += __uint_as_float(raw[j][1] & 0xFFFF0000u);
+        } else {
+          acc[0] += __uint_as_float(raw[j][0]);
+          acc[1] += __uint_as_float(raw[j][1]);
+        }
+        // q1 is a run start, so the walk ends on a run's last position
+        if ((ends >> j) & 1ull) {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            sq += q < nq ? acc[e] * acc[e] : 0.f;
+            acc[e] = 0.f;
+          }
+        }
+      }
+    }
+  }
+  sq = wave_sum(sq);
+  if ((tid & 63) == 0) red[tid >> 6] = sq;
+  __syncthreads();
+  if (tid == 0) {
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) t += red[w];
+    a.ws[(int64_t)b * a.n_chunks + s] = t;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Batch-wide clipped sum of the input embedding:
 // out[v, f] (+)= sum over tokens k with ids[k] = v of c[k / T] * E[k, f].
 // ---------------------------------------------------------------------------
@@ -410,6 +547,16 @@ __global__ void fill_zero_kernel(float* p, int64_t n) {
 hipError_t launch_embed_norm(const EmbedNormArgs& a, int dt, hipStream_t s) {
   if (a.B == 0) return hipSuccess;
   const dim3 g(a.B, a.n_chunks), blk(EN_THREADS);
+  if (a.runs) {
+    if (dt == DT_BF16) {
+      if (a.T <= EN_CT_T) hipLaunchKernelGGL((embed_norm_runs_kernel<DT_BF16, EN_CT_T>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((embed_norm_runs_kernel<DT_BF16, EN_MAX_T>), g, blk, 0, s, a);
+    } else {
+      if (a.T <= EN_CT_T) hipLaunchKernelGGL((embed_norm_runs_kernel<DT_F32, EN_CT_T>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((embed_norm_runs_kernel<DT_F32, EN_MAX_T>), g, blk, 0, s, a);
+    }
+    return hipGetLastError();
+  }
   if (dt == DT_BF16)
     hipLaunchKernelGGL(embed_norm_kernel<DT_BF16>, g, blk, 0, s, a);
   else

@@ -63,7 +63,18 @@ hipError_t launch_gram_norm(const GramArgs& a, int dt, bool vec, hipStream_t s);
 // Tied cross term: sum_{t,s} Gz[s, ids[t]] <dE_t, H_s>, all T-tile pairs.
 constexpr int CR_FCHUNK = 128;  // features per cross-term work item
 constexpr int CR_DL_ROWS = 64;  // row block of the direct-load cross kernel
-inline bool cross_direct(int dt, bool vec) { return dt == DT_BF16 && vec; }
+constexpr int CR_RX_ROWS = 32;  // token and row blocks of the register-direct cross kernel
+constexpr int CX_SORT_T = 256;  // longest example whose tokens that kernel sorts by id
+constexpr int CX_ROWS_T = 128;  // longest example given to it (measured: at T = 256 its
+                                // 32-row blocks re-read E and H more than dl_cross's 64-row ones)
+// Cross-term kernel of a call: the register-staged tied_cross_kernel (fp32 or
+// unaligned rows), the register-direct cross_rows_kernel (bf16, aligned rows,
+// T <= CX_ROWS_T) or the direct-load dl_cross_kernel (bf16, aligned, longer T).
+enum { CROSS_STAGED = 0, CROSS_DL = 1, CROSS_ROWS = 2 };
+inline int cross_kind(int dt, bool vec, int T) {
+  if (dt != DT_BF16 || !vec) return CROSS_STAGED;
+  return T <= CX_ROWS_T ? CROSS_ROWS : CROSS_DL;
+}
 
 struct CrossArgs {
   const int32_t* ids;   // [B,T]
@@ -71,8 +82,10 @@ struct CrossArgs {
   const void* H;        // [B*T, ldh]
   const void* Gz;       // [B*T, ldz]
   int64_t lde, ldh, ldz;
-  int32_t B, T, V, d, n_t;  // n_t: row blocks per example (128 rows, 64 for bf16 aligned)
+  int32_t B, T, V, d, n_t;  // n_t: row blocks per example (128, 64 or 32 rows by kernel)
   int32_t n_fc;         // feature chunks (1 for bf16 aligned: all features per item)
+  int32_t kind;         // CROSS_STAGED, CROSS_DL or CROSS_ROWS
+  int32_t sort, pbits;  // CROSS_ROWS: tokens taken in (id, position) order; position bits of a key
   int32_t slots;        // n_t * n_t * n_fc
   float* ws;            // [B, slots]
 };
@@ -177,7 +190,8 @@ struct EmbedNormArgs {
   int64_t lde;
   int32_t B, T, V, d;
   int32_t pbits;        // bits for a position in a sort key
-  int32_t n_chunks;     // feature chunks of 64
+  int32_t n_chunks;     // partials per example: feature chunks of 64, or (runs) position ranges
+  int32_t runs;         // 1: embed_norm_runs_kernel (rows read EN_VB bytes per lane)
   int32_t* seg_id;      // nullable [B,T]
   int32_t* n_unique;    // nullable [B]
   float* ws;            // [B, n_chunks]
@@ -185,6 +199,10 @@ struct EmbedNormArgs {
 hipError_t launch_embed_norm(const EmbedNormArgs& a, int dt, hipStream_t s);
 
 constexpr int EN_MAX_T = 4096;   // tokens per example sorted in LDS (bucketing)
+constexpr int EN_CT_T = 256;     // up to this T the norm ranks keys by counting (one per thread)
+constexpr int EN_P = 32;         // sorted positions whose runs one workgroup of the norm owns
+constexpr int EN_VB = 8;         // bytes per lane load of the run-walking norm
+constexpr int EN_BATCH = 32;     // row loads a lane has in flight (EN_P: one batch per range)
 constexpr int ES_MAX_K = 16384;  // tokens per batch sorted in LDS (embedding sum)
 constexpr int ES_BLOCK = 32;     // sorted tokens per reduction block
 

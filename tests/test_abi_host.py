@@ -185,7 +185,8 @@ def test_cross_and_clip_reject_bad_arguments(L):
     assert f(*no_ws) == EINVAL
     # T = 300: 5 x 5 blocks of 64 rows (direct-load kernel) > 3 x 3 tile pairs x 1 chunk
     assert L.dp_tied_cross_term_workspace(4, 300, 64) == 512
-    assert L.dp_tied_cross_term_workspace(32, 128, 768) == 32 * 6 * 4
+    # T = 128: 4 x 4 blocks of 32 rows (register-direct kernel) > 1 x 6 chunks > 2 x 2 blocks
+    assert L.dp_tied_cross_term_workspace(32, 128, 768) == 32 * 16 * 4
     assert L.dp_clip_factors(1 << 20, 4, 0.0, 1 << 21, None) == EINVAL
     assert L.dp_clip_factors(1 << 20, 4, float("nan"), 1 << 21, None) == EINVAL
     assert L.dp_clip_factors(1 << 20, 0, 1.0, 1 << 21, None) == EINVAL

@@ -142,11 +142,19 @@ def test_head_norm(dp, dtype, V, ldz):
 @pytest.mark.parametrize("kind,T,V", [("zipf", 130, 50257), ("uniform", 16, 512),
                                       ("same", 64, 1000), ("distinct", 100, 300),
                                       ("zipf", 1, 50257), ("zipf", 1024, 50257),
+                                      ("zipf", 256, 50257), ("zipf", 257, 50257),
+                                      ("same", 300, 1000),
                                       ("zipf", 4096, 50257)])  # the most tokens bucketed in LDS
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_embedding_norm_and_buckets(dp, kind, T, V, dtype):
-    B, d = 3, 200
-    _say(f"embedding {kind} T={T} V={V} {dtype}")
+@pytest.mark.parametrize("d,lde", [(200, 200), (201, 201), (200, 204)],
+                         ids=["d200", "d201-scalar-rows", "d200-lde204"])
+def test_embedding_norm_and_buckets(dp, kind, T, V, dtype, d, lde):
+    """d = 200: rows read 8 bytes per lane, each example's runs split over
+    workgroups (counting rank up to T = 256, radix sort above); d = 201 (rows
+    not a multiple of 8 bytes in bf16): the per-feature kernel; lde = 204:
+    padded rows (NaN in the padding, never read)."""
+    B = 3
+    _say(f"embedding {kind} T={T} V={V} {dtype} d={d} lde={lde}")
     ids = gen.draw_ids(4, 1, (B, T), V, kind)
     dE = gen.draw(4, 2, (B, T, d), 1e-2, dtype)
     ref = O.embedding_norm2(ids, O.decode(dE, dtype), V)
@@ -154,7 +162,12 @@ def test_embedding_norm_and_buckets(dp, kind, T, V, dtype):
     n2 = torch.zeros(B, device="cuda")
     seg = torch.full((B, T), -1, dtype=torch.int32, device="cuda")
     nu = torch.zeros(B, dtype=torch.int32, device="cuda")
-    dp.dp_ghost_norm_embedding(dev(ids), dev(dE, dtype), V, n2, seg_id=seg, n_unique=nu)
+    dEd = dev(dE, dtype)
+    if lde != d:
+        pad = torch.full((B, T, lde), float("nan"), device="cuda", dtype=dEd.dtype)
+        pad[:, :, :d] = dEd
+        dEd = pad[:, :, :d]
+    dp.dp_ghost_norm_embedding(dev(ids), dEd, V, n2, seg_id=seg, n_unique=nu)
     np.testing.assert_array_equal(host(seg), seg_ref)
     np.testing.assert_array_equal(host(nu), nu_ref)
     err = rel(host(n2), ref).max()
@@ -178,9 +191,17 @@ def _tied_inputs(dtype, B, T, V, d, ldz, seed):
 
 
 @pytest.mark.parametrize("dtype,B,T,V,d,ldz", [("f32", 4, 16, 512, 64, 512),
+                                               ("bf16", 4, 128, 50257, 768, 50304),
+                                               ("bf16", 3, 100, 3000, 200, 3000),
+                                               ("bf16", 3, 32, 2000, 40, 2000),
+                                               ("bf16", 1, 1, 300, 16, 304),
                                                ("bf16", 3, 130, 5003, 96, 5003),
+                                               ("bf16", 2, 256, 50257, 768, 50304),
                                                ("bf16", 2, 260, 777, 100, 784)])
 def test_tied_cross_term(dp, dtype, B, T, V, d, ldz):
+    """fp32: the register-staged kernel; bf16 up to T = 128: 32 x 32 blocks
+    with the tokens in sorted-id order (GPT-2 shape, ragged T, a partial
+    16-feature step, T = 1); longer: the direct-load 64-row kernel."""
     _say(f"cross {dtype} B={B} T={T} V={V} d={d}")
     ids, dE, H, Gz = _tied_inputs(dtype, B, T, V, d, ldz, seed=21)
     dEd, Hd, Gzd = O.decode(dE, dtype), O.decode(H, dtype), O.decode(Gz, dtype)
@@ -202,10 +223,12 @@ def test_tied_cross_term(dp, dtype, B, T, V, d, ldz):
     assert rel(host(n2), tied_ref).max() <= TOL[dtype]
 
 
-def test_tied_cross_term_padded_rows(dp):
+@pytest.mark.parametrize("T", [100, 200])
+def test_tied_cross_term_padded_rows(dp, T):
     """dE and H on 16-byte aligned strides wider than d (NaN in the padding):
-    the direct-load kernel's last feature chunk straddles d."""
-    B, T, V, d, ld = 2, 200, 900, 100, 104
+    the last feature chunk straddles d, in the register-direct kernel
+    (T = 100) and the direct-load one (T = 200)."""
+    B, V, d, ld = 2, 900, 100, 104
     ids, dE, H, Gz = _tied_inputs("bf16", B, T, V, d, V, seed=23)
     dEp = np.full((B, T, ld), 0x7FC0, np.uint16)
     Hp = np.full((B, T, ld), 0x7FC0, np.uint16)
