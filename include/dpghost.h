@@ -246,8 +246,11 @@ dp_status_t dp_clip_factors_scaled2(const float* norm2_a, const float* norm2_b, 
  * parts in one buffer: call the head form, then the embedding form with
  * accumulate = 1.
  * Workspace: only the embedding form needs one,
- * dp_clipped_grad_sum_workspace(B, T, d_out, 1) bytes; limits for it:
- * B*T <= 16384 and ceil(log2(V + 1)) + ceil(log2(B*T)) <= 32.
+ * dp_clipped_grad_sum_workspace(B, T, d_out, 1) bytes; limit for it:
+ * ceil(log2(V + 1)) + ceil(log2(B*T)) <= 32 (a sort key holds an id
+ * clamped to V and a token index; B*T <= 65536 at V = 50257). Up to 16384
+ * tokens are sorted in one workgroup's LDS, more by a radix sort through
+ * the workspace (same order, so the same result).
  * ------------------------------------------------------------------- */
 size_t dp_clipped_grad_sum_workspace(int B, int T, int d_out, int with_ids);
 dp_status_t dp_clipped_grad_sum(const void* A, int64_t lda, const void* G, int64_t ldg,

@@ -400,9 +400,11 @@ dp_status_t static_scratch(void** out) {
 
 // Embedding-sum workspace layout (bytes): sorted keys, block head/tail partials.
 struct EsLayout {
-  size_t keys, head, tail, rank, seg, n_runs, rows, total;
+  size_t keys, head, tail, rank, seg, n_runs, rows, keys2, hist, gs_runs, total;
 };
-// compact: also the ranks, run starts, run count and [K, d] run rows.
+// compact: also the ranks, run starts, run count and [K, d] run rows. More
+// than ES_MAX_K keys: also the second key buffer, the digit counts and the
+// block run counts of the workspace radix sort.
 EsLayout es_layout(int64_t K, int d, bool compact = false) {
   EsLayout l{};
   const int64_t nb = ceil_div(K, dpg::ES_BLOCK);
@@ -415,6 +417,12 @@ EsLayout es_layout(int64_t K, int d, bool compact = false) {
     l.seg = off; off = align_up(off + (size_t)(K + 1) * 4);
     l.n_runs = off; off = align_up(off + 4);
     l.rows = off; off = align_up(off + (size_t)K * d * 4);
+  }
+  if (K > dpg::ES_MAX_K) {
+    const int64_t gb = ceil_div(K, dpg::GS_KB);
+    l.keys2 = off; off = align_up(off + (size_t)K * 4);
+    l.hist = off; off = align_up(off + (size_t)gb * 256 * 4);
+    l.gs_runs = off; off = align_up(off + (size_t)gb * 4);
   }
   l.total = off;
   return l;
@@ -887,8 +895,8 @@ static dp_status_t embed_sum_args(const int32_t* ids, const void* G, int64_t ldg
   if (B <= 0 || T <= 0 || V <= 0 || d <= 0)
     return fail(DP_EINVAL, "B, T, V and d must be positive");
   const int64_t K = (int64_t)B * T;
-  if (K > dpg::ES_MAX_K)
-    return fail(DP_EUNSUPPORTED, "B*T = %lld exceeds %d", (long long)K, dpg::ES_MAX_K);
+  if (K > INT32_MAX)
+    return fail(DP_EUNSUPPORTED, "B*T = %lld exceeds 2^31 - 1", (long long)K);
   const int pbits = std::max(1, bits_for(K));
   if (bits_for((int64_t)V + 1) + pbits > 32)  // ids are clamped to V, so V + 1 values
     return fail(DP_EUNSUPPORTED, "V and B*T do not fit a 32-bit sort key");
@@ -908,6 +916,12 @@ static dp_status_t embed_sum_args(const int32_t* ids, const void* G, int64_t ldg
     a.seg = reinterpret_cast<int32_t*>(w + l.seg);
     a.n_runs = reinterpret_cast<int32_t*>(w + l.n_runs);
     a.rows = reinterpret_cast<float*>(w + l.rows);
+  }
+  if (K > dpg::ES_MAX_K) {
+    a.gs_blocks = (int32_t)ceil_div(K, dpg::GS_KB);
+    a.keys2 = reinterpret_cast<uint32_t*>(w + l.keys2);
+    a.hist = reinterpret_cast<int32_t*>(w + l.hist);
+    a.gs_runs = reinterpret_cast<int32_t*>(w + l.gs_runs);
   }
   return DP_OK;
 }

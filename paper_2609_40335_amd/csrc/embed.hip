@@ -78,57 +78,76 @@ __device__ int rank_sorted(const uint32_t* keys, int n, int pbits, int32_t* rank
 // wave's keys 64 at a time: lanes with equal digits are found with eight
 // ballots and ranked by lane; the group's lowest lane advances the wave's
 // running offset. Returns the index of the buffer that holds the result.
+// One stable LSD radix pass, 8 bits at bit `sh`, of n keys from LDS buffer
+// `in` to `out`. NW waves; wave w owns a contiguous segment of the keys. The
+// pass counts digits per wave (cnt[w][digit]), turns the counts into
+// offsets in digit-major, wave-minor order, and scatters each wave's keys 64
+// at a time: lanes with equal digits are found with eight ballots and ranked
+// by lane; the group's lowest lane advances the wave's running offset.
 template <int NW>
-__device__ int lds_radix_sort(uint32_t* buf0, uint32_t* buf1, int n, int pb, uint32_t V, int* cnt,
-                              int* wave_tot) {
+__device__ void lds_radix_pass(const uint32_t* in, uint32_t* out, int n, int sh, int* cnt,
+                               int* wave_tot) {
   static_assert(NW % 4 == 0, "4 (digit, wave) entries per thread");
   constexpr int NT = NW * WAVE;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  int idbits = 0;  // bits of the values 0..V
-  while ((1u << idbits) <= V) ++idbits;
   const int seg_len = ((n + NW - 1) / NW + WAVE - 1) / WAVE * WAVE;
   const int s0 = min(w * seg_len, n), s1 = min(s0 + seg_len, n);
   const uint64_t lt = (1ull << lane) - 1ull;
-  int src = 0;
-  for (int shift = 0; shift < idbits; shift += 8, src ^= 1) {
-    const int sh = pb + shift;
-    const uint32_t* in = src ? buf1 : buf0;
-    uint32_t* out = src ? buf0 : buf1;
-    for (int i = tid; i < NW * 256; i += NT) cnt[i] = 0;
-    __syncthreads();
-    for (int p = s0 + lane; p < s1; p += WAVE) atomicAdd(&cnt[w * 256 + ((in[p] >> sh) & 255)], 1);
-    __syncthreads();
-    {
-      // thread t holds entries 4t .. 4t+3 of the (digit, wave) order
-      const int d = (4 * tid) / NW, w0 = (4 * tid) % NW;
-      int v[4], loc = 0;
+  for (int i = tid; i < NW * 256; i += NT) cnt[i] = 0;
+  __syncthreads();
+  for (int p = s0 + lane; p < s1; p += WAVE) atomicAdd(&cnt[w * 256 + ((in[p] >> sh) & 255)], 1);
+  __syncthreads();
+  {
+    // thread t holds entries 4t .. 4t+3 of the (digit, wave) order
+    const int d = (4 * tid) / NW, w0 = (4 * tid) % NW;
+    int v[4], loc = 0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) { v[q] = cnt[(w0 + q) * 256 + d]; loc += v[q]; }
-      int total;
-      const int incl = block_inclusive_scan(loc, wave_tot, tid, NT, &total);
-      int run = incl - loc;
+    for (int q = 0; q < 4; ++q) { v[q] = cnt[(w0 + q) * 256 + d]; loc += v[q]; }
+    int total;
+    const int incl = block_inclusive_scan(loc, wave_tot, tid, NT, &total);
+    int run = incl - loc;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) { cnt[(w0 + q) * 256 + d] = run; run += v[q]; }
-    }
-    __syncthreads();
-    for (int base = s0; base < s1; base += WAVE) {
-      const int p = base + lane;
-      const bool valid = p < s1;
-      const uint32_t key = valid ? in[p] : 0u;
-      const int dg = (int)((key >> sh) & 255);
-      uint64_t m = __ballot(valid);
-#pragma unroll
-      for (int bit = 0; bit < 8; ++bit) {
-        const uint64_t mb = __ballot(valid && ((dg >> bit) & 1));
-        m &= ((dg >> bit) & 1) ? mb : ~mb;
-      }
-      const int rank = __popcll(m & lt);
-      const int off = valid ? cnt[w * 256 + dg] : 0;
-      if (valid) out[off + rank] = key;
-      if (valid && rank == 0) cnt[w * 256 + dg] = off + __popcll(m);
-    }
-    __syncthreads();
+    for (int q = 0; q < 4; ++q) { cnt[(w0 + q) * 256 + d] = run; run += v[q]; }
   }
+  __syncthreads();
+  for (int base = s0; base < s1; base += WAVE) {
+    const int p = base + lane;
+    const bool valid = p < s1;
+    const uint32_t key = valid ? in[p] : 0u;
+    const int dg = (int)((key >> sh) & 255);
+    uint64_t m = __ballot(valid);
+#pragma unroll
+    for (int bit = 0; bit < 8; ++bit) {
+      const uint64_t mb = __ballot(valid && ((dg >> bit) & 1));
+      m &= ((dg >> bit) & 1) ? mb : ~mb;
+    }
+    const int rank = __popcll(m & lt);
+    const int off = valid ? cnt[w * 256 + dg] : 0;
+    if (valid) out[off + rank] = key;
+    if (valid && rank == 0) cnt[w * 256 + dg] = off + __popcll(m);
+  }
+  __syncthreads();
+}
+
+// Bits of the values 0..V (the ids, clamped to V).
+__device__ __forceinline__ int id_bits(uint32_t V) {
+  int b = 0;
+  while ((1u << b) <= V) ++b;
+  return b;
+}
+
+// Stable LSD radix sort, 8 bits per pass, of n keys (id << pb | position)
+// held in LDS buffer buf0, over the bits of the ids 0..V (ids at or past V
+// must already be clamped to V). The keys arrive in position order, so the
+// result is the (id, position) order. Returns the index of the buffer that
+// holds the result.
+template <int NW>
+__device__ int lds_radix_sort(uint32_t* buf0, uint32_t* buf1, int n, int pb, uint32_t V, int* cnt,
+                              int* wave_tot) {
+  const int idbits = id_bits(V);
+  int src = 0;
+  for (int shift = 0; shift < idbits; shift += 8, src ^= 1)
+    lds_radix_pass<NW>(src ? buf1 : buf0, src ? buf0 : buf1, n, pb + shift, cnt, wave_tot);
   return src;
 }
 
@@ -406,6 +425,132 @@ __global__ __launch_bounds__(ES_THREADS) void embed_sort_kernel(EmbedSumArgs a) 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Batch-wide sort of more keys than one workgroup's LDS holds: a stable LSD
+// radix sort through the workspace, 8 id bits per pass, GS_KB keys per
+// block. A pass counts each block's digits (hist, digit-major and
+// block-minor), turns the counts into exclusive offsets in that order (one
+// workgroup), and scatters: each block sorts its keys by the digit in LDS
+// (one stable LDS pass), then writes its j-th key of digit d to
+// offset[d][block] + (j - first local index of d). Blocks and keys within a
+// block keep their order, so the pass is stable and the result is the same
+// (id, position) order as the single-workgroup sort. Pass 0 builds the keys
+// from the ids.
+// ---------------------------------------------------------------------------
+constexpr int GS_THREADS = 1024;
+constexpr int GS_NW = GS_THREADS / WAVE;
+
+__device__ __forceinline__ uint32_t make_key(const EmbedSumArgs& a, int64_t p) {
+  const uint32_t id = (uint32_t)a.ids[p];
+  return ((id < (uint32_t)a.V ? id : (uint32_t)a.V) << a.pbits) | (uint32_t)p;
+}
+
+__global__ __launch_bounds__(GS_THREADS) void gsort_hist_kernel(EmbedSumArgs a, const uint32_t* src,
+                                                                 int sh) {
+  __shared__ int h[256];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int64_t p0 = (int64_t)b * GS_KB;
+  const int n = (int)min((int64_t)GS_KB, (int64_t)a.K - p0);
+  if (tid < 256) h[tid] = 0;
+  __syncthreads();
+  for (int p = tid; p < n; p += GS_THREADS) {
+    const uint32_t key = src ? src[p0 + p] : make_key(a, p0 + p);
+    atomicAdd(&h[(key >> sh) & 255], 1);  // integer counts: order-free
+  }
+  __syncthreads();
+  if (tid < 256) a.hist[(int64_t)tid * a.gs_blocks + b] = h[tid];
+}
+
+// Exclusive prefix sum, in place, of n ints (one workgroup; each thread
+// scans a contiguous chunk). *total receives the sum when not NULL.
+__global__ __launch_bounds__(GS_THREADS) void gscan_kernel(int* v, int n, int* total) {
+  __shared__ int wave_tot[GS_NW];
+  const int tid = threadIdx.x;
+  const int per = (n + GS_THREADS - 1) / GS_THREADS;
+  const int i0 = min(tid * per, n), i1 = min(i0 + per, n);
+  int loc = 0;
+  for (int i = i0; i < i1; ++i) loc += v[i];
+  int tot;
+  const int incl = block_inclusive_scan(loc, wave_tot, tid, GS_THREADS, &tot);
+  int run = incl - loc;
+  for (int i = i0; i < i1; ++i) {
+    const int x = v[i];
+    v[i] = run;
+    run += x;
+  }
+  if (total && tid == 0) *total = tot;
+}
+
+__global__ __launch_bounds__(GS_THREADS) void gsort_scatter_kernel(EmbedSumArgs a,
+                                                                   const uint32_t* src,
+                                                                   uint32_t* dst, int sh) {
+  __shared__ uint32_t kin[GS_KB], kout[GS_KB];
+  __shared__ int cnt[GS_NW * 256];
+  __shared__ int wave_tot[GS_NW];
+  __shared__ int lstart[256];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int64_t p0 = (int64_t)b * GS_KB;
+  const int n = (int)min((int64_t)GS_KB, (int64_t)a.K - p0);
+  for (int p = tid; p < n; p += GS_THREADS) kin[p] = src ? src[p0 + p] : make_key(a, p0 + p);
+  if (tid < 256) lstart[tid] = 0;
+  __syncthreads();
+  lds_radix_pass<GS_NW>(kin, kout, n, sh, cnt, wave_tot);
+  // first local index of each digit: the count of smaller digits
+  for (int p = tid; p < n; p += GS_THREADS) atomicAdd(&lstart[(kout[p] >> sh) & 255], 1);
+  __syncthreads();
+  {
+    int c = tid < 256 ? lstart[tid] : 0, tot;
+    const int incl = block_inclusive_scan(c, wave_tot, tid, GS_THREADS, &tot);
+    __syncthreads();
+    if (tid < 256) lstart[tid] = incl - c;
+  }
+  __syncthreads();
+  for (int j = tid; j < n; j += GS_THREADS) {
+    const uint32_t key = kout[j];
+    const int d = (int)((key >> sh) & 255);
+    dst[a.hist[(int64_t)d * a.gs_blocks + b] + (j - lstart[d])] = key;
+  }
+}
+
+// Runs of equal ids in the globally sorted keys: heads per block, then (after
+// an exclusive scan of the block counts, which also gives the run count)
+// every sorted position's run index and every run's first position.
+__device__ __forceinline__ bool run_head(const EmbedSumArgs& a, int64_t p) {
+  return p == 0 || (a.keys[p] >> a.pbits) != (a.keys[p - 1] >> a.pbits);
+}
+
+__global__ __launch_bounds__(GS_THREADS) void gruns_count_kernel(EmbedSumArgs a) {
+  __shared__ int wave_tot[GS_NW];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int64_t p0 = (int64_t)b * GS_KB;
+  const int n = (int)min((int64_t)GS_KB, (int64_t)a.K - p0);
+  int c = 0;
+  for (int p = tid; p < n; p += GS_THREADS) c += run_head(a, p0 + p) ? 1 : 0;
+  int tot;
+  block_inclusive_scan(c, wave_tot, tid, GS_THREADS, &tot);
+  if (tid == 0) a.gs_runs[b] = tot;
+}
+
+__global__ __launch_bounds__(GS_THREADS) void gruns_write_kernel(EmbedSumArgs a) {
+  __shared__ int wave_tot[GS_NW];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int64_t p0 = (int64_t)b * GS_KB;
+  const int n = (int)min((int64_t)GS_KB, (int64_t)a.K - p0);
+  const int per = (n + GS_THREADS - 1) / GS_THREADS;
+  const int i0 = min(tid * per, n), i1 = min(i0 + per, n);
+  int c = 0;
+  for (int i = i0; i < i1; ++i) c += run_head(a, p0 + i) ? 1 : 0;
+  int tot;
+  const int incl = block_inclusive_scan(c, wave_tot, tid, GS_THREADS, &tot);
+  int r = a.gs_runs[b] + incl - c;  // runs that start before this thread's first position
+  for (int i = i0; i < i1; ++i) {
+    const int64_t p = p0 + i;
+    if (run_head(a, p)) a.seg[r++] = (int32_t)p;
+    a.rank[p] = r - 1;
+  }
+  if (b == a.gs_blocks - 1 && tid == 0) a.seg[*a.n_runs] = a.K;
+}
+
 __device__ __forceinline__ void out_add(const EmbedSumArgs& a, uint32_t v, int f, float val) {
   if (v >= (uint32_t)a.V) return;  // invalid id: contributes nothing
   float* o = a.transpose ? a.out + (int64_t)f * a.ldo + v : a.out + (int64_t)v * a.ldo + f;
@@ -564,10 +709,39 @@ hipError_t launch_embed_norm(const EmbedNormArgs& a, int dt, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Sorted keys into a.keys (and, for the compact form, ranks, run starts and
+// the run count): one workgroup up to ES_MAX_K keys, the radix sort through
+// the workspace beyond.
+static hipError_t launch_embed_keys(const EmbedSumArgs& a, bool compact, hipStream_t s) {
+  if (a.K <= ES_MAX_K) {
+    hipLaunchKernelGGL(embed_sort_kernel, dim3(1), dim3(ES_THREADS), 0, s, a);
+    return hipGetLastError();
+  }
+  int idbits = 0;
+  while ((1u << idbits) <= (uint32_t)a.V) ++idbits;
+  const int passes = (idbits + 7) / 8;
+  const dim3 g(a.gs_blocks), blk(GS_THREADS);
+  for (int q = 0; q < passes; ++q) {
+    // the last pass writes a.keys
+    uint32_t* dst = ((passes - 1 - q) & 1) ? a.keys2 : a.keys;
+    const uint32_t* src = q == 0 ? nullptr : (((passes - q) & 1) ? a.keys2 : a.keys);
+    const int sh = a.pbits + 8 * q;
+    hipLaunchKernelGGL(gsort_hist_kernel, g, blk, 0, s, a, src, sh);
+    hipLaunchKernelGGL(gscan_kernel, dim3(1), blk, 0, s, a.hist, 256 * a.gs_blocks,
+                       (int*)nullptr);
+    hipLaunchKernelGGL(gsort_scatter_kernel, g, blk, 0, s, a, src, dst, sh);
+  }
+  if (compact) {
+    hipLaunchKernelGGL(gruns_count_kernel, g, blk, 0, s, a);
+    hipLaunchKernelGGL(gscan_kernel, dim3(1), blk, 0, s, a.gs_runs, a.gs_blocks, a.n_runs);
+    hipLaunchKernelGGL(gruns_write_kernel, g, blk, 0, s, a);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_embed_sum(const EmbedSumArgs& a, int dt, hipStream_t s) {
   if (a.K == 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_sort_kernel, dim3(1), dim3(ES_THREADS), 0, s, a);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_embed_keys(a, false, s);
   if (e != hipSuccess) return e;
   const int n_fc = (a.d + WAVE - 1) / WAVE;
   const int n_blocks = (a.K + ES_BLOCK - 1) / ES_BLOCK;
@@ -585,8 +759,7 @@ hipError_t launch_embed_sum(const EmbedSumArgs& a, int dt, hipStream_t s) {
 
 hipError_t launch_embed_rows(const EmbedSumArgs& a, int dt, hipStream_t s) {
   if (a.K == 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_sort_kernel, dim3(1), dim3(ES_THREADS), 0, s, a);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_embed_keys(a, true, s);
   if (e != hipSuccess) return e;
   const int n_fc = (a.d + WAVE - 1) / WAVE;
   const int n_blocks = (a.K + ES_BLOCK - 1) / ES_BLOCK;

@@ -205,6 +205,7 @@ constexpr int EN_VB = 8;         // bytes per lane load of the run-walking norm
 constexpr int EN_BATCH = 32;     // row loads a lane has in flight (EN_P: one batch per range)
 constexpr int ES_MAX_K = 16384;  // tokens per batch sorted in LDS (embedding sum)
 constexpr int ES_BLOCK = 32;     // sorted tokens per reduction block
+constexpr int GS_KB = 4096;      // keys per block of the workspace radix sort (more than ES_MAX_K keys)
 
 struct EmbedSumArgs {
   const int32_t* ids;   // [K] flattened B*T
@@ -226,6 +227,13 @@ struct EmbedSumArgs {
   int32_t* seg;         // workspace [K + 1] first sorted position of every run
   int32_t* n_runs;      // workspace [1] number of runs
   float* rows;          // workspace [K, d] run sums
+  // More than ES_MAX_K keys: the workspace radix sort over gs_blocks blocks
+  // of GS_KB keys (keys2: the other key buffer, hist: [256, gs_blocks]
+  // digit counts, then offsets; gs_runs: [gs_blocks] run counts, then bases).
+  int32_t gs_blocks;
+  uint32_t* keys2;
+  int32_t* hist;
+  int32_t* gs_runs;
 };
 hipError_t launch_embed_sum(const EmbedSumArgs& a, int dt, hipStream_t s);
 // The compact form: sort, ranks, run sums into a.rows.

@@ -213,8 +213,9 @@ def test_clipped_sum_rejects_bad_arguments(L):
     # embedding form without workspace
     assert f(None, 0, 1 << 21, 64, 1 << 22, 1 << 23, 4, 16, 512, 64, 0, 0, 1 << 24, 0,
              None, 0, None) == EINVAL
-    # batch too large for the in-LDS sort
-    assert f(None, 0, 1 << 21, 64, 1 << 22, 1 << 23, 64, 512, 512, 64, 0, 0, 1 << 24, 0,
+    # a sort key would need more than 32 bits: 21 for ids up to V = 2^20, 15
+    # for B*T = 32768 token indices
+    assert f(None, 0, 1 << 21, 64, 1 << 22, 1 << 23, 64, 512, 1 << 20, 64, 0, 0, 1 << 24, 0,
              1 << 25, 1 << 30, None) == EUNSUP
     assert L.dp_clipped_grad_sum_workspace(4, 16, 64, 0) == 0
     assert L.dp_clipped_grad_sum_workspace(64, 256, 768, 1) > 2 * 512 * 768 * 4
@@ -271,7 +272,7 @@ def test_embedding_rows_workspace_and_validation(L):
         a[i] = bad
         assert f(*a) == EINVAL, (i, bad)
     big = list(args)
-    big[4], big[5] = 64, 512                  # B*T past the in-LDS sort
+    big[4], big[5], big[6] = 64, 512, 1 << 20  # ids of 21 bits + 15 bits of B*T: no 32-bit key
     big[10] = 1 << 40
     assert f(*big) == EUNSUP
     g = L.dp_embedding_rows_add

@@ -1,5 +1,7 @@
 """GPU: the embedding form of the clipped sum in two calls (dp_embedding_rows,
 then dp_embedding_rows_add) against the one-call form and the fp64 oracle.
+Batches of up to 16384 tokens are sorted in one workgroup, larger ones by the
+radix sort through the workspace (to B*T = 65536 at V = 50257).
 
 The two-call form adds each run's finished row with one fp32 addition, as the
 one-call form does, so the two agree bit for bit; the oracle bounds both.
@@ -60,7 +62,13 @@ CASES = [
     ("bf16", 4, 64, 50, 64, "same", 0, False),      # one run through every block
     ("f32", 1, 1, 10, 8, "uniform", 0, False),      # a single token
     ("bf16", 32, 128, 50257, 768, "zipf", 0, False),  # GPT-2 step
-    ("bf16", 64, 256, 50257, 768, "zipf", 0, False),  # B*T = 16384, the most the sort takes
+    ("bf16", 64, 256, 50257, 768, "zipf", 0, False),  # B*T = 16384, the most one workgroup sorts
+    # past it, the radix sort through the workspace:
+    ("bf16", 65, 256, 50257, 768, "zipf", 0, False),  # B*T = 16640, a ragged last sort block
+    ("bf16", 128, 256, 50257, 768, "zipf", 0, False),  # B*T = 32768
+    ("bf16", 256, 256, 50257, 256, "zipf", 0, False),  # B*T = 65536, the most a 32-bit key holds
+    ("f32", 40, 500, 3000, 40, "zipf", 9, True),      # B*T = 20000, invalid ids, transposed
+    ("bf16", 20, 1000, 64, 32, "same", 0, False),     # one run across every sort block
 ]
 
 
