@@ -175,8 +175,12 @@ dp_status_t dp_ghost_norm_linear_bias_grouped_noalloc(const dp_linear_t* layers,
  *   seg_id[b,t]  = rank of ids[b,t] among the sorted distinct ids of b
  *   n_unique[b]  = number of distinct ids of b
  * seg_id and n_unique may be NULL. Exact (integer) outputs.
- * Limits: T <= 4096 and ceil(log2(V + 1)) + ceil(log2 T) <= 32 (a sort key
- * holds an id clamped to V and a position).
+ * Limits: ceil(log2(V + 1)) + ceil(log2 T) <= 32 (a sort key holds an id
+ * clamped to V and a position; T <= 65536 at V = 50257) and B*T < 2^31.
+ * Up to T = 4096 an example is sorted in LDS, longer ones by a radix sort
+ * through the workspace; those need rows of whole 8-byte units (lde and d
+ * times the element size multiples of 8, dE 8-byte aligned) whose T rows
+ * span less than 4 GiB, and are refused with DP_EUNSUPPORTED otherwise.
  * ------------------------------------------------------------------- */
 size_t dp_ghost_norm_embedding_workspace(int B, int T, int d);
 dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t lde, int B, int T,

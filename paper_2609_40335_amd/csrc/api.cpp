@@ -668,9 +668,32 @@ dp_status_t dp_ghost_norm_linear(const void* A, int64_t lda, const void* G, int6
 // Partials per example: one per 64-feature chunk (embed_norm_kernel) or per
 // EN_P sorted positions (embed_norm_runs_kernel); the size query cannot know
 // which kernel a call takes, so it covers both.
+// Past EN_MAX_T tokens an example is sorted through the workspace: keys and
+// their second buffer, digit counts, block run counts, run indices, run
+// starts and run counts follow the partials.
+struct EnLayout {
+  size_t gkeys, gkeys2, ghist, gruns, grank, gseg, gnseg, total;
+};
+EnLayout en_layout(int B, int T, int d) {
+  EnLayout l{};
+  size_t off = align_up((size_t)B * std::max(ceil_div(d, 64), ceil_div(T, dpg::EN_P)) * 4);
+  if (T > dpg::EN_MAX_T) {
+    const size_t K = (size_t)B * T, nbs = (size_t)ceil_div(T, dpg::GS_KB);
+    l.gkeys = off; off = align_up(off + K * 4);
+    l.gkeys2 = off; off = align_up(off + K * 4);
+    l.ghist = off; off = align_up(off + (size_t)B * 256 * nbs * 4);
+    l.gruns = off; off = align_up(off + (size_t)B * nbs * 4);
+    l.grank = off; off = align_up(off + K * 4);
+    l.gseg = off; off = align_up(off + (size_t)B * (T + 1) * 4);
+    l.gnseg = off; off = align_up(off + (size_t)B * 4);
+  }
+  l.total = off;
+  return l;
+}
+
 size_t dp_ghost_norm_embedding_workspace(int B, int T, int d) {
   if (B <= 0 || T <= 0 || d <= 0) return 0;
-  return align_up((size_t)B * std::max(ceil_div(d, 64), ceil_div(T, dpg::EN_P)) * 4);
+  return en_layout(B, T, d).total;
 }
 
 dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t lde, int B, int T,
@@ -682,7 +705,7 @@ dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t 
     return fail(DP_EINVAL, "B, T, V and d must be positive");
   if (lde < d) return fail(DP_EINVAL, "lde (%lld) < d (%d)", (long long)lde, d);
   if (!dtype_ok(dt)) return fail(DP_EINVAL, "unknown dtype %d", (int)dt);
-  if (T > dpg::EN_MAX_T) return fail(DP_EUNSUPPORTED, "T = %d exceeds %d", T, dpg::EN_MAX_T);
+  if ((int64_t)B * T > INT32_MAX) return fail(DP_EUNSUPPORTED, "B*T exceeds 2^31 - 1");
   const int pbits = std::max(1, bits_for(T));
   if (bits_for((int64_t)V + 1) + pbits > 32)  // ids are clamped to V, so V + 1 values
     return fail(DP_EUNSUPPORTED, "V = %d and T = %d do not fit a 32-bit sort key", V, T);
@@ -700,6 +723,20 @@ dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t 
             (d * es) % dpg::EN_VB == 0 && span_ok(T, lde, dt)) ? 1 : 0;
   a.n_chunks = (int)(a.runs ? ceil_div(T, dpg::EN_P) : ceil_div(d, 64));
   a.seg_id = seg_id; a.n_unique = n_unique;
+  if (T > dpg::EN_MAX_T) {
+    if (!a.runs)
+      return fail(DP_EUNSUPPORTED, "T = %d exceeds %d for rows that are not whole 8-byte units "
+                  "within a 4 GiB span", T, dpg::EN_MAX_T);
+    const EnLayout l = en_layout(B, T, d);
+    char* w = static_cast<char*>(workspace);
+    a.gkeys = reinterpret_cast<uint32_t*>(w + l.gkeys);
+    a.gkeys2 = reinterpret_cast<uint32_t*>(w + l.gkeys2);
+    a.ghist = reinterpret_cast<int32_t*>(w + l.ghist);
+    a.gruns = reinterpret_cast<int32_t*>(w + l.gruns);
+    a.grank = reinterpret_cast<int32_t*>(w + l.grank);
+    a.gseg = reinterpret_cast<int32_t*>(w + l.gseg);
+    a.gnseg = reinterpret_cast<int32_t*>(w + l.gnseg);
+  }
   a.ws = static_cast<float*>(workspace);
   hipStream_t s = as_stream(stream);
   dp_status_t st = hip_status(dpg::launch_embed_norm(a, kdt(dt), s), "embed_norm launch");
@@ -918,7 +955,8 @@ static dp_status_t embed_sum_args(const int32_t* ids, const void* G, int64_t ldg
     a.rows = reinterpret_cast<float*>(w + l.rows);
   }
   if (K > dpg::ES_MAX_K) {
-    a.gs_blocks = (int32_t)ceil_div(K, dpg::GS_KB);
+    a.gs_blocks = a.gs_nbs = (int32_t)ceil_div(K, dpg::GS_KB);
+    a.gs_seg = (int32_t)K;
     a.keys2 = reinterpret_cast<uint32_t*>(w + l.keys2);
     a.hist = reinterpret_cast<int32_t*>(w + l.hist);
     a.gs_runs = reinterpret_cast<int32_t*>(w + l.gs_runs);

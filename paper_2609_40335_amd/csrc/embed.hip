@@ -277,9 +277,10 @@ template <int DT, int MAXT>
 __global__ __launch_bounds__(EN_THREADS) void embed_norm_runs_kernel(EmbedNormArgs a) {
   constexpr int VEC = EN_VB / ((DT == DT_BF16) ? 2 : 4);  // elements per lane load
   constexpr int NW = EN_THREADS / WAVE;
-  __shared__ __attribute__((aligned(16))) uint32_t kbuf[(MAXT > EN_CT_T) ? 2 : 1][MAXT];
-  __shared__ int32_t rank[MAXT];
-  __shared__ int32_t seg[MAXT + 1];
+  constexpr int LT = MAXT > 0 ? MAXT : 1;  // MAXT = 0: keys, ranks and runs from the workspace
+  __shared__ __attribute__((aligned(16))) uint32_t kbuf[(MAXT > EN_CT_T) ? 2 : 1][LT];
+  __shared__ int32_t rank_l[LT];
+  __shared__ int32_t seg_l[LT + 1];
   __shared__ int cnt[(MAXT > EN_CT_T) ? NW * 256 : 1];
   __shared__ int wave_tot[NW];
   __shared__ float red[NW];
@@ -289,7 +290,16 @@ __global__ __launch_bounds__(EN_THREADS) void embed_norm_runs_kernel(EmbedNormAr
   const uint32_t V = (uint32_t)a.V;
   const int32_t* ids = a.ids + (int64_t)b * T;
   const uint32_t* keys;
-  if constexpr (MAXT <= EN_CT_T) {
+  const int32_t* rank = rank_l;
+  const int32_t* seg = seg_l;
+  int nseg;
+  if constexpr (MAXT == 0) {
+    // sorted and ranked per example by the workspace radix sort
+    keys = a.gkeys + (int64_t)b * T;
+    rank = a.grank + (int64_t)b * T;
+    seg = a.gseg + (int64_t)b * (T + 1);
+    nseg = a.gnseg[b];
+  } else if constexpr (MAXT <= EN_CT_T) {
     // Keys are distinct (the position is in the low bits), so a key's rank
     // is the number of smaller keys: T <= EN_THREADS, one key per thread.
     uint32_t k = 0xFFFFFFFFu;
@@ -312,7 +322,7 @@ __global__ __launch_bounds__(EN_THREADS) void embed_norm_runs_kernel(EmbedNormAr
     __syncthreads();
     keys = kbuf[lds_radix_sort<NW>(kbuf[0], kbuf[1], T, pb, V, cnt, wave_tot)];
   }
-  const int nseg = rank_sorted(keys, T, pb, rank, seg, wave_tot, tid, EN_THREADS);
+  if constexpr (MAXT > 0) nseg = rank_sorted(keys, T, pb, rank_l, seg_l, wave_tot, tid, EN_THREADS);
   // Sorted positions [p_lo, p_hi) of this workgroup: bucket ids for them, and
   // the runs that start there.
   const int p_lo = min(s * EN_P, T), p_hi = min(p_lo + EN_P, T);
@@ -426,46 +436,64 @@ __global__ __launch_bounds__(ES_THREADS) void embed_sort_kernel(EmbedSumArgs a) 
 }
 
 // ---------------------------------------------------------------------------
-// Batch-wide sort of more keys than one workgroup's LDS holds: a stable LSD
-// radix sort through the workspace, 8 id bits per pass, GS_KB keys per
-// block. A pass counts each block's digits (hist, digit-major and
-// block-minor), turns the counts into exclusive offsets in that order (one
-// workgroup), and scatters: each block sorts its keys by the digit in LDS
-// (one stable LDS pass), then writes its j-th key of digit d to
-// offset[d][block] + (j - first local index of d). Blocks and keys within a
-// block keep their order, so the pass is stable and the result is the same
-// (id, position) order as the single-workgroup sort. Pass 0 builds the keys
-// from the ids.
+// Sort of more keys than one workgroup's LDS holds: a stable LSD radix sort
+// through the workspace, 8 id bits per pass, in segments of gs_seg keys
+// sorted independently (the whole batch for the embedding sum, one example
+// each for the norm's buckets), GS_KB keys per block, gs_nbs blocks per
+// segment. A pass counts each block's digits (hist: per segment, digit-major
+// and block-minor), turns the counts into exclusive offsets in that order
+// (one workgroup per segment), and scatters: each block sorts its keys by
+// the digit in LDS (one stable LDS pass), then writes its j-th key of digit
+// d to offset[d][block] + (j - first local index of d) within its segment.
+// Blocks and keys within a block keep their order, so the pass is stable
+// and the result is the (id, position) order of the single-workgroup sort.
+// Pass 0 builds the keys from the ids; the position field of a key is the
+// token's index within its segment.
 // ---------------------------------------------------------------------------
 constexpr int GS_THREADS = 1024;
 constexpr int GS_NW = GS_THREADS / WAVE;
 
-__device__ __forceinline__ uint32_t make_key(const EmbedSumArgs& a, int64_t p) {
-  const uint32_t id = (uint32_t)a.ids[p];
-  return ((id < (uint32_t)a.V ? id : (uint32_t)a.V) << a.pbits) | (uint32_t)p;
+struct GsBlock {
+  int64_t s0, p0;  // first key of the segment, of the block
+  int n, seg, lb;  // keys in the block, segment, block within the segment
+};
+__device__ __forceinline__ GsBlock gs_block(const EmbedSumArgs& a) {
+  GsBlock g;
+  g.seg = (int)(blockIdx.x / (uint32_t)a.gs_nbs);
+  g.lb = (int)(blockIdx.x - (uint32_t)g.seg * a.gs_nbs);
+  g.s0 = (int64_t)g.seg * a.gs_seg;
+  g.p0 = g.s0 + (int64_t)g.lb * GS_KB;
+  g.n = (int)min((int64_t)GS_KB, g.s0 + a.gs_seg - g.p0);
+  return g;
+}
+
+__device__ __forceinline__ uint32_t make_key(const EmbedSumArgs& a, const GsBlock& g, int i) {
+  const uint32_t id = (uint32_t)a.ids[g.p0 + i];
+  return ((id < (uint32_t)a.V ? id : (uint32_t)a.V) << a.pbits) | (uint32_t)(g.p0 + i - g.s0);
 }
 
 __global__ __launch_bounds__(GS_THREADS) void gsort_hist_kernel(EmbedSumArgs a, const uint32_t* src,
                                                                  int sh) {
   __shared__ int h[256];
-  const int b = blockIdx.x, tid = threadIdx.x;
-  const int64_t p0 = (int64_t)b * GS_KB;
-  const int n = (int)min((int64_t)GS_KB, (int64_t)a.K - p0);
+  const GsBlock g = gs_block(a);
+  const int tid = threadIdx.x;
   if (tid < 256) h[tid] = 0;
   __syncthreads();
-  for (int p = tid; p < n; p += GS_THREADS) {
-    const uint32_t key = src ? src[p0 + p] : make_key(a, p0 + p);
+  for (int i = tid; i < g.n; i += GS_THREADS) {
+    const uint32_t key = src ? src[g.p0 + i] : make_key(a, g, i);
     atomicAdd(&h[(key >> sh) & 255], 1);  // integer counts: order-free
   }
   __syncthreads();
-  if (tid < 256) a.hist[(int64_t)tid * a.gs_blocks + b] = h[tid];
+  if (tid < 256) a.hist[((int64_t)g.seg * 256 + tid) * a.gs_nbs + g.lb] = h[tid];
 }
 
-// Exclusive prefix sum, in place, of n ints (one workgroup; each thread
-// scans a contiguous chunk). *total receives the sum when not NULL.
+// Exclusive prefix sum, in place, of the n ints of segment blockIdx.x
+// (v + blockIdx.x * n), one workgroup each; each thread scans a contiguous
+// chunk. total[blockIdx.x] receives the sum when total is not NULL.
 __global__ __launch_bounds__(GS_THREADS) void gscan_kernel(int* v, int n, int* total) {
   __shared__ int wave_tot[GS_NW];
   const int tid = threadIdx.x;
+  v += (int64_t)blockIdx.x * n;
   const int per = (n + GS_THREADS - 1) / GS_THREADS;
   const int i0 = min(tid * per, n), i1 = min(i0 + per, n);
   int loc = 0;
@@ -478,7 +506,7 @@ __global__ __launch_bounds__(GS_THREADS) void gscan_kernel(int* v, int n, int* t
     v[i] = run;
     run += x;
   }
-  if (total && tid == 0) *total = tot;
+  if (total && tid == 0) total[blockIdx.x] = tot;
 }
 
 __global__ __launch_bounds__(GS_THREADS) void gsort_scatter_kernel(EmbedSumArgs a,
@@ -488,15 +516,14 @@ __global__ __launch_bounds__(GS_THREADS) void gsort_scatter_kernel(EmbedSumArgs 
   __shared__ int cnt[GS_NW * 256];
   __shared__ int wave_tot[GS_NW];
   __shared__ int lstart[256];
-  const int b = blockIdx.x, tid = threadIdx.x;
-  const int64_t p0 = (int64_t)b * GS_KB;
-  const int n = (int)min((int64_t)GS_KB, (int64_t)a.K - p0);
-  for (int p = tid; p < n; p += GS_THREADS) kin[p] = src ? src[p0 + p] : make_key(a, p0 + p);
+  const GsBlock g = gs_block(a);
+  const int tid = threadIdx.x;
+  for (int i = tid; i < g.n; i += GS_THREADS) kin[i] = src ? src[g.p0 + i] : make_key(a, g, i);
   if (tid < 256) lstart[tid] = 0;
   __syncthreads();
-  lds_radix_pass<GS_NW>(kin, kout, n, sh, cnt, wave_tot);
+  lds_radix_pass<GS_NW>(kin, kout, g.n, sh, cnt, wave_tot);
   // first local index of each digit: the count of smaller digits
-  for (int p = tid; p < n; p += GS_THREADS) atomicAdd(&lstart[(kout[p] >> sh) & 255], 1);
+  for (int i = tid; i < g.n; i += GS_THREADS) atomicAdd(&lstart[(kout[i] >> sh) & 255], 1);
   __syncthreads();
   {
     int c = tid < 256 ? lstart[tid] : 0, tot;
@@ -505,50 +532,78 @@ __global__ __launch_bounds__(GS_THREADS) void gsort_scatter_kernel(EmbedSumArgs 
     if (tid < 256) lstart[tid] = incl - c;
   }
   __syncthreads();
-  for (int j = tid; j < n; j += GS_THREADS) {
+  const int* off = a.hist + (int64_t)g.seg * 256 * a.gs_nbs + g.lb;
+  for (int j = tid; j < g.n; j += GS_THREADS) {
     const uint32_t key = kout[j];
     const int d = (int)((key >> sh) & 255);
-    dst[a.hist[(int64_t)d * a.gs_blocks + b] + (j - lstart[d])] = key;
+    dst[g.s0 + off[(int64_t)d * a.gs_nbs] + (j - lstart[d])] = key;
   }
 }
 
-// Runs of equal ids in the globally sorted keys: heads per block, then (after
-// an exclusive scan of the block counts, which also gives the run count)
-// every sorted position's run index and every run's first position.
-__device__ __forceinline__ bool run_head(const EmbedSumArgs& a, int64_t p) {
-  return p == 0 || (a.keys[p] >> a.pbits) != (a.keys[p - 1] >> a.pbits);
+// Runs of equal ids in the sorted keys of each segment: heads per block,
+// then (after an exclusive scan of each segment's block counts, which also
+// gives its run count n_runs[segment]) every sorted position's run index
+// within its segment and every run's first position (seg: gs_seg + 1
+// entries per segment, the last one gs_seg).
+__device__ __forceinline__ bool run_head(const EmbedSumArgs& a, const GsBlock& g, int64_t p) {
+  return p == g.s0 || (a.keys[p] >> a.pbits) != (a.keys[p - 1] >> a.pbits);
 }
 
 __global__ __launch_bounds__(GS_THREADS) void gruns_count_kernel(EmbedSumArgs a) {
   __shared__ int wave_tot[GS_NW];
-  const int b = blockIdx.x, tid = threadIdx.x;
-  const int64_t p0 = (int64_t)b * GS_KB;
-  const int n = (int)min((int64_t)GS_KB, (int64_t)a.K - p0);
+  const GsBlock g = gs_block(a);
+  const int tid = threadIdx.x;
   int c = 0;
-  for (int p = tid; p < n; p += GS_THREADS) c += run_head(a, p0 + p) ? 1 : 0;
+  for (int i = tid; i < g.n; i += GS_THREADS) c += run_head(a, g, g.p0 + i) ? 1 : 0;
   int tot;
   block_inclusive_scan(c, wave_tot, tid, GS_THREADS, &tot);
-  if (tid == 0) a.gs_runs[b] = tot;
+  if (tid == 0) a.gs_runs[blockIdx.x] = tot;
 }
 
 __global__ __launch_bounds__(GS_THREADS) void gruns_write_kernel(EmbedSumArgs a) {
   __shared__ int wave_tot[GS_NW];
-  const int b = blockIdx.x, tid = threadIdx.x;
-  const int64_t p0 = (int64_t)b * GS_KB;
-  const int n = (int)min((int64_t)GS_KB, (int64_t)a.K - p0);
-  const int per = (n + GS_THREADS - 1) / GS_THREADS;
-  const int i0 = min(tid * per, n), i1 = min(i0 + per, n);
+  const GsBlock g = gs_block(a);
+  const int tid = threadIdx.x;
+  const int per = (g.n + GS_THREADS - 1) / GS_THREADS;
+  const int i0 = min(tid * per, g.n), i1 = min(i0 + per, g.n);
   int c = 0;
-  for (int i = i0; i < i1; ++i) c += run_head(a, p0 + i) ? 1 : 0;
+  for (int i = i0; i < i1; ++i) c += run_head(a, g, g.p0 + i) ? 1 : 0;
   int tot;
   const int incl = block_inclusive_scan(c, wave_tot, tid, GS_THREADS, &tot);
-  int r = a.gs_runs[b] + incl - c;  // runs that start before this thread's first position
+  int32_t* seg = a.seg + (int64_t)g.seg * (a.gs_seg + 1);
+  int r = a.gs_runs[blockIdx.x] + incl - c;  // runs that start before this thread's first key
   for (int i = i0; i < i1; ++i) {
-    const int64_t p = p0 + i;
-    if (run_head(a, p)) a.seg[r++] = (int32_t)p;
+    const int64_t p = g.p0 + i;
+    if (run_head(a, g, p)) seg[r++] = (int32_t)(p - g.s0);
     a.rank[p] = r - 1;
   }
-  if (b == a.gs_blocks - 1 && tid == 0) a.seg[*a.n_runs] = a.K;
+  if (g.lb == a.gs_nbs - 1 && tid == 0) seg[a.n_runs[g.seg]] = a.gs_seg;
+}
+
+// Sorted keys into a.keys (and, when `runs`, ranks, run starts and run
+// counts) with the workspace radix sort over a.gs_blocks blocks.
+static hipError_t launch_gsort(const EmbedSumArgs& a, bool runs, hipStream_t s) {
+  int idbits = 0;
+  while ((1u << idbits) <= (uint32_t)a.V) ++idbits;
+  const int passes = (idbits + 7) / 8;
+  const dim3 g(a.gs_blocks), blk(GS_THREADS);
+  const int n_seg = a.gs_blocks / a.gs_nbs;
+  for (int q = 0; q < passes; ++q) {
+    // the last pass writes a.keys
+    uint32_t* dst = ((passes - 1 - q) & 1) ? a.keys2 : a.keys;
+    const uint32_t* src = q == 0 ? nullptr : (((passes - q) & 1) ? a.keys2 : a.keys);
+    const int sh = a.pbits + 8 * q;
+    hipLaunchKernelGGL(gsort_hist_kernel, g, blk, 0, s, a, src, sh);
+    hipLaunchKernelGGL(gscan_kernel, dim3(n_seg), blk, 0, s, a.hist, 256 * a.gs_nbs,
+                       (int*)nullptr);
+    hipLaunchKernelGGL(gsort_scatter_kernel, g, blk, 0, s, a, src, dst, sh);
+  }
+  if (runs) {
+    hipLaunchKernelGGL(gruns_count_kernel, g, blk, 0, s, a);
+    hipLaunchKernelGGL(gscan_kernel, dim3(n_seg), blk, 0, s, a.gs_runs, a.gs_nbs, a.n_runs);
+    hipLaunchKernelGGL(gruns_write_kernel, g, blk, 0, s, a);
+  }
+  return hipGetLastError();
 }
 
 __device__ __forceinline__ void out_add(const EmbedSumArgs& a, uint32_t v, int f, float val) {
@@ -692,6 +747,22 @@ __global__ void fill_zero_kernel(float* p, int64_t n) {
 hipError_t launch_embed_norm(const EmbedNormArgs& a, int dt, hipStream_t s) {
   if (a.B == 0) return hipSuccess;
   const dim3 g(a.B, a.n_chunks), blk(EN_THREADS);
+  if (a.runs && a.T > EN_MAX_T) {
+    // each example sorted and ranked through the workspace, then the walk
+    EmbedSumArgs sa{};
+    sa.ids = a.ids; sa.B = a.B; sa.T = a.T; sa.V = a.V; sa.pbits = a.pbits;
+    sa.K = a.B * a.T;
+    sa.keys = a.gkeys; sa.keys2 = a.gkeys2; sa.hist = a.ghist; sa.gs_runs = a.gruns;
+    sa.rank = a.grank; sa.seg = a.gseg; sa.n_runs = a.gnseg;
+    sa.gs_seg = a.T;
+    sa.gs_nbs = (a.T + GS_KB - 1) / GS_KB;
+    sa.gs_blocks = a.B * sa.gs_nbs;
+    const hipError_t e = launch_gsort(sa, true, s);
+    if (e != hipSuccess) return e;
+    if (dt == DT_BF16) hipLaunchKernelGGL((embed_norm_runs_kernel<DT_BF16, 0>), g, blk, 0, s, a);
+    else hipLaunchKernelGGL((embed_norm_runs_kernel<DT_F32, 0>), g, blk, 0, s, a);
+    return hipGetLastError();
+  }
   if (a.runs) {
     if (dt == DT_BF16) {
       if (a.T <= EN_CT_T) hipLaunchKernelGGL((embed_norm_runs_kernel<DT_BF16, EN_CT_T>), g, blk, 0, s, a);
@@ -717,26 +788,7 @@ static hipError_t launch_embed_keys(const EmbedSumArgs& a, bool compact, hipStre
     hipLaunchKernelGGL(embed_sort_kernel, dim3(1), dim3(ES_THREADS), 0, s, a);
     return hipGetLastError();
   }
-  int idbits = 0;
-  while ((1u << idbits) <= (uint32_t)a.V) ++idbits;
-  const int passes = (idbits + 7) / 8;
-  const dim3 g(a.gs_blocks), blk(GS_THREADS);
-  for (int q = 0; q < passes; ++q) {
-    // the last pass writes a.keys
-    uint32_t* dst = ((passes - 1 - q) & 1) ? a.keys2 : a.keys;
-    const uint32_t* src = q == 0 ? nullptr : (((passes - q) & 1) ? a.keys2 : a.keys);
-    const int sh = a.pbits + 8 * q;
-    hipLaunchKernelGGL(gsort_hist_kernel, g, blk, 0, s, a, src, sh);
-    hipLaunchKernelGGL(gscan_kernel, dim3(1), blk, 0, s, a.hist, 256 * a.gs_blocks,
-                       (int*)nullptr);
-    hipLaunchKernelGGL(gsort_scatter_kernel, g, blk, 0, s, a, src, dst, sh);
-  }
-  if (compact) {
-    hipLaunchKernelGGL(gruns_count_kernel, g, blk, 0, s, a);
-    hipLaunchKernelGGL(gscan_kernel, dim3(1), blk, 0, s, a.gs_runs, a.gs_blocks, a.n_runs);
-    hipLaunchKernelGGL(gruns_write_kernel, g, blk, 0, s, a);
-  }
-  return hipGetLastError();
+  return launch_gsort(a, compact, s);
 }
 
 hipError_t launch_embed_sum(const EmbedSumArgs& a, int dt, hipStream_t s) {

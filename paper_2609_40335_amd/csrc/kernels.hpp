@@ -195,6 +195,12 @@ struct EmbedNormArgs {
   int32_t* seg_id;      // nullable [B,T]
   int32_t* n_unique;    // nullable [B]
   float* ws;            // [B, n_chunks]
+  // T > EN_MAX_T (runs only): each example sorted and ranked by the
+  // workspace radix sort (keys [B*T] and their second buffer, digit counts
+  // [B, 256, blocks per example], block run counts [B * blocks], run index of
+  // every sorted position [B*T], run starts [B, T+1], run counts [B]).
+  uint32_t *gkeys, *gkeys2;
+  int32_t *ghist, *gruns, *grank, *gseg, *gnseg;
 };
 hipError_t launch_embed_norm(const EmbedNormArgs& a, int dt, hipStream_t s);
 
@@ -227,10 +233,11 @@ struct EmbedSumArgs {
   int32_t* seg;         // workspace [K + 1] first sorted position of every run
   int32_t* n_runs;      // workspace [1] number of runs
   float* rows;          // workspace [K, d] run sums
-  // More than ES_MAX_K keys: the workspace radix sort over gs_blocks blocks
-  // of GS_KB keys (keys2: the other key buffer, hist: [256, gs_blocks]
+  // More than ES_MAX_K keys: the workspace radix sort in segments of gs_seg
+  // keys (here one: the batch), gs_nbs blocks of GS_KB keys each, gs_blocks
+  // in all (keys2: the other key buffer; hist: [segments, 256, gs_nbs]
   // digit counts, then offsets; gs_runs: [gs_blocks] run counts, then bases).
-  int32_t gs_blocks;
+  int32_t gs_blocks, gs_nbs, gs_seg;
   uint32_t* keys2;
   int32_t* hist;
   int32_t* gs_runs;

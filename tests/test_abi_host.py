@@ -167,7 +167,9 @@ def test_embedding_rejects_bad_arguments(L):
     assert call(lde=32) == EINVAL
     assert call(V=0) == EINVAL
     assert call(wsb=0) == EINVAL
-    assert call(T=5000) == EUNSUP
+    # past T = 4096 only rows of whole 8-byte units (here fp32 rows of 65)
+    assert call(T=5000, lde=65, d=65) == EUNSUP
+    assert b"8-byte" in L.dp_last_error()
     assert call(V=1 << 30, T=64) == EUNSUP     # 30 + 6 bits > 32
     assert L.dp_ghost_norm_embedding_workspace(4, 16, 64) == 256
     assert L.dp_ghost_norm_embedding_workspace(64, 256, 768) == 64 * 12 * 4

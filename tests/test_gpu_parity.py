@@ -144,15 +144,19 @@ def test_head_norm(dp, dtype, V, ldz):
                                       ("zipf", 1, 50257), ("zipf", 1024, 50257),
                                       ("zipf", 256, 50257), ("zipf", 257, 50257),
                                       ("same", 300, 1000),
-                                      ("zipf", 4096, 50257)])  # the most tokens bucketed in LDS
+                                      ("zipf", 4096, 50257),   # the most tokens bucketed in LDS
+                                      ("zipf", 4097, 50257),   # past it: the workspace sort
+                                      ("zipf", 12000, 50257),  # three sort blocks per example
+                                      ("same", 9000, 1000)])   # one run across sort blocks
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("d,lde", [(200, 200), (201, 201), (200, 204)],
                          ids=["d200", "d201-scalar-rows", "d200-lde204"])
 def test_embedding_norm_and_buckets(dp, kind, T, V, dtype, d, lde):
     """d = 200: rows read 8 bytes per lane, each example's runs split over
-    workgroups (counting rank up to T = 256, radix sort above); d = 201 (rows
-    not a multiple of 8 bytes in bf16): the per-feature kernel; lde = 204:
-    padded rows (NaN in the padding, never read)."""
+    workgroups (counting rank up to T = 256, the LDS radix sort to 4096, the
+    workspace radix sort beyond); d = 201 (rows not a multiple of 8 bytes in
+    bf16): the per-feature kernel, which sorts in LDS and is refused past
+    T = 4096; lde = 204: padded rows (NaN in the padding, never read)."""
     B = 3
     _say(f"embedding {kind} T={T} V={V} {dtype} d={d} lde={lde}")
     ids = gen.draw_ids(4, 1, (B, T), V, kind)
@@ -167,6 +171,10 @@ def test_embedding_norm_and_buckets(dp, kind, T, V, dtype, d, lde):
         pad = torch.full((B, T, lde), float("nan"), device="cuda", dtype=dEd.dtype)
         pad[:, :, :d] = dEd
         dEd = pad[:, :, :d]
+    if T > 4096 and (d * (2 if dtype == "bf16" else 4)) % 8:
+        with pytest.raises(dp.DPError, match="8-byte"):
+            dp.dp_ghost_norm_embedding(dev(ids), dEd, V, n2, seg_id=seg, n_unique=nu)
+        return
     dp.dp_ghost_norm_embedding(dev(ids), dEd, V, n2, seg_id=seg, n_unique=nu)
     np.testing.assert_array_equal(host(seg), seg_ref)
     np.testing.assert_array_equal(host(nu), nu_ref)
