@@ -251,8 +251,18 @@ dp_status_t check_layers(const dp_linear_t* layers, int n, int B, int T, dp_dtyp
       return fail(DP_EINVAL, "layer %d: row stride smaller than row width", i);
     if (L.algo < DP_NORM_AUTO || L.algo > DP_NORM_DIRECT)
       return fail(DP_EINVAL, "layer %d: unknown algo %d", i, L.algo);
-    if (!span_ok((int64_t)B * T, L.lda, dt) || !span_ok((int64_t)B * T, L.ldg, dt))
-      return fail(DP_EUNSUPPORTED, "layer %d: an operand spans 4 GiB or more", i);
+    // Offsets within one example are 32-bit everywhere. Offsets across the
+    // batch are 32-bit too except in the direct-load GEMM (bf16, 16-byte rows,
+    // whole 32-row stages), which moves its descriptors' base per stage: only
+    // layers that take it may span 4 GiB or more.
+    if (!span_ok(T, L.lda, dt) || !span_ok(T, L.ldg, dt))
+      return fail(DP_EUNSUPPORTED, "layer %d: one example's rows span 4 GiB or more", i);
+    const bool dl = dpg::dl_sum_applies(kdt(dt), vec_ok(L.A, L.lda, dt) && vec_ok(L.G, L.ldg, dt),
+                                        T, B);
+    if (!dl && (!span_ok((int64_t)B * T, L.lda, dt) || !span_ok((int64_t)B * T, L.ldg, dt)))
+      return fail(DP_EUNSUPPORTED,
+                  "layer %d: an operand spans 4 GiB or more (allowed only for bf16 16-byte rows "
+                  "with T a multiple of 32 and B <= 4096)", i);
     if (ceil_div(L.d_in, dpg::GM_BM) > 65535 || ceil_div(L.d_out, dpg::GM_BN) > 65535)
       return fail(DP_EUNSUPPORTED, "layer %d: a width exceeds 65535 tiles of 256", i);
   }
@@ -353,6 +363,7 @@ dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int
       L.X = e.X; L.Y = e.Y; L.ldx = e.ldx; L.ldy = e.ldy;
       L.M = e.M; L.N = e.N;
       L.tm = (uint16_t)e.tm; L.tn = (uint16_t)e.tn;
+      if (!span_ok((int64_t)B * T, e.ldx, dt) || !span_ok((int64_t)B * T, e.ldy, dt)) a.big = 1;
       L.tile_begin = (uint32_t)items;
       if (mode == 0) L.tensor_id = e.tensor_id;
       else L.slot_begin = e.slot_begin;
@@ -594,6 +605,10 @@ dp_status_t norm_bias_grouped(const dp_linear_t* layers, float* const* bias_grad
   if (!norm2) return fail(DP_EINVAL, "norm2 is NULL");
   const NormPlan p = plan_norm(layers, n_layers, B, T, dt, bias_grads);
   if ((uint64_t)B * p.slots > 0x7FFFFFFFull) return fail(DP_EUNSUPPORTED, "too many partials");
+  for (const BiasEntry& e : p.bias_vec)  // the vector kernel's offsets span the batch in 32 bits
+    if (!span_ok((int64_t)B * T, e.ldg, dt))
+      return fail(DP_EUNSUPPORTED, "a bias whose G spans 4 GiB or more must be fused into the "
+                  "Gram launch (bf16, 16-byte rows, T <= 256)");
   VecPlan vp;
   for (const BiasEntry& e : p.bias_vec)
     plan_vec(vp, nullptr, 0, e.G, e.ldg, e.d, dpg::VEC_GRAD, e.grad, dt, T);

@@ -687,7 +687,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 // MODE_SUM: the clipped sum over all K = B*T rows. MODE_NORM (the direct
 // norm): K restricted to example b's T rows, no factors, and the tile's
 // in-range elements squared and summed in registers.
-template <int MODE>
+// BIG: some operand of the launch spans 4 GiB or more (see issue()).
+template <int MODE, bool BIG>
 __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
   const GemmArgs& a = *(const GemmArgs*)__builtin_amdgcn_kernarg_segment_ptr();
   (void)args;
@@ -757,10 +758,27 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
   const uint32_t ring_base = (uint32_t)(uintptr_t)ring;
   const int nS = (int)((k_end - k_begin) / DL_BK);
   // Load t (of DL_LOADS) of this wave's share of stage s.
+  // An operand of 4 GiB or more does not fit the 32-bit offsets: its
+  // descriptor's base moves to each stage's first row instead (the records
+  // left from there, none past the last stage). A separate instance, so that
+  // launches without such an operand keep the plain loop.
+  const bool big = BIG && nrec64 > 0xFFFFFFFFull;
   auto issue = [&](int s, int t) {
     const uint32_t dst = ring_base + (uint32_t)((s % DL_NS) * DL_STB) + lds_role;
     const int64_t row0 = k_begin + (int64_t)s * DL_BK + wq * 8;
-    const uint32_t sbase = s < nS ? (uint32_t)(row0 * ld_bytes) : nrec;
+    uint32_t sbase;
+    u32x4 d = desc;
+    if (big) {
+      const uint64_t base = gbase + (uint64_t)row0 * ld_bytes;
+      const uint64_t rem = s < nS ? (uint64_t)(K - row0) * ld_bytes : 0ull;
+      const uint32_t nr = rem > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)rem;
+      d = u32x4{(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)base),
+                (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(base >> 32)),
+                (uint32_t)__builtin_amdgcn_readfirstlane((int)nr), (uint32_t)RSRC_WORD3};
+      sbase = 0;
+    } else {
+      sbase = s < nS ? (uint32_t)(row0 * ld_bytes) : nrec;
+    }
     {
       const uint32_t m0v = (uint32_t)__builtin_amdgcn_readfirstlane((int)(dst + t * 1024));
       const uint32_t so = (uint32_t)__builtin_amdgcn_readfirstlane((int)(sbase + 2 * t * ld_bytes));
@@ -770,7 +788,7 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
       // Gram's streams they keep the temporal hint, as neighbouring tiles
       // share operand panels through L2 (nt measured slower).
       asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 lds"
-                   :: "s"(m0v), "v"(lvo[t & 1]), "s"(desc), "s"(so));
+                   :: "s"(m0v), "v"(lvo[t & 1]), "s"(d), "s"(so));
     }
   };
 
@@ -1008,7 +1026,10 @@ static hipError_t launch_kt(const GemmArgs& a0, int dt, bool vec, int cus, size_
         grid = t.n_full + t.n_split * (uint32_t)t.ks;
       }
     }
-    hipLaunchKernelGGL(dl_gemm_kernel<MODE>, dim3(grid), dim3(GM_THREADS), 0, s, a);
+    if (a.big)
+      hipLaunchKernelGGL((dl_gemm_kernel<MODE, true>), dim3(grid), dim3(GM_THREADS), 0, s, a);
+    else
+      hipLaunchKernelGGL((dl_gemm_kernel<MODE, false>), dim3(grid), dim3(GM_THREADS), 0, s, a);
     if (a.n_split > 0) {
       hipLaunchKernelGGL(split_fixup_kernel, dim3(a.n_split * (GM_BM * GM_BN / 4 / 256)),
                          dim3(256), 0, s, a);

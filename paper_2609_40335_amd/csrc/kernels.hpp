@@ -138,6 +138,7 @@ struct GemmArgs {
   uint32_t n_full, n_split;
   int32_t ksplit;
   float* part;
+  int32_t big;          // some operand spans 4 GiB or more (direct-load kernel rebases per stage)
 };
 
 static_assert(sizeof(GemmArgs) <= 4096, "kernel arguments must stay within 4 KiB");

@@ -90,10 +90,17 @@ def test_norm_workspace_sizes(L):
         assert ws == ((B * nc * 4 + 255) // 256) * 256
     assert _head_chunks(50257, 64, 32, 0, 512) == 16          # 512 items: one full round
     assert _head_chunks(50257, 64, 32, 48 * 32, 512) == 16    # with 48 body layers: 2048 items
-    # an operand spanning 4 GiB or more is refused (32-bit buffer offsets)
-    assert L.dp_ghost_norm_linear_workspace(head, 1, 1000, 128, D.DP_BF16) == 0
-    assert L.dp_ghost_norm_linear_grouped(head, 1, 1000, 128, D.DP_BF16, 1 << 22, 0, 1 << 23,
+    # an operand spanning 4 GiB or more (G: 1000 * 128 rows of 50304 bf16) is
+    # taken only where the direct-load kernels rebase per example or per stage
+    # (bf16, 16-byte rows, T a multiple of 32), refused otherwise (32-bit
+    # buffer offsets across the batch)
+    assert L.dp_ghost_norm_linear_workspace(head, 1, 1000, 128, D.DP_BF16) > 0
+    assert L.dp_ghost_norm_linear_workspace(head, 1, 1000, 100, D.DP_BF16) == 0
+    assert L.dp_ghost_norm_linear_grouped(head, 1, 1000, 100, D.DP_BF16, 1 << 22, 0, 1 << 23,
                                           1 << 30, None) == EUNSUP
+    assert b"4 GiB" in L.dp_last_error()
+    odd = (D.dp_linear_t * 1)(_lin(d_in=768, lda=768, d_out=50257, ldg=50257))  # rows not 16 B
+    assert L.dp_ghost_norm_linear_workspace(odd, 1, 1000, 128, D.DP_BF16) == 0
     # AUTO picks the direct form once T + 1 > 0.57 * 2 d_in d_out / (d_in + d_out)
     # (0.57 * 64 here): one 256x256 output tile per example
     auto = (D.dp_linear_t * 1)(_lin())
