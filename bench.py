@@ -46,8 +46,8 @@ PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
 # HBM bytes per launch of the clipped-sum kernel: rocprofv3 FETCH_SIZE x 2 +
 # WRITE_SIZE x 1 (factors from a plain 1 GiB copy), recorded for the kernel
 # source with this SHA-256; any other source reports null.
-GEMM_TRAFFIC = {"gemm.hip sha256": "052ae33183eea6e1cb318d15784a30ec1e567337c7b8998f5f4ab13a94a110e3",
-                "bytes": 2697537801}
+GEMM_TRAFFIC = {"gemm.hip sha256": "dba178dafff7afc449751c1baac8011b9274f33e6cacda086f9494133c358a48",
+                "bytes": 2697872384}
 
 
 def log(*a):
