@@ -261,17 +261,20 @@ class Step:
             self.ev_start.record(main)
             self.side.wait_event(self.ev_start)
             with self.torch.cuda.stream(self.side):
-                self.n2b.zero_()
+                # the first term writes n2b, the others add to it
+                acc = False
                 if h is not None:
-                    dp.dp_ghost_norm_embedding(self.ids, self.dE, h.V, self.n2b, accumulate=True,
+                    dp.dp_ghost_norm_embedding(self.ids, self.dE, h.V, self.n2b, accumulate=acc,
                                                seg_id=self.seg, n_unique=self.nu)
+                    acc = True
                     if h.H is not None and h.tied:
                         dp.dp_tied_cross_term(self.ids, self.dE, self.H, self.Gz, h.V, self.n2b,
                                               scale=2.0, accumulate=True)
                 if self.vg is not None:
-                    self.vg.grads_and_norm(self.n2b, accumulate=True)
+                    self.vg.grads_and_norm(self.n2b, accumulate=acc)
+                    acc = True
                 if self.P is not None:
-                    dp.dp_ghost_norm_positional(self.dE, self.n2b, accumulate=True)
+                    dp.dp_ghost_norm_positional(self.dE, self.n2b, accumulate=acc)
             self.ev_norms.record(self.side)
         self.norm_group.ghost_norm(self.n2, accumulate=False)
         mark("norms")

@@ -937,7 +937,7 @@ __global__ __launch_bounds__(GR_THREADS, 2) void dl_cross_kernel(CrossArgs a) {
 // of H): the 32 x 32 block P[s, t] = <h_s, dE_t> on MFMA, each of the 8 waves
 // over an eighth of the features with its operands loaded straight into
 // registers (no LDS staging: a lane's 8 consecutive features are one 16-byte
-// load), the parts added in LDS in wave order, then sum P[s, t] Gz[s, x_t].
+// load), the parts added in LDS in a fixed order, then sum P[s, t] Gz[s, x_t].
 // In the MFMA output a lane holds one token t and 16 rows s, so one gather
 // instruction reads two rows of Gz at 32 columns x_t; with the tokens in
 // sorted-id order those columns are ascending (equal ids share an address),
@@ -954,7 +954,7 @@ __global__ __launch_bounds__(CX_THREADS) void cross_rows_kernel(CrossArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t keys[CX_SORT_T];
   __shared__ int32_t tpos[CR_RX_ROWS];
   __shared__ uint32_t tids[CR_RX_ROWS];
-  __shared__ float part[CX_NW][16][WAVE];
+  __shared__ float part[CX_NW / 2][16][WAVE];  // 16 KB: leaves room beside a Gram launch
   __shared__ float red[CX_NW];
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
   const int nb = a.n_t;
@@ -1064,16 +1064,31 @@ __global__ __launch_bounds__(CX_THREADS) void cross_rows_kernel(CrossArgs a) {
 #pragma unroll
     for (int j = 0; j < CX_KB; ++j) acc = mfma32_bf16(fh[j], fe[j], acc);
   }
+  // The waves' parts of each accumulator meet in a fixed order in half as
+  // much LDS: wave w + CX_NW/2 hands its part to wave w, which adds it; then
+  // every wave sums the CX_NW/2 pair sums of its EPW accumulators in order.
+  constexpr int NH = CX_NW / 2;
+  if (w >= NH) {
 #pragma unroll
-  for (int e = 0; e < 16; ++e) part[w][e][lane] = acc[e];
+    for (int e = 0; e < 16; ++e) part[w - NH][e][lane] = acc[e];
+  }
   __syncthreads();
-  // the waves' parts of each accumulator added in wave order
+  if (w < NH) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] += part[w][e][lane];
+  }
+  __syncthreads();
+  if (w < NH) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) part[w][e][lane] = acc[e];
+  }
+  __syncthreads();
   float sum = 0.f;
 #pragma unroll
   for (int i = 0; i < EPW; ++i) {
     float pv = part[0][EPW * w + i][lane];
 #pragma unroll
-    for (int q = 1; q < CX_NW; ++q) pv += part[q][EPW * w + i][lane];
+    for (int q = 1; q < NH; ++q) pv += part[q][EPW * w + i][lane];
     sum += pv * bf16_to_f32((uint16_t)zr[i]);
   }
   sum = wave_sum(sum);
