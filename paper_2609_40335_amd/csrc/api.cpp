@@ -807,11 +807,6 @@ dp_status_t dp_tied_cross_term(const int32_t* ids, const void* dE, int64_t lde, 
   a.n_t = (int)cross_blocks(T, a.kind);
   a.n_fc = a.kind == dpg::CROSS_STAGED ? (int)ceil_div(d, dpg::CR_FCHUNK) : 1;
   a.slots = (int32_t)cross_slots(T, d, a.kind);
-  a.pbits = std::max(1, bits_for(T));
-  // Sorting only orders the gathers; where a key would not fit 32 bits the
-  // tokens stay in position order.
-  a.sort = (a.kind == dpg::CROSS_ROWS && T <= dpg::CX_SORT_T &&
-            bits_for((int64_t)V + 1) + a.pbits <= 32) ? 1 : 0;
   a.ws = static_cast<float*>(workspace);
   hipStream_t s = as_stream(stream);
   dp_status_t st = hip_status(dpg::launch_tied_cross(a, kdt(dt), vec, s), "tied_cross launch");

@@ -933,27 +933,22 @@ __global__ __launch_bounds__(GR_THREADS, 2) void dl_cross_kernel(CrossArgs a) {
 }
 
 // Register-direct cross term (bf16, 16-byte aligned rows). Work item =
-// (example b, block tb of 32 tokens in sorted-id order, block sb of 32 rows
-// of H): the 32 x 32 block P[s, t] = <h_s, dE_t> on MFMA, each of the 8 waves
-// over an eighth of the features with its operands loaded straight into
-// registers (no LDS staging: a lane's 8 consecutive features are one 16-byte
-// load), the parts added in LDS in a fixed order, then sum P[s, t] Gz[s, x_t].
-// In the MFMA output a lane holds one token t and 16 rows s, so one gather
-// instruction reads two rows of Gz at 32 columns x_t; with the tokens in
-// sorted-id order those columns are ascending (equal ids share an address),
-// which cuts the sectors the gathers touch. Up to CX_SORT_T tokens each
-// workgroup ranks its example's (id, position) keys by counting; longer
-// examples keep position order (same result, more sectors).
+// (example b, block tb of 32 tokens, block sb of 32 rows of H): the 32 x 32
+// block P[s, t] = <h_s, dE_t> on MFMA, each of the 8 waves over an eighth of
+// the features with its operands loaded straight into registers (no LDS
+// staging: a lane's 8 consecutive features are one 16-byte load), the parts
+// added in LDS in a fixed order, then sum P[s, t] Gz[s, x_t]. In the MFMA
+// output a lane holds one token t and 16 rows s, so one gather instruction
+// reads two rows of Gz at 32 columns x_t (equal ids share an address). Every
+// load is issued at the start: the H and dE rows and the ids depend on
+// nothing, the gathers only on the ids. (Ranking the tokens by id first, for
+// gathers at ascending columns, fetched no fewer bytes and took ~1 us more.)
 constexpr int CX_THREADS = 512;
 constexpr int CX_NW = CX_THREADS / WAVE;
 constexpr int CX_KB = 6;  // 16-feature MFMA steps whose loads a wave issues together
-static_assert(CX_SORT_T <= CX_THREADS, "counting rank: one key per thread");
 static_assert(16 % CX_NW == 0, "accumulators finished per wave");
 
 __global__ __launch_bounds__(CX_THREADS) void cross_rows_kernel(CrossArgs a) {
-  __shared__ __attribute__((aligned(16))) uint32_t keys[CX_SORT_T];
-  __shared__ int32_t tpos[CR_RX_ROWS];
-  __shared__ uint32_t tids[CR_RX_ROWS];
   __shared__ float part[CX_NW / 2][16][WAVE];  // 16 KB: leaves room beside a Gram launch
   __shared__ float red[CX_NW];
   const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
@@ -965,21 +960,23 @@ __global__ __launch_bounds__(CX_THREADS) void cross_rows_kernel(CrossArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int T = a.T;
   const uint32_t V = (uint32_t)a.V;
-  const int32_t* ids = a.ids + (int64_t)b * T;
   const int t_lo = tb * CR_RX_ROWS;
   const int r = lane & 31, h = lane >> 5;
   const uint64_t ex_rows = (uint64_t)b * T;
   const uint32_t lde = (uint32_t)(a.lde * 2), ldh = (uint32_t)(a.ldh * 2);
   const rsrc_t rE = make_rsrc((const char*)a.E + ex_rows * lde, (uint64_t)T * lde);
   const rsrc_t rH = make_rsrc((const char*)a.H + ex_rows * ldh, (uint64_t)T * ldh);
+  const rsrc_t rI = make_rsrc(a.ids + ex_rows, (uint64_t)T * 4);
   const int nk = (a.d + 15) / 16;         // 16-feature MFMA steps
   const int kq = (nk + CX_NW - 1) / CX_NW;  // per wave
   const int k0 = min(w * kq, nk), k1 = min(k0 + kq, nk);
   // Rows past the example read zeros through offsets past the range. A lane
   // takes features 16k + 8h .. +7 of its row in both operands; the chunk
   // that straddles d is zeroed on both sides.
-  const int s_row = sb * CR_RX_ROWS + r;
+  const int s_row = sb * CR_RX_ROWS + r, t_row = t_lo + r;
+  const bool t_ok = t_row < T;
   const uint32_t hoff = s_row < T ? (uint32_t)s_row * ldh : (uint32_t)T * ldh;
+  const uint32_t eoff = t_ok ? (uint32_t)t_row * lde : (uint32_t)T * lde;
   auto load_op = [&](rsrc_t rs, uint32_t roff, uint32_t end, int k) {
     const int f = k * 16 + 8 * h;
     const bool live = k < k1 && f < a.d;
@@ -996,46 +993,23 @@ __global__ __launch_bounds__(CX_THREADS) void cross_rows_kernel(CrossArgs a) {
       v[q] &= e2 + 1 < nv ? 0xFFFFFFFFu : (e2 < nv ? 0xFFFFu : 0u);
     }
   };
-  // The id this thread ranks is requested first (loads complete in order);
-  // the H rows do not depend on the token order, so their first batch is
-  // requested before the ranking.
-  const rsrc_t rI = make_rsrc(ids, (uint64_t)T * 4);
-  const uint32_t my_id = buf_load4(rI, tid < T ? (uint32_t)tid * 4 : (uint32_t)T * 4);
+  // The id of this lane's token first (loads complete in order), then the
+  // first batch of H and dE rows.
+  const uint32_t id_raw = buf_load4(rI, t_ok ? (uint32_t)t_row * 4 : (uint32_t)T * 4);
   u32x4 fh[CX_KB], fe[CX_KB];
 #pragma unroll
-  for (int j = 0; j < CX_KB; ++j) fh[j] = load_op(rH, hoff, (uint32_t)T * ldh, k0 + j);
-  __builtin_amdgcn_sched_barrier(0);  // keep the wait for the id after these loads
-
-  if (a.sort) {
-    // (id, position) keys, distinct: a key's rank is the number of smaller
-    // ones. T <= CX_THREADS; past T the largest key, counted by no real key.
-    const int pb = a.pbits;
-    const uint32_t key =
-        tid < T ? ((my_id < V ? my_id : V) << pb) | (uint32_t)tid : 0xFFFFFFFFu;
-    if (tid < CX_SORT_T) keys[tid] = key;
-    __syncthreads();
-    const int rk = count_below(keys, (T + 7) & ~7, key);
-    if (tid < T && rk >= t_lo && rk < t_lo + CR_RX_ROWS) {
-      tpos[rk - t_lo] = tid;
-      tids[rk - t_lo] = key >> pb;
-    }
-  } else if (tid < CR_RX_ROWS && t_lo + tid < T) {
-    const uint32_t id = (uint32_t)ids[t_lo + tid];
-    tpos[tid] = t_lo + tid;
-    tids[tid] = id < V ? id : V;
+  for (int j = 0; j < CX_KB; ++j) {
+    fh[j] = load_op(rH, hoff, (uint32_t)T * ldh, k0 + j);
+    fe[j] = load_op(rE, eoff, (uint32_t)T * lde, k0 + j);
   }
-  __syncthreads();
-
-  const bool t_ok = t_lo + r < T;
-  const uint32_t eoff = t_ok ? (uint32_t)tpos[r] * lde : (uint32_t)T * lde;
-  // The logit gradients this wave multiplies in the end depend only on the
-  // order: requested now, beside the dE rows. Wave w finishes accumulators
-  // e = EPW*w .. +EPW-1 of the block: row s = sb*32 + 8(e/4) + 4h + e%4,
-  // token t_lo + r.
+  __builtin_amdgcn_sched_barrier(0);  // keep the wait for the id after these loads
+  // The logit gradients this wave multiplies in the end: wave w finishes
+  // accumulators e = EPW*w .. +EPW-1 of the block, row s = sb*32 + 8(e/4) +
+  // 4h + e%4, token t_row.
   constexpr int EPW = 16 / CX_NW;
   const uint32_t ldz = (uint32_t)(a.ldz * 2);
   const rsrc_t rZ = make_rsrc((const char*)a.Gz + ex_rows * ldz, (uint64_t)T * ldz);
-  const uint32_t v = t_ok ? tids[r] : V;
+  const uint32_t v = t_ok ? id_raw : V;
   uint32_t zr[EPW];
 #pragma unroll
   for (int i = 0; i < EPW; ++i) {
@@ -1050,10 +1024,11 @@ __global__ __launch_bounds__(CX_THREADS) void cross_rows_kernel(CrossArgs a) {
   for (int kb = k0; kb < k1; kb += CX_KB) {
     if (kb != k0) {
 #pragma unroll
-      for (int j = 0; j < CX_KB; ++j) fh[j] = load_op(rH, hoff, (uint32_t)T * ldh, kb + j);
+      for (int j = 0; j < CX_KB; ++j) {
+        fh[j] = load_op(rH, hoff, (uint32_t)T * ldh, kb + j);
+        fe[j] = load_op(rE, eoff, (uint32_t)T * lde, kb + j);
+      }
     }
-#pragma unroll
-    for (int j = 0; j < CX_KB; ++j) fe[j] = load_op(rE, eoff, (uint32_t)T * lde, kb + j);
     if (straddle) {
 #pragma unroll
       for (int j = 0; j < CX_KB; ++j) {

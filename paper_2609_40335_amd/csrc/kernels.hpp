@@ -64,7 +64,6 @@ hipError_t launch_gram_norm(const GramArgs& a, int dt, bool vec, hipStream_t s);
 constexpr int CR_FCHUNK = 128;  // features per cross-term work item
 constexpr int CR_DL_ROWS = 64;  // row block of the direct-load cross kernel
 constexpr int CR_RX_ROWS = 32;  // token and row blocks of the register-direct cross kernel
-constexpr int CX_SORT_T = 256;  // longest example whose tokens that kernel sorts by id
 constexpr int CX_ROWS_T = 128;  // longest example given to it (measured: at T = 256 its
                                 // 32-row blocks re-read E and H more than dl_cross's 64-row ones)
 // Cross-term kernel of a call: the register-staged tied_cross_kernel (fp32 or
@@ -85,7 +84,6 @@ struct CrossArgs {
   int32_t B, T, V, d, n_t;  // n_t: row blocks per example (128, 64 or 32 rows by kernel)
   int32_t n_fc;         // feature chunks (1 for bf16 aligned: all features per item)
   int32_t kind;         // CROSS_STAGED, CROSS_DL or CROSS_ROWS
-  int32_t sort, pbits;  // CROSS_ROWS: tokens taken in (id, position) order; position bits of a key
   int32_t slots;        // n_t * n_t * n_fc
   float* ws;            // [B, slots]
 };
