@@ -356,6 +356,13 @@ dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int
     a.noise = nz.on ? 1 : 0;
     a.sigma_c = nz.sigma_c; a.inv_b = nz.inv_b; a.step = nz.step; a.seed = nz.seed;
     a.part = part;
+    a.eg = 1;
+    if (mode == 1 && kdt(dt) == dpg::DT_BF16 && vec && T % dpg::DL_SUM_BK == 0) {
+      uint64_t tiles = 0;
+      for (const GemmEntry* e : sel) tiles += (uint64_t)e->tm * e->tn;
+      a.eg = dpg::norm_group(tiles, B, T / dpg::DL_SUM_BK, device_cus());
+    }
+    const uint64_t groups = (uint64_t)((B + a.eg - 1) / a.eg);
     uint64_t items = 0;
     for (size_t j = 0; j < sel.size(); ++j) {
       const GemmEntry& e = *sel[j];
@@ -369,7 +376,7 @@ dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int
       else L.slot_begin = e.slot_begin;
       L.accumulate = e.acc;
       L.out = e.out; L.ldo = e.ldo;
-      items += (uint64_t)e.tm * e.tn * (mode == 1 ? (uint64_t)B : 1ull);
+      items += (uint64_t)e.tm * e.tn * (mode == 1 ? groups : 1ull);
     }
     if (items > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many work items");
     a.n_layers = (int32_t)sel.size();

@@ -649,6 +649,7 @@ constexpr int DL_MAXB = DL_SUM_MAXB;        // clip factors held in LDS
 constexpr int DL_LOADS = 4;                 // loads per wave per stage
 static_assert(GM_BM == GM_BN, "square tiles");
 static_assert(DL_STB == (GM_THREADS / WAVE) * DL_LOADS * 1024, "one KB per load");
+static_assert(NG_MAX * (GM_THREADS / WAVE) <= DL_MAXB, "direct norm: a part per example and wave fits the factor table");
 static_assert((GM_THREADS / WAVE) * 32 * EP_LD * 4 <= DL_NS * DL_STB, "epilogue slices fit the ring");
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -719,12 +720,15 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
     k_begin = kc * per;
     k_end = k_begin + per < K ? k_begin + per : K;
   }
+  int n_ex = 1;  // direct norm: examples b .. b + n_ex - 1 of this item
   if constexpr (MODE == MODE_NORM) {
     const uint32_t ntile = (uint32_t)L.tm * (uint32_t)L.tn;
-    b = (int)(rel / ntile);
-    rel -= (uint32_t)b * ntile;
+    const int grp = (int)(rel / ntile);
+    rel -= (uint32_t)grp * ntile;
+    b = grp * a.eg;
+    n_ex = a.B - b < a.eg ? a.B - b : a.eg;
     k_begin = (int64_t)b * a.T;
-    k_end = k_begin + a.T;
+    k_end = k_begin + (int64_t)n_ex * a.T;
   }
   int mt, nt;
   tile_of(L, rel, mt, nt);
@@ -834,10 +838,61 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
   float c_nx = 0.f;             // factor of the example that starts at stage s_nx
   bool skip = false;
   int s_nx = 0, e_nx = e0;      // next example boundary (a local stage) and its example
+  // Direct norm: the squared Frobenius norm of this wave's part of the tile
+  // for local example le goes to red[le * 8 + w] (the factor table is unused
+  // in this mode); the workgroup adds the 8 waves' parts at the end. The
+  // columns past M or N were loaded from beyond the rows' valid width and
+  // only reach out-of-range elements, which the sum leaves out.
+  float* red = cs;
+  const bool full = m0 + GM_BM <= L.M && n0 + GM_BN <= L.N;
+  int le = 0;
+  if constexpr (MODE == MODE_NORM) s_nx = spe;
+  auto fin = [&]() __attribute__((always_inline)) {
+    float part = 0.f;
+    if (full) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) part = fmaf(acc[i][j][e], acc[i][j][e], part);
+    } else {
+      // Rows and columns left in the tile past this lane's first element.
+      // Opaque here, so that the compiler does not keep the masks of every
+      // accumulator live across the main loop.
+      int lim_m = (int)(L.M - m0) - (wm * 128 + (lane >> 5) * 4);
+      int lim_n = (int)(L.N - n0) - (wn * 64 + (lane & 31));
+      asm volatile("" : "+v"(lim_m), "+v"(lim_n));
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const bool nin = j * 32 < lim_n;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const float v = acc[i][j][e];
+            part += (nin && i * 32 + (e >> 2) * 8 + (e & 3) < lim_m) ? v * v : 0.f;
+          }
+        }
+    }
+    part = wave_sum(part);
+    if (lane == 0) red[le * (GM_THREADS / WAVE) + w] = part;
+    ++le;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+  };
   // Called once per stage, in increasing order, in the memory phase before
-  // that stage's MFMAs: at an example boundary, rescales the accumulators by
-  // c_prev / c_next and fetches the factor of the example after.
+  // that stage's MFMAs. Clipped sum: at an example boundary, rescales the
+  // accumulators by c_prev / c_next and fetches the factor of the example
+  // after. Direct norm: at an example boundary, reduces the finished
+  // example's part of the tile and clears the accumulators.
   auto enter = [&](int s) {
+    if (MODE == MODE_NORM && s == s_nx) {
+      fin();
+      s_nx += spe;
+    }
     if (MODE == MODE_SUM && s == s_nx) {
       const float ce = c_nx;
       ++e_nx;
@@ -961,32 +1016,13 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
       store_tile_rows(a, L, m0, n0, wm, wn, lane, acc, slice);
     }
   } else {
-    // Columns past M or N were loaded from beyond the rows' valid width and
-    // only reach out-of-range elements, which the sum leaves out.
-    const int mw = (int)m0 + wm * 128 + (lane >> 5) * 4;
-    const int nw = (int)n0 + wn * 64 + (lane & 31);
-    float part = 0.f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const bool nin = nw + j * 32 < L.N;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int m = mw + i * 32 + (e >> 2) * 8 + (e & 3);
-          const float v = acc[i][j][e];
-          part += (nin && m < L.M) ? v * v : 0.f;
-        }
-      }
-    part = wave_sum(part);
-    float* red = cs;  // the factor table is unused in this mode
-    if (lane == 0) red[w] = part;
+    fin();  // the last example
     __syncthreads();
-    if (tid == 0) {
+    if (tid < n_ex) {
       float t = 0.f;
 #pragma unroll
-      for (int q = 0; q < GM_THREADS / WAVE; ++q) t += red[q];
-      a.ws[(int64_t)b * a.slots + L.slot_begin + rel] = t;
+      for (int q = 0; q < GM_THREADS / WAVE; ++q) t += red[tid * (GM_THREADS / WAVE) + q];
+      a.ws[(int64_t)(b + tid) * a.slots + L.slot_begin + rel] = t;
     }
   }
 }
@@ -1015,6 +1051,9 @@ static hipError_t launch_kt(const GemmArgs& a0, int dt, bool vec, int cus, size_
   // The accumulator form needs every K-stage inside one example.
   const int ks = dt == DT_BF16 ? KT<DT_BF16>::KS : KT<DT_F32>::KS;
   const int sc = MODE == MODE_NORM ? SC_NONE : (a.T % ks == 0 ? SC_ACC : SC_STAGE);
+  if (MODE == MODE_NORM &&
+      (a.eg < 1 || a.eg > NG_MAX || (a.eg > 1 && !(dt == DT_BF16 && vec && a.T % DL_BK == 0))))
+    return hipErrorInvalidValue;  // example groups exist only on the direct-load kernel
   if (dt == DT_BF16 && vec && a.T % DL_BK == 0 && (MODE == MODE_NORM || a.B <= DL_MAXB)) {
     uint32_t grid = a.n_items;
     if (MODE == MODE_SUM && a.part != nullptr) {

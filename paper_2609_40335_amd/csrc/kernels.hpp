@@ -137,6 +137,9 @@ struct GemmArgs {
   int32_t ksplit;
   float* part;
   int32_t big;          // some operand spans 4 GiB or more (direct-load kernel rebases per stage)
+  // Direct norm, direct-load kernel: examples per work item (a tile over eg
+  // consecutive examples; items of one layer are group-major). 1 elsewhere.
+  int32_t eg;
 };
 
 static_assert(sizeof(GemmArgs) <= 4096, "kernel arguments must stay within 4 KiB");
@@ -173,6 +176,29 @@ inline TailSplit tail_split(uint64_t n_tiles, int k_stages, int cus) {
   return t;
 }
 constexpr size_t SPLIT_TILE_BYTES = (size_t)GM_BM * GM_BN * 4;  // one fp32 partial tile
+
+// Direct norm on the direct-load kernel: the number of consecutive examples
+// one work item covers. An item streams its examples' K stages without a gap
+// and pays the ring's fill and drain once (about NG_OVERHEAD stages), so
+// longer items cost less per stage, while fewer, longer items leave more of
+// the chip idle in the last round. The choice minimises
+// rounds(items) * (eg * stages per example + NG_OVERHEAD) over 1 <= eg <= B
+// (eg <= NG_MAX: the item keeps a partial per example and wave in LDS).
+constexpr int NG_OVERHEAD = 6;
+constexpr int NG_MAX = 512;
+inline int norm_group(uint64_t n_tiles, int B, int spe, int cus) {
+  if (n_tiles == 0 || B <= 1 || cus <= 0) return 1;
+  int best = 1;
+  uint64_t best_cost = ~0ull;
+  const int top = B < NG_MAX ? B : NG_MAX;
+  for (int eg = 1; eg <= top; ++eg) {
+    const uint64_t items = n_tiles * (uint64_t)((B + eg - 1) / eg);
+    const uint64_t rounds = (items + (uint64_t)cus - 1) / (uint64_t)cus;
+    const uint64_t cost = rounds * (uint64_t)(eg * spe + NG_OVERHEAD);
+    if (cost < best_cost) { best_cost = cost; best = eg; }
+  }
+  return best;
+}
 
 // Clipped sum: out (+)= sum_i c_i X_i^T Y_i over all B*T rows (K = B*T).
 // With a.part set (and room for the split that tail_split gives on `cus` CUs),

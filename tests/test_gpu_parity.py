@@ -705,6 +705,52 @@ def test_full_size_long_sequence(dp, algo):
     assert rel(host(n_out)[0], ref_out) <= TOL["bf16"]
 
 
+def _norm_group(n_tiles, B, spe, cus):
+    """Examples per work item of the direct-load direct norm, as the library
+    chooses them: the fewest rounds times the item length (stages of its
+    examples plus ~6 of fill and drain). Only names the case below."""
+    best, best_cost = 1, None
+    for eg in range(1, min(B, 512) + 1):
+        rounds = -(-n_tiles * -(-B // eg) // cus)
+        cost = rounds * (eg * spe + 6)
+        if best_cost is None or cost < best_cost:
+            best, best_cost = eg, cost
+    return best
+
+
+@pytest.mark.parametrize("B,T,d_in,d_out,lda,ldg", [
+    (45, 1024, 300, 520, 304, 520),     # 2 x 3 ragged tiles, 32 stages per example
+    (13, 64, 2500, 1500, 2504, 1504),   # 10 x 6 ragged tiles, 2 stages per example
+])
+def test_direct_norm_example_groups(dp, B, T, d_in, d_out, lda, ldg):
+    """The direct-load direct norm gives a work item a run of consecutive
+    examples when that shortens the launch (eq. 6 per example, reduced at each
+    example boundary): a ragged last group, ragged output tiles, NaN in the
+    stride padding."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    tiles = -(-d_in // 256) * -(-d_out // 256)
+    eg = _norm_group(tiles, B, T // 32, cus)
+    _say(f"direct norm groups B={B} T={T} {d_in}x{d_out}: {eg} examples per item on {cus} CUs")
+    assert eg > 1 and B % eg != 0
+    A, G = _layer_inputs("bf16", B, T, d_in, d_out, seed=61, lda=lda, ldg=ldg)
+    nan = np.uint16(0x7FC0)
+    A[:, :, d_in:] = nan
+    G[:, :, d_out:] = nan
+    ref = _oracle_linear_norm2(A, G, d_in, d_out, "bf16")
+    n2 = torch.full((B,), 3.0, device="cuda")
+    At, Gt = dev(A, "bf16")[:, :, :d_in], dev(G, "bf16")[:, :, :d_out]
+    dp.dp_ghost_norm_linear(At, Gt, n2, accumulate=False, algo=dp.DP_NORM_DIRECT)
+    got = host(n2)
+    _say(f"  max rel err {rel(got, ref).max():.3e}")
+    assert rel(got, ref).max() <= TOL["bf16"]
+    dp.dp_ghost_norm_linear(At, Gt, n2, accumulate=True, algo=dp.DP_NORM_DIRECT)
+    assert rel(host(n2), 2 * ref).max() <= TOL["bf16"]
+    # The partials are reduced in a fixed order: the same bits every call.
+    n2b = torch.zeros(B, device="cuda")
+    dp.dp_ghost_norm_linear(At, Gt, n2b, accumulate=False, algo=dp.DP_NORM_DIRECT)
+    assert host(n2b).tobytes() == got.tobytes()
+
+
 def test_full_size_gpt2_head_sampled(dp):
     wl = gen.make_workload("c3")
     h = wl.head
