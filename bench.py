@@ -75,6 +75,9 @@ def parse(argv=None):
     ap.add_argument("--crossover", action="store_true",
                     help="instead of the step: time each distinct layer shape's grouped norm "
                          "with the Gram kernel and with the direct kernel (one JSON line)")
+    ap.add_argument("--crossover-shape", default=None, metavar="B,T",
+                    help="with --crossover: the workload's layer shapes at this batch size and "
+                         "sequence length instead of its own")
     ap.add_argument("--token-kernels", action="store_true",
                     help="instead of the step: time the token-keyed norm calls (embedding norm "
                          "with buckets, tied cross term) alone on the workload's inputs, "
@@ -240,7 +243,8 @@ class Step:
         self.norm_flops, self.norm_direct = 0.0, 0
         for a, g in norm_layers:
             di, do = a.shape[2], g.shape[2]
-            if T + 1 > 0.57 * 2.0 * di * do / (di + do):
+            r = 0.38 if do > 4096 else 0.49   # the library's throughput ratios (AUTO)
+            if T + 1 > r * 2.0 * di * do / (di + do):
                 self.norm_flops += 2.0 * K * di * do
                 self.norm_direct += 1
             else:
@@ -553,9 +557,16 @@ def main(argv=None) -> int:
     V = gen.GPT2_VOCAB
     ldz = round_up(V, args.ldz_multiple)
 
+    bt = {}
+    if args.crossover_shape:
+        if not args.crossover:
+            raise SystemExit("--crossover-shape applies to --crossover only")
+        b_, t_ = (int(x) for x in args.crossover_shape.split(","))
+        bt = {"B": b_, "T": t_}
+
     def load(name):
         t0 = time.perf_counter()
-        wl = gen.make_workload(name, seed=args.seed, ldz=ldz)
+        wl = gen.make_workload(name, seed=args.seed, ldz=ldz, **bt)
         log(f"[bench] generated {name}: {wl.description} in {time.perf_counter() - t0:.1f}s")
         return wl, Step(wl, dp, torch)
 

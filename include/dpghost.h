@@ -79,10 +79,12 @@ typedef DP_INT_ENUM(dp_status_e) {
  *         "normal clipping", Sec. "Training Configurations").
  * AUTO:   DIRECT when T + 1 > R * 2 d_in d_out / (d_in + d_out), else GRAM,
  *         where 2 d_in d_out / (d_in + d_out) equates the two flop counts
- *         and R = 0.57 is the measured ratio of the Gram kernel's throughput
- *         to the direct kernel's on MI355X (bf16, T = 1024: ~560 vs ~980
- *         TFLOP/s). With it AUTO picked the faster kernel for every GPT-2
- *         layer shape at T = 128, 256 and 1024. */
+ *         and R is the measured ratio of the Gram kernel's throughput to the
+ *         direct kernel's on MI355X near the crossover (bf16, T = 384 .. 768):
+ *         R = 0.49, or 0.38 when d_out > 4096 (G is then read in feature
+ *         chunks, as for an output head). With it AUTO picked the faster
+ *         kernel for every GPT-2 layer shape at T = 128, 256, 384, 512, 640,
+ *         768 and 1024. */
 typedef DP_INT_ENUM(dp_norm_algo_e) { DP_NORM_AUTO = 0, DP_NORM_GRAM = 1, DP_NORM_DIRECT = 2 } dp_norm_algo_t;
 
 /* One linear layer y = x W with W [d_in, d_out]: activations A [B,T,d_in]

@@ -130,13 +130,17 @@ struct NormPlan {
 };
 
 // Gram flops T(T+1)(d_in+d_out) against direct flops 2 T d_in d_out, the
-// Gram's weighted by the measured ratio of the two kernels' throughputs.
-constexpr double GRAM_VS_DIRECT_THROUGHPUT = 0.57;
+// Gram's weighted by the measured ratio of the two kernels' throughputs near
+// the crossover (T = 384 .. 768): ~0.49 for layers whose G is read whole,
+// ~0.38 for those whose G is split into feature chunks (an output head).
+constexpr double GRAM_VS_DIRECT_THROUGHPUT = 0.49;
+constexpr double CHUNKED_GRAM_VS_DIRECT_THROUGHPUT = 0.38;
 bool use_direct(const dp_linear_t& L, int T) {
   if (L.algo == DP_NORM_DIRECT) return true;
   if (L.algo == DP_NORM_GRAM) return false;
   const double crossover = 2.0 * (double)L.d_in * L.d_out / ((double)L.d_in + L.d_out);
-  return (double)T + 1.0 > GRAM_VS_DIRECT_THROUGHPUT * crossover;
+  const double r = L.d_out > KG_SPLIT ? CHUNKED_GRAM_VS_DIRECT_THROUGHPUT : GRAM_VS_DIRECT_THROUGHPUT;
+  return (double)T + 1.0 > r * crossover;
 }
 
 // One GEMM entry over the output region [0,M) x [0,N); 16-byte loads when

@@ -101,15 +101,25 @@ def test_norm_workspace_sizes(L):
     assert b"4 GiB" in L.dp_last_error()
     odd = (D.dp_linear_t * 1)(_lin(d_in=768, lda=768, d_out=50257, ldg=50257))  # rows not 16 B
     assert L.dp_ghost_norm_linear_workspace(odd, 1, 1000, 128, D.DP_BF16) == 0
-    # AUTO picks the direct form once T + 1 > 0.57 * 2 d_in d_out / (d_in + d_out)
-    # (0.57 * 64 here): one 256x256 output tile per example
+    # AUTO picks the direct form once T + 1 > R * 2 d_in d_out / (d_in + d_out)
+    # (R * 64 here): one 256x256 output tile per example
     auto = (D.dp_linear_t * 1)(_lin())
     assert L.dp_ghost_norm_linear_workspace(auto, 1, 100, 300, D.DP_F32) == 512
-    # at d_in = d_out = 512 the switch sits at T + 1 > 291.84: T = 290 keeps the
-    # Gram (3 T-tiles, 6 pairs per example), T = 291 goes direct (2 x 2 tiles)
+    # R = 0.49 when G is read whole: at d_in = d_out = 512 the switch sits at
+    # T + 1 > 250.88, so T = 249 keeps the Gram (2 T-tiles, 3 pairs per
+    # example) and T = 250 goes direct (2 x 2 tiles)
     sq = (D.dp_linear_t * 1)(_lin(d_in=512, lda=512, d_out=512, ldg=512))
-    assert L.dp_ghost_norm_linear_workspace(sq, 1, 100, 290, D.DP_F32) == 2560
-    assert L.dp_ghost_norm_linear_workspace(sq, 1, 100, 291, D.DP_F32) == 1792
+    assert L.dp_ghost_norm_linear_workspace(sq, 1, 100, 249, D.DP_F32) == 1280
+    assert L.dp_ghost_norm_linear_workspace(sq, 1, 100, 250, D.DP_F32) == 1792
+    # R = 0.38 when G is read in feature chunks (d_out > 4096): at d_in = 768,
+    # d_out = 50304 the switch sits at T + 1 > 574.93 (with 0.49: 741.4)
+    def ws(d_out, T, algo):
+        h = (D.dp_linear_t * 1)(_lin(d_in=768, lda=768, d_out=d_out, ldg=d_out, algo=algo))
+        return L.dp_ghost_norm_linear_workspace(h, 1, 2, T, D.DP_BF16)
+    for T in (573, 574):
+        want = D.DP_NORM_GRAM if T == 573 else D.DP_NORM_DIRECT
+        assert ws(50304, T, D.DP_NORM_AUTO) == ws(50304, T, want)
+    assert ws(50304, 573, D.DP_NORM_GRAM) != ws(50304, 573, D.DP_NORM_DIRECT)
     assert L.dp_ghost_norm_linear_workspace(None, 1, 4, 16, D.DP_F32) == 0
 
 
