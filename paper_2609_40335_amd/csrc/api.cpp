@@ -748,6 +748,15 @@ dp_status_t dp_ghost_norm_embedding(const int32_t* ids, const void* dE, int64_t 
   a.runs = ((uintptr_t)dE % dpg::EN_VB == 0 && (lde * es) % dpg::EN_VB == 0 &&
             (d * es) % dpg::EN_VB == 0 && span_ok(T, lde, dt)) ? 1 : 0;
   a.n_chunks = (int)(a.runs ? ceil_div(T, dpg::EN_P) : ceil_div(d, 64));
+  // Short bf16 examples with 16-byte rows (and pieces of 8 features): the
+  // pairwise form, one partial per chunk of EN_GF features (fewer than the
+  // ceil(d / 64) the workspace holds).
+  if (kdt(dt) == dpg::DT_BF16 && T <= dpg::EN_G_T && (uintptr_t)dE % 16 == 0 &&
+      (lde * es) % 16 == 0 && d % 8 == 0 && (int64_t)T * lde * es < 0x80000000ll) {
+    a.gram = 1;
+    a.runs = 0;
+    a.n_chunks = (int)ceil_div(d, dpg::EN_GF);
+  }
   a.seg_id = seg_id; a.n_unique = n_unique;
   if (T > dpg::EN_MAX_T) {
     if (!a.runs)

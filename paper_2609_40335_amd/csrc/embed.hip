@@ -406,6 +406,142 @@ __global__ __launch_bounds__(EN_THREADS) void embed_norm_runs_kernel(EmbedNormAr
   }
 }
 
+// Pairwise form of the same norm for short examples (bf16, 16-byte rows,
+// T <= EN_G_T): sum_v ||sum_{t: x_t = v} dE_t||^2 = sum_{t,s} [x_t = x_s]
+// <dE_t, dE_s>, the ghost-norm identity with one-hot inputs. Nothing waits on
+// a sort: the ids and the rows load together, in position order.
+// Workgroup (b, c) takes features [c' EN_GF, +EN_GF) of example b, with
+// c' = c, or c - 1 when workgroup (b, 0) ranks the ids (dispatched first).
+// Wave i loads rows 32i .. 32i+31 straight into MFMA operand fragments (lane
+// l: row l % 32, features 16k + 8 (l / 32) .. +7 of step k; the A operand of
+// E_i E_j^T and the B operand of E_j E_i^T have this same layout, so every
+// product pairs equal features), stages them in LDS, and multiplies its block
+// with every row block j; the pairs (t, s) with equal ids are summed. Rows at
+// or past T load as zeros (buffer bounds), features at or past d are zeroed.
+// Workgroup (b, 0), when buckets are asked for: each token's bucket (the
+// rank of its id among the example's distinct ids) from pairwise
+// comparisons, and the number of buckets.
+constexpr int EG_THREADS = 512;
+constexpr int EG_NW = EG_THREADS / WAVE;
+constexpr int EG_NB = EN_G_T / 32;        // row blocks
+constexpr int EG_JG = EG_NW / EG_NB;      // waves per row block, each over every EG_JG-th column block
+constexpr int EG_KS = EN_GF / 16;         // 16-feature steps per workgroup
+constexpr int EG_LPT = EG_THREADS / EN_G_T;  // lanes per token when ranking ids
+static_assert(EG_NB * EG_JG == EG_NW, "waves split evenly over the row blocks");
+static_assert(EG_LPT == 4, "ranking: four lanes per token, halves met by two shuffles");
+
+__global__ __launch_bounds__(EG_THREADS) void embed_norm_gram_kernel(EmbedNormArgs a) {
+  __shared__ u32x4 frag[EG_NB][EG_KS][WAVE];
+  __shared__ __attribute__((aligned(16))) uint32_t uid[EN_G_T];
+  __shared__ __attribute__((aligned(16))) uint32_t firsts[EN_G_T];
+  __shared__ float red[EG_NW];
+  __shared__ int cnt[EG_NW];
+  const int b = blockIdx.x, c = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int T = a.T;
+  const uint32_t V = (uint32_t)a.V;
+  const int32_t* ids = a.ids + (int64_t)b * T;
+  // Ids clamped to V (one bucket for every id outside [0, V)); positions past
+  // T get distinct values above any id, so they pair with nothing.
+  const uint32_t u = tid < T ? min((uint32_t)ids[min(tid, T - 1)], V) : 0x80000000u + (uint32_t)tid;
+
+  if (c == 0 && a.gram > 1) {
+    // Four lanes per token (t = tid / 4), each comparing against a quarter
+    // of the ids; the quarters meet through lane shuffles, which run on
+    // every lane (a lane that skipped one would not supply its value).
+    if (tid < EN_G_T) uid[tid] = u;
+    __syncthreads();
+    const int t = tid / EG_LPT, h = tid % EG_LPT;
+    constexpr int Q4 = EN_G_T / EG_LPT / 4;  // u32x4 per quarter
+    const uint32_t ut = uid[t];
+    const u32x4* part_ids = (const u32x4*)uid + h * Q4;
+    int dup = 0;  // an earlier position holds the same id
+#pragma unroll
+    for (int s4 = 0; s4 < Q4; ++s4) {
+      const u32x4 v = part_ids[s4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) dup |= (h * 4 * Q4 + 4 * s4 + q < t && v[q] == ut) ? 1 : 0;
+    }
+    dup |= __shfl_xor(dup, 1);
+    dup |= __shfl_xor(dup, 2);
+    const bool first = dup == 0 && t < T;
+    if (h == 0) firsts[t] = first ? 1u : 0u;
+    const uint64_t m = __ballot(first && h == 0);
+    if (lane == 0) cnt[w] = __popcll(m);
+    __syncthreads();
+    // bucket: the distinct ids below this one
+    const u32x4* part_f = (const u32x4*)firsts + h * Q4;
+    int r = 0;
+#pragma unroll
+    for (int s4 = 0; s4 < Q4; ++s4) {
+      const u32x4 v = part_ids[s4], f = part_f[s4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) r += (f[q] != 0u && v[q] < ut) ? 1 : 0;
+    }
+    r += __shfl_xor(r, 1);
+    r += __shfl_xor(r, 2);
+    if (a.seg_id && h == 0 && t < T) a.seg_id[(int64_t)b * T + t] = r;
+    if (a.n_unique && tid == 0) {
+      int n = 0;
+#pragma unroll
+      for (int q = 0; q < EG_NW; ++q) n += cnt[q];
+      a.n_unique[b] = n;
+    }
+    return;
+  }
+  const int chunk = c - (a.gram > 1 ? 1 : 0);
+
+  const uint32_t ldb = (uint32_t)(a.lde * 2);
+  const rsrc_t rE = make_rsrc((const char*)a.E + (int64_t)b * T * ldb, (uint64_t)T * ldb);
+  const int nb = (T + 31) / 32;
+  const int i = w % EG_NB, g = w / EG_NB;  // row block; column blocks g, g + EG_JG, ...
+  u32x4 fa[EG_KS];
+  if (g == 0 && i < nb) {
+    const uint32_t row = (uint32_t)(32 * i + (lane & 31));
+#pragma unroll
+    for (int k = 0; k < EG_KS; ++k) {
+      const int f = chunk * EN_GF + 16 * k + 8 * (lane >> 5);
+      // a feature piece past d reads past the buffer's end, i.e. zeros
+      const uint32_t off = f < a.d ? row * ldb + (uint32_t)f * 2 : 0x80000000u;
+      fa[k] = buf_load16<CPOL_STREAM>(rE, off);
+    }
+  }
+  if (tid < EN_G_T) uid[tid] = u;
+  if (g == 0 && i < nb) {
+#pragma unroll
+    for (int k = 0; k < EG_KS; ++k) frag[i][k][lane] = fa[k];
+  }
+  __syncthreads();
+  float part = 0.f;
+  if (i < nb && g < nb) {
+    if (g > 0) {
+#pragma unroll
+      for (int k = 0; k < EG_KS; ++k) fa[k] = frag[i][k][lane];
+    }
+    // rows t of this lane's accumulators e: 32 i + (e / 4) 8 + (l / 32) 4 + e % 4
+    uint32_t ut[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) ut[e] = uid[32 * i + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3)];
+    for (int j = g; j < nb; j += EG_JG) {
+      f32x16 acc = {};
+#pragma unroll
+      for (int k = 0; k < EG_KS; ++k) acc = mfma32_bf16(fa[k], frag[j][k][lane], acc);
+      const uint32_t us = uid[32 * j + (lane & 31)];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) part += ut[e] == us ? acc[e] : 0.f;
+    }
+  }
+  part = wave_sum(part);
+  if (lane == 0) red[w] = part;
+  __syncthreads();
+  if (tid == 0) {
+    float t = 0.f;
+#pragma unroll
+    for (int q = 0; q < EG_NW; ++q) t += red[q];
+    a.ws[(int64_t)b * a.n_chunks + chunk] = t;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Batch-wide clipped sum of the input embedding:
 // out[v, f] (+)= sum over tokens k with ids[k] = v of c[k / T] * E[k, f].
@@ -761,6 +897,14 @@ hipError_t launch_embed_norm(const EmbedNormArgs& a, int dt, hipStream_t s) {
     if (e != hipSuccess) return e;
     if (dt == DT_BF16) hipLaunchKernelGGL((embed_norm_runs_kernel<DT_BF16, 0>), g, blk, 0, s, a);
     else hipLaunchKernelGGL((embed_norm_runs_kernel<DT_F32, 0>), g, blk, 0, s, a);
+    return hipGetLastError();
+  }
+  if (a.gram) {
+    if (dt != DT_BF16 || a.T > EN_G_T) return hipErrorInvalidValue;
+    EmbedNormArgs ga = a;
+    ga.gram = (a.seg_id || a.n_unique) ? 2 : 1;  // 2: workgroup row 0 ranks the ids
+    const dim3 gg(a.B, a.n_chunks + ga.gram - 1);
+    hipLaunchKernelGGL(embed_norm_gram_kernel, gg, dim3(EG_THREADS), 0, s, ga);
     return hipGetLastError();
   }
   if (a.runs) {

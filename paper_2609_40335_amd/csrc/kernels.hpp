@@ -217,6 +217,8 @@ struct EmbedNormArgs {
   int32_t pbits;        // bits for a position in a sort key
   int32_t n_chunks;     // partials per example: feature chunks of 64, or (runs) position ranges
   int32_t runs;         // 1: embed_norm_runs_kernel (rows read EN_VB bytes per lane)
+  int32_t gram;         // embed_norm_gram_kernel (bf16, 16-byte rows, T <= EN_G_T): n_chunks
+                        // feature chunks; 2 (set at launch): workgroup row 0 ranks the ids
   int32_t* seg_id;      // nullable [B,T]
   int32_t* n_unique;    // nullable [B]
   float* ws;            // [B, n_chunks]
@@ -234,6 +236,8 @@ constexpr int EN_CT_T = 256;     // up to this T the norm ranks keys by counting
 constexpr int EN_P = 32;         // sorted positions whose runs one workgroup of the norm owns
 constexpr int EN_VB = 8;         // bytes per lane load of the run-walking norm
 constexpr int EN_BATCH = 32;     // row loads a lane has in flight (EN_P: one batch per range)
+constexpr int EN_G_T = 128;      // up to this T (bf16) the norm takes the pairwise (Gram) form
+constexpr int EN_GF = 128;       // features per workgroup of the pairwise form
 constexpr int ES_MAX_K = 16384;  // tokens per batch sorted in LDS (embedding sum)
 constexpr int ES_BLOCK = 32;     // sorted tokens per reduction block
 constexpr int GS_KB = 4096;      // keys per block of the workspace radix sort (more than ES_MAX_K keys)

@@ -183,6 +183,42 @@ def test_embedding_norm_and_buckets(dp, kind, T, V, dtype, d, lde):
     assert err <= TOL[dtype]
 
 
+@pytest.mark.parametrize("kind,B,T,V,d,lde", [
+    ("zipf", 4, 128, 50257, 768, 768),     # GPT-2 shape: six 128-feature chunks, four row blocks
+    ("zipf", 3, 100, 50257, 200, 208),     # ragged row block, last chunk past d, NaN padding
+    ("same", 3, 33, 1000, 64, 64),         # one bucket; a second row block of one row
+    ("distinct", 2, 32, 300, 136, 136),    # every id once; one row block, 8-feature tail piece
+    ("uniform", 3, 128, 512, 768, 768),    # many repeats per id
+    ("zipf", 2, 1, 50257, 8, 8),           # T = 1, one 8-feature piece
+])
+def test_embedding_norm_pairwise_form(dp, kind, B, T, V, d, lde):
+    """bf16 examples up to T = 128 with 16-byte rows take the pairwise form,
+    sum_{t,s} [x_t = x_s] <dE_t, dE_s> on MFMA (the ghost-norm identity with
+    one-hot inputs), next to a workgroup that ranks the ids for the buckets."""
+    _say(f"embedding pairwise {kind} B={B} T={T} V={V} d={d} lde={lde}")
+    ids = gen.draw_ids(5, 1, (B, T), V, kind)
+    dE = gen.draw(5, 2, (B, T, d), 1e-2, "bf16")
+    ref = O.embedding_norm2(ids, O.decode(dE, "bf16"), V)
+    seg_ref, nu_ref = O.buckets(ids)
+    dEd = dev(dE, "bf16")
+    if lde != d:
+        pad = torch.full((B, T, lde), float("nan"), device="cuda", dtype=dEd.dtype)
+        pad[:, :, :d] = dEd
+        dEd = pad[:, :, :d]
+    n2 = torch.full((B,), 9.0, device="cuda")
+    seg = torch.full((B, T), -1, dtype=torch.int32, device="cuda")
+    nu = torch.zeros(B, dtype=torch.int32, device="cuda")
+    dp.dp_ghost_norm_embedding(dev(ids), dEd, V, n2, seg_id=seg, n_unique=nu)
+    np.testing.assert_array_equal(host(seg), seg_ref)
+    np.testing.assert_array_equal(host(nu), nu_ref)
+    got = host(n2)
+    _say(f"  max rel err {rel(got, ref).max():.3e}")
+    assert rel(got, ref).max() <= TOL["bf16"]
+    # without buckets (no ranking workgroup), accumulating onto what is there
+    dp.dp_ghost_norm_embedding(dev(ids), dEd, V, n2, accumulate=True)
+    assert rel(host(n2), 2 * ref).max() <= TOL["bf16"]
+
+
 # ---------------------------------------------------------------------------
 # a5: tied cross term
 # ---------------------------------------------------------------------------
