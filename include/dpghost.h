@@ -179,6 +179,9 @@ dp_status_t dp_ghost_norm_linear_bias_grouped_noalloc(const dp_linear_t* layers,
  * seg_id and n_unique may be NULL. Exact (integer) outputs.
  * Limits: ceil(log2(V + 1)) + ceil(log2 T) <= 32 (a sort key holds an id
  * clamped to V and a position; T <= 65536 at V = 50257) and B*T < 2^31.
+ * bf16 examples up to T = 128 whose rows are whole 16-byte units (d a
+ * multiple of 8) take the pairwise form sum_{t,s: ids equal} <dE_t, dE_s>
+ * (the same sum, in another rounding order) and rank ids by comparison.
  * Up to T = 4096 an example is sorted in LDS, longer ones by a radix sort
  * through the workspace; those need rows of whole 8-byte units (lde and d
  * times the element size multiples of 8, dE 8-byte aligned) whose T rows

@@ -237,7 +237,7 @@ constexpr int EN_P = 32;         // sorted positions whose runs one workgroup of
 constexpr int EN_VB = 8;         // bytes per lane load of the run-walking norm
 constexpr int EN_BATCH = 32;     // row loads a lane has in flight (EN_P: one batch per range)
 constexpr int EN_G_T = 128;      // up to this T (bf16) the norm takes the pairwise (Gram) form
-constexpr int EN_GF = 128;       // features per workgroup of the pairwise form
+constexpr int EN_GF = 96;        // features per workgroup of the pairwise form
 constexpr int ES_MAX_K = 16384;  // tokens per batch sorted in LDS (embedding sum)
 constexpr int ES_BLOCK = 32;     // sorted tokens per reduction block
 constexpr int GS_KB = 4096;      // keys per block of the workspace radix sort (more than ES_MAX_K keys)
