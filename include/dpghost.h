@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define DP_ABI_VERSION 2
+#define DP_ABI_VERSION 3
 
 /* Enumerations are int-sized in both languages. Compiled as C++ they have
  * int as their fixed underlying type, so that every int a C caller passes
@@ -346,6 +346,47 @@ dp_status_t dp_clipped_grad_sum_noised_grouped_ws(const dp_linear_t* layers, flo
                                                   int B_norm, uint64_t seed, uint64_t step,
                                                   void* workspace, size_t workspace_bytes,
                                                   void* stream);
+
+/* ---------------------------------------------------------------------
+ * Per-example gradient store: the materialising ("normal clipping") form of
+ * the clipped sum (Sec. "Training Configurations"; eq. 2-3), for the long
+ * sequences where the direct norm is taken anyway (dp_norm_algo_t). The
+ * direct norm forms every example's gradient A_b^T G_b tile by tile in
+ * registers; dp_ghost_norm_linear_store also writes those fp32 tiles to the
+ * store (B * tiles * 256 KB: 7.9 GB for GPT-2 small at B = 16), and
+ * dp_clipped_grad_sum_noised_store then forms
+ *   outs[l] = (prior + sum_b c_b (A_b^T G_b) + sigma*C*z) / B_norm
+ * from the stored tiles, an HBM-bound weighted sum, instead of multiplying
+ * the operands again. The result, noise included, is that of
+ * dp_clipped_grad_sum_noised_grouped on the same arguments up to fp32
+ * rounding order; an example with c_b = 0 is left out, as there.
+ * Conditions: bf16, T a multiple of 32, every layer's A and G rows 16-byte
+ * aligned (else DP_EUNSUPPORTED, and dp_grad_store_bytes returns 0).
+ * dp_grad_store_bytes: the store size for this layer table (the tiles plus
+ * B * tiles fp32 norm partials), 0 when the conditions fail.
+ * dp_ghost_norm_linear_store: norm2[b] (+)= sum over layers of
+ * ||A_b^T G_b||_F^2, every layer by the direct form whatever its algo field
+ * (bit-identical to dp_ghost_norm_linear_grouped with DP_NORM_DIRECT), and
+ * the tiles into the store.
+ * dp_clipped_grad_sum_noised_store: outs, tensor_ids, accumulate, the noise
+ * arguments and the output layouts as for dp_clipped_grad_sum_noised_grouped;
+ * layers must be the table the store was written with (its pointers are not
+ * read again, only its shapes). store: device memory owned by the caller,
+ * 16-byte aligned, at least dp_grad_store_bytes() bytes (the sum reads the
+ * tiles only); it holds one step's tiles until the next store call.
+ * ------------------------------------------------------------------- */
+size_t dp_grad_store_bytes(const dp_linear_t* layers, int n_layers, int B, int T,
+                           dp_dtype_t dt);
+dp_status_t dp_ghost_norm_linear_store(const dp_linear_t* layers, int n_layers, int B, int T,
+                                       dp_dtype_t dt, float* norm2, int accumulate, void* store,
+                                       size_t store_bytes, void* stream);
+dp_status_t dp_clipped_grad_sum_noised_store(const dp_linear_t* layers, float* const* outs,
+                                             const uint64_t* tensor_ids,
+                                             const int32_t* accumulate, int n_layers,
+                                             const float* c, int B, int T, dp_dtype_t dt,
+                                             int transpose_out, float sigma, float C, int B_norm,
+                                             uint64_t seed, uint64_t step, const void* store,
+                                             size_t store_bytes, void* stream);
 
 /* ---------------------------------------------------------------------
  * Gaussian mechanism (eq. 3): grad[j] = (grad[j] + sigma*C*z_j) / B_norm

@@ -352,11 +352,13 @@ size_t sum_split_bytes(const std::vector<GemmEntry>& entries, int B, int T, dp_d
 // given `part` (part_bytes) splits the tail of its direct-load launches.
 dp_status_t run_gemm(const std::vector<GemmEntry>& entries, int mode, int B, int T, dp_dtype_t dt,
                      const float* c, float* ws, int64_t slots, int transpose, const NoiseCfg& nz,
-                     hipStream_t s, float* part = nullptr, size_t part_bytes = 0) {
+                     hipStream_t s, float* part = nullptr, size_t part_bytes = 0,
+                     float* store = nullptr) {
   for (const auto& [vec, sel] : gemm_launches(entries)) {
     dpg::GemmArgs a{};
     a.B = B; a.T = T; a.c = c; a.ws = ws; a.slots = (int32_t)slots;
     a.transpose = transpose;
+    a.store = store;
     a.noise = nz.on ? 1 : 0;
     a.sigma_c = nz.sigma_c; a.inv_b = nz.inv_b; a.step = nz.step; a.seed = nz.seed;
     a.part = part;
@@ -953,6 +955,129 @@ dp_status_t dp_clipped_grad_sum_noised_grouped(const dp_linear_t* layers, float*
   return dp_clipped_grad_sum_noised_grouped_ws(layers, outs, tensor_ids, accumulate, n_layers, c,
                                                B, T, dt, transpose_out, sigma, C, B_norm, seed,
                                                step, nullptr, 0, stream);
+}
+
+// ------------------------------------------------------- gradient store
+// The direct norm's per-example tiles kept in HBM and summed with the clip
+// factors afterwards (see the header). Entries are planned in table order,
+// X = A, Y = G, so that entry i's slot_begin is its first tile slot.
+static dp_status_t store_plan(const dp_linear_t* layers, int n_layers, int B, int T,
+                              dp_dtype_t dt, std::vector<GemmEntry>& entries, int64_t* tiles) {
+  dp_status_t st = check_layers(layers, n_layers, B, T, dt);
+  if (st != DP_OK) return st;
+  if (kdt(dt) != dpg::DT_BF16 || T % dpg::DL_SUM_BK != 0)
+    return fail(DP_EUNSUPPORTED, "the gradient store needs bf16 and T a multiple of %d",
+                dpg::DL_SUM_BK);
+  int64_t slots = 0;
+  for (int i = 0; i < n_layers; ++i) {
+    const dp_linear_t& L = layers[i];
+    plan_gemm(L.A, L.lda, L.d_in, L.G, L.ldg, L.d_out, dt, nullptr, 0, entries, &slots, 1);
+    if (!entries.back().vec)
+      return fail(DP_EUNSUPPORTED, "layer %d: the gradient store needs 16-byte aligned rows", i);
+  }
+  if ((uint64_t)B * (uint64_t)slots > 0x7FFFFFFFull)
+    return fail(DP_EUNSUPPORTED, "too many tiles for the gradient store");
+  *tiles = slots;
+  return DP_OK;
+}
+
+static size_t store_tiles_bytes(int B, int64_t tiles) {
+  return (size_t)B * (size_t)tiles * dpg::STORE_TILE_FLOATS * 4;
+}
+
+size_t dp_grad_store_bytes(const dp_linear_t* layers, int n_layers, int B, int T,
+                           dp_dtype_t dt) {
+  std::vector<GemmEntry> entries;
+  int64_t tiles = 0;
+  if (store_plan(layers, n_layers, B, T, dt, entries, &tiles) != DP_OK) return 0;
+  return store_tiles_bytes(B, tiles) + align_up((size_t)B * (size_t)tiles * 4);
+}
+
+dp_status_t dp_ghost_norm_linear_store(const dp_linear_t* layers, int n_layers, int B, int T,
+                                       dp_dtype_t dt, float* norm2, int accumulate, void* store,
+                                       size_t store_bytes, void* stream) {
+  std::vector<GemmEntry> entries;
+  int64_t tiles = 0;
+  dp_status_t st = store_plan(layers, n_layers, B, T, dt, entries, &tiles);
+  if (st != DP_OK) return st;
+  if (!norm2) return fail(DP_EINVAL, "norm2 is NULL");
+  const size_t need = store_tiles_bytes(B, tiles) + align_up((size_t)B * (size_t)tiles * 4);
+  if (!store || store_bytes < need)
+    return fail(DP_EINVAL, "gradient store of %zu bytes needed, %zu given", need,
+                store ? store_bytes : (size_t)0);
+  if ((uintptr_t)store % 16)
+    return fail(DP_EINVAL, "the gradient store must be 16-byte aligned");
+  hipStream_t s = as_stream(stream);
+  float* tiles_f = static_cast<float*>(store);
+  float* ws = reinterpret_cast<float*>(static_cast<char*>(store) + store_tiles_bytes(B, tiles));
+  st = run_gemm(entries, 1, B, T, dt, nullptr, ws, tiles, 0, NoiseCfg{}, s, nullptr, 0, tiles_f);
+  if (st != DP_OK) return st;
+  return hip_status(dpg::launch_finish_rows(ws, B, (int)tiles, norm2, accumulate, 1.f, s),
+                    "finish launch");
+}
+
+dp_status_t dp_clipped_grad_sum_noised_store(const dp_linear_t* layers, float* const* outs,
+                                             const uint64_t* tensor_ids,
+                                             const int32_t* accumulate, int n_layers,
+                                             const float* c, int B, int T, dp_dtype_t dt,
+                                             int transpose_out, float sigma, float C, int B_norm,
+                                             uint64_t seed, uint64_t step, const void* store,
+                                             size_t store_bytes, void* stream) {
+  if (!outs || !c || !tensor_ids) return fail(DP_EINVAL, "outs, c or tensor_ids is NULL");
+  std::vector<GemmEntry> entries;
+  int64_t tiles = 0;
+  dp_status_t st = store_plan(layers, n_layers, B, T, dt, entries, &tiles);
+  if (st != DP_OK) return st;
+  st = check_noise_args(sigma, C, B_norm, step);
+  if (st != DP_OK) return st;
+  if (!store || store_bytes < store_tiles_bytes(B, tiles))
+    return fail(DP_EINVAL, "gradient store of %zu bytes needed, %zu given",
+                store_tiles_bytes(B, tiles), store ? store_bytes : (size_t)0);
+  if ((uintptr_t)store % 16)
+    return fail(DP_EINVAL, "the gradient store must be 16-byte aligned");
+  for (int i = 0; i < n_layers; ++i) {
+    if (!outs[i]) return fail(DP_EINVAL, "outs[%d] is NULL", i);
+    if (tensor_ids[i] >> 32) return fail(DP_EINVAL, "tensor_ids[%d] must be < 2^32", i);
+    GemmEntry& e = entries[i];
+    e.out = outs[i];
+    e.ldo = transpose_out ? layers[i].d_in : layers[i].d_out;
+    e.acc = accumulate && accumulate[i] ? 1 : 0;
+    e.tensor_id = (uint32_t)tensor_ids[i];
+  }
+  hipStream_t s = as_stream(stream);
+  for (size_t i0 = 0; i0 < entries.size(); i0 += dpg::GM_MAX_LAYERS) {
+    const size_t n = std::min(entries.size() - i0, (size_t)dpg::GM_MAX_LAYERS);
+    dpg::GemmArgs a{};
+    a.B = B; a.T = T; a.c = c;
+    a.transpose = transpose_out ? 1 : 0;
+    a.noise = 1;
+    a.sigma_c = (float)((double)sigma * (double)C);
+    a.inv_b = B_norm > 0 ? (float)(1.0 / (double)B_norm) : 1.f;
+    a.seed = seed;
+    a.step = (uint32_t)step;
+    a.store = static_cast<float*>(const_cast<void*>(store));
+    a.eg = 1;
+    uint64_t items = 0;
+    for (size_t j = 0; j < n; ++j) {
+      const GemmEntry& e = entries[i0 + j];
+      dpg::GemmLayer& L = a.L[j];
+      L.X = nullptr; L.Y = nullptr;
+      L.store_slot = e.slot_begin;
+      L.M = e.M; L.N = e.N;
+      L.tm = (uint16_t)e.tm; L.tn = (uint16_t)e.tn;
+      L.tile_begin = (uint32_t)items;
+      L.tensor_id = e.tensor_id;
+      L.accumulate = e.acc;
+      L.out = e.out; L.ldo = e.ldo;
+      items += (uint64_t)e.tm * e.tn;
+    }
+    if (items > 0xFFFFFFFFull) return fail(DP_EUNSUPPORTED, "too many work items");
+    a.n_layers = (int32_t)n;
+    a.n_items = (uint32_t)items;
+    st = hip_status(dpg::launch_store_sum(a, s), "store_sum launch");
+    if (st != DP_OK) return st;
+  }
+  return DP_OK;
 }
 
 // Shared checks and argument set-up of the embedding-form sums.

@@ -688,6 +688,17 @@ __device__ __forceinline__ void wait_vmcnt() {
 // MODE_SUM: the clipped sum over all K = B*T rows. MODE_NORM (the direct
 // norm): K restricted to example b's T rows, no factors, and the tile's
 // in-range elements squared and summed in registers.
+// Gradient store layout (GRAD_STORE): within a tile's 65536 floats, wave w's
+// accumulator block (i, j), floats 4q .. 4q+3 of lane l, sit at
+// ((w * 8 + i * 2 + j) * 4 + q) * 256 + 4 l: every store and load moves one
+// contiguous KB per wave.
+__device__ __forceinline__ size_t store_lane_offset(int w, int lane) {
+  return (size_t)w * 8 * 4 * 256 + (size_t)lane * 4;
+}
+__device__ __forceinline__ size_t store_chunk(int i, int j, int q) {
+  return (size_t)((i * 2 + j) * 4 + q) * 256;
+}
+
 // BIG: some operand of the launch spans 4 GiB or more (see issue()).
 template <int MODE, bool BIG>
 __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
@@ -877,6 +888,21 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
     }
     part = wave_sum(part);
     if (lane == 0) red[le * (GM_THREADS / WAVE) + w] = part;
+    if (a.store) {
+      // the example's tile, for a later clipped sum from the store
+      float* dst = a.store + ((((size_t)L.slot_begin + rel) * (size_t)a.B + (size_t)(b + le))
+                              << 16) + store_lane_offset(w, lane);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                             acc[i][j][4 * q + 3]};
+            __builtin_nontemporal_store(v, (f32x4*)(dst + store_chunk(i, j, q)));
+          }
+    }
     ++le;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -1027,6 +1053,77 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
   }
 }
 
+// Clipped sum from a gradient store (the materialising form of eq. 3: the
+// per-example gradients, already formed by the direct norm, weighted and
+// added): one workgroup per output tile, its 8 waves in the register layout
+// of dl_gemm_kernel, acc = sum_e c_e tile_e in example order (examples with
+// c_e = 0 are left out, as in the GEMM), then the GEMM's own epilogue (prior,
+// fused noise, 1/B, row-major or transposed store). HBM-bound: B tiles read
+// per output tile.
+__global__ __launch_bounds__(GM_THREADS) void store_sum_kernel(GemmArgs args) {
+  const GemmArgs& a = *(const GemmArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  (void)args;
+  __shared__ __attribute__((aligned(1024))) char stage[(GM_THREADS / WAVE) * 32 * EP_LD * 4];
+  const uint32_t item = xcd_remap(blockIdx.x, gridDim.x);
+  const int ln = (int)(threadIdx.x & (WAVE - 1));
+  const int l = wave_find(item, ln < a.n_layers ? a.L[ln].tile_begin : 0u, a.n_layers);
+  const GemmLayer& L = a.L[l];
+  const uint32_t rel = item - L.tile_begin;
+  int mt, nt;
+  tile_of(L, rel, mt, nt);
+  const int64_t m0 = (int64_t)mt * GM_BM, n0 = (int64_t)nt * GM_BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = w & 1, wn = w >> 1;
+  const float* src = a.store + ((((size_t)L.store_slot + rel) * (size_t)a.B) << 16) +
+                     store_lane_offset(w, lane);
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+  const int nB = __builtin_amdgcn_readfirstlane(a.B);
+  for (int e = 0; e < nB; ++e) {
+    const float ce = a.c[e];
+    if (!(ce != 0.f)) continue;
+    const float* p = src + ((size_t)e << 16);
+    // two halves of 16 loads each (i = 0, 1 and i = 2, 3), all in flight
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      f32x4 v[2][2][4];
+#pragma unroll
+      for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            v[ii][j][q] = __builtin_nontemporal_load((const f32x4*)(p + store_chunk(2 * hh + ii, j, q)));
+#pragma unroll
+      for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              acc[2 * hh + ii][j][4 * q + r] = fmaf(ce, v[ii][j][q][r], acc[2 * hh + ii][j][4 * q + r]);
+    }
+  }
+  if (a.transpose) {
+    store_tile(a, L, m0, n0, wm, wn, lane, acc);
+  } else {
+    float* slice = (float*)stage + w * 32 * EP_LD;
+    store_tile_rows(a, L, m0, n0, wm, wn, lane, acc, slice);
+  }
+}
+
+hipError_t launch_store_sum(const GemmArgs& a, hipStream_t s) {
+  if (a.n_items == 0) return hipSuccess;
+  if (!a.store || !a.c) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(store_sum_kernel, dim3(a.n_items), dim3(GM_THREADS), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int DT, bool VEC, int MODE>
 static void launch_sc(const GemmArgs& a, int sc, hipStream_t s) {
   const dim3 g(a.n_items), blk(GM_THREADS);
@@ -1051,9 +1148,11 @@ static hipError_t launch_kt(const GemmArgs& a0, int dt, bool vec, int cus, size_
   // The accumulator form needs every K-stage inside one example.
   const int ks = dt == DT_BF16 ? KT<DT_BF16>::KS : KT<DT_F32>::KS;
   const int sc = MODE == MODE_NORM ? SC_NONE : (a.T % ks == 0 ? SC_ACC : SC_STAGE);
-  if (MODE == MODE_NORM &&
-      (a.eg < 1 || a.eg > NG_MAX || (a.eg > 1 && !(dt == DT_BF16 && vec && a.T % DL_BK == 0))))
-    return hipErrorInvalidValue;  // example groups exist only on the direct-load kernel
+  // Example groups and the gradient store exist only on the direct-load kernel.
+  const bool dl = dt == DT_BF16 && vec && a.T % DL_BK == 0;
+  if (MODE == MODE_NORM && (a.eg < 1 || a.eg > NG_MAX || ((a.eg > 1 || a.store) && !dl)))
+    return hipErrorInvalidValue;
+  if (MODE == MODE_SUM && a.store) return hipErrorInvalidValue;
   if (dt == DT_BF16 && vec && a.T % DL_BK == 0 && (MODE == MODE_NORM || a.B <= DL_MAXB)) {
     uint32_t grid = a.n_items;
     if (MODE == MODE_SUM && a.part != nullptr) {

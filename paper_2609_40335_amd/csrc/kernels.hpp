@@ -101,7 +101,11 @@ struct GemmLayer {
   const void* X;        // [K rows, ldx]
   const void* Y;        // [K rows, ldy]
   float* out;           // clipped sum: [M, ldo] or transposed [N, ldo]
-  int64_t ldx, ldy, ldo;  // row strides in elements
+  union {
+    int64_t ldx;          // row stride of X in elements
+    int64_t store_slot;   // sum from a gradient store (X, Y unread): first tile slot
+  };
+  int64_t ldy, ldo;     // row strides in elements
   int32_t M, N;         // X columns (output rows) and Y columns (output columns)
   uint16_t tm, tn;      // 256-wide tiles along M and N
   uint32_t tile_begin;  // first work item of this entry
@@ -140,6 +144,11 @@ struct GemmArgs {
   // Direct norm, direct-load kernel: examples per work item (a tile over eg
   // consecutive examples; items of one layer are group-major). 1 elsewhere.
   int32_t eg;
+  // Per-example gradient store: the direct norm (direct-load kernel) also
+  // writes each example's fp32 tile there; store_sum_kernel reads it back.
+  // Tile slot q of example e is the 65536 floats at ((q * B + e) << 16), in
+  // the register order of the 8 waves (GRAD_STORE layout below).
+  float* store;
 };
 
 static_assert(sizeof(GemmArgs) <= 4096, "kernel arguments must stay within 4 KiB");
@@ -207,6 +216,11 @@ hipError_t launch_clipped_sum(const GemmArgs& a, int dt, bool vec, int cus, size
                               hipStream_t s);
 // Direct norm: ws[b, slot] = ||tile of X_b^T Y_b||_F^2 for every output tile.
 hipError_t launch_direct_norm(const GemmArgs& a, int dt, bool vec, hipStream_t s);
+// Clipped sum from a gradient store: for every tile of every layer,
+// out (+)= sum_e c_e * tile_e (then the fused noise and 1/B), one workgroup
+// per tile; the layers' store_slot give each layer's first tile slot.
+hipError_t launch_store_sum(const GemmArgs& a, hipStream_t s);
+constexpr size_t STORE_TILE_FLOATS = (size_t)GM_BM * GM_BN;
 
 // --------------------------------------------------------- embedding / ids
 struct EmbedNormArgs {

@@ -22,6 +22,7 @@ __all__ = [
     "dp_tied_cross_term", "dp_clip_factors", "dp_clip_factors_scaled", "dp_clipped_grad_sum",
     "dp_embedding_rows", "dp_embedding_rows_add", "EmbeddingRows",
     "dp_clipped_grad_sum_grouped", "dp_clipped_grad_sum_noised_grouped", "dp_add_noise",
+    "dp_grad_store_bytes", "dp_ghost_norm_linear_store", "dp_clipped_grad_sum_noised_store",
     "dp_noise_fill", "dp_vector_grads_grouped", "dp_vector_clipped_sum_noised_grouped",
     "dp_ghost_norm_linear_bias_grouped", "VectorSums",
     "dp_ghost_norm_positional", "dp_clipped_grad_sum_positional_noised",
@@ -100,6 +101,13 @@ _SIGS = {
                                                ctypes.POINTER(_U64), ctypes.POINTER(ctypes.c_int32),
                                                _I, _VP, _I, _I, _I, _I, _F, _F, _I, _U64, _U64,
                                                _VP, _SZ, _VP], _I),
+    "dp_grad_store_bytes": ([ctypes.POINTER(dp_linear_t), _I, _I, _I, _I], _SZ),
+    "dp_ghost_norm_linear_store": ([ctypes.POINTER(dp_linear_t), _I, _I, _I, _I, _VP, _I, _VP,
+                                    _SZ, _VP], _I),
+    "dp_clipped_grad_sum_noised_store": ([ctypes.POINTER(dp_linear_t), ctypes.POINTER(_VP),
+                                          ctypes.POINTER(_U64), ctypes.POINTER(ctypes.c_int32),
+                                          _I, _VP, _I, _I, _I, _I, _F, _F, _I, _U64, _U64,
+                                          _VP, _SZ, _VP], _I),
     "dp_clip_factors_scaled": ([_VP, _I, _F, _F, _VP, _VP, _VP], _I),
     "dp_clip_factors_scaled2": ([_VP, _VP, _I, _F, _F, _VP, _VP, _VP], _I),
     "dp_noise_fill": ([_VP, _I64, _F, _F, _I, _U64, _U64, _U64, _VP], _I),
@@ -627,6 +635,52 @@ class VectorGroup:
                "dp_vector_clipped_sum_noised_grouped")
 
 
+def dp_grad_store_bytes(layers: Sequence) -> int:
+    """Bytes of the per-example gradient store for these (A, G) layers; 0 when
+    the store form does not apply (bf16, T % 32 == 0, 16-byte rows)."""
+    descs = [_layer(l[0], l[1]) for l in layers]
+    arr = (dp_linear_t * len(descs))(*descs)
+    A0 = layers[0][0]
+    return lib().dp_grad_store_bytes(arr, len(descs), A0.shape[0], A0.shape[1], _dtype(A0))
+
+
+def dp_ghost_norm_linear_store(layers: Sequence, norm2: torch.Tensor, store: torch.Tensor,
+                               accumulate: bool = False, stream=None) -> torch.Tensor:
+    """Direct norms of every layer, each example's gradient tiles kept in
+    ``store`` (a byte tensor of dp_grad_store_bytes(layers) bytes)."""
+    descs = [_layer(l[0], l[1]) for l in layers]
+    arr = (dp_linear_t * len(descs))(*descs)
+    A0 = layers[0][0]
+    _check(lib().dp_ghost_norm_linear_store(arr, len(descs), A0.shape[0], A0.shape[1],
+                                            _dtype(A0), norm2.data_ptr(), int(accumulate),
+                                            store.data_ptr(), store.numel() * store.element_size(),
+                                            _stream(stream)),
+           "dp_ghost_norm_linear_store")
+    return norm2
+
+
+def dp_clipped_grad_sum_noised_store(layers: Sequence, outs: Sequence[torch.Tensor], c,
+                                     tensor_ids: Sequence[int], sigma: float, C: float,
+                                     B_norm: int, seed: int, step: int, store: torch.Tensor,
+                                     accumulate=None, transpose_out: bool = False,
+                                     stream=None) -> None:
+    """The noised clipped sums from the tiles dp_ghost_norm_linear_store kept
+    for the same layers."""
+    descs = [_layer(l[0], l[1]) for l in layers]
+    arr = (dp_linear_t * len(descs))(*descs)
+    optrs = (ctypes.c_void_p * len(outs))(*[o.data_ptr() for o in outs])
+    tids, acc = _noise_arrays(len(descs), tensor_ids, accumulate)
+    A0 = layers[0][0]
+    _check(lib().dp_clipped_grad_sum_noised_store(arr, optrs, tids, acc, len(descs), c.data_ptr(),
+                                                  A0.shape[0], A0.shape[1], _dtype(A0),
+                                                  int(transpose_out), float(sigma), float(C),
+                                                  int(B_norm), int(seed), int(step),
+                                                  store.data_ptr(),
+                                                  store.numel() * store.element_size(),
+                                                  _stream(stream)),
+           "dp_clipped_grad_sum_noised_store")
+
+
 class LinearGroup:
     """Descriptors of many linear layers of one batch, prepared once.
 
@@ -720,3 +774,42 @@ class LinearGroup:
                                                        0 if ws is None else ws.numel(),
                                                        _stream(stream)),
                "dp_clipped_grad_sum_noised_grouped_ws")
+
+    def store_bytes(self) -> int:
+        """Bytes of the per-example gradient store for this group (0: the
+        store form does not apply; see dp_grad_store_bytes)."""
+        return lib().dp_grad_store_bytes(self.descs, self.n, self.B, self.T, self.dt)
+
+    def ghost_norm_store(self, norm2: torch.Tensor, store: torch.Tensor,
+                         accumulate: bool = False, stream=None) -> torch.Tensor:
+        """Direct norms of every layer, the examples' gradient tiles into store."""
+        _check(lib().dp_ghost_norm_linear_store(self.descs, self.n, self.B, self.T, self.dt,
+                                                norm2.data_ptr(), int(accumulate),
+                                                store.data_ptr(),
+                                                store.numel() * store.element_size(),
+                                                _stream(stream)),
+               "dp_ghost_norm_linear_store")
+        return norm2
+
+    def clipped_sum_noised_store(self, c: torch.Tensor, store: torch.Tensor,
+                                 tensor_ids: Sequence[int], sigma: float, C: float, B_norm: int,
+                                 seed: int, step: int, accumulate=None,
+                                 transpose_out: bool = False, stream=None) -> None:
+        """clipped_sum_noised from the tiles ghost_norm_store kept."""
+        if self.outs is None:
+            raise DPError("set_outputs() first")
+        key = (tuple(int(t) for t in tensor_ids),
+               accumulate if isinstance(accumulate, (bool, int, type(None)))
+               else tuple(bool(a) for a in accumulate))
+        if getattr(self, "_noise_key", None) != key:
+            self._noise_key = key
+            self._noise_arr = _noise_arrays(self.n, tensor_ids, accumulate)
+        tids, acc = self._noise_arr
+        _check(lib().dp_clipped_grad_sum_noised_store(self.descs, self.outs, tids, acc, self.n,
+                                                      c.data_ptr(), self.B, self.T, self.dt,
+                                                      int(transpose_out), float(sigma), float(C),
+                                                      int(B_norm), int(seed), int(step),
+                                                      store.data_ptr(),
+                                                      store.numel() * store.element_size(),
+                                                      _stream(stream)),
+               "dp_clipped_grad_sum_noised_store")

@@ -46,7 +46,7 @@ def test_binding_covers_every_entry_point():
 
 
 def test_version_and_strings(L):
-    assert L.dp_abi_version() == 2
+    assert L.dp_abi_version() == 3
     assert L.dp_status_string(0) == b"ok"
     assert L.dp_status_string(1) == b"invalid argument"
 
@@ -121,6 +121,47 @@ def test_norm_workspace_sizes(L):
         assert ws(50304, T, D.DP_NORM_AUTO) == ws(50304, T, want)
     assert ws(50304, 573, D.DP_NORM_GRAM) != ws(50304, 573, D.DP_NORM_DIRECT)
     assert L.dp_ghost_norm_linear_workspace(None, 1, 4, 16, D.DP_F32) == 0
+
+
+def test_grad_store_size_and_argument_checks(L):
+    """The per-example gradient store: B * tiles * 256 KB of fp32 tiles plus
+    B * tiles norm partials; only bf16, T % 32 == 0 and 16-byte rows; every
+    failure is found on the host before any launch."""
+    two = (D.dp_linear_t * 2)(_lin(d_in=300, lda=304, d_out=520, ldg=520),   # 2 x 3 tiles
+                              _lin(d_in=256, lda=256, d_out=256, ldg=256))   # 1 tile
+    tiles, B, T = 7, 5, 64
+    need = B * tiles * 256 * 256 * 4 + 256                    # partials: 140 B, one 256-B unit
+    assert L.dp_grad_store_bytes(two, 2, B, T, D.DP_BF16) == need
+    assert L.dp_grad_store_bytes(two, 2, B, T, D.DP_F32) == 0
+    assert L.dp_grad_store_bytes(two, 2, B, 48, D.DP_BF16) == 0     # T not a multiple of 32
+    odd = (D.dp_linear_t * 1)(_lin(d_in=300, lda=300, d_out=520, ldg=520))  # 600-byte rows
+    assert L.dp_grad_store_bytes(odd, 1, B, T, D.DP_BF16) == 0
+    n2, st = ctypes.c_void_p(1 << 22), ctypes.c_void_p(1 << 24)
+    f = L.dp_ghost_norm_linear_store
+    assert f(two, 2, B, T, D.DP_BF16, n2, 0, st, need - 1, None) == EINVAL
+    assert b"gradient store of" in L.dp_last_error()
+    assert f(two, 2, B, T, D.DP_BF16, None, 0, st, need, None) == EINVAL
+    assert f(two, 2, B, T, D.DP_BF16, n2, 0, ctypes.c_void_p((1 << 24) + 8), need, None) == EINVAL
+    assert b"16-byte" in L.dp_last_error()
+    assert f(two, 2, B, T, D.DP_F32, n2, 0, st, need, None) == EUNSUP
+    assert f(odd, 1, B, T, D.DP_BF16, n2, 0, st, need, None) == EUNSUP
+    assert b"16-byte aligned rows" in L.dp_last_error()
+    g = L.dp_clipped_grad_sum_noised_store
+    outs = (ctypes.c_void_p * 2)(1 << 26, 1 << 27)
+    tids = (ctypes.c_uint64 * 2)(1, 2)
+    c = ctypes.c_void_p(1 << 23)
+    tiles_bytes = B * tiles * 256 * 256 * 4                  # the sum reads the tiles only
+    args = (two, outs, tids, None, 2, c, B, T, D.DP_BF16, 0, 1.0, 1.0, B, 7, 0)
+    assert g(*args, st, tiles_bytes - 1, None) == EINVAL
+    assert g(two, None, tids, None, 2, c, B, T, D.DP_BF16, 0, 1.0, 1.0, B, 7, 0, st,
+             tiles_bytes, None) == EINVAL
+    assert g(two, outs, tids, None, 2, c, B, T, D.DP_BF16, 0, -1.0, 1.0, B, 7, 0, st,
+             tiles_bytes, None) == EINVAL                     # sigma < 0
+    assert g(two, outs, tids, None, 2, c, B, T, D.DP_F32, 0, 1.0, 1.0, B, 7, 0, st,
+             tiles_bytes, None) == EUNSUP
+    big = (ctypes.c_uint64 * 2)(1, 1 << 32)
+    assert g(two, outs, big, None, 2, c, B, T, D.DP_BF16, 0, 1.0, 1.0, B, 7, 0, st,
+             tiles_bytes, None) == EINVAL
 
 
 def test_linear_norm_rejects_bad_arguments(L):
