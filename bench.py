@@ -75,6 +75,9 @@ def parse(argv=None):
     ap.add_argument("--crossover", action="store_true",
                     help="instead of the step: time each distinct layer shape's grouped norm "
                          "with the Gram kernel and with the direct kernel (one JSON line)")
+    ap.add_argument("--no-grad-store", action="store_true",
+                    help="form the clipped sums by the GEMM even where every norm layer takes "
+                         "the direct form (default: from the per-example gradient store)")
     ap.add_argument("--crossover-shape", default=None, metavar="B,T",
                     help="with --crossover: the workload's layer shapes at this batch size and "
                          "sequence length instead of its own")
@@ -100,9 +103,12 @@ def round_up(x, m):
 
 
 class Step:
-    """Device inputs, outputs and the prepared calls of one DP-SGD step."""
+    """Device inputs, outputs and the prepared calls of one DP-SGD step.
+    grad_store: when every norm layer takes the direct form, keep the
+    examples' gradient tiles in HBM and form the clipped sums from them
+    (dp_ghost_norm_linear_store, dp_clipped_grad_sum_noised_store)."""
 
-    def __init__(self, wl, dp, torch):
+    def __init__(self, wl, dp, torch, grad_store=True):
         self.wl, self.dp, self.torch = wl, dp, torch
         B, T = wl.B, wl.T
         def dev(a):  # bf16 bit patterns or fp32 values
@@ -250,6 +256,24 @@ class Step:
             else:
                 self.norm_flops += float(B) * T * (T + 1) * (di + do)
         self.step_id = 0
+        # Long sequences: every norm layer takes the direct form, which forms
+        # each example's gradient tiles anyway. Kept in HBM (B * tiles * 256 KB,
+        # 7.9 GB for GPT-2 small at B = 16) they give the clipped sums as a
+        # weighted sum instead of a second GEMM. The norm table is the sum
+        # table: the linears' outputs [d_in, d_out], a head (H, Gz) written
+        # transposed into its [V, d] matrix.
+        self.store = None
+        if grad_store and self.norm_direct == len(norm_layers) and not self.n_fused_biases:
+            nbytes = self.norm_group.store_bytes()
+            free, _ = torch.cuda.mem_get_info()
+            if nbytes and nbytes < 0.8 * free:
+                self.store = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+                head = h is not None and h.H is not None
+                self.norm_group.set_outputs(list(self.outs) + ([self.W] if head else []))
+                self.store_tr = [False] * len(self.lin) + ([True] if head else [])
+                tiles = sum(-(-a.shape[2] // 256) * -(-g.shape[2] // 256) for a, g in norm_layers)
+                self.store_bytes_read = float(B) * tiles * 256 * 256 * 4
+                self.store_out_bytes = 4.0 * sum(a.shape[2] * g.shape[2] for a, g in norm_layers)
 
     def total_norm2(self):
         """Per-example squared norms of the last step (both parts summed)."""
@@ -280,7 +304,10 @@ class Step:
                 if self.P is not None:
                     dp.dp_ghost_norm_positional(self.dE, self.n2b, accumulate=acc)
             self.ev_norms.record(self.side)
-        self.norm_group.ghost_norm(self.n2, accumulate=False)
+        if self.store is not None:
+            self.norm_group.ghost_norm_store(self.n2, self.store)
+        else:
+            self.norm_group.ghost_norm(self.n2, accumulate=False)
         mark("norms")
         if self.side_norms:
             main.wait_event(self.ev_norms)
@@ -311,9 +338,15 @@ class Step:
                 if self.emb_rows is not None:
                     self.emb_rows.compute(self.dE, self.ids, self.c_b)
             self.ev_side.record(self.side)
-        for grp, tids in self.sum_groups:
-            grp.clipped_sum_noised(self.c, tids, wl.sigma, wl.C, wl.B, **kw)
+        if self.store is not None:
+            self.norm_group.clipped_sum_noised_store(self.c, self.store, self.sum_tids, wl.sigma,
+                                                     wl.C, wl.B, transpose_out=self.store_tr,
+                                                     **kw)
             mark("clipped_sum_noise")
+        else:
+            for grp, tids in self.sum_groups:
+                grp.clipped_sum_noised(self.c, tids, wl.sigma, wl.C, wl.B, **kw)
+                mark("clipped_sum_noise")
         if self.side_sums:
             main.wait_event(self.ev_side)
             mark("side_sums_join")
@@ -502,15 +535,29 @@ def rooflines(st, gemm_us, phase_us):
     the Gram form and against the MFMA peak when every layer takes the direct
     form."""
     peak = PEAK_BF16_TFLOPS if st.wl.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS
-    achieved = st.gemm_flops / (gemm_us * 1e-6) / 1e12
-    gemm = {"bound": "mfma", "kernel": "dl_gemm_kernel (clipped sum with fused noise)",
-            "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-            "timed": "HIP events on the main stream around the grouped clipped-sum call, "
-                     "inside the timed steps: the GEMM launch and the split-tail fix-up "
-                     "kernel that follows it (~16 us at the GPT-2 step), beside the second "
-                     "stream's embedding rows",
-            "algorithmic_flop_per_launch": st.gemm_flops,
-            "algorithmic_bytes_per_launch": st.gemm_bytes}
+    if st.store is not None:
+        # the clipped sums from the per-example gradient store: read every
+        # example's tiles once, write every output once
+        q = st.store_bytes_read + st.store_out_bytes
+        achieved = q / (gemm_us * 1e-6) / 1e9
+        gemm = {"bound": "hbm", "kernel": "store_sum_kernel (clipped sums from the per-example "
+                                          "gradient store, noise fused)",
+                "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS,
+                "timed": "HIP events on the main stream around the clipped-sum call, inside "
+                         "the timed steps (one launch), beside the second stream's sums",
+                "algorithmic_flop_per_launch": st.gemm_flops,
+                "algorithmic_bytes_per_launch": q}
+    else:
+        achieved = st.gemm_flops / (gemm_us * 1e-6) / 1e12
+        gemm = {"bound": "mfma", "kernel": "dl_gemm_kernel (clipped sum with fused noise)",
+                "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+                "timed": "HIP events on the main stream around the grouped clipped-sum call, "
+                         "inside the timed steps: the GEMM launch and the split-tail fix-up "
+                         "kernel that follows it (~16 us at the GPT-2 step), beside the second "
+                         "stream's embedding rows",
+                "algorithmic_flop_per_launch": st.gemm_flops,
+                "algorithmic_bytes_per_launch": st.gemm_bytes}
     norm_us = phase_us["norms"]
     n_layers = len(st.norm_layers)
     if st.norm_direct == n_layers:
@@ -522,7 +569,9 @@ def rooflines(st, gemm_us, phase_us):
         norm = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": ach / PEAK_HBM_GBS}
     norm.update({"kernel": f"grouped norm launch ({n_layers - st.norm_direct} Gram, "
-                           f"{st.norm_direct} direct layers)",
+                           f"{st.norm_direct} direct layers"
+                           + (", each example's gradient tiles written to the store)"
+                              if st.store is not None else ")"),
                  "timed": "the norms phase of the phase-marked steps",
                  "algorithmic_bytes_per_launch": st.norm_bytes,
                  "algorithmic_flop_per_launch": st.norm_flops})
@@ -568,7 +617,7 @@ def main(argv=None) -> int:
         t0 = time.perf_counter()
         wl = gen.make_workload(name, seed=args.seed, ldz=ldz, **bt)
         log(f"[bench] generated {name}: {wl.description} in {time.perf_counter() - t0:.1f}s")
-        return wl, Step(wl, dp, torch)
+        return wl, Step(wl, dp, torch, grad_store=not args.no_grad_store)
 
     wl, st = load(args.workload)
     log(f"[bench] {len(wl.linears)} linear layers, head={'none' if wl.head is None else ('tied' if wl.head.tied else 'untied')}, "
@@ -589,13 +638,14 @@ def main(argv=None) -> int:
     for k, v in phase_us.items():
         log(f"[bench]   {k:16s} {v:9.1f} us")
     gemm_rf, norm_rf = rooflines(st, gemm_us, phase_us)
-    gemm_rf["traffic"] = gemm_traffic()
+    gemm_rf["traffic"] = gemm_traffic() if args.workload == "gpt2-step" and st.store is None \
+        else None
     gemm_rf["traffic_source"] = (
-        "rocprofv3 FETCH_SIZE and WRITE_SIZE of this kernel source at this workload, scaled "
-        "by a 1 GiB copy (profiles/hbm_traffic_gpt2_step_B32_T128.md); null when the source "
-        "differs from the one measured")
-    log(f"[bench] clipped-sum GEMM {st.gemm_flops / 1e9:.1f} GFLOP in {gemm_us:.1f} us = "
-        f"{gemm_rf['achieved']:.1f} TFLOP/s ({gemm_rf['frac']:.3f}); grouped norm "
+        "rocprofv3 FETCH_SIZE and WRITE_SIZE of this kernel source at the GPT-2 step, scaled "
+        "by a 1 GiB copy (profiles/hbm_traffic_gpt2_step_B32_T128.md); null for another "
+        "workload or when the source differs from the one measured")
+    log(f"[bench] clipped sum ({gemm_rf['kernel'].split(' ')[0]}) in {gemm_us:.1f} us = "
+        f"{gemm_rf['achieved']:.1f} {gemm_rf['unit']} ({gemm_rf['frac']:.3f}); grouped norm "
         f"{st.norm_bytes / 1e9:.3f} GB in {phase_us['norms']:.1f} us: {norm_rf['frac']:.3f} of "
         f"its {norm_rf['bound']} peak")
 
@@ -631,11 +681,13 @@ def main(argv=None) -> int:
             "workload": wl_c.description, "B": wl_c.B, "T": wl_c.T, "dtype": wl_c.dtype,
             "head": None if hc is None else ("tied" if hc.tied else "untied"),
             "ms_per_step": ms_c, "examples_per_s": wl_c.B / (ms_c / 1e3),
-            "clipped_sum_us": gemm_c, "clipped_sum_mfma_frac": g_c["frac"],
+            "clipped_sum_us": gemm_c, "clipped_sum_form": "gradient store" if st_c.store
+            is not None else "GEMM", "clipped_sum_bound": g_c["bound"],
+            "clipped_sum_frac": g_c["frac"],
             "norms_us": ph_c["norms"], "norms_bound": n_c["bound"], "norms_frac": n_c["frac"],
             "phase_us": {k: round(v, 1) for k, v in ph_c.items()}}
         log(f"[bench] {name}: {ms_c:.3f} ms/step, {wl_c.B / (ms_c / 1e3):.0f} ex/s, clipped sum "
-            f"{gemm_c:.1f} us ({g_c['frac']:.3f} of MFMA), norms {ph_c['norms']:.1f} us "
+            f"{gemm_c:.1f} us ({g_c['frac']:.3f} of {g_c['bound']}), norms {ph_c['norms']:.1f} us "
             f"({n_c['frac']:.3f} of {n_c['bound']})")
         del st_c, wl_c
         torch.cuda.empty_cache()

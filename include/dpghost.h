@@ -368,10 +368,12 @@ dp_status_t dp_clipped_grad_sum_noised_grouped_ws(const dp_linear_t* layers, flo
  * ||A_b^T G_b||_F^2, every layer by the direct form whatever its algo field
  * (bit-identical to dp_ghost_norm_linear_grouped with DP_NORM_DIRECT), and
  * the tiles into the store.
- * dp_clipped_grad_sum_noised_store: outs, tensor_ids, accumulate, the noise
- * arguments and the output layouts as for dp_clipped_grad_sum_noised_grouped;
- * layers must be the table the store was written with (its pointers are not
- * read again, only its shapes). store: device memory owned by the caller,
+ * dp_clipped_grad_sum_noised_store: outs, tensor_ids, accumulate and the
+ * noise arguments as for dp_clipped_grad_sum_noised_grouped; the output
+ * layout is chosen per layer: transpose_out[l] != 0 writes outs[l] as
+ * [d_out, d_in] (transpose_out may be NULL: all [d_in, d_out]; a host array
+ * of n_layers entries, like accumulate). layers must be the table the store
+ * was written with (its pointers are not read again, only its shapes). store: device memory owned by the caller,
  * 16-byte aligned, at least dp_grad_store_bytes() bytes (the sum reads the
  * tiles only); it holds one step's tiles until the next store call.
  * ------------------------------------------------------------------- */
@@ -382,10 +384,11 @@ dp_status_t dp_ghost_norm_linear_store(const dp_linear_t* layers, int n_layers, 
                                        size_t store_bytes, void* stream);
 dp_status_t dp_clipped_grad_sum_noised_store(const dp_linear_t* layers, float* const* outs,
                                              const uint64_t* tensor_ids,
-                                             const int32_t* accumulate, int n_layers,
+                                             const int32_t* accumulate,
+                                             const int32_t* transpose_out, int n_layers,
                                              const float* c, int B, int T, dp_dtype_t dt,
-                                             int transpose_out, float sigma, float C, int B_norm,
-                                             uint64_t seed, uint64_t step, const void* store,
+                                             float sigma, float C, int B_norm, uint64_t seed,
+                                             uint64_t step, const void* store,
                                              size_t store_bytes, void* stream);
 
 /* ---------------------------------------------------------------------

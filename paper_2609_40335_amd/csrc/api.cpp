@@ -1018,10 +1018,11 @@ dp_status_t dp_ghost_norm_linear_store(const dp_linear_t* layers, int n_layers, 
 
 dp_status_t dp_clipped_grad_sum_noised_store(const dp_linear_t* layers, float* const* outs,
                                              const uint64_t* tensor_ids,
-                                             const int32_t* accumulate, int n_layers,
+                                             const int32_t* accumulate,
+                                             const int32_t* transpose_out, int n_layers,
                                              const float* c, int B, int T, dp_dtype_t dt,
-                                             int transpose_out, float sigma, float C, int B_norm,
-                                             uint64_t seed, uint64_t step, const void* store,
+                                             float sigma, float C, int B_norm, uint64_t seed,
+                                             uint64_t step, const void* store,
                                              size_t store_bytes, void* stream) {
   if (!outs || !c || !tensor_ids) return fail(DP_EINVAL, "outs, c or tensor_ids is NULL");
   std::vector<GemmEntry> entries;
@@ -1040,7 +1041,7 @@ dp_status_t dp_clipped_grad_sum_noised_store(const dp_linear_t* layers, float* c
     if (tensor_ids[i] >> 32) return fail(DP_EINVAL, "tensor_ids[%d] must be < 2^32", i);
     GemmEntry& e = entries[i];
     e.out = outs[i];
-    e.ldo = transpose_out ? layers[i].d_in : layers[i].d_out;
+    e.ldo = transpose_out && transpose_out[i] ? layers[i].d_in : layers[i].d_out;
     e.acc = accumulate && accumulate[i] ? 1 : 0;
     e.tensor_id = (uint32_t)tensor_ids[i];
   }
@@ -1049,7 +1050,6 @@ dp_status_t dp_clipped_grad_sum_noised_store(const dp_linear_t* layers, float* c
     const size_t n = std::min(entries.size() - i0, (size_t)dpg::GM_MAX_LAYERS);
     dpg::GemmArgs a{};
     a.B = B; a.T = T; a.c = c;
-    a.transpose = transpose_out ? 1 : 0;
     a.noise = 1;
     a.sigma_c = (float)((double)sigma * (double)C);
     a.inv_b = B_norm > 0 ? (float)(1.0 / (double)B_norm) : 1.f;
@@ -1063,6 +1063,7 @@ dp_status_t dp_clipped_grad_sum_noised_store(const dp_linear_t* layers, float* c
       dpg::GemmLayer& L = a.L[j];
       L.X = nullptr; L.Y = nullptr;
       L.store_slot = e.slot_begin;
+      L.store_transpose = transpose_out && transpose_out[i0 + j] ? 1 : 0;
       L.M = e.M; L.N = e.N;
       L.tm = (uint16_t)e.tm; L.tn = (uint16_t)e.tn;
       L.tile_begin = (uint32_t)items;

@@ -186,7 +186,7 @@ __device__ __forceinline__ float noise_at(const GemmArgs& a, uint32_t tid, uint6
 
 __device__ __forceinline__ void store_tile(const GemmArgs& a, const GemmLayer& L, int64_t m0,
                                            int64_t n0, int wm, int wn, int lane,
-                                           f32x16 (&acc)[4][2]) {
+                                           f32x16 (&acc)[4][2], bool transposed) {
   float* out = L.out;
   const int64_t ldo = L.ldo;
   const bool accum = L.accumulate != 0;
@@ -195,7 +195,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const GemmLayer& L
   const int mw = (int)m0 + wm * 128 + (lane >> 5) * 4;  // row of e = 0 in block i = 0
   const int nw = (int)n0 + wn * 64 + (lane & 31);         // column in block j = 0
   const bool full = m0 + GM_BM <= L.M && n0 + GM_BN <= L.N;
-  if (a.transpose) {
+  if (transposed) {
     // out[n][m]: the 4 accumulators e = 4g..4g+3 are 4 consecutive rows m.
     const bool vec4 = full && (ldo & 3) == 0 && (((uintptr_t)out) & 15) == 0 &&
                       (!noise || (L.M & 3) == 0);
@@ -580,7 +580,7 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
   }
 
   if constexpr (MODE == MODE_SUM) {
-    store_tile(a, L, m0, n0, wm, wn, lane, acc);
+    store_tile(a, L, m0, n0, wm, wn, lane, acc, a.transpose != 0);
   } else {
     float part = 0.f;
 #pragma unroll
@@ -1034,7 +1034,7 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
       store_partial(a.part + ((size_t)(item - a.n_full) * a.ksplit + kc) * (GM_BM * GM_BN),
                     wm, wn, lane, acc, slice);
     } else if (a.transpose) {
-      store_tile(a, L, m0, n0, wm, wn, lane, acc);
+      store_tile(a, L, m0, n0, wm, wn, lane, acc, true);
     } else {
       // The ring is free once every wave is past its last read of it.
       __syncthreads();
@@ -1058,8 +1058,8 @@ __global__ __launch_bounds__(GM_THREADS) void dl_gemm_kernel(GemmArgs args) {
 // added): one workgroup per output tile, its 8 waves in the register layout
 // of dl_gemm_kernel, acc = sum_e c_e tile_e in example order (examples with
 // c_e = 0 are left out, as in the GEMM), then the GEMM's own epilogue (prior,
-// fused noise, 1/B, row-major or transposed store). HBM-bound: B tiles read
-// per output tile.
+// fused noise, 1/B; row-major, or transposed per layer). HBM-bound: B tiles
+// read per output tile.
 __global__ __launch_bounds__(GM_THREADS) void store_sum_kernel(GemmArgs args) {
   const GemmArgs& a = *(const GemmArgs*)__builtin_amdgcn_kernarg_segment_ptr();
   (void)args;
@@ -1109,8 +1109,8 @@ __global__ __launch_bounds__(GM_THREADS) void store_sum_kernel(GemmArgs args) {
               acc[2 * hh + ii][j][4 * q + r] = fmaf(ce, v[ii][j][q][r], acc[2 * hh + ii][j][4 * q + r]);
     }
   }
-  if (a.transpose) {
-    store_tile(a, L, m0, n0, wm, wn, lane, acc);
+  if (L.store_transpose) {
+    store_tile(a, L, m0, n0, wm, wn, lane, acc, true);
   } else {
     float* slice = (float*)stage + w * 32 * EP_LD;
     store_tile_rows(a, L, m0, n0, wm, wn, lane, acc, slice);

@@ -105,7 +105,11 @@ struct GemmLayer {
     int64_t ldx;          // row stride of X in elements
     int64_t store_slot;   // sum from a gradient store (X, Y unread): first tile slot
   };
-  int64_t ldy, ldo;     // row strides in elements
+  union {
+    int64_t ldy;          // row stride of Y in elements
+    int64_t store_transpose;  // sum from a gradient store: 1 = output [N, ldo]
+  };
+  int64_t ldo;          // row stride of out in elements
   int32_t M, N;         // X columns (output rows) and Y columns (output columns)
   uint16_t tm, tn;      // 256-wide tiles along M and N
   uint32_t tile_begin;  // first work item of this entry

@@ -106,8 +106,8 @@ _SIGS = {
                                     _SZ, _VP], _I),
     "dp_clipped_grad_sum_noised_store": ([ctypes.POINTER(dp_linear_t), ctypes.POINTER(_VP),
                                           ctypes.POINTER(_U64), ctypes.POINTER(ctypes.c_int32),
-                                          _I, _VP, _I, _I, _I, _I, _F, _F, _I, _U64, _U64,
-                                          _VP, _SZ, _VP], _I),
+                                          ctypes.POINTER(ctypes.c_int32), _I, _VP, _I, _I, _I,
+                                          _F, _F, _I, _U64, _U64, _VP, _SZ, _VP], _I),
     "dp_clip_factors_scaled": ([_VP, _I, _F, _F, _VP, _VP, _VP], _I),
     "dp_clip_factors_scaled2": ([_VP, _VP, _I, _F, _F, _VP, _VP, _VP], _I),
     "dp_noise_fill": ([_VP, _I64, _F, _F, _I, _U64, _U64, _U64, _VP], _I),
@@ -659,21 +659,32 @@ def dp_ghost_norm_linear_store(layers: Sequence, norm2: torch.Tensor, store: tor
     return norm2
 
 
+def _flags(n: int, flags, what: str):
+    """A bool for every layer, or one bool per layer, as a ctypes int32 array."""
+    if flags is None or isinstance(flags, (bool, int)):
+        return (ctypes.c_int32 * n)(*([int(bool(flags))] * n))
+    if len(flags) != n:
+        raise DPError(f"one {what} flag per layer")
+    return (ctypes.c_int32 * n)(*[int(bool(f)) for f in flags])
+
+
 def dp_clipped_grad_sum_noised_store(layers: Sequence, outs: Sequence[torch.Tensor], c,
                                      tensor_ids: Sequence[int], sigma: float, C: float,
                                      B_norm: int, seed: int, step: int, store: torch.Tensor,
-                                     accumulate=None, transpose_out: bool = False,
+                                     accumulate=None, transpose_out=False,
                                      stream=None) -> None:
     """The noised clipped sums from the tiles dp_ghost_norm_linear_store kept
-    for the same layers."""
+    for the same layers. ``accumulate`` and ``transpose_out`` are a bool or
+    one bool per layer."""
     descs = [_layer(l[0], l[1]) for l in layers]
     arr = (dp_linear_t * len(descs))(*descs)
     optrs = (ctypes.c_void_p * len(outs))(*[o.data_ptr() for o in outs])
     tids, acc = _noise_arrays(len(descs), tensor_ids, accumulate)
+    tr = _flags(len(descs), transpose_out, "transpose")
     A0 = layers[0][0]
-    _check(lib().dp_clipped_grad_sum_noised_store(arr, optrs, tids, acc, len(descs), c.data_ptr(),
-                                                  A0.shape[0], A0.shape[1], _dtype(A0),
-                                                  int(transpose_out), float(sigma), float(C),
+    _check(lib().dp_clipped_grad_sum_noised_store(arr, optrs, tids, acc, tr, len(descs),
+                                                  c.data_ptr(), A0.shape[0], A0.shape[1],
+                                                  _dtype(A0), float(sigma), float(C),
                                                   int(B_norm), int(seed), int(step),
                                                   store.data_ptr(),
                                                   store.numel() * store.element_size(),
@@ -793,21 +804,25 @@ class LinearGroup:
 
     def clipped_sum_noised_store(self, c: torch.Tensor, store: torch.Tensor,
                                  tensor_ids: Sequence[int], sigma: float, C: float, B_norm: int,
-                                 seed: int, step: int, accumulate=None,
-                                 transpose_out: bool = False, stream=None) -> None:
-        """clipped_sum_noised from the tiles ghost_norm_store kept."""
+                                 seed: int, step: int, accumulate=None, transpose_out=False,
+                                 stream=None) -> None:
+        """clipped_sum_noised from the tiles ghost_norm_store kept;
+        ``transpose_out`` is a bool or one bool per layer."""
         if self.outs is None:
             raise DPError("set_outputs() first")
         key = (tuple(int(t) for t in tensor_ids),
                accumulate if isinstance(accumulate, (bool, int, type(None)))
-               else tuple(bool(a) for a in accumulate))
-        if getattr(self, "_noise_key", None) != key:
-            self._noise_key = key
-            self._noise_arr = _noise_arrays(self.n, tensor_ids, accumulate)
-        tids, acc = self._noise_arr
-        _check(lib().dp_clipped_grad_sum_noised_store(self.descs, self.outs, tids, acc, self.n,
-                                                      c.data_ptr(), self.B, self.T, self.dt,
-                                                      int(transpose_out), float(sigma), float(C),
+               else tuple(bool(a) for a in accumulate),
+               transpose_out if isinstance(transpose_out, (bool, int))
+               else tuple(bool(t) for t in transpose_out))
+        if getattr(self, "_store_key", None) != key:
+            self._store_key = key
+            self._store_arr = (*_noise_arrays(self.n, tensor_ids, accumulate),
+                               _flags(self.n, transpose_out, "transpose"))
+        tids, acc, tr = self._store_arr
+        _check(lib().dp_clipped_grad_sum_noised_store(self.descs, self.outs, tids, acc, tr,
+                                                      self.n, c.data_ptr(), self.B, self.T,
+                                                      self.dt, float(sigma), float(C),
                                                       int(B_norm), int(seed), int(step),
                                                       store.data_ptr(),
                                                       store.numel() * store.element_size(),

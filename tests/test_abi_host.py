@@ -151,16 +151,16 @@ def test_grad_store_size_and_argument_checks(L):
     tids = (ctypes.c_uint64 * 2)(1, 2)
     c = ctypes.c_void_p(1 << 23)
     tiles_bytes = B * tiles * 256 * 256 * 4                  # the sum reads the tiles only
-    args = (two, outs, tids, None, 2, c, B, T, D.DP_BF16, 0, 1.0, 1.0, B, 7, 0)
-    assert g(*args, st, tiles_bytes - 1, None) == EINVAL
-    assert g(two, None, tids, None, 2, c, B, T, D.DP_BF16, 0, 1.0, 1.0, B, 7, 0, st,
+    assert g(two, outs, tids, None, None, 2, c, B, T, D.DP_BF16, 1.0, 1.0, B, 7, 0, st,
+             tiles_bytes - 1, None) == EINVAL
+    assert g(two, None, tids, None, None, 2, c, B, T, D.DP_BF16, 1.0, 1.0, B, 7, 0, st,
              tiles_bytes, None) == EINVAL
-    assert g(two, outs, tids, None, 2, c, B, T, D.DP_BF16, 0, -1.0, 1.0, B, 7, 0, st,
+    assert g(two, outs, tids, None, None, 2, c, B, T, D.DP_BF16, -1.0, 1.0, B, 7, 0, st,
              tiles_bytes, None) == EINVAL                     # sigma < 0
-    assert g(two, outs, tids, None, 2, c, B, T, D.DP_F32, 0, 1.0, 1.0, B, 7, 0, st,
+    assert g(two, outs, tids, None, None, 2, c, B, T, D.DP_F32, 1.0, 1.0, B, 7, 0, st,
              tiles_bytes, None) == EUNSUP
     big = (ctypes.c_uint64 * 2)(1, 1 << 32)
-    assert g(two, outs, big, None, 2, c, B, T, D.DP_BF16, 0, 1.0, 1.0, B, 7, 0, st,
+    assert g(two, outs, big, None, None, 2, c, B, T, D.DP_BF16, 1.0, 1.0, B, 7, 0, st,
              tiles_bytes, None) == EINVAL
 
 

@@ -62,10 +62,17 @@ CASES = [
     ("gpt2-full", dict(B=4, T=32, n_blocks=1, V=4000, ldz=4032)),     # bf16, tied, every parameter
     ("c5", dict(B=2, T=64, n_blocks=1, V=3000, ldz=3008)),            # bf16, untied head + E_in
     ("c4", dict(B=3, T=256, n_blocks=1, V=3000, ldz=3008)),           # bf16, T = 256 whole-example Gram
+    # d = 64: every layer takes the direct norm at T = 64, so the step keeps the
+    # examples' gradient tiles and forms the clipped sums from them
+    ("c5", dict(B=3, T=64, n_blocks=1, V=3000, ldz=3008, d=64)),
 ]
 
 
-@pytest.mark.parametrize("name,kw", CASES, ids=[c[0] for c in CASES])
+def _case_id(c):
+    return c[0] + ("-store" if c[1].get("d") == 64 else "")
+
+
+@pytest.mark.parametrize("name,kw", CASES, ids=[_case_id(c) for c in CASES])
 def test_bench_step_matches_oracle(parts, name, kw):
     bench, dp = parts
     _say(f"bench step {name} {kw}")
@@ -91,10 +98,12 @@ NONFINITE_CASES = [
     ("gpt2-full", dict(B=4, T=32, n_blocks=1, V=4000, ldz=4032)),   # direct-load GEMM, split tail
     ("gpt2-full", dict(B=4, T=40, n_blocks=1, V=4000, ldz=4032)),   # rows scaled while staged
     ("c1-tied", dict(full_params=True)),                              # fp32
+    ("c5", dict(B=4, T=64, n_blocks=1, V=3000, ldz=3008, d=64)),      # per-example gradient store
 ]
 
 
-@pytest.mark.parametrize("name,kw", NONFINITE_CASES, ids=["T32", "T40", "c1-tied-f32"])
+@pytest.mark.parametrize("name,kw", NONFINITE_CASES,
+                         ids=["T32", "T40", "c1-tied-f32", "c5-store"])
 def test_nonfinite_example_left_out(parts, name, kw):
     """One NaN activation in example 1 and one inf embedding-output gradient
     in example 2: their squared norms are not finite, their clip factors are

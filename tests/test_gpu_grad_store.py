@@ -42,8 +42,10 @@ CASES = [
     (5, 64, [(300, 520, 304, 520), (256, 256, 256, 256)], [0.5, 0.0, 1.0, 0.25, 0.7]),
     # 32 stages per example, two examples per work item (boundaries inside the K loop)
     (45, 1024, [(300, 520, 304, 520)], None),
-    # two 52-layer launches' worth of tables is not needed; three layers of mixed shapes
+    # three layers of mixed shapes, 136-feature rows
     (3, 96, [(64, 768, 64, 768), (768, 64, 768, 64), (128, 136, 136, 136)], None),
+    # 53 layers: two launches of the layer table, store slots numbered across them
+    (2, 64, [(64, 72, 64, 72)] * 53, None),
 ]
 
 
@@ -59,9 +61,11 @@ def _case_inputs(B, T, shapes, seed):
     return layers_np, layers
 
 
-@pytest.mark.parametrize("transpose", [False, True])
+@pytest.mark.parametrize("transpose", [False, True, "mixed"])
 @pytest.mark.parametrize("case", CASES, ids=lambda c: f"B{c[0]}-T{c[1]}-{len(c[2])}layers")
 def test_store_norms_and_noised_sums(dp, case, transpose):
+    """transpose: every output [d_in, d_out], every one [d_out, d_in], or the
+    layers alternating (the layout is chosen per layer)."""
     B, T, shapes, c = case
     c = np.linspace(0.3, 1.0, B) if c is None else np.asarray(c)
     c = c.astype(np.float32)
@@ -85,17 +89,19 @@ def test_store_norms_and_noised_sums(dp, case, transpose):
     sigma, C, seed, step = 0.7, 0.9, 0xBEEF, 5
     tids = [3 + l for l in range(len(shapes))]
     acc = [l % 2 == 1 for l in range(len(shapes))]
+    tr = [l % 2 == 1 for l in range(len(shapes))] if transpose == "mixed" \
+        else [transpose] * len(shapes)
     sums, priors = [], []
     for l, (A, G) in enumerate(layers_np):
         S = O.clipped_sum_linear(A, G, c.astype(np.float64))
-        sums.append(S.T if transpose else S)
+        sums.append(S.T if tr[l] else S)
         priors.append(gen.draw(90 + l, 3, sums[-1].shape, 1e-2, "f32") if acc[l]
                       else np.zeros(sums[-1].shape, np.float32))
 
     # without noise (sigma = 0, B_norm = 0): the sums themselves
     outs0 = [dev(p.copy()) for p in priors]
     dp.dp_clipped_grad_sum_noised_store(layers, outs0, dev(c), tids, 0.0, C, 0, seed, step,
-                                        store, accumulate=acc, transpose_out=transpose)
+                                        store, accumulate=acc, transpose_out=tr)
     for l in range(len(shapes)):
         err = assert_close(host(outs0[l]), priors[l].astype(np.float64) + sums[l], TOL["bf16"],
                            f"layer {l} sum")
@@ -104,10 +110,12 @@ def test_store_norms_and_noised_sums(dp, case, transpose):
     # with noise: the oracle's add_noise(prior + sum), and the GEMM form's output
     outs = [dev(p.copy()) for p in priors]
     dp.dp_clipped_grad_sum_noised_store(layers, outs, dev(c), tids, sigma, C, B, seed, step,
-                                        store, accumulate=acc, transpose_out=transpose)
+                                        store, accumulate=acc, transpose_out=tr)
     gemm = [dev(p.copy()) for p in priors]
-    dp.dp_clipped_grad_sum_noised_grouped(layers, gemm, dev(c), tids, sigma, C, B, seed, step,
-                                          accumulate=acc, transpose_out=transpose)
+    for l in range(len(shapes)):   # the GEMM form takes one layout per call
+        dp.dp_clipped_grad_sum_noised_grouped([layers[l]], [gemm[l]], dev(c), [tids[l]], sigma,
+                                              C, B, seed, step, accumulate=acc[l],
+                                              transpose_out=tr[l])
     for l in range(len(shapes)):
         ref = O.add_noise(priors[l].astype(np.float64) + sums[l], sigma, C, B, seed, tids[l], step)
         got = host(outs[l])
