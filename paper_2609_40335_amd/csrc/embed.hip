@@ -412,12 +412,14 @@ __global__ __launch_bounds__(EN_THREADS) void embed_norm_runs_kernel(EmbedNormAr
 // a sort: the ids and the rows load together, in position order.
 // Workgroup (b, c) takes features [c' EN_GF, +EN_GF) of example b, with
 // c' = c, or c - 1 when workgroup (b, 0) ranks the ids (dispatched first).
-// Wave i loads rows 32i .. 32i+31 straight into MFMA operand fragments (lane
-// l: row l % 32, features 16k + 8 (l / 32) .. +7 of step k; the A operand of
-// E_i E_j^T and the B operand of E_j E_i^T have this same layout, so every
-// product pairs equal features), stages them in LDS, and multiplies its block
-// with every row block j; the pairs (t, s) with equal ids are summed. Rows at
-// or past T load as zeros (buffer bounds), features at or past d are zeroed.
+// Wave (i, g) of 8 (row block i of 32 rows, g = 0, 1): the g = 0 waves load
+// rows 32i .. 32i+31 straight into MFMA operand fragments (lane l: row l % 32,
+// features 16k + 8 (l / 32) .. +7 of step k; the A operand of E_i E_j^T and
+// the B operand of E_j E_i^T have this same layout, so every product pairs
+// equal features) and stage them in LDS; wave (i, g) multiplies block i with
+// the column blocks j = g, g + 2, ...; the pairs (t, s) with equal ids are
+// summed. Rows at or past T load as zeros (buffer bounds), features at or past
+// d are zeroed.
 // Workgroup (b, 0), when buckets are asked for: each token's bucket (the
 // rank of its id among the example's distinct ids) from pairwise
 // comparisons, and the number of buckets.
@@ -428,7 +430,7 @@ constexpr int EG_JG = EG_NW / EG_NB;      // waves per row block, each over ever
 constexpr int EG_KS = EN_GF / 16;         // 16-feature steps per workgroup
 constexpr int EG_LPT = EG_THREADS / EN_G_T;  // lanes per token when ranking ids
 static_assert(EG_NB * EG_JG == EG_NW, "waves split evenly over the row blocks");
-static_assert(EG_LPT == 4, "ranking: four lanes per token, halves met by two shuffles");
+static_assert(EG_LPT == 4, "ranking: four lanes per token, quarters met by two shuffles");
 
 __global__ __launch_bounds__(EG_THREADS) void embed_norm_gram_kernel(EmbedNormArgs a) {
   __shared__ u32x4 frag[EG_NB][EG_KS][WAVE];
