@@ -304,6 +304,13 @@ class Step:
                 if self.P is not None:
                     dp.dp_ghost_norm_positional(self.dE, self.n2b, accumulate=acc)
             self.ev_norms.record(self.side)
+            if h is not None and not self.tied:
+                # An untied embedding's noise needs no clip factor: it is written
+                # beside the norm launch (after the event the clip waits for),
+                # and its clipped sum follows on the same stream.
+                with self.torch.cuda.stream(self.side):
+                    dp.dp_noise_fill(self.E, wl.sigma, wl.C, wl.B, tensor_id=self.e_tid,
+                                     seed=1234, step=self.step_id)
         if self.store is not None:
             self.norm_group.ghost_norm_store(self.n2, self.store)
         else:
@@ -324,7 +331,6 @@ class Step:
             self.side.wait_event(self.ev_clip)
             with self.torch.cuda.stream(self.side):
                 if h is not None and not self.tied:
-                    dp.dp_noise_fill(self.E, wl.sigma, wl.C, wl.B, tensor_id=self.e_tid, **kw)
                     dp.dp_clipped_grad_sum(None, self.dE, self.c_b, self.E, ids=self.ids, V=h.V,
                                            accumulate=True)
                 if self.vsum is not None:
