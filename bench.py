@@ -29,6 +29,7 @@ line; per-phase times go to stderr.
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -496,6 +497,18 @@ def timed_run(st, torch, steps, warmup):
     for _ in range(warmup):
         st.run()
     torch.cuda.synchronize()
+    # No garbage collection inside the timed steps: a full pass over this
+    # process's objects stalls the host for tens of milliseconds, and early in
+    # the loop the host is only a step ahead of the GPU, so the GPU would idle.
+    gc.collect()
+    gc.disable()
+    try:
+        return _timed(st, torch, steps)
+    finally:
+        gc.enable()
+
+
+def _timed(st, torch, steps):
     stream = torch.cuda.current_stream()
     ev = []
 
