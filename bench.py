@@ -494,21 +494,15 @@ def timed_run(st, torch, steps, warmup):
     only the two events around the clipped-sum launch inside them; then up to
     10 more steps with every phase marked. Returns (ms per step, clipped-sum
     launch us, {phase: us})."""
+    # A full garbage collection first, so that none falls due in the steps
+    # below: a full pass over this process's objects stalls the host for tens
+    # of milliseconds, and early in the timed loop the host is only a step
+    # ahead of the GPU, which would idle. It runs before the warm-up, because
+    # the GPU lowers its clock while idle and the warm-up brings it back.
+    gc.collect()
     for _ in range(warmup):
         st.run()
     torch.cuda.synchronize()
-    # No garbage collection inside the timed steps: a full pass over this
-    # process's objects stalls the host for tens of milliseconds, and early in
-    # the loop the host is only a step ahead of the GPU, so the GPU would idle.
-    gc.collect()
-    gc.disable()
-    try:
-        return _timed(st, torch, steps)
-    finally:
-        gc.enable()
-
-
-def _timed(st, torch, steps):
     stream = torch.cuda.current_stream()
     ev = []
 
