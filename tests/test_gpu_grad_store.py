@@ -85,6 +85,10 @@ def test_store_norms_and_noised_sums(dp, case, transpose):
     ref_n2 = sum(O.linear_norm2(A, G) for A, G in layers_np)
     _say(f"  norms max rel err {rel(host(n2), ref_n2).max():.3e}")
     assert rel(host(n2), ref_n2).max() <= TOL["bf16"]
+    # accumulate adds onto what is there (and rewrites the same tiles)
+    n2a = n2.clone()
+    dp.dp_ghost_norm_linear_store(layers, n2a, store, accumulate=True)
+    assert rel(host(n2a), 2 * ref_n2).max() <= TOL["bf16"]
 
     sigma, C, seed, step = 0.7, 0.9, 0xBEEF, 5
     tids = [3 + l for l in range(len(shapes))]

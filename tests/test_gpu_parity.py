@@ -217,6 +217,14 @@ def test_embedding_norm_pairwise_form(dp, kind, B, T, V, d, lde):
     # without buckets (no ranking workgroup), accumulating onto what is there
     dp.dp_ghost_norm_embedding(dev(ids), dEd, V, n2, accumulate=True)
     assert rel(host(n2), 2 * ref).max() <= TOL["bf16"]
+    # one of the two bucket outputs alone
+    seg2 = torch.full((B, T), -1, dtype=torch.int32, device="cuda")
+    dp.dp_ghost_norm_embedding(dev(ids), dEd, V, n2, seg_id=seg2)
+    np.testing.assert_array_equal(host(seg2), seg_ref)
+    nu2 = torch.zeros(B, dtype=torch.int32, device="cuda")
+    dp.dp_ghost_norm_embedding(dev(ids), dEd, V, n2, n_unique=nu2)
+    np.testing.assert_array_equal(host(nu2), nu_ref)
+    assert rel(host(n2), ref).max() <= TOL["bf16"]
 
 
 # ---------------------------------------------------------------------------
