@@ -160,6 +160,11 @@ def test_embedding_special_cases():
     dE3 = _rand(3, T, d)
     onehot = np.eye(V)[ids]
     np.testing.assert_allclose(O.embedding_norm2(ids, dE3, V), O.linear_norm2(onehot, dE3), rtol=1e-12)
+    # ... so, written out pairwise (the form the short-example kernel sums):
+    # sum_{t,s} [x_t = x_s] <e_t, e_s>
+    pair = np.array([sum(float(dE3[i, t] @ dE3[i, u]) for t in range(T) for u in range(T)
+                         if ids[i, t] == ids[i, u]) for i in range(3)])
+    np.testing.assert_allclose(O.embedding_norm2(ids, dE3, V), pair, rtol=1e-12)
 
 
 def test_head_is_linear_layer_d_to_V():
