@@ -47,8 +47,8 @@ PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
 # HBM bytes per launch of the clipped-sum kernel: rocprofv3 FETCH_SIZE x 2 +
 # WRITE_SIZE x 1 (factors from a plain 1 GiB copy), recorded for the kernel
 # source with this SHA-256; any other source reports null.
-GEMM_TRAFFIC = {"gemm.hip sha256": "4a439936d7c39c0d0ae4fe6f7afe7e614709f9ecd236e6d365801f1809f41183",
-                "bytes": 2697582373}
+GEMM_TRAFFIC = {"gemm.hip sha256": "96d562c289fb13693e63dad4ba0cf414f31125565fdae8be0b096701fa25c151",
+                "bytes": 2697373696}
 
 
 def log(*a):
