@@ -47,8 +47,8 @@ PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
 # HBM bytes per launch of the clipped-sum kernel: rocprofv3 FETCH_SIZE x 2 +
 # WRITE_SIZE x 1 (factors from a plain 1 GiB copy), recorded for the kernel
 # source with this SHA-256; any other source reports null.
-GEMM_TRAFFIC = {"gemm.hip sha256": "96d562c289fb13693e63dad4ba0cf414f31125565fdae8be0b096701fa25c151",
-                "bytes": 2697373696}
+GEMM_TRAFFIC = {"gemm.hip sha256": "20a516046e8ec0075a10114599a86fe85807deb8bdc67f6725925aeecdc36701",
+                "bytes": 2699592320}
 
 
 def log(*a):

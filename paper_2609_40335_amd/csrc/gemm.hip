@@ -659,7 +659,6 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(3))) char lds_char_t;
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4_t;
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // Physical chunk of chunk c in stage row r is c ^ dl_sw(r). The 4 rows read
 // together are r = 4a..4a+3; dl_sw maps them to 0, 6, 12, 10, whose bits 1-2

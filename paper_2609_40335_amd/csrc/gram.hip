@@ -425,35 +425,34 @@ __device__ __forceinline__ void dg_wait_vmcnt() {
 }
 
 // Fused bias gradient. While a G stage (64 features of every example row)
-// sits in LDS, NT threads sum its columns: thread t adds chunk t%8 (8
-// features) of rows t/8, t/8 + NT/8, ...; the 8 row groups of a wave meet
-// by shuffles and each wave leaves 64 partials in bred. After the next
-// barrier wave 0 adds the waves' partials, writes the example's bias row for
-// those features and keeps its square.
+// sits in LDS, NT threads sum its columns: thread t adds features
+// 4*(t%16) .. +3 of rows t/16, t/16 + NT/16, ... (8-byte reads); the 4 row
+// groups of a wave meet by two shuffle levels and each wave leaves 64
+// partials in bred. After the next barrier wave 0 adds the waves' partials,
+// writes the example's bias row for those features and keeps its square.
 template <int ROWS, int NT>
 __device__ __forceinline__ void bias_stage(const u32x4* st, float* bred, int tid) {
-  const int c = tid & 7;
-  float sm[8];
+  const int q = tid & 15, c = q >> 1, h = q & 1;
+  const u32x2* st2 = (const u32x2*)st;
+  float sm[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int e = 0; e < 8; ++e) sm[e] = 0.f;
+  for (int i = 0; i < ROWS / (NT / 16); ++i) {
+    const int r = (tid >> 4) + i * (NT / 16);
+    const u32x2 v = st2[(r * 8 + swz(r, c)) * 2 + h];
 #pragma unroll
-  for (int i = 0; i < ROWS / (NT / 8); ++i) {
-    const int r = (tid >> 3) + i * (NT / 8);
-    const u32x4 v = st[r * 8 + swz(r, c)];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      sm[2 * q] += __builtin_bit_cast(float, v[q] << 16);
-      sm[2 * q + 1] += __builtin_bit_cast(float, v[q] & 0xFFFF0000u);
+    for (int k = 0; k < 2; ++k) {
+      sm[2 * k] += __builtin_bit_cast(float, v[k] << 16);
+      sm[2 * k + 1] += __builtin_bit_cast(float, v[k] & 0xFFFF0000u);
     }
   }
 #pragma unroll
-  for (int off = 8; off < WAVE; off <<= 1)
+  for (int off = 16; off < WAVE; off <<= 1)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) sm[e] += __shfl_xor(sm[e], off, WAVE);
+    for (int e = 0; e < 4; ++e) sm[e] += __shfl_xor(sm[e], off, WAVE);
   const int lane = tid & 63;
-  if (lane < 8)
+  if (lane < 16)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) bred[(tid >> 6) * 64 + lane * 8 + e] = sm[e];
+    for (int e = 0; e < 4; ++e) bred[(tid >> 6) * 64 + lane * 4 + e] = sm[e];
 }
 
 // Wave 0: features c0 .. c0+63 of the bias row `out` (up to c1); returns the
