@@ -48,6 +48,23 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// x plus the x of the lane 16 (or 32) lanes away, in every lane, from the
+// gfx950 cross-lane swaps (VALU instructions, no LDS permute). permlane16_swap
+// of x with itself returns rows (0, 0, 2, 2) of x in one result and rows
+// (1, 1, 3, 3) in the other (a row is 16 lanes); permlane32_swap returns the
+// low half twice and the high half twice. Both lanes of a pair add the same
+// two values in the same order, so they hold the same bits.
+__device__ __forceinline__ float xor16_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xor32_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ double wave_sum_d(double v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, WAVE);

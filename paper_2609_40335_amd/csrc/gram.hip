@@ -427,7 +427,7 @@ __device__ __forceinline__ void dg_wait_vmcnt() {
 // Fused bias gradient. While a G stage (64 features of every example row)
 // sits in LDS, NT threads sum its columns: thread t adds features
 // 4*(t%16) .. +3 of rows t/16, t/16 + NT/16, ... (8-byte reads); the 4 row
-// groups of a wave meet by two shuffle levels and each wave leaves 64
+// groups of a wave meet by two cross-lane swaps and each wave leaves 64
 // partials in bred. After the next barrier wave 0 adds the waves' partials,
 // writes the example's bias row for those features and keeps its square.
 template <int ROWS, int NT>
@@ -446,9 +446,7 @@ __device__ __forceinline__ void bias_stage(const u32x4* st, float* bred, int tid
     }
   }
 #pragma unroll
-  for (int off = 16; off < WAVE; off <<= 1)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) sm[e] += __shfl_xor(sm[e], off, WAVE);
+  for (int e = 0; e < 4; ++e) sm[e] = xor32_sum(xor16_sum(sm[e]));
   const int lane = tid & 63;
   if (lane < 16)
 #pragma unroll
