@@ -230,8 +230,8 @@ def test_embedding_norm_pairwise_form(dp, kind, B, T, V, d, lde):
 # ---------------------------------------------------------------------------
 # a5: tied cross term
 # ---------------------------------------------------------------------------
-def _tied_inputs(dtype, B, T, V, d, ldz, seed):
-    ids = gen.draw_ids(seed, 1, (B, T), V, "zipf")
+def _tied_inputs(dtype, B, T, V, d, ldz, seed, kind="zipf"):
+    ids = gen.draw_ids(seed, 1, (B, T), V, kind)
     dE = gen.draw(seed, 2, (B, T, d), 1e-2, dtype)
     H = gen.draw(seed, 3, (B, T, d), 1.0, dtype)
     z = gen._normal(seed, 4, (B, T, V), 1.0)
@@ -273,6 +273,33 @@ def test_tied_cross_term(dp, dtype, B, T, V, d, ldz):
     dp.dp_tied_cross_term(dev(ids), dev(dE, dtype), dev(H, dtype), dev(Gz, dtype)[:, :, :V], V,
                           n2, scale=2.0, accumulate=True)
     assert rel(host(n2), tied_ref).max() <= TOL[dtype]
+
+
+@pytest.mark.parametrize("kind", ["same", "distinct"])
+@pytest.mark.parametrize("T", [64, 128, 200])
+def test_tied_cross_term_degenerate_ids(dp, kind, T):
+    """Every token of an example with one id (one bucket: every pair (t, s)
+    meets at the same logit column, so cross = <sum_t dE_t, sum_s Gz[s, x] h_s>)
+    and every id distinct, in the register-direct kernel (T <= 128) and the
+    direct-load one (T = 200)."""
+    B, V, d = 3, 1000, 128
+    _say(f"cross degenerate ids {kind} T={T}")
+    ids, dE, H, Gz = _tied_inputs("bf16", B, T, V, d, V, seed=25, kind=kind)
+    dEd, Hd, Gzd = O.decode(dE, "bf16"), O.decode(H, "bf16"), O.decode(Gz, "bf16")
+    cross = O.tied_cross(ids, dEd, Hd, Gzd, V)
+    if kind == "same":
+        assert all(len(np.unique(ids[b])) == 1 for b in range(B))
+        closed = np.array([dEd[b].sum(0) @ (Gzd[b][:, ids[b, 0]] @ Hd[b]) for b in range(B)])
+        np.testing.assert_allclose(cross, closed, rtol=1e-10, atol=1e-12)
+    else:
+        assert all(len(np.unique(ids[b])) == T for b in range(B))
+    n_in = O.embedding_norm2(ids, dEd, V)
+    n_out = O.head_norm2(Hd, Gzd, V)
+    out = torch.zeros(B, device="cuda")
+    dp.dp_tied_cross_term(dev(ids), dev(dE, "bf16"), dev(H, "bf16"), dev(Gz, "bf16"), V, out)
+    got = host(out)
+    _say(f"  max |err| / (||gin|| ||gout||) {np.max(np.abs(got - cross) / np.sqrt(n_in * n_out)):.3e}")
+    assert np.all(np.abs(got - cross) <= TOL["bf16"] * np.sqrt(n_in * n_out))
 
 
 @pytest.mark.parametrize("T", [100, 200])

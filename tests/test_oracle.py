@@ -148,6 +148,22 @@ def test_cross_cauchy_schwarz_and_sign():
     np.testing.assert_allclose(O.tied_cross(ids, -dE, H, Gz, 7), -cross, rtol=1e-14)
 
 
+def test_cross_special_cases():
+    """One bucket: when every token of an example has id x, the input-embedding
+    gradient is a single row sum_t dE_t at x, so the cross term is that row
+    dotted with row x of the head gradient, sum_s Gz[s, x] h_s. Distinct ids:
+    each token's row meets only its own column of Gz, so the cross term is
+    sum_t <dE_t, sum_s Gz[s, x_t] h_s>, one dot product per token."""
+    T, d, V = 9, 6, 11
+    dE, H, Gz = _rand(1, T, d), _rand(1, T, d), _rand(1, T, V)
+    same = np.full((1, T), 4, np.int32)
+    want = dE[0].sum(0) @ (Gz[0][:, 4] @ H[0])
+    np.testing.assert_allclose(O.tied_cross(same, dE, H, Gz, V)[0], want, rtol=1e-12)
+    distinct = RNG.permutation(V)[:T].astype(np.int32)[None]
+    want = sum(dE[0, t] @ (Gz[0][:, distinct[0, t]] @ H[0]) for t in range(T))
+    np.testing.assert_allclose(O.tied_cross(distinct, dE, H, Gz, V)[0], want, rtol=1e-12)
+
+
 def test_embedding_special_cases():
     T, d, V = 8, 5, 32
     dE = _rand(1, T, d)
