@@ -184,7 +184,7 @@ def test_embedding_norm_and_buckets(dp, kind, T, V, dtype, d, lde):
 
 
 @pytest.mark.parametrize("kind,B,T,V,d,lde", [
-    ("zipf", 4, 128, 50257, 768, 768),     # GPT-2 shape: six 128-feature chunks, four row blocks
+    ("zipf", 4, 128, 50257, 768, 768),     # GPT-2 shape: eight 96-feature chunks, four row blocks
     ("zipf", 3, 100, 50257, 200, 208),     # ragged row block, last chunk past d, NaN padding
     ("same", 3, 33, 1000, 64, 64),         # one bucket; a second row block of one row
     ("distinct", 2, 32, 300, 136, 136),    # every id once; one row block, 8-feature tail piece
