@@ -47,8 +47,8 @@ PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
 # HBM bytes per launch of the clipped-sum kernel: rocprofv3 FETCH_SIZE x 2 +
 # WRITE_SIZE x 1 (factors from a plain 1 GiB copy), recorded for the kernel
 # source with this SHA-256; any other source reports null.
-GEMM_TRAFFIC = {"gemm.hip sha256": "20a516046e8ec0075a10114599a86fe85807deb8bdc67f6725925aeecdc36701",
-                "bytes": 2699592320}
+GEMM_TRAFFIC = {"gemm.hip sha256": "7a91e1ae131f658f382149bc039c08b59f6395901af6ec1a497ba5057e6b5138",
+                "bytes": 2698230107}
 
 
 def log(*a):

@@ -8,15 +8,21 @@
 // equals the gradient of the loss reweighted by the clip factors.
 //
 // Direct norm (the materialising alternative, "normal clipping" of Sec.
-// "Training Configurations"): ||A_i^T G_i||_F^2 for one example, from the same
+// "Training Configurations"): ||A_i^T G_i||_F^2 per example, from the same
 // GEMM restricted to the example's T rows; each 256x256 output tile is
-// squared and summed in registers and never stored. It beats the Gram form
-// when T exceeds about 2 d_in d_out / (d_in + d_out).
+// squared and summed in registers at the example's last row. A work item of
+// the direct-load kernel covers a run of consecutive examples of one tile.
+// Optionally each example's tile is also written to a gradient store, from
+// which store_sum_kernel forms the clipped sums as weighted sums of the
+// stored tiles instead of a second GEMM. The direct form beats the Gram form
+// when T + 1 exceeds about R * 2 d_in d_out / (d_in + d_out), R the measured
+// ratio of the two kernels' throughputs (about 0.4 to 0.5).
 //
-// Two kernels. dl_gemm_kernel (below, the bf16 clipped sum on aligned rows)
-// loads rows straight into LDS and transposes on the way out of LDS. The
-// general kernel kt_gemm_kernel (fp32, unaligned strides, any T, and the
-// direct norm) stages through registers:
+// Kernels. dl_gemm_kernel (bf16, 16-byte rows, whole 32-row stages per
+// example: the clipped sum and the direct norm) loads rows straight into LDS
+// and transposes on the way out of LDS; split_fixup_kernel finishes the tiles
+// of its split tail. The general kernel kt_gemm_kernel (fp32, unaligned
+// strides, any T) stages through registers:
 //
 // MFMA wants 8 consecutive k per lane, but both operands are contiguous along
 // M/N. Each staging thread loads an 8(k) x 8(m) block with 16-byte buffer
@@ -605,8 +611,9 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
 }
 
 // ---------------------------------------------------------------------------
-// Direct-load kernel for the bf16 clipped sum (16-byte aligned rows, T a
-// multiple of 32, B <= 4096): no staging through VGPRs at all.
+// Direct-load kernel for the bf16 clipped sum and direct norm (16-byte
+// aligned rows, T a multiple of 32; B <= 4096 for the clipped sum's factor
+// table): no staging through VGPRs at all.
 //
 // Global rows go straight into LDS through buffer loads that write LDS
 // (each lane's 16 bytes land at M0 + 16*lane), so LDS keeps the token-major
@@ -642,7 +649,9 @@ __global__ __launch_bounds__(GM_THREADS) void kt_gemm_kernel(GemmArgs args) {
 // Clip factors are staged in LDS so that the loop issues no other vector
 // memory instruction; each is read one example ahead, so that a rescale never
 // waits behind the fragment reads. Scaling is on the fp32 accumulators as in
-// SC_ACC.
+// SC_ACC. In the direct norm the example boundary instead squares and sums
+// each wave's part of the tile (and writes the tile to the gradient store,
+// if there is one), then clears the accumulators for the next example.
 constexpr int DL_BK = DL_SUM_BK;            // k rows per stage
 constexpr int DL_NS = 4;                    // stages in the ring
 constexpr int DL_ROWB = GM_BM * 2;          // bytes per LDS row (256 bf16)
