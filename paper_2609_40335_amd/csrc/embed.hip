@@ -9,9 +9,13 @@
 // Bucketing sorts the packed keys (id << pbits | position) of one example in
 // LDS (a stable radix sort on the id bits), marks the first token of each run
 // of equal ids, and turns the marks into dense ranks with a wavefront-shuffle
-// prefix scan. The norm then
-// sums each bucket's rows (lanes = 64 features, coalesced row reads) and
-// squares. The clipped sum sorts all B*T tokens of the batch (radix sort on
+// prefix scan. The norm takes one of two forms. Short bf16 examples (T up
+// to 128, 16-byte rows) take the pairwise form of the same quantity, sum over
+// token pairs with equal ids of <dE_t, dE_s> (the ghost-norm identity with
+// one-hot inputs), on MFMA, beside a workgroup that ranks the ids for the
+// buckets. Otherwise each bucket's rows are summed (runs split over
+// workgroups, coalesced row reads) and squared. The clipped sum sorts all
+// B*T tokens of the batch (radix sort on
 // the ids, below) and reduces runs of equal ids in fixed 32-token blocks; a run that crosses a
 // block boundary is closed by a fix-up pass that adds the block partials in
 // order. Every output row is written by exactly one wave: no atomics, and
