@@ -409,6 +409,37 @@ def test_clipped_sum_linear(dp, case, transpose):
     assert_close(got2, 2 * ref, TOL[dtype])
 
 
+@pytest.mark.parametrize("dtype,T", [("bf16", 64), ("f32", 64), ("bf16", 48)],
+                         ids=["bf16-direct-load", "f32-register-staged", "bf16-staged-rows"])
+def test_clipped_sum_wide_factor_range(dp, dtype, T):
+    """Examples with finite but huge gradients (G scaled by 2^60) next to
+    ordinary ones, with clip factors ~2^-60 against 1, as min(1, C/N) gives
+    them: every clipped contribution is O(1). The kernels that scale their
+    fp32 accumulators by c_prev / c_next at each example boundary then
+    multiply by factors up to ~2^61 and back; the sum must keep fp32's
+    relative precision across that range (T = 48 takes the kernel that scales
+    the rows as it stages them)."""
+    B, d_in, d_out = 6, 300, 520
+    _say(f"clipped sum wide factor range {dtype} T={T}")
+    A, G = _layer_inputs(dtype, B, T, d_in, d_out, seed=37)
+    Ad, Gd = O.decode(A, dtype), O.decode(G, dtype)
+    big = [1, 3, 5]
+    Gd[big] *= 2.0 ** 60                     # exact: a power of two
+    G = gen.f32_to_bf16_bits(Gd.astype(np.float32)) if dtype == "bf16" else Gd.astype(np.float32)
+    assert np.array_equal(O.decode(G, dtype), Gd)
+    c = np.array([1.0, 0.5 * 2.0 ** -60, 0.7, 0.3 * 2.0 ** -60, 1.0, 2.0 ** -61], np.float32)
+    ref = O.clipped_sum_linear(Ad, Gd, c.astype(np.float64))
+    # every example contributes at the same scale
+    parts = [np.abs(c[i] * O.linear_grad(Ad[i], Gd[i])).max() for i in range(B)]
+    assert max(parts) / min(parts) < 1e3
+    out = torch.zeros((d_in, d_out), device="cuda")
+    dp.dp_clipped_grad_sum(dev(A, dtype), dev(G, dtype), dev(c), out)
+    got = host(out)
+    assert np.isfinite(got).all()
+    err = assert_close(got, ref, TOL[dtype])
+    _say(f"  fro / element rel err {err[0]:.3e} / {err[1]:.3e}")
+
+
 # bf16 sums on 16-byte aligned rows with T % 32 == 0 take the direct-load
 # kernel (rows loaded straight into LDS, 4-stage ring, per-example factors on
 # the accumulators); these cases pin its edges.
